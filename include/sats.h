@@ -1,0 +1,166 @@
+/*
+ * sats.h -- C ABI of the routed, threshold-sparsified gated-MLP library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (per token, independently):
+ *
+ *   route:  r = route_lut[token_id]      1 = base path, 0 = sparse path
+ *           (the decision of the token-routing rule, Section 3.2, Eq. 13,
+ *            precomputed per vocabulary id; a score below tau selects the
+ *            sparse path, any other the base path)
+ *   for each layer l = 0 .. n_layers-1, with h the layer input:
+ *     a    = h . W_gate[l]                               gated MLP, Eq. 1
+ *     g    = SiLU(a) = a / (1 + exp(-a))                 Eq. 2
+ *     keep = all columns                   if r == 1     (base MLP, Eq. 1)
+ *            { j : |g_j| >= thresholds[l] } if r == 0    (CATS mask, Eq. 4-5)
+ *     u_j  = W_up_T[l][j] . h              for j in keep  (x W_up, Eq. 1)
+ *     y    = sum_{j in keep} g_j u_j W_down[l][j]         (Eq. 1)
+ *     next h = rho(y / sqrt(mean(y^2) + 1e-6))    between layers
+ *   out = rho(y of the last layer)
+ *
+ * rho rounds to the activation type (bf16: round to nearest even).  All
+ * products and sums are float32.  The normalisation between layers is this
+ * library's convention for chaining bare MLP layers (the paper places each
+ * MLP inside a transformer block); a one-layer call is exactly Eq. 1 with the
+ * Eq. 5 mask.
+ *
+ * Layouts (row-major, dense, no padding):
+ *   x, out        [n_tokens][d]
+ *   token_ids     [n_tokens]
+ *   W_gate        [n_layers][d][d_ff]      orientation of x . W_gate
+ *   W_up_T        [n_layers][d_ff][d]      W_up transposed: row j = column j of W_up
+ *   W_down        [n_layers][d_ff][d]
+ *   thresholds    [n_layers]               float32, >= 0 or +inf
+ *   route_lut     [vocab]                  uint8
+ *
+ * Ownership: every pointer is a DEVICE pointer owned by the caller and must
+ * stay valid until the enqueued work has completed.  The library keeps no
+ * pointer past that.  It owns a device workspace per (device, stream),
+ * allocated on first use and grown when a larger shape arrives (a hipMalloc
+ * on that call: call sats_reserve() first where allocation is not allowed).
+ *
+ * Errors: every call returns SATS_OK or a negative code synchronously, for
+ * conditions the host can check (null pointers, shapes, overlap of out with
+ * x other than exact equality, HIP launch failures).  The text of the last
+ * error of the calling thread is returned by sats_last_error().  Execution
+ * is asynchronous on `stream`; device-side faults surface at the caller's
+ * next synchronisation.  n_tokens == 0 returns SATS_OK and enqueues nothing.
+ *
+ * Unchecked preconditions (device contents): 0 <= token_ids[i] < vocab;
+ * thresholds not NaN and not negative; x and weights finite.
+ *
+ * Determinism: results do not depend on the run, on the batch a token is in
+ * (for batches of one size class) or on the stream; every reduction has a
+ * fixed order and no floating-point atomics are used.
+ *
+ * Concurrency: calls on different streams use different workspaces and may
+ * overlap.  Calls on one stream are ordered by the stream.
+ */
+#ifndef SATS_H
+#define SATS_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t sats_bf16; /* raw bfloat16 bits */
+
+enum {
+  SATS_OK = 0,
+  SATS_ERR_NULL = -1,      /* a required pointer is NULL                        */
+  SATS_ERR_SHAPE = -2,     /* d < 1, d_ff < 1, n_layers < 1, n_tokens < 0, or too large */
+  SATS_ERR_HIP = -3,       /* a HIP runtime call or kernel launch failed        */
+  SATS_ERR_WORKSPACE = -4, /* workspace allocation failed                       */
+  SATS_ERR_ARG = -5        /* other invalid argument (partial overlap of out and x, bad id) */
+};
+
+/*
+ * Routed sparse forward (Section 3.2 routing over the Section 2 CATS-masked
+ * gated MLP).  route_lut == NULL sends every token to the sparse path (the
+ * static sparse model) and token_ids may then be NULL.  out may equal x
+ * exactly (in-place); any other overlap is rejected.
+ */
+int sats_mlp_forward(const sats_bf16 *x, const int32_t *token_ids,
+                     const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                     const sats_bf16 *W_down, const float *thresholds,
+                     const uint8_t *route_lut, sats_bf16 *out,
+                     int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
+                     hipStream_t stream);
+
+/* Base path for every token: the unmasked gated MLP of Eq. 1, same layout. */
+int sats_mlp_dense(const sats_bf16 *x, const sats_bf16 *W_gate,
+                   const sats_bf16 *W_up_T, const sats_bf16 *W_down,
+                   sats_bf16 *out, int64_t n_tokens, int64_t d, int64_t d_ff,
+                   int64_t n_layers, hipStream_t stream);
+
+/* float32 twins: x, weights and out are float32; rho rounds to float32. */
+int sats_mlp_forward_f32(const float *x, const int32_t *token_ids,
+                         const float *W_gate, const float *W_up_T,
+                         const float *W_down, const float *thresholds,
+                         const uint8_t *route_lut, float *out,
+                         int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
+                         hipStream_t stream);
+int sats_mlp_dense_f32(const float *x, const float *W_gate, const float *W_up_T,
+                       const float *W_down, float *out, int64_t n_tokens, int64_t d,
+                       int64_t d_ff, int64_t n_layers, hipStream_t stream);
+
+/*
+ * Introspection for tests and measurement: the same computation as
+ * sats_mlp_forward, plus extra stores.  Any of the extra outputs may be NULL.
+ *   route_out     [n_tokens]                 decision used (1 base, 0 sparse)
+ *   active_count  [n_layers][n_tokens]       |keep| of each token at each layer
+ *   active_idx    [n_layers][n_tokens][d_ff] keep set, ascending, first
+ *                                            active_count entries valid
+ *   layer_in      [n_layers][n_tokens][d]    input h of each layer
+ */
+int sats_mlp_forward_inspect(const sats_bf16 *x, const int32_t *token_ids,
+                             const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                             const sats_bf16 *W_down, const float *thresholds,
+                             const uint8_t *route_lut, sats_bf16 *out,
+                             int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
+                             hipStream_t stream, uint8_t *route_out,
+                             int32_t *active_count, int32_t *active_idx,
+                             sats_bf16 *layer_in);
+int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids,
+                                 const float *W_gate, const float *W_up_T,
+                                 const float *W_down, const float *thresholds,
+                                 const uint8_t *route_lut, float *out,
+                                 int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
+                                 hipStream_t stream, uint8_t *route_out,
+                                 int32_t *active_count, int32_t *active_idx,
+                                 float *layer_in);
+
+/*
+ * Allocate the workspace of (current device, stream) for calls of up to
+ * max_tokens tokens at this d, d_ff and element size (2 = bf16, 4 = f32), so
+ * that later calls of that size or smaller allocate nothing.
+ */
+int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int elem_bytes,
+                 hipStream_t stream);
+
+/* Free every workspace of the calling process (synchronises each device). */
+int sats_release(void);
+
+/* Thread-local text of the last error returned on this thread ("" if none). */
+const char *sats_last_error(void);
+
+/*
+ * Kernel timing for measurement.  sats_timing_begin(kind, capacity) arms
+ * HIP-event pairs around the next `capacity` launches of one kernel kind
+ * (SATS_K_*), recorded on the stream the kernel is launched on.
+ * sats_timing_end(kind, &total_ms, &count) waits for the recorded events,
+ * returns the summed duration and the number of launches timed, and disarms.
+ */
+enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_COUNT = 4 };
+int sats_timing_begin(int kind, int capacity);
+int sats_timing_end(int kind, double *total_ms, int64_t *count);
+const char *sats_kernel_name(int kind);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SATS_H */

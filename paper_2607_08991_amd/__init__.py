@@ -1,0 +1,11 @@
+"""Routed, threshold-sparsified gated MLP for AMD Instinct MI355X (gfx950).
+
+The computation lives in libsats.so (hand-written HIP kernels behind the C ABI
+of include/sats.h).  This package is its ctypes binding, the build script and
+nothing else.
+"""
+from ._lib import (  # noqa: F401
+    SatsError, load, sats_mlp_forward, sats_mlp_dense, sats_mlp_forward_inspect,
+    sats_reserve, sats_release, sats_last_error, sats_timing_begin, sats_timing_end,
+    sats_kernel_name, SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, LIB_PATH,
+)

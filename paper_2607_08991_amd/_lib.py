@@ -1,0 +1,155 @@
+"""ctypes binding of libsats.so: the C ABI of include/sats.h, one Python
+function per entry point with the same name.
+
+Marshalling only: tensors are passed as device pointers, the stream defaults
+to torch's current stream, and a nonzero return code raises SatsError with the
+library's own message.  Every step of the computation runs in the library's
+HIP kernels; there is no fallback of any kind.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsats.so")
+
+SATS_OK, SATS_ERR_NULL, SATS_ERR_SHAPE, SATS_ERR_HIP, SATS_ERR_WORKSPACE, SATS_ERR_ARG = 0, -1, -2, -3, -4, -5
+SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT = 0, 1, 2, 3
+
+# exported symbols and their argument types (p = pointer, i = int64, s = stream, n = int32)
+_P, _I, _S, _N = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+_FWD = [_P] * 8 + [_I] * 4 + [_S]
+_DENSE = [_P] * 5 + [_I] * 4 + [_S]
+_INSPECT = _FWD + [_P] * 4
+SIGNATURES = {
+    "sats_mlp_forward": (_FWD, _N),
+    "sats_mlp_dense": (_DENSE, _N),
+    "sats_mlp_forward_f32": (_FWD, _N),
+    "sats_mlp_dense_f32": (_DENSE, _N),
+    "sats_mlp_forward_inspect": (_INSPECT, _N),
+    "sats_mlp_forward_inspect_f32": (_INSPECT, _N),
+    "sats_reserve": ([_I, _I, _I, _N, _S], _N),
+    "sats_release": ([], _N),
+    "sats_last_error": ([], ctypes.c_char_p),
+    "sats_timing_begin": ([_N, _N], _N),
+    "sats_timing_end": ([_N, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], _N),
+    "sats_kernel_name": ([_N], ctypes.c_char_p),
+}
+
+
+class SatsError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"sats error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libsats.so (built by paper_2607_08991_amd.build); raise if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_2607_08991_amd.build` "
+                          "(the HIP library is required: there is no other implementation)")
+    lib = ctypes.CDLL(path)
+    for name, (args, res) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("device tensors are required")
+    if not t.is_contiguous():
+        raise ValueError("contiguous tensors are required")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(rc: int):
+    if rc != SATS_OK:
+        raise SatsError(rc, load().sats_last_error().decode())
+
+
+def _call(name, *args):
+    _check(getattr(load(), name)(*args))
+
+
+def sats_mlp_forward(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out,
+                     n_tokens, d, d_ff, n_layers, stream=None):
+    name = "sats_mlp_forward_f32" if _is_f32(x) else "sats_mlp_forward"
+    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+          _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers, _stream(stream))
+
+
+def sats_mlp_dense(x, W_gate, W_up_T, W_down, out, n_tokens, d, d_ff, n_layers, stream=None):
+    name = "sats_mlp_dense_f32" if _is_f32(x) else "sats_mlp_dense"
+    _call(name, _ptr(x), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down), _ptr(out), n_tokens, d, d_ff,
+          n_layers, _stream(stream))
+
+
+def sats_mlp_forward_inspect(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out,
+                             n_tokens, d, d_ff, n_layers, stream=None, route_out=None,
+                             active_count=None, active_idx=None, layer_in=None):
+    name = "sats_mlp_forward_inspect_f32" if _is_f32(x) else "sats_mlp_forward_inspect"
+    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+          _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers,
+          _stream(stream), _ptr(route_out), _ptr(active_count), _ptr(active_idx), _ptr(layer_in))
+
+
+def sats_reserve(max_tokens, d, d_ff, elem_bytes, stream=None):
+    _call("sats_reserve", max_tokens, d, d_ff, elem_bytes, _stream(stream))
+
+
+def sats_release():
+    _call("sats_release")
+
+
+def sats_last_error() -> str:
+    return load().sats_last_error().decode()
+
+
+def sats_timing_begin(kind: int, capacity: int):
+    _call("sats_timing_begin", kind, capacity)
+
+
+def sats_timing_end(kind: int):
+    """Returns (total_ms, count) of the launches timed since sats_timing_begin."""
+    ms = ctypes.c_double(0.0)
+    cnt = ctypes.c_int64(0)
+    _check(load().sats_timing_end(kind, ctypes.byref(ms), ctypes.byref(cnt)))
+    return ms.value, cnt.value
+
+
+def sats_kernel_name(kind: int) -> str:
+    return load().sats_kernel_name(kind).decode()
+
+
+def _is_f32(x) -> bool:
+    if isinstance(x, int) or x is None:
+        raise ValueError("pass a tensor for x so the element type is known, or call load() directly")
+    import torch
+    if x.dtype == torch.float32:
+        return True
+    if x.dtype == torch.bfloat16:
+        return False
+    raise ValueError(f"x must be bfloat16 or float32, got {x.dtype}")

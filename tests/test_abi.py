@@ -1,0 +1,89 @@
+"""The C-ABI library loads, exports every entry point of include/sats.h, and
+rejects bad arguments before touching the GPU (no device needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_08991_amd as sats
+from paper_2607_08991_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sats.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sats_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_entry_points():
+    syms = declared_symbols()
+    for name in ["sats_mlp_forward", "sats_mlp_dense", "sats_mlp_forward_f32", "sats_mlp_dense_f32",
+                 "sats_mlp_forward_inspect", "sats_last_error"]:
+        assert name in syms
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    missing = [s for s in declared_symbols() if not hasattr(lib, s)]
+    assert not missing, missing
+    assert set(declared_symbols()) == set(_lib.SIGNATURES)
+
+
+def test_library_is_built_for_gfx950():
+    data = open(_lib.LIB_PATH, "rb").read()
+    assert b"gfx950" in data
+
+
+FAKE = 1 << 20  # a non-null address: never dereferenced by the host checks below
+
+
+def fwd(**kw):
+    args = dict(x=FAKE, ids=FAKE, wg=FAKE, wu=FAKE, wd=FAKE, thr=FAKE, lut=FAKE, out=FAKE * 16,
+                n=1, d=8, dff=8, L=1)
+    args.update(kw)
+    a = args
+    return sats.load().sats_mlp_forward(a["x"], a["ids"], a["wg"], a["wu"], a["wd"], a["thr"],
+                                        a["lut"], a["out"], a["n"], a["d"], a["dff"], a["L"], None)
+
+
+@pytest.mark.parametrize("field", ["x", "wg", "wu", "wd", "out", "thr"])
+def test_null_pointers_rejected(field):
+    assert fwd(**{field: None}) == _lib.SATS_ERR_NULL
+    assert sats.sats_last_error()
+
+
+def test_ids_required_with_lut_but_not_without():
+    assert fwd(ids=None) == _lib.SATS_ERR_NULL
+    assert "token_ids" in sats.sats_last_error()
+    assert fwd(ids=None, lut=None, n=0) == _lib.SATS_OK
+
+
+@pytest.mark.parametrize("kw", [dict(d=0), dict(dff=0), dict(L=0), dict(n=-1), dict(d=1 << 25)])
+def test_bad_shapes_rejected(kw):
+    assert fwd(**kw) == _lib.SATS_ERR_SHAPE
+
+
+def test_zero_tokens_is_a_no_op():
+    assert fwd(n=0) == _lib.SATS_OK
+    assert sats.sats_last_error() == ""
+    lib = sats.load()
+    assert lib.sats_mlp_dense(FAKE, FAKE, FAKE, FAKE, FAKE, 0, 8, 8, 1, None) == _lib.SATS_OK
+
+
+def test_partial_overlap_of_out_and_x_rejected():
+    # x spans [FAKE, FAKE + 2*8*2) in bf16; out starting 2 bytes in overlaps without being equal
+    assert fwd(n=2, out=FAKE + 2) == _lib.SATS_ERR_ARG
+    assert "overlap" in sats.sats_last_error()
+
+
+def test_dense_needs_no_thresholds_but_checks_weights():
+    lib = sats.load()
+    assert lib.sats_mlp_dense(FAKE, None, FAKE, FAKE, FAKE, 1, 8, 8, 1, None) == _lib.SATS_ERR_NULL
+
+
+def test_reserve_rejects_bad_element_size():
+    assert sats.load().sats_reserve(4, 8, 8, 3, None) == _lib.SATS_ERR_ARG

@@ -1,0 +1,193 @@
+"""GPU parity: the HIP library through its C ABI against the CPU oracle.
+
+Inputs are seeded (workloads.synth); thresholds are CATS percentiles computed
+by the oracle (Eq. 3).  See tests/harness.py for the comparison rules.
+"""
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import calibrate, mlp, numerics
+from workloads import get_config, synth
+
+from harness import TOL, check_against_oracle, from_dev, rel_err, run_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "thresholds.json")
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    import paper_2607_08991_amd as sats
+    sats.load()
+
+
+def case_thresholds(case, dtype, k=0.5, n_cal=24, seed=0):
+    """CATS thresholds (oracle, Eq. 3) of a small case from its own calibration tokens."""
+    L, d, _ = case["W_gate"].shape
+    xcal = synth.activations(900 + seed, synth.S_CAL, n_cal, d, dtype)
+    return calibrate.calibrate_stack(xcal, case["W_gate"], case["W_up_T"], case["W_down"],
+                                     [k] * L, dtype)
+
+
+SMALL = [
+    # seed, layers, d, d_ff, dtype, tokens
+    (1, 1, 512, 1536, "f32", 1),     # the small fp32 layer shape, one token
+    (2, 1, 256, 1000, "bf16", 1),    # ragged last column block
+    (3, 3, 256, 1000, "bf16", 5),    # stack; one full and one ragged token tile
+    (4, 2, 24, 40, "bf16", 3),       # tiny vector path, every block ragged
+    (5, 2, 25, 41, "bf16", 3),       # odd sizes: scalar path
+    (6, 2, 25, 41, "f32", 2),        # odd sizes, fp32
+    (7, 2, 128, 512, "f32", 67),     # more tokens than one pass (64)
+    (8, 1, 4096, 1024, "bf16", 2),   # long rows: several row chunks in the gate split
+]
+
+
+@pytest.mark.parametrize("seed,L,d,dff,dtype,n", SMALL)
+def test_small_cases_match_oracle(seed, L, d, dff, dtype, n):
+    say(f"case seed={seed} L={L} d={d} d_ff={dff} {dtype} n={n}")
+    c = synth.small_case(seed, L, d, dff, dtype, n, vocab=40, n_dense_ids=12,
+                         w_std=1.0 / np.sqrt(d))
+    ts = case_thresholds(c, dtype, seed=seed)
+    for lut in (None, c["route_lut"]):
+        res = run_gpu(c, ts, lut, dtype)
+        worst = check_against_oracle(c, ts, lut, dtype, res)
+        say(f"  lut={'yes' if lut is not None else 'no'} worst rel err {worst:.3g}")
+        kept = res["count"].mean() / dff
+        assert 0.05 < kept < 0.95 or lut is not None
+
+
+def test_forward_equals_inspect_bitwise_and_is_deterministic():
+    c = synth.small_case(21, 2, 256, 1024, "bf16", 6, vocab=40, n_dense_ids=12, w_std=1 / 16)
+    ts = case_thresholds(c, "bf16")
+    a = run_gpu(c, ts, c["route_lut"], "bf16", inspect=False)
+    b = run_gpu(c, ts, c["route_lut"], "bf16", inspect=False)
+    r = run_gpu(c, ts, c["route_lut"], "bf16", inspect=True)
+    np.testing.assert_array_equal(a["out"], b["out"])
+    np.testing.assert_array_equal(a["out"], r["out"])
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_threshold_zero_equals_dense_and_all_dense_lut(dtype):
+    c = synth.small_case(22, 2, 128, 384, dtype, 5, vocab=40, n_dense_ids=12, w_std=1 / 11)
+    z = run_gpu(c, [0.0, 0.0], None, dtype, inspect=False)
+    dn = run_gpu(c, [0.3, 0.3], None, dtype, dense=True)
+    allb = run_gpu(c, [0.3, 0.3], np.ones(40, np.uint8), dtype, inspect=False)
+    np.testing.assert_array_equal(z["out"], dn["out"])
+    np.testing.assert_array_equal(allb["out"], dn["out"])
+    ref = mlp.forward_dense(c["x"], c["W_gate"], c["W_up_T"], c["W_down"], dtype)
+    for i in range(5):
+        assert rel_err(numerics.decode(dn["out"][i], dtype), ref[i]) <= TOL[dtype]
+
+
+def test_threshold_inf_gives_exact_zero():
+    c = synth.small_case(23, 3, 64, 256, "bf16", 4, w_std=0.125)
+    for ts in ([np.inf] * 3, [0.0, np.inf, 0.1]):
+        res = run_gpu(c, ts, None, "bf16")
+        assert np.all(numerics.decode(res["out"], "bf16") == 0)
+    res = run_gpu(c, [0.05, np.inf, 0.0], None, "bf16")
+    assert np.all(res["count"][1] == 0) and np.all(res["count"][2] == 256)
+
+
+def test_mixed_groups_duplicates_and_last_id():
+    c = synth.small_case(24, 2, 128, 512, "bf16", 7, vocab=50, w_std=1 / 11)
+    lut = np.zeros(50, np.uint8)
+    lut[[3, 49]] = 1
+    c["token_ids"] = np.array([3, 3, 49, 0, 49, 7, 7], np.int32)
+    ts = case_thresholds(c, "bf16")
+    res = run_gpu(c, ts, lut, "bf16")
+    np.testing.assert_array_equal(res["route"], [1, 1, 1, 0, 1, 0, 0])
+    check_against_oracle(c, ts, lut, "bf16", res)
+    # duplicate tokens with the same id and input give identical rows
+    c["x"][1] = c["x"][0]
+    res = run_gpu(c, ts, lut, "bf16", inspect=False)
+    np.testing.assert_array_equal(res["out"][0], res["out"][1])
+    # only dense, only sparse
+    for ids in ([3, 49, 3, 49, 3, 3, 49], [0, 1, 2, 4, 5, 6, 8]):
+        c["token_ids"] = np.array(ids, np.int32)
+        res = run_gpu(c, ts, lut, "bf16")
+        check_against_oracle(c, ts, lut, "bf16", res)
+
+
+def test_in_place_output():
+    c = synth.small_case(25, 2, 128, 512, "bf16", 3, w_std=1 / 11)
+    ts = case_thresholds(c, "bf16")
+    ref = run_gpu(c, ts, None, "bf16", inspect=False)
+    inpl = run_gpu(c, ts, None, "bf16", inspect=False, out_is_x=True)
+    np.testing.assert_array_equal(ref["out"], inpl["out"])
+
+
+def test_zero_tokens_leaves_output_untouched():
+    import torch
+    import paper_2607_08991_amd as sats
+    out = torch.full((1, 8), 5.0, dtype=torch.bfloat16, device="cuda")
+    w = torch.zeros(8 * 8, dtype=torch.bfloat16, device="cuda")
+    thr = torch.zeros(1, device="cuda")
+    sats.sats_mlp_forward(out, None, w, w, w, thr, None, out, 0, 8, 8, 1)
+    torch.cuda.synchronize()
+    assert torch.all(out == 5.0)
+
+
+def test_batch_rows_match_single_token_calls():
+    c = synth.small_case(26, 2, 256, 768, "bf16", 9, vocab=40, n_dense_ids=12, w_std=1 / 16)
+    ts = case_thresholds(c, "bf16")
+    full = run_gpu(c, ts, c["route_lut"], "bf16")
+    for i in range(9):
+        one = dict(c, x=c["x"][i:i + 1], token_ids=c["token_ids"][i:i + 1])
+        r1 = run_gpu(one, ts, c["route_lut"], "bf16")
+        for l in range(2):
+            k = r1["count"][l][0]
+            np.testing.assert_array_equal(r1["count"][l][0], full["count"][l][i])
+            np.testing.assert_array_equal(r1["idx"][l][0][:k], full["idx"][l][i][:k])
+        e = rel_err(numerics.decode(full["out"][i], "bf16"), numerics.decode(r1["out"][0], "bf16"))
+        assert e <= TOL["bf16"]
+
+
+def _golden(cfg):
+    with open(GOLDEN) as f:
+        g = json.load(f)[cfg.name]
+    return np.asarray(g["thresholds"], np.float32)
+
+
+def test_config_small_fp32_layer():
+    """One fp32 layer d=512, d_ff=1536, 1000 ids with 300 routed to the base path."""
+    cfg = get_config(0)
+    ts = _golden(cfg)
+    wg, wu, wd = synth.layer_weights(cfg.seed, 0, cfg.d, cfg.d_ff, cfg.dtype)
+    n = 64
+    c = dict(x=synth.decode_x(cfg, n), token_ids=synth.token_ids(cfg, n), W_gate=wg[None],
+             W_up_T=wu[None], W_down=wd[None])
+    lut = synth.config_lut(cfg)
+    res = run_gpu(c, ts, lut, cfg.dtype)
+    worst = check_against_oracle(c, ts, lut, cfg.dtype, res)
+    say(f"c1 worst rel err {worst:.3g}; dense tokens {int(res['route'].sum())}/{n}")
+    assert 0 < res["route"].sum() < n
+
+
+def test_config_llama_layer_full_size():
+    """Llama-3.1-8B-shaped layer (4096 x 14336, bf16), all tokens sparse, batch 1 and 4."""
+    cfg = get_config(1)
+    ts = _golden(cfg)
+    say("generating c2 weights")
+    wg, wu, wd = synth.layer_weights(cfg.seed, 0, cfg.d, cfg.d_ff, cfg.dtype)
+    dec = [numerics.decode(w, "bf16") for w in (wg, wu, wd)]
+    for n in (1, 4):
+        c = dict(x=synth.decode_x(cfg, n), token_ids=np.zeros(n, np.int32), W_gate=wg[None],
+                 W_up_T=wu[None], W_down=wd[None])
+        res = run_gpu(c, ts, None, cfg.dtype)
+        worst = check_against_oracle(c, ts, None, cfg.dtype, res, weights=lambda l: dec)
+        sp = 1 - res["count"].mean() / cfg.d_ff
+        say(f"c2 n={n}: worst rel err {worst:.3g}, realized sparsity {sp:.4f}")
+        assert 0.4 < sp < 0.6
