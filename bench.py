@@ -1,0 +1,243 @@
+"""Routed sparse-MLP decode throughput on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c2]
+
+A step is one call of ``sats_mlp_forward`` on one decode batch: routing,
+gate projection, SiLU + threshold + compaction, up-projection over the kept
+rows and the gathered down-projection with its two-stage reduction.  The
+default workload is one Llama-3.1-8B-shaped gated-MLP layer (d=4096,
+d_ff=14336, bf16 weights N(0, 0.02^2)), decode batch 1, every token on the
+sparse path, threshold = CATS 50th percentile over 1024 seeded calibration
+tokens.  Inputs are synthetic and resident in HBM before timing starts.
+
+To keep the 256 MB Infinity Cache from serving weights, the step rotates over
+several copies of the layer's weights at different addresses (identical
+bytes, so identical results).  The same steps are timed for
+``sats_mlp_dense`` (base path) to give the speedup over dense.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "routed sparse-MLP decode tok/s at 8B shape; achieved HBM GB/s; speedup vs dense"
+GOLDEN = os.path.join(ROOT, "tests", "golden", "thresholds.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=2000)
+    p.add_argument("--warmup", type=int, default=100)
+    p.add_argument("--workload", default="c2")
+    p.add_argument("--copies", type=int, default=8, help="weight copies rotated to defeat the MALL")
+    p.add_argument("--tokens", type=int, default=64, help="distinct decode tokens cycled over")
+    p.add_argument("--cpu-sample", type=int, default=48, help="tokens the CPU oracle is timed on")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--no-dense", action="store_true")
+    return p.parse_args()
+
+
+def thresholds_for(cfg):
+    with open(GOLDEN) as f:
+        return np.asarray(json.load(f)[cfg.name]["thresholds"], np.float32)
+
+
+def cpu_baseline(cfg, weights_np, ts, x_np, n_sample):
+    """The CPU oracle, as it is, on the first n_sample decode tokens."""
+    from oracle import mlp  # test infrastructure: only this leg of the benchmark uses it
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [(i.get("internal_api"), i.get("num_threads")) for i in threadpool_info()]
+    except Exception:  # pragma: no cover
+        blas = []
+    cores = len(os.sched_getaffinity(0))
+    threads = max([t for _, t in blas if t] or [1])
+    wg, wu, wd = weights_np
+    x = x_np[:n_sample]
+    t0 = time.perf_counter()
+    mlp.forward(x, np.zeros(len(x), np.int32), wg[None], wu[None], wd[None], ts, None, cfg.dtype)
+    dt = time.perf_counter() - t0
+    return {"value": round(len(x) / dt, 3), "unit": "tok/s", "cores": int(min(threads, cores)),
+            "kind": "oracle",
+            "sample": f"{len(x)} decode tokens of the same workload through the float64 numpy oracle "
+                      f"(weights decoded once per call); {dt:.1f} s; host has {cores} cores; "
+                      f"BLAS {blas}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(sharding is described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_08991_amd as sats
+    from workloads import get_config, synth
+
+    sats.load()
+    cfg = get_config({"c1": 0, "c2": 1}.get(args.workload, args.workload))
+    if cfg.n_layers != 1:
+        raise SystemExit("only the one-layer workloads are benchmarked by this script")
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ts = thresholds_for(cfg)
+    d, d_ff, L = cfg.d, cfg.d_ff, cfg.n_layers
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    esz = cfg.elem_bytes
+
+    log(f"[bench] generating {cfg.name} weights")
+    wnp = synth.layer_weights(cfg.seed, 0, d, d_ff, cfg.dtype)
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        t = torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a)
+        return t.view(tdt).to(dev) if a.dtype == np.uint16 else t.to(dev)
+
+    base = [up(w) for w in wnp]
+    copies = [base] + [[w.clone() for w in base] for _ in range(args.copies - 1)]
+    xnp = synth.decode_x(cfg, args.tokens)
+    X = up(xnp)
+    lut = synth.config_lut(cfg)
+    ids = torch.from_numpy(synth.token_ids(cfg, args.tokens)).to(dev)
+    dlut = torch.from_numpy(lut).to(dev) if lut is not None else None
+    thr = torch.from_numpy(ts).to(dev)
+    out = torch.empty((args.tokens, d), dtype=tdt, device=dev)
+    n = 1  # decode batch
+    stream = torch.cuda.current_stream()
+
+    # kept-row counts of every decode token (identical inputs -> identical counts in the timed run)
+    cnt = torch.zeros((L, args.tokens), dtype=torch.int32, device=dev)
+    route = torch.zeros(args.tokens, dtype=torch.uint8, device=dev)
+    for i in range(args.tokens):
+        sats.sats_mlp_forward_inspect(X[i:i + 1], ids[i:i + 1] if dlut is not None else None,
+                                      *base, thr, dlut, out[i:i + 1], 1, d, d_ff, L,
+                                      route_out=route[i:i + 1], active_count=cnt[:, i:i + 1])
+    torch.cuda.synchronize()
+    kept = cnt.cpu().numpy().astype(np.float64)
+    routed_base = route.cpu().numpy()
+
+    def step_fwd(s):
+        i = s % args.tokens
+        w = copies[s % args.copies]
+        sats.sats_mlp_forward(X[i:i + 1], ids[i:i + 1] if dlut is not None else None, w[0], w[1],
+                              w[2], thr, dlut, out[i:i + 1], n, d, d_ff, L, stream)
+
+    def step_dense(s):
+        i = s % args.tokens
+        w = copies[s % args.copies]
+        sats.sats_mlp_dense(X[i:i + 1], w[0], w[1], w[2], out[i:i + 1], n, d, d_ff, L, stream)
+
+    def timed(fn, kinds=()):
+        for s in range(args.warmup):
+            fn(s)
+        torch.cuda.synchronize()
+        for k in kinds:
+            sats.sats_timing_begin(k, args.steps)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for s in range(args.steps):
+            fn(args.warmup + s)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        kt = {}
+        for k in kinds:
+            tot, c = sats.sats_timing_end(k)
+            if c:
+                kt[sats.sats_kernel_name(k)] = (tot / c, c)
+        return ms, kt
+
+    log(f"[bench] timing {args.steps} steps (warmup {args.warmup}), {args.copies} weight copies")
+    kinds = (sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_DECODE)
+    # headline timing without per-kernel events (recording them costs a few us
+    # per launch); per-kernel durations come from an identical second region
+    ms, _ = timed(step_fwd)
+    ms_ev, kt = timed(step_fwd, kinds)
+    dense_ms = None
+    if not args.no_dense:
+        dense_ms, _ = timed(step_dense)
+
+    # algorithmic bytes: all of W_gate, the kept rows of W_up_T and W_down, x and out
+    steps_idx = (args.warmup + np.arange(args.steps)) % args.tokens
+    a_mean = float(kept[:, steps_idx].sum(axis=0).mean())           # kept rows per step (all layers)
+    gate_bytes = d * d_ff * esz + n * d * esz
+    updown_row = d * esz
+    touched = L * d * d_ff * esz + 2 * updown_row * a_mean + 2 * n * d * esz
+    gbps = touched / (ms * 1e-3) / 1e9
+    sparsity = 1.0 - a_mean / (L * d_ff)
+
+    up_bytes = updown_row * a_mean / L
+    kern = {}
+    for name, (kms, c) in kt.items():
+        b = {"gate_kernel": gate_bytes, "up_kernel": up_bytes, "down_kernel": up_bytes,
+             "decode_kernel": touched}[name]
+        kern[name] = {"avg_us": round(kms * 1e3, 3), "launches": c,
+                      "algorithmic_bytes": int(b), "achieved_gbps": round(b / (kms * 1e-3) / 1e9, 1)}
+    dom = max(kern, key=lambda k: kern[k]["avg_us"])
+    dom_b = kern[dom]["algorithmic_bytes"]
+    dom_gbps = dom_b / (kern[dom]["avg_us"] * 1e-6) / 1e9
+
+    cpu = None
+    if not args.no_cpu:
+        log(f"[bench] timing the CPU oracle on {args.cpu_sample} tokens")
+        cpu = cpu_baseline(cfg, wnp, ts, xnp, args.cpu_sample)
+
+    res = {
+        "metric": METRIC,
+        "value": round(1e3 / ms * n, 2),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: one Llama-3.1-8B-shaped gated-MLP layer" if cfg.index == 1
+                   else cfg.name,
+                   "d": d, "d_ff": d_ff, "n_layers": L, "decode_batch": n,
+                   "route": "all tokens sparse" if lut is None else "route_lut",
+                   "threshold": [float(t) for t in ts], "target_sparsity": cfg.k_fixed,
+                   "weight_copies_rotated": args.copies},
+        "hbm_gbps_touched": round(gbps, 1),
+        "hbm_frac_touched": round(gbps / HBM_PEAK_GBPS, 4),
+        "touched_bytes_per_step": int(touched),
+        "realized_sparsity": round(sparsity, 5),
+        "realized_base_routed_fraction": float(routed_base.mean()),
+        "ms_per_step_with_kernel_events": round(ms_ev, 6),
+        "dense_ms_per_step": None if dense_ms is None else round(dense_ms, 6),
+        "dense_hbm_gbps": None if dense_ms is None else
+        round((3 * L * d * d_ff * esz + 2 * n * d * esz) / (dense_ms * 1e-3) / 1e9, 1),
+        "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 4),
+        "kernels": kern,
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(dom_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

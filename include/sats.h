@@ -74,7 +74,8 @@ enum {
   SATS_ERR_SHAPE = -2,     /* d < 1, d_ff < 1, n_layers < 1, n_tokens < 0, or too large */
   SATS_ERR_HIP = -3,       /* a HIP runtime call or kernel launch failed        */
   SATS_ERR_WORKSPACE = -4, /* workspace allocation failed                       */
-  SATS_ERR_ARG = -5        /* other invalid argument (partial overlap of out and x, bad id) */
+  SATS_ERR_ARG = -5,       /* other invalid argument (partial overlap of out and x)        */
+  SATS_ERR_DEVICE = -6     /* reported by sats_device_status: a device-side wait gave up  */
 };
 
 /*
@@ -135,11 +136,20 @@ int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids,
 
 /*
  * Allocate the workspace of (current device, stream) for calls of up to
- * max_tokens tokens at this d, d_ff and element size (2 = bf16, 4 = f32), so
- * that later calls of that size or smaller allocate nothing.
+ * max_tokens tokens at this d, d_ff, n_layers and element size (2 = bf16,
+ * 4 = f32), so that later calls of that size or smaller allocate nothing.
  */
-int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int elem_bytes,
-                 hipStream_t stream);
+int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
+                 int elem_bytes, hipStream_t stream);
+
+/*
+ * Synchronise `stream` and report whether any kernel of this library on it
+ * gave up a bounded device-side wait since the last check (SATS_ERR_DEVICE;
+ * the flag is cleared).  Such a wait only gives up when workgroups of one
+ * launch could not all run at once, which the cooperative launch rules out;
+ * the bound exists so that a kernel always terminates.
+ */
+int sats_device_status(hipStream_t stream);
 
 /* Free every workspace of the calling process (synchronises each device). */
 int sats_release(void);
@@ -154,7 +164,8 @@ const char *sats_last_error(void);
  * sats_timing_end(kind, &total_ms, &count) waits for the recorded events,
  * returns the summed duration and the number of launches timed, and disarms.
  */
-enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_COUNT = 4 };
+enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_DECODE = 4,
+       SATS_K_COUNT = 5 };
 int sats_timing_begin(int kind, int capacity);
 int sats_timing_end(int kind, double *total_ms, int64_t *count);
 const char *sats_kernel_name(int kind);

@@ -15,7 +15,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libsats.so")
 
 SATS_OK, SATS_ERR_NULL, SATS_ERR_SHAPE, SATS_ERR_HIP, SATS_ERR_WORKSPACE, SATS_ERR_ARG = 0, -1, -2, -3, -4, -5
-SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT = 0, 1, 2, 3
+SATS_ERR_DEVICE = -6
+SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DECODE = 0, 1, 2, 3, 4
 
 # exported symbols and their argument types (p = pointer, i = int64, s = stream, n = int32)
 _P, _I, _S, _N = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
@@ -29,7 +30,8 @@ SIGNATURES = {
     "sats_mlp_dense_f32": (_DENSE, _N),
     "sats_mlp_forward_inspect": (_INSPECT, _N),
     "sats_mlp_forward_inspect_f32": (_INSPECT, _N),
-    "sats_reserve": ([_I, _I, _I, _N, _S], _N),
+    "sats_reserve": ([_I, _I, _I, _I, _N, _S], _N),
+    "sats_device_status": ([_S], _N),
     "sats_release": ([], _N),
     "sats_last_error": ([], ctypes.c_char_p),
     "sats_timing_begin": ([_N, _N], _N),
@@ -116,8 +118,13 @@ def sats_mlp_forward_inspect(x, token_ids, W_gate, W_up_T, W_down, thresholds, r
           _stream(stream), _ptr(route_out), _ptr(active_count), _ptr(active_idx), _ptr(layer_in))
 
 
-def sats_reserve(max_tokens, d, d_ff, elem_bytes, stream=None):
-    _call("sats_reserve", max_tokens, d, d_ff, elem_bytes, _stream(stream))
+def sats_reserve(max_tokens, d, d_ff, n_layers, elem_bytes, stream=None):
+    _call("sats_reserve", max_tokens, d, d_ff, n_layers, elem_bytes, _stream(stream))
+
+
+def sats_device_status(stream=None):
+    """Synchronise the stream; raise SatsError if a device-side bounded wait gave up."""
+    _call("sats_device_status", _stream(stream))
 
 
 def sats_release():

@@ -19,9 +19,9 @@
 //                 (or the rounded output for the last layer) and the slice's
 //                 sum of squares for the next layer's normalisation.
 //
-// Cross-workgroup hand-off (partials -> last workgroup) uses a release fence
-// and an agent-scope counter; the counters reset themselves so no memset is
-// needed between launches.  No floating-point atomics: results are
+// Cross-workgroup hand-off (partials -> last workgroup) uses device-coherent
+// stores and loads and an agent-scope counter; the counters reset themselves
+// so no memset is needed between launches.  No floating-point atomics: results are
 // deterministic.
 #pragma once
 
@@ -85,6 +85,22 @@ __device__ __forceinline__ void load_vec(const T *__restrict__ p, float (&w)[VEC
   }
 }
 
+// Raw 16-byte loads, unpacked element by element where they are used (keeps
+// bf16 data packed in registers).
+template <typename T>
+__device__ __forceinline__ u32x4 load_raw(const T *__restrict__ p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+template <typename T>
+__device__ __forceinline__ float unpack(const u32x4 &q, int v) {
+  if constexpr (sizeof(T) == 2) {
+    const uint32_t w = q[v >> 1];
+    return __uint_as_float((v & 1) ? (w & 0xffff0000u) : (w << 16));
+  } else {
+    return __uint_as_float(q[v]);
+  }
+}
+
 // Same for small, reused operands (cached load).
 template <typename T, int VEC>
 __device__ __forceinline__ void load_vec_cached(const T *__restrict__ p, float (&w)[VEC]) {
@@ -112,23 +128,49 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Release this thread's prior global writes, count one arrival of the
-// workgroup, and report whether it was the last of `expected` arrivals.  On
-// the last arrival the counter is reset to zero for the next launch and an
-// acquire fence makes the other workgroups' writes visible.
+// Cross-workgroup hand-off without cache-wide maintenance.  Partials that
+// another workgroup will read are written with device-coherent stores
+// (agent-scope atomic stores: written through to the device-coherent level)
+// and read back with device-coherent loads, so no L2 writeback or invalidate
+// is needed.  arrive_last() waits for this thread's stores to complete,
+// counts one arrival of the workgroup and reports whether it was the last of
+// `expected`; the last arrival resets the counter for the next launch.
+__device__ __forceinline__ void store_coherent(float *p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float *p) {
+  return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// sum_{q < n} p[q * stride], added in index order.  The loads are issued 16 at
+// a time before any is used (one memory latency per 16 terms instead of one
+// per term); addresses past n are clamped in bounds and their values dropped.
+__device__ __forceinline__ float sum_coherent(const float *p, size_t stride, int n) {
+  float s = 0.0f;
+  for (int q0 = 0; q0 < n; q0 += 16) {
+    float v[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) v[q] = load_coherent(p + (size_t)min(q0 + q, n - 1) * stride);
+#pragma unroll
+    for (int q = 0; q < 16; ++q)
+      if (q0 + q < n) s += v[q];
+  }
+  return s;
+}
+
 __device__ __forceinline__ bool arrive_last(unsigned *counter, unsigned expected, int *flag_lds) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's coherent stores have completed
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __syncthreads();
   if (threadIdx.x == 0) {
-    unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int last = (prev == expected - 1);
     if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *flag_lds = last;
   }
   __syncthreads();
-  const bool last = *flag_lds != 0;
-  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return last;
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  return *flag_lds != 0;
 }
 
 // Route modes: every token sparse, table lookup, every token base.
@@ -235,7 +277,22 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
   if (c0 < a.d_ff) {
     const T *__restrict__ wp = W + (size_t)k0 * a.d_ff + c0;
     int k = rg;
-#pragma unroll 4
+    if constexpr (VEC > 1) {
+      // whole batches of 8 rows: 8 loads in flight before the first use
+      for (; k + 7 * RG < kc; k += 8 * RG) {
+        u32x4 wq[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) wq[u] = load_raw<T>(wp + (size_t)(k + u * RG) * a.d_ff);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int t = 0; t < NT; ++t) {
+            const float hv = hs[t * a.KC + k + u * RG];
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(hv, unpack<T>(wq[u], v), acc[t][v]);
+          }
+      }
+    }
     for (; k < kc; k += RG) {
       float w[VEC];
       load_vec<T, VEC>(wp + (size_t)k * a.d_ff, w);
@@ -261,7 +318,7 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
       float s = 0.0f;
 #pragma unroll
       for (int r = 0; r < RG; ++r) s += red[(r * NT + t) * CB + c];
-      a.gpart[(((size_t)tile * a.KS + ks) * NT + t) * a.d_ff + col] = s;
+      store_coherent(a.gpart + (((size_t)tile * a.KS + ks) * NT + t) * a.d_ff + col, s);
     }
   }
 
@@ -274,8 +331,7 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
   if (tid < CB && col < a.d_ff) {
     for (int t = 0; t < nt; ++t) {
       const float *pp = a.gpart + ((size_t)tile * a.KS * NT + t) * a.d_ff + col;
-      float s = 0.0f;
-      for (int q = 0; q < a.KS; ++q) s += pp[(size_t)q * NT * a.d_ff];
+      const float s = sum_coherent(pp, (size_t)NT * a.d_ff, a.KS);
       const float g = silu(s);
       const bool keep = tbase[t] || (fabsf(g) >= thr);
       a.gval[((size_t)tile * NT + t) * a.d_ff + col] = g;
@@ -365,7 +421,28 @@ __global__ __launch_bounds__(kThreads) void up_kernel(UpArgs a) {
     float u[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) u[t] = 0.0f;
-    for (int k = lane * VEC; k < a.d; k += 64 * VEC) {
+    int k = lane * VEC;
+    if constexpr (VEC > 1) {
+      // 8 wavefront-wide loads of the row in flight at a time
+      for (; k + 7 * 64 * VEC < a.d; k += 8 * 64 * VEC) {
+        u32x4 wq[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) wq[q] = load_raw<T>(wr + k + q * 64 * VEC);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          if (t < nt && ((m >> t) & 1u)) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              float h[VEC];
+              load_vec_cached<T, VEC>(H + (size_t)t * a.d + k + q * 64 * VEC, h);
+#pragma unroll
+              for (int v = 0; v < VEC; ++v) u[t] = fmaf(h[v], unpack<T>(wq[q], v), u[t]);
+            }
+          }
+        }
+      }
+    }
+    for (; k < a.d; k += 64 * VEC) {
       float w[VEC];
       load_vec<T, VEC>(wr + k, w);
 #pragma unroll
@@ -434,8 +511,27 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownArgs a) {
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[t][v] = 0.0f;
   if (c0 < a.d) {
-#pragma unroll 4
-    for (int pos = p0 + rg; pos < p1; pos += RG) {
+    int pos = p0 + rg;
+    if constexpr (VEC > 1) {
+      // whole batches of 8 rows: row indices, then 8 row loads in flight
+      for (; pos + 7 * RG < p1; pos += 8 * RG) {
+        int jj[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) jj[u] = jl[pos + u * RG];
+        u32x4 wq[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) wq[u] = load_raw<T>(W + (size_t)jj[u] * a.d + c0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int t = 0; t < NT; ++t) {
+            const float pv = pb[(size_t)t * a.d_ff + pos + u * RG];
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(pv, unpack<T>(wq[u], v), acc[t][v]);
+          }
+      }
+    }
+    for (; pos < p1; pos += RG) {
       const int j = jl[pos];
       float w[VEC];
       load_vec<T, VEC>(W + (size_t)j * a.d + c0, w);
@@ -460,7 +556,7 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownArgs a) {
       float s = 0.0f;
 #pragma unroll
       for (int r = 0; r < RG; ++r) s += red[(r * NT + t) * SW + c];
-      a.dpart[(((size_t)tile * a.KCH + ch) * NT + t) * a.d + col] = s;
+      store_coherent(a.dpart + (((size_t)tile * a.KCH + ch) * NT + t) * a.d + col, s);
     }
   }
 
@@ -474,7 +570,7 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownArgs a) {
     float y = 0.0f;
     if (t < nt && col < a.d) {
       const float *pp = a.dpart + ((size_t)tile * a.KCH * NT + t) * a.d + col;
-      for (int q = 0; q < a.KCH; ++q) y += pp[(size_t)q * NT * a.d];
+      y = sum_coherent(pp, (size_t)NT * a.d, a.KCH);
       const size_t off = (size_t)(tok0 + t) * a.d + col;
       if (a.out) static_cast<T *>(a.out)[off] = Elem<T>::round(y);
       else a.ybuf[off] = y;

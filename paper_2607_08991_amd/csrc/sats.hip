@@ -15,6 +15,7 @@
 
 #include "../../include/sats.h"
 #include "kernels.hpp"
+#include "decode.hpp"
 
 namespace {
 
@@ -133,11 +134,19 @@ struct Buffers {
   int *blk_cnt, *blk_idx, *jlist, *ucount;
   uint32_t *blk_mask;
   uint8_t *keep;
+  float *ypart, *sspart;  // single-token path: per-workgroup partial y and sums of squares
+  int *kcount, *kidx;     // single-token path: kept columns of each strip
+  float *kg;
 };
 
 // Layout for passes of up to `pass` tokens (the counters live in their own
 // zero-initialised allocation).
-size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, int esz, Buffers *b) {
+struct DecodePlan {
+  int G = 0;  // co-resident workgroups of the single-token kernel (0: path not used)
+};
+
+size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, int esz, int64_t L,
+              const DecodePlan &dp, Buffers *b) {
   const int64_t Pp = ((pass + 3) / 4) * 4;  // tokens rounded up to whole tiles
   const int64_t tiles = Pp;                  // upper bound over tile sizes
   Carve c{base};
@@ -154,14 +163,34 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.jlist = c.take<int>(tiles * d_ff);
   t.ucount = c.take<int>(tiles);
   t.blk_mask = c.take<uint32_t>(tiles * d_ff);
-  t.keep = c.take<uint8_t>(Pp * d_ff);
+  t.keep = c.take<uint8_t>(std::max(Pp, L) * d_ff);
+  t.ypart = c.take<float>((int64_t)dp.G * d);
+  t.sspart = c.take<float>(dp.G);
+  t.kcount = c.take<int>(dp.G);
+  t.kidx = c.take<int>((int64_t)dp.G * sats::kStripMax);
+  t.kg = c.take<float>((int64_t)dp.G * sats::kStripMax);
   if (b) *b = t;
   return c.off;
 }
 
+// The counter allocation starts with control words (barrier count and
+// generation, device error flag); the per-block counters follow.  Every
+// counter is zero whenever no kernel is running.
+constexpr size_t kCtl = 512;
+constexpr size_t kBar = 0, kErr = 320;
+
 size_t counter_count(const Plan &p, int64_t pass) {
   const int64_t tiles = ((pass + 3) / 4) * 4;
-  return (size_t)(tiles * p.nblocks + tiles * p.n_slices);
+  return kCtl + (size_t)std::max<int64_t>(tiles * p.nblocks + tiles * p.n_slices, 2 * (int64_t)p.nblocks + 64);
+}
+
+// ------------------------------------------------------- single-token plan
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return cus;
 }
 
 struct Workspace {
@@ -201,6 +230,18 @@ int ensure_workspace(hipStream_t stream, size_t bytes, size_t n_counters, Worksp
   return SATS_OK;
 }
 
+// The single-token kernel holds h in LDS (d <= 4096), gives each workgroup a
+// strip of at most kStripMax columns and each reduction workgroup at most
+// one column per thread.
+bool decode_fits(int64_t d, int64_t d_ff, int esz, int G) {
+  const int64_t vec = 16 / esz, unit = 128 / esz;  // elements per 16-byte vector, per 128-byte unit
+  const int64_t units = (d_ff + unit - 1) / unit;
+  const int64_t per_wg = (G % 8 == 0) ? ((units + 7) / 8 + G / 8 - 1) / (G / 8) : (units + G - 1) / G;
+  (void)vec;
+  return G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD && per_wg * unit <= sats::kStripMax &&
+         (d + G - 1) / G <= sats::kDecodeThreads;
+}
+
 // --------------------------------------------------------------- the call
 
 struct Call {
@@ -219,14 +260,15 @@ struct Call {
   void *layer_in;
 };
 
+
 template <typename T, int VEC, int NT>
 int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters, int64_t base, int np) {
   using namespace sats;
   const int tiles = (np + NT - 1) / NT;
   const int64_t d = c.d, d_ff = c.d_ff;
   const size_t wl = (size_t)d * (size_t)d_ff;
-  unsigned *gcnt = counters;
-  unsigned *dcnt = counters + (size_t)tiles * p.nblocks;
+  unsigned *gcnt = counters + kCtl;
+  unsigned *dcnt = gcnt + (size_t)tiles * p.nblocks;
   const bool inspect_lists = c.active_count || c.active_idx;
 
   for (int64_t l = 0; l < c.L; ++l) {
@@ -323,6 +365,66 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
   return SATS_OK;
 }
 
+template <typename T>
+int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *counters) {
+  using namespace sats;
+  DecodeArgs a{};
+  a.x = c.x;
+  a.out = c.out;
+  a.Wg = c.Wg;
+  a.Wu = c.Wu;
+  a.Wd = c.Wd;
+  a.thr = c.thr;
+  a.ids = c.ids;
+  a.lut = c.lut;
+  a.route_mode = c.route_mode;
+  a.L = (int)c.L;
+  a.d = (int)c.d;
+  a.d_ff = (int)c.d_ff;
+  a.kcount = b.kcount;
+  a.kidx = b.kidx;
+  a.kg = b.kg;
+  a.ypart = b.ypart;
+  a.ybuf = b.ybuf;
+  a.sspart = b.sspart;
+  a.bar = counters + kBar;
+  a.err = counters + kErr;
+  a.route_out = c.route_out;
+  const bool lists = c.active_count || c.active_idx;
+  a.keep_out = lists ? b.keep : nullptr;
+  a.layer_in = c.layer_in;
+  void *args[] = {&a};
+  {
+    TimedLaunch tl(SATS_K_DECODE, c.stream);
+    // One workgroup per CU: every workgroup is resident when no other work
+    // shares the device.  A plain launch costs ~18 us less than a cooperative
+    // one, which guarantees residency (SATS_COOPERATIVE_LAUNCH=1 selects it);
+    // either way every wait is bounded and a failed one is reported by
+    // sats_device_status().
+    if (getenv("SATS_COOPERATIVE_LAUNCH")) {
+      HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void *>(&decode_kernel<T>), dim3(dp.G),
+                                         dim3(kDecodeThreads), args, 0, c.stream));
+    } else {
+      hipLaunchKernelGGL((decode_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream, a);
+      HIP_TRY(hipGetLastError());
+    }
+  }
+  if (lists) {
+    for (int64_t l = 0; l < c.L; ++l) {
+      CompactArgs ca{};
+      ca.keep = b.keep + l * c.d_ff;
+      ca.idx = c.active_idx ? c.active_idx + l * c.d_ff : nullptr;
+      ca.count = c.active_count ? c.active_count + l : nullptr;
+      ca.n = 1;
+      ca.d_ff = (int)c.d_ff;
+      TimedLaunch tl(SATS_K_INSPECT, c.stream);
+      hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(kThreads), 0, c.stream, ca);
+      HIP_TRY(hipGetLastError());
+    }
+  }
+  return SATS_OK;
+}
+
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 template <typename T>
@@ -349,12 +451,26 @@ int run(const Call &c) {
                       (!c.layer_in || aligned16(c.layer_in));
   const int pass = (int)std::min<int64_t>(c.n, kMaxPass);
   const Plan p = make_plan(c.d, c.d_ff, esz, vec_ok, pass);
-  const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, nullptr);
+  // single-token persistent path: one token, vector layout, h fits the LDS copy
+  bool decode = c.n == 1 && vec_ok && !getenv("SATS_NO_DECODE");
+  DecodePlan dp;
+  if (decode) {
+    int occ = 0;
+    HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, reinterpret_cast<const void *>(&sats::decode_kernel<T>),
+                                                         sats::kDecodeThreads, 0));
+    const int per_cu = std::min(occ, env_int("SATS_DECODE_WG_PER_CU", 1));
+    dp.G = device_cus() * per_cu;
+    decode = per_cu >= 1 && decode_fits(c.d, c.d_ff, esz, dp.G);
+    if (!decode) dp.G = 0;
+  }
+  const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, c.L, dp, nullptr);
   Workspace *ws = nullptr;
-  int rc = ensure_workspace(c.stream, bytes, counter_count(p, pass), &ws);
+  size_t ncount = counter_count(p, pass);
+  int rc = ensure_workspace(c.stream, bytes, ncount, &ws);
   if (rc) return rc;
   Buffers b{};
-  layout(ws->mem, p, pass, c.d, c.d_ff, esz, &b);
+  layout(ws->mem, p, pass, c.d, c.d_ff, esz, c.L, dp, &b);
+  if (decode) return run_decode<T>(c, dp, b, ws->counters);
 
   for (int64_t base = 0; base < c.n; base += kMaxPass) {
     const int np = (int)std::min<int64_t>(kMaxPass, c.n - base);
@@ -454,17 +570,22 @@ int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids, const
   return run<float>(c);
 }
 
-int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int elem_bytes, hipStream_t stream) {
+int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, int elem_bytes,
+                 hipStream_t stream) {
   g_err.clear();
   if (elem_bytes != 2 && elem_bytes != 4) return fail(SATS_ERR_ARG, "elem_bytes must be 2 or 4");
-  if (d < 1 || d_ff < 1 || max_tokens < 1 || d > (1 << 24) || d_ff > (1 << 24))
+  if (d < 1 || d_ff < 1 || max_tokens < 1 || n_layers < 1 || d > (1 << 24) || d_ff > (1 << 24))
     return fail(SATS_ERR_SHAPE, "bad shape for sats_reserve");
   const int pass = (int)std::min<int64_t>(max_tokens, kMaxPass);
   size_t bytes = 0, nc = 0;
+  int cus = device_cus();
+  if (cus < 1) return fail(SATS_ERR_HIP, "no device");
+  DecodePlan dp;
+  dp.G = cus * 2;
   for (int v = 0; v < 2; ++v)
     for (int np : {1, pass}) {
       const Plan p = make_plan(d, d_ff, elem_bytes, v == 1, np);
-      bytes = std::max(bytes, layout(nullptr, p, pass, d, d_ff, elem_bytes, nullptr));
+      bytes = std::max(bytes, layout(nullptr, p, pass, d, d_ff, elem_bytes, n_layers, dp, nullptr));
       nc = std::max(nc, counter_count(p, pass));
     }
   Workspace *ws = nullptr;
@@ -488,6 +609,24 @@ int sats_release(void) {
 }
 
 const char *sats_last_error(void) { return g_err.c_str(); }
+
+int sats_device_status(hipStream_t stream) {
+  g_err.clear();
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  HIP_TRY(hipStreamSynchronize(stream));
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  auto it = g_ws.find({dev, stream});
+  if (it == g_ws.end() || !it->second.counters) return SATS_OK;
+  unsigned flag = 0;
+  HIP_TRY(hipMemcpy(&flag, it->second.counters + kErr, sizeof flag, hipMemcpyDeviceToHost));
+  if (flag) {
+    const unsigned zero = 0;
+    HIP_TRY(hipMemcpy(it->second.counters + kErr, &zero, sizeof zero, hipMemcpyHostToDevice));
+    return fail(SATS_ERR_DEVICE, "a bounded device-side wait gave up (results of the affected call are invalid)");
+  }
+  return SATS_OK;
+}
 
 int sats_timing_begin(int kind, int capacity) {
   g_err.clear();
@@ -526,12 +665,22 @@ int sats_timing_end(int kind, double *total_ms, int64_t *count) {
   return SATS_OK;
 }
 
+#ifdef SATS_TRACE
+int sats_trace_read(unsigned long long *host, int64_t count) {
+  HIP_TRY(hipDeviceSynchronize());
+  HIP_TRY(hipMemcpyFromSymbol(host, HIP_SYMBOL(sats::sats_trace_buf),
+                              sizeof(unsigned long long) * (size_t)std::min<int64_t>(count, 4096 * 8)));
+  return SATS_OK;
+}
+#endif
+
 const char *sats_kernel_name(int kind) {
   switch (kind) {
     case SATS_K_GATE: return "gate_kernel";
     case SATS_K_UP: return "up_kernel";
     case SATS_K_DOWN: return "down_kernel";
     case SATS_K_INSPECT: return "compact_kernel";
+    case SATS_K_DECODE: return "decode_kernel";
     default: return "";
   }
 }

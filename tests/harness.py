@@ -83,6 +83,7 @@ def run_gpu(case, thresholds, lut, dtype, inspect=True, dense=False, out_is_x=Fa
         sats.sats_mlp_forward(dx, ids if lut is not None else None, wg, wu, wd, thr, dl, out,
                               n, d, d_ff, L)
     torch.cuda.synchronize()
+    sats.sats_device_status()
     res["out"] = from_dev(out)
     return res
 

@@ -86,4 +86,4 @@ def test_dense_needs_no_thresholds_but_checks_weights():
 
 
 def test_reserve_rejects_bad_element_size():
-    assert sats.load().sats_reserve(4, 8, 8, 3, None) == _lib.SATS_ERR_ARG
+    assert sats.load().sats_reserve(4, 8, 8, 1, 3, None) == _lib.SATS_ERR_ARG

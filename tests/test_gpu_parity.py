@@ -52,6 +52,12 @@ SMALL = [
     (6, 2, 25, 41, "f32", 2),        # odd sizes, fp32
     (7, 2, 128, 512, "f32", 67),     # more tokens than one pass (64)
     (8, 1, 4096, 1024, "bf16", 2),   # long rows: several row chunks in the gate split
+    # single tokens take the persistent one-launch path
+    (9, 3, 256, 1000, "bf16", 1),    # stack, ragged block
+    (10, 2, 4096, 1024, "bf16", 1),  # widest h the single-token path holds
+    (11, 2, 512, 1536, "f32", 1),    # fp32 stack
+    (12, 2, 24, 40, "bf16", 1),      # tiny: one gate tile, most workgroups idle
+    (13, 4, 64, 4096, "bf16", 1),    # many short rows
 ]
 
 
