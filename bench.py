@@ -50,7 +50,21 @@ def parse():
     p.add_argument("--cpu-sample", type=int, default=48, help="tokens the CPU oracle is timed on")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                   help="only run a plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
+
+
+def copy_probe(mib):
+    """A plain copy kernel of known size: HBM counters of it calibrate the counter scale."""
+    import torch
+    n = mib * 1024 * 1024 // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 5}))
 
 
 def thresholds_for(cfg):
@@ -86,6 +100,10 @@ def main():
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(sharding is described in DESIGN.md); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
 
     import torch
     import paper_2607_08991_amd as sats

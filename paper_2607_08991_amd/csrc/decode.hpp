@@ -191,7 +191,14 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(DecodeArgs a) {
   const int lc = LC > 0 ? tid % LC : 0, rg = LC > 0 ? tid / LC : THREADS;
 
   SATS_TRACE_POINT(0);
+  // gate rows of this thread: k = rg + RG * r, r < nrows, loaded GB at a time
+  // (GB 16-byte loads in flight per thread; a tail batch re-reads the last
+  // row and gives it weight 0)
+  constexpr int GB = 32;
+  const int nrows = (rg < RG) ? (d - rg + RG - 1) / RG : 0;
+  const int nb = (nrows + GB - 1) / GB;
   for (int l = 0; l < a.L; ++l) {
+    const T *__restrict__ Wg = static_cast<const T *>(a.Wg) + (size_t)l * wl + c0 + lc * VEC;
     // ------------------------------------------------ 1. layer input
     if (l == 0) {
       for (int k0 = tid * VEC; k0 < d; k0 += THREADS * VEC) {  // one 16-byte load per thread
@@ -229,29 +236,22 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(DecodeArgs a) {
 
     // ------------------------------------------------ 2. gate over the strip
     {
-      const T *__restrict__ Wg = static_cast<const T *>(a.Wg) + (size_t)l * wl + c0 + lc * VEC;
       float acc[VEC];
 #pragma unroll
       for (int v = 0; v < VEC; ++v) acc[v] = 0.0f;
-      if (rg < RG) {
-        // whole batches of 16 rows: 16 loads in flight before the first use
-        int k = rg;
-        for (; k + 15 * RG < d; k += 16 * RG) {
-          u32x4 wq[16];
+      if (rg < RG) {  // every row group writes its partial, zero when it has no rows
+        for (int b = 0; b < nb; ++b) {
+          u32x4 gbuf[GB];
 #pragma unroll
-          for (int u = 0; u < 16; ++u) wq[u] = load_raw<T>(Wg + (size_t)(k + u * RG) * d_ff);
+          for (int u = 0; u < GB; ++u)
+            gbuf[u] = load_raw<T>(Wg + (size_t)(rg + min(b * GB + u, nrows - 1) * RG) * d_ff);
 #pragma unroll
-          for (int u = 0; u < 16; ++u) {
-            const float hv = hs[k + u * RG];
+          for (int u = 0; u < GB; ++u) {
+            const int r = b * GB + u;
+            const float hv = (r < nrows) ? hs[rg + r * RG] : 0.0f;
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[v] = fmaf(hv, unpack<T>(wq[u], v), acc[v]);
+            for (int v = 0; v < VEC; ++v) acc[v] = fmaf(hv, unpack<T>(gbuf[u], v), acc[v]);
           }
-        }
-        for (; k < d; k += RG) {
-          const u32x4 wq = load_raw<T>(Wg + (size_t)k * d_ff);
-          const float hv = hs[k];
-#pragma unroll
-          for (int v = 0; v < VEC; ++v) acc[v] = fmaf(hv, unpack<T>(wq, v), acc[v]);
         }
 #pragma unroll
         for (int v = 0; v < VEC; ++v) red[rg * ncols + lc * VEC + v] = acc[v];
@@ -382,11 +382,12 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(DecodeArgs a) {
         }
         __syncthreads();
 
-        // down pass: this wavefront's column chunks of every row, 16 rows in flight
-        for (int i0 = 0; i0 < mn; i0 += 16) {
-          u32x4 wr[16][NCH];
+        // down pass: this wavefront's column chunks of every row, RD rows in flight
+        constexpr int RD = (sizeof(T) == 2) ? 32 : 16;
+        for (int i0 = 0; i0 < mn; i0 += RD) {
+          u32x4 wr[RD][NCH];
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
+          for (int r = 0; r < RD; ++r) {
             const int jr = __builtin_amdgcn_readfirstlane(mj[min(i0 + r, mn - 1)]);
             const T *__restrict__ dr = Wd + (size_t)jr * d;
 #pragma unroll
@@ -396,7 +397,7 @@ __global__ __launch_bounds__(kDecodeThreads) void decode_kernel(DecodeArgs a) {
             }
           }
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
+          for (int r = 0; r < RD; ++r) {
             const float pr = (i0 + r < mn) ? mp[i0 + r] : 0.0f;
 #pragma unroll
             for (int c = 0; c < NCH; ++c)

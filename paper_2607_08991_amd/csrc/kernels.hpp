@@ -204,6 +204,8 @@ struct GateArgs {
   int *blk_idx;          // [tiles][d_ff], block b's entries from b*CB
   uint32_t *blk_mask;    // [tiles][d_ff], bit t = token t keeps the column
   uint8_t *keep_out;     // optional, [tiles][NT][d_ff]
+  const uint8_t *skip;   // [n] 1: token done by the dense MFMA path (see dense.hpp)
+  const int *ctl;        // [0] tokens on that path
   int n, d, d_ff, KS, KC, nblocks;
 };
 
@@ -217,9 +219,11 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
   __shared__ int wcnt[kThreads / 64];
   __shared__ float tscale[NT];
   __shared__ int tbase[NT];
+  __shared__ int tskip[NT];
 
   const int tid = threadIdx.x;
   const int blk = blockIdx.x, ks = blockIdx.y, tile = blockIdx.z;
+  if (a.ctl[0] == a.n && a.skip[0]) return;  // every token is on the dense MFMA path
   const int tok0 = tile * NT;
   const int nt = min(NT, a.n - tok0);
   const int k0 = ks * a.KC;
@@ -242,6 +246,7 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
     }
     tscale[tid] = s;
     tbase[tid] = base;
+    tskip[tid] = (tid < nt) ? a.skip[tok0 + tid] : 1;
   }
   __syncthreads();
   float *hs = smem;  // [NT][KC]
@@ -259,7 +264,8 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
       v = Elem<T>::value(hv);
       if (blk == 0) {
         static_cast<T *>(a.hbuf)[off] = hv;
-        if (a.layer_in) static_cast<T *>(a.layer_in)[off] = hv;
+        // a token on the dense MFMA path has its layer inputs written there
+        if (a.layer_in && (a.x != nullptr || !tskip[t])) static_cast<T *>(a.layer_in)[off] = hv;
       }
     }
     hs[i] = v;
@@ -335,7 +341,7 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
       const float g = silu(s);
       const bool keep = tbase[t] || (fabsf(g) >= thr);
       a.gval[((size_t)tile * NT + t) * a.d_ff + col] = g;
-      mask |= (uint32_t)keep << t;
+      mask |= (uint32_t)(keep && !tskip[t]) << t;
       if (a.keep_out) a.keep_out[((size_t)tile * NT + t) * a.d_ff + col] = (uint8_t)keep;
     }
   }
@@ -371,6 +377,8 @@ struct UpArgs {
   float *pbuf;            // [tiles][NT][d_ff], by compacted position
   int *jlist;             // [tiles][d_ff], row index by compacted position
   int *ucount;            // [tiles]
+  const uint8_t *skip;
+  const int *ctl;
   int n, d, d_ff, nblocks, CB;
 };
 
@@ -379,6 +387,7 @@ __global__ __launch_bounds__(kThreads) void up_kernel(UpArgs a) {
   extern __shared__ int pref[];  // [nblocks + 1]
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int tile = blockIdx.y;
+  if (a.ctl[0] == a.n && a.skip[0]) return;  // every token is on the dense MFMA path
   const int tok0 = tile * NT;
   const int nt = min(NT, a.n - tok0);
   const int *cnt = a.blk_cnt + (size_t)tile * a.nblocks;
@@ -481,6 +490,8 @@ struct DownArgs {
   float *ybuf;            // [P][d]
   float *ss;              // [tiles][n_slices][NT]
   void *out;              // last layer: [n][d] (storage type); otherwise null
+  const uint8_t *skip;    // tokens whose output the dense MFMA path writes
+  const int *ctl;
   int n, d, d_ff, KCH, n_slices;
 };
 
@@ -494,6 +505,7 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownArgs a) {
 
   const int tid = threadIdx.x;
   const int slice = blockIdx.x, ch = blockIdx.y, tile = blockIdx.z;
+  if (a.ctl[0] == a.n && a.skip[0]) return;  // every token is on the dense MFMA path
   const int tok0 = tile * NT;
   const int nt = min(NT, a.n - tok0);
   const int U = a.ucount[tile];
@@ -572,8 +584,10 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownArgs a) {
       const float *pp = a.dpart + ((size_t)tile * a.KCH * NT + t) * a.d + col;
       y = sum_coherent(pp, (size_t)NT * a.d, a.KCH);
       const size_t off = (size_t)(tok0 + t) * a.d + col;
-      if (a.out) static_cast<T *>(a.out)[off] = Elem<T>::round(y);
-      else a.ybuf[off] = y;
+      if (!a.skip[tok0 + t]) {
+        if (a.out) static_cast<T *>(a.out)[off] = Elem<T>::round(y);
+        else a.ybuf[off] = y;
+      }
     }
     yv[o] = y;
   }
@@ -590,6 +604,7 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownArgs a) {
 // Ascending list of the kept columns of one token at one layer.
 struct CompactArgs {
   const uint8_t *keep;    // [tiles][NT][d_ff] == [P'][d_ff] with P' = tiles*NT
+  const uint8_t *skip;    // optional [n]: tokens of the dense MFMA path keep every column
   int32_t *idx;           // [n][d_ff] (this layer, offset by the pass)
   int32_t *count;         // [n]
   int n, d_ff;
@@ -601,11 +616,12 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const int tok = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const uint8_t *kp = a.keep + (size_t)tok * a.d_ff;
+  const bool all = a.skip && a.skip[tok];
   if (tid == 0) carry_s = 0;
   __syncthreads();
   for (int c0 = 0; c0 < a.d_ff; c0 += kThreads) {
     const int c = c0 + tid;
-    const bool on = c < a.d_ff && kp[c];
+    const bool on = c < a.d_ff && (all || kp[c]);
     const uint64_t bal = __ballot(on);
     const int rank = __popcll(bal & ((1ull << lane) - 1ull));
     if (lane == 0) wsum[wv] = __popcll(bal);

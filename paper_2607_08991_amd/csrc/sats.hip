@@ -16,6 +16,7 @@
 #include "../../include/sats.h"
 #include "kernels.hpp"
 #include "decode.hpp"
+#include "dense.hpp"
 
 namespace {
 
@@ -67,6 +68,7 @@ struct TimedLaunch {
 // --------------------------------------------------------------- planning
 
 constexpr int kMaxPass = 64;  // tokens per pass through the layers
+constexpr int kDenseKsplit = 4;  // d_ff chunks of the dense group's down-projection
 
 int round_pow2_down(int v) {
   int p = 1;
@@ -137,6 +139,10 @@ struct Buffers {
   float *ypart, *sspart;  // single-token path: per-workgroup partial y and sums of squares
   int *kcount, *kidx;     // single-token path: kept columns of each strip
   float *kg;
+  int *perm, *ctl;        // batched path: token partition and dense-group control words
+  uint8_t *skip;
+  uint16_t *xd, *hnext, *pdense;  // dense group (MFMA): inputs, next inputs, p
+  float *ddpart;                   // dense group down-projection partials
 };
 
 // Layout for passes of up to `pass` tokens (the counters live in their own
@@ -166,6 +172,13 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.keep = c.take<uint8_t>(std::max(Pp, L) * d_ff);
   t.ypart = c.take<float>((int64_t)dp.G * d);
   t.sspart = c.take<float>(dp.G);
+  t.perm = c.take<int>(Pp);
+  t.ctl = c.take<int>(64);
+  t.skip = c.take<uint8_t>(Pp);
+  t.xd = c.take<uint16_t>(Pp * d);
+  t.hnext = c.take<uint16_t>(Pp * d);
+  t.pdense = c.take<uint16_t>(Pp * d_ff);
+  t.ddpart = c.take<float>((int64_t)kDenseKsplit * Pp * d);
   t.kcount = c.take<int>(dp.G);
   t.kidx = c.take<int>((int64_t)dp.G * sats::kStripMax);
   t.kg = c.take<float>((int64_t)dp.G * sats::kStripMax);
@@ -271,7 +284,71 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
   unsigned *dcnt = gcnt + (size_t)tiles * p.nblocks;
   const bool inspect_lists = c.active_count || c.active_idx;
 
+  // routing for the pass: partition, dense-group size and whether MFMA takes it
+  const bool mfma = sizeof(T) == 2 && VEC > 1 && c.route_mode != ROUTE_SPARSE && np >= kMfmaMinTokens &&
+                    d % kDenseKT == 0 && d_ff % kDenseNT == 0 && d % kDenseNT == 0 && d <= 4096 &&
+                    !getenv("SATS_NO_MFMA");
+  {
+    RouteArgs ra{};
+    ra.ids = c.ids ? c.ids + base : nullptr;
+    ra.lut = c.lut;
+    ra.route_mode = c.route_mode;
+    ra.n = np;
+    ra.d = (int)d;
+    ra.x = static_cast<const uint16_t *>(c.x) + base * d;  // read only on the MFMA path (bf16)
+    ra.perm = b.perm;
+    ra.ctl = b.ctl;
+    ra.skip = b.skip;
+    ra.route_out = c.route_out ? c.route_out + base : nullptr;
+    ra.xd = b.xd;
+    ra.layer_in0 = c.layer_in ? static_cast<uint16_t *>(c.layer_in) + base * d : nullptr;
+    ra.mfma = mfma ? 1 : 0;
+    hipLaunchKernelGGL(route_kernel, dim3(1), dim3(kThreads), 0, c.stream, ra);
+    HIP_TRY(hipGetLastError());
+  }
+
   for (int64_t l = 0; l < c.L; ++l) {
+    if (mfma) {
+      // base-path group on MFMA (kernels return at once when the group is small)
+      DenseArgs da{};
+      da.ctl = b.ctl;
+      da.H = (l == 0) ? b.xd : b.hnext;
+      da.Wb = static_cast<const uint16_t *>(c.Wg) + l * wl;
+      da.Wt = static_cast<const uint16_t *>(c.Wu) + l * wl;
+      da.P = b.pdense;
+      da.K = (int)d;
+      da.N = (int)d_ff;
+      {
+        TimedLaunch tl(SATS_K_DENSE, c.stream);
+        hipLaunchKernelGGL(dense_gateup_kernel, dim3(d_ff / kDenseNT), dim3(kThreads), 0, c.stream, da);
+      }
+      HIP_TRY(hipGetLastError());
+      DenseArgs dd{};
+      dd.ctl = b.ctl;
+      dd.H = b.pdense;
+      dd.Wb = static_cast<const uint16_t *>(c.Wd) + l * wl;
+      dd.part = b.ddpart;
+      dd.K = (int)d_ff;
+      dd.N = (int)d;
+      dd.kchunk = (int)(((d_ff + kDenseKsplit - 1) / kDenseKsplit + kDenseKT - 1) / kDenseKT * kDenseKT);
+      {
+        TimedLaunch tl(SATS_K_DENSE, c.stream);
+        hipLaunchKernelGGL(dense_down_kernel, dim3(d / kDenseNT, kDenseKsplit), dim3(kThreads), 0, c.stream, dd);
+      }
+      HIP_TRY(hipGetLastError());
+      GlueArgs ga{};
+      ga.ctl = b.ctl;
+      ga.perm = b.perm;
+      ga.part = b.ddpart;
+      ga.ksplit = kDenseKsplit;
+      ga.d = (int)d;
+      ga.out = (l == c.L - 1) ? static_cast<uint16_t *>(c.out) + base * d : nullptr;
+      ga.hnext = b.hnext;
+      ga.layer_in = (c.layer_in && l + 1 < c.L) ? static_cast<uint16_t *>(c.layer_in) + ((l + 1) * c.n + base) * d
+                                                 : nullptr;
+      hipLaunchKernelGGL(dense_glue_kernel, dim3(np), dim3(kThreads), 0, c.stream, ga);
+      HIP_TRY(hipGetLastError());
+    }
     GateArgs g{};
     g.W = static_cast<const T *>(c.Wg) + l * wl;
     g.x = (l == 0) ? static_cast<const void *>(static_cast<const T *>(c.x) + base * d) : nullptr;
@@ -292,6 +369,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     g.blk_idx = b.blk_idx;
     g.blk_mask = b.blk_mask;
     g.keep_out = inspect_lists ? b.keep : nullptr;
+    g.skip = b.skip;
+    g.ctl = b.ctl;
     g.n = np;
     g.d = (int)d;
     g.d_ff = (int)d_ff;
@@ -309,6 +388,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     if (inspect_lists) {
       CompactArgs ca{};
       ca.keep = b.keep;
+      ca.skip = b.skip;
       ca.idx = c.active_idx ? c.active_idx + (l * c.n + base) * d_ff : nullptr;
       ca.count = c.active_count ? c.active_count + l * c.n + base : nullptr;
       ca.n = np;
@@ -328,6 +408,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     u.pbuf = b.pbuf;
     u.jlist = b.jlist;
     u.ucount = b.ucount;
+    u.skip = b.skip;
+    u.ctl = b.ctl;
     u.n = np;
     u.d = (int)d;
     u.d_ff = (int)d_ff;
@@ -350,6 +432,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     dn.ybuf = b.ybuf;
     dn.ss = b.ss;
     dn.out = (l == c.L - 1) ? static_cast<void *>(static_cast<T *>(c.out) + base * d) : nullptr;
+    dn.skip = b.skip;
+    dn.ctl = b.ctl;
     dn.n = np;
     dn.d = (int)d;
     dn.d_ff = (int)d_ff;
@@ -681,6 +765,7 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_DOWN: return "down_kernel";
     case SATS_K_INSPECT: return "compact_kernel";
     case SATS_K_DECODE: return "decode_kernel";
+    case SATS_K_DENSE: return "dense_mfma_kernels";
     default: return "";
   }
 }

@@ -197,3 +197,35 @@ def test_config_llama_layer_full_size():
         sp = 1 - res["count"].mean() / cfg.d_ff
         say(f"c2 n={n}: worst rel err {worst:.3g}, realized sparsity {sp:.4f}")
         assert 0.4 < sp < 0.6
+
+
+# ------------------------------------------------------------ dense group on MFMA
+
+@pytest.mark.parametrize("seed,L,n,n_dense_ids", [(31, 1, 20, 30), (32, 3, 40, 20), (33, 2, 64, 40)])
+def test_mfma_dense_group_matches_oracle(seed, L, n, n_dense_ids):
+    """Batches whose base-routed group has >= 8 tokens: that group runs on MFMA."""
+    c = synth.small_case(seed, L, 256, 1024, "bf16", n, vocab=40, n_dense_ids=n_dense_ids,
+                         w_std=1 / 16)
+    ts = case_thresholds(c, "bf16", seed=seed)
+    res = run_gpu(c, ts, c["route_lut"], "bf16")
+    assert res["route"].sum() >= 8
+    worst = check_against_oracle(c, ts, c["route_lut"], "bf16", res)
+    say(f"mfma seed={seed} L={L} n={n} dense={int(res['route'].sum())} worst {worst:.3g}")
+    # same tokens with the dense group on the compacted path instead
+    os.environ["SATS_NO_MFMA"] = "1"
+    try:
+        ref = run_gpu(c, ts, c["route_lut"], "bf16")
+    finally:
+        del os.environ["SATS_NO_MFMA"]
+    for i in range(n):
+        e = rel_err(numerics.decode(res["out"][i], "bf16"), numerics.decode(ref["out"][i], "bf16"))
+        assert e <= TOL["bf16"]
+        np.testing.assert_array_equal(res["count"][:, i], ref["count"][:, i])
+
+
+def test_mfma_dense_api_batch():
+    c = synth.small_case(34, 2, 256, 1024, "bf16", 24, w_std=1 / 16)
+    res = run_gpu(c, [0.3, 0.3], None, "bf16", dense=True)
+    ref = mlp.forward_dense(c["x"], c["W_gate"], c["W_up_T"], c["W_down"], "bf16")
+    for i in range(24):
+        assert rel_err(numerics.decode(res["out"][i], "bf16"), ref[i]) <= TOL["bf16"]

@@ -1,0 +1,107 @@
+"""GPU parity at the full 8B-model shapes: 32-layer Llama-3.1-8B and 36-layer
+Qwen3-8B MLP stacks, routed by token id, at the decode batch sizes of the
+workloads (1, 4, 16, 64).
+
+The whole call runs on the GPU in the launch configuration the library picks
+for that batch; the oracle then recomputes sampled layers from the GPU's own
+input of each layer (tests/harness.py), since a full float64 pass over 36
+layers per token would take minutes.  Thresholds are the oracle's CATS
+percentiles (tests/golden/thresholds.json).
+"""
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+from oracle import numerics
+from workloads import get_config, synth
+
+from harness import check_against_oracle, run_gpu
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "thresholds.json")
+_CACHE = {}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+
+
+def stack(cfg):
+    if cfg.name not in _CACHE:
+        _CACHE.clear()
+        t0 = time.time()
+        say(f"generating {cfg.name} weights ({cfg.n_layers} layers)")
+        _CACHE[cfg.name] = synth.stack_weights(cfg.seed, cfg.n_layers, cfg.d, cfg.d_ff, cfg.dtype)
+        say(f"  done in {time.time() - t0:.1f}s")
+    return _CACHE[cfg.name]
+
+
+def golden(cfg):
+    with open(GOLDEN) as f:
+        g = json.load(f)[cfg.name]
+    return np.asarray(g["thresholds"], np.float32)
+
+
+def run_config(key, n, layers, tokens, idx=0):
+    cfg = get_config(key)
+    wg, wu, wd = stack(cfg)
+    ts = golden(cfg)
+    lut = synth.config_lut(cfg)
+    c = dict(x=synth.decode_x(cfg, n, idx=idx), token_ids=synth.token_ids(cfg, n, idx=idx),
+             W_gate=wg, W_up_T=wu, W_down=wd)
+    t0 = time.time()
+    res = run_gpu(c, ts, lut, cfg.dtype)
+    say(f"{cfg.name} n={n}: GPU call {time.time() - t0:.1f}s; base-routed {int(res['route'].sum())}/{n}")
+    dec = {}
+
+    def weights(l):
+        if l not in dec:
+            dec.clear()
+            dec[l] = tuple(numerics.decode(w[l], cfg.dtype) for w in (wg, wu, wd))
+            say(f"  checking layer {l}")
+        return dec[l]
+
+    worst = check_against_oracle(c, ts, lut, cfg.dtype, res, layers=layers, tokens=tokens,
+                                 weights=weights)
+    kept = res["count"].astype(np.float64)
+    sparse_tok = res["route"] == 0
+    if sparse_tok.any():
+        sp = 1 - kept[:, sparse_tok].mean(axis=1) / cfg.d_ff
+        say(f"  realized sparsity of sparse-routed tokens: mean {sp.mean():.3f}, "
+            f"range [{sp.min():.3f}, {sp.max():.3f}]")
+    if (~sparse_tok).any():
+        assert np.all(kept[:, ~sparse_tok] == cfg.d_ff)
+    say(f"  worst relative error {worst:.3g}")
+    return res
+
+
+def test_llama_stack_batch1():
+    """32 layers, per-layer k ~ U[0.4, 0.7], 25 % base-routed ids, Zipf ids, batch 1."""
+    for idx in range(3):
+        run_config(2, 1, layers=[0, 1, 16, 31], tokens=[0], idx=idx)
+
+
+@pytest.mark.parametrize("n", [1, 4, 16])
+def test_qwen_stack_batches(n):
+    """36 layers, 70 % sparsity, 25 % base-routed ids, batches 1, 4, 16."""
+    run_config(3, n, layers=[0, 1, 18, 35], tokens=list(range(min(n, 4))), idx=n)
+
+
+def test_llama_stack_batch64():
+    """32 layers, 60 % sparsity, 40 % base-routed ids, one 64-token step."""
+    res = run_config(4, 64, layers=[0, 31], tokens=[0, 1, 2, 3, 62, 63], idx=64)
+    frac = res["route"].mean()
+    assert 0.1 < frac < 0.9
