@@ -50,6 +50,7 @@ def parse():
     p.add_argument("--cpu-sample", type=int, default=48, help="tokens the CPU oracle is timed on")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--batch", type=int, default=0, help="decode batch of a stack workload (default: its first)")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
@@ -94,6 +95,97 @@ def cpu_baseline(cfg, weights_np, ts, x_np, n_sample):
                       f"BLAS {blas}"}
 
 
+def bench_stack(args, cfg):
+    """A 32/36-layer workload: one step = one call on one decode batch through every layer."""
+    import torch
+    import paper_2607_08991_amd as sats
+    from workloads import synth
+
+    batch = args.batch or cfg.batches[0]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ts = thresholds_for(cfg)
+    d, d_ff, L, esz = cfg.d, cfg.d_ff, cfg.n_layers, cfg.elem_bytes
+    log(f"[bench] generating {cfg.name} weights ({L} layers)")
+    W = []
+    for w in synth.stack_weights(cfg.seed, L, d, d_ff, cfg.dtype):
+        W.append(torch.from_numpy(w.view(np.int16)).view(torch.bfloat16).to(dev))
+        del w
+    slots = max(1, args.tokens // batch)
+    X = torch.from_numpy(synth.decode_x(cfg, slots * batch, idx=batch).view(np.int16)).view(
+        torch.bfloat16).to(dev).view(slots, batch, d)
+    ids = torch.from_numpy(synth.token_ids(cfg, slots * batch, idx=batch)).to(dev).view(slots, batch)
+    lut = synth.config_lut(cfg)
+    dlut = torch.from_numpy(lut).to(dev)
+    thr = torch.from_numpy(ts).to(dev)
+    out = torch.empty((slots, batch, d), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+
+    # per slot: routes and the union of kept columns per layer (algorithmic bytes)
+    union = np.zeros((slots, L))
+    kept = []
+    routes = []
+    idx = torch.empty((L, batch, d_ff), dtype=torch.int32, device=dev)
+    cnt = torch.empty((L, batch), dtype=torch.int32, device=dev)
+    route = torch.empty(batch, dtype=torch.uint8, device=dev)
+    ar = torch.arange(d_ff, device=dev)
+    for s in range(slots):
+        sats.sats_mlp_forward_inspect(X[s], ids[s], *W, thr, dlut, out[s], batch, d, d_ff, L,
+                                      route_out=route, active_count=cnt, active_idx=idx)
+        valid = ar[None, None, :] < cnt[:, :, None].long()
+        m = torch.zeros((L, d_ff), dtype=torch.bool, device=dev)
+        for l in range(L):
+            m[l, idx[l][valid[l]].long()] = True
+        union[s] = m.sum(dim=1).cpu().numpy()
+        kept.append(cnt.cpu().numpy())
+        routes.append(route.cpu().numpy().copy())
+    torch.cuda.synchronize()
+    routes = np.array(routes)
+    kept = np.array(kept, dtype=np.float64)  # [slots][L][batch]
+
+    def step(s, dense=False):
+        k = s % slots
+        if dense:
+            sats.sats_mlp_dense(X[k], *W, out[k], batch, d, d_ff, L, stream)
+        else:
+            sats.sats_mlp_forward(X[k], ids[k], *W, thr, dlut, out[k], batch, d, d_ff, L, stream)
+
+    def timed(dense=False):
+        for s in range(args.warmup):
+            step(s, dense)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for s in range(args.steps):
+            step(args.warmup + s, dense)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    ms = timed()
+    dense_ms = None if args.no_dense else timed(True)
+    sl = (args.warmup + np.arange(args.steps)) % slots
+    alg = (L * d * d_ff * esz + 2 * d * esz * union[sl].sum(axis=1)).mean() + 2 * batch * d * esz
+    sparse_mask = routes[sl] == 0
+    sp = 1.0 - (kept[sl].transpose(0, 2, 1)[sparse_mask].mean() / d_ff) if sparse_mask.any() else None
+    res = {
+        "metric": METRIC, "value": round(batch * 1e3 / ms, 2), "unit": "tok/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "d": d, "d_ff": d_ff, "n_layers": L, "decode_batch": batch,
+                   "route": "route_lut", "base_routed_ids": cfg.n_dense_ids, "vocab": cfg.vocab},
+        "algorithmic_bytes_per_step": int(alg),
+        "hbm_gbps_algorithmic": round(alg / (ms * 1e-3) / 1e9, 1),
+        "hbm_frac_algorithmic": round(alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "realized_sparsity_sparse_tokens": None if sp is None else round(float(sp), 4),
+        "realized_base_routed_fraction": round(float(routes[sl].mean()), 4),
+        "dense_ms_per_step": None if dense_ms is None else round(dense_ms, 5),
+        "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 4),
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -110,9 +202,9 @@ def main():
     from workloads import get_config, synth
 
     sats.load()
-    cfg = get_config({"c1": 0, "c2": 1}.get(args.workload, args.workload))
+    cfg = get_config(args.workload)
     if cfg.n_layers != 1:
-        raise SystemExit("only the one-layer workloads are benchmarked by this script")
+        return bench_stack(args, cfg)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     ts = thresholds_for(cfg)

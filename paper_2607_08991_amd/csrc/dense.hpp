@@ -8,10 +8,14 @@
 //                by the kernels below and the compacted sparse path skips
 //                those tokens (flag per token); otherwise the sparse path
 //                also takes the base-path tokens, keeping every column.
-// dense_gateup   [n_dense x d] . W_gate and . W_up for 64 columns of d_ff per
+// dense_gateup   [rows x d] . W_gate and . W_up for 64 columns of d_ff per
 //                workgroup with v_mfma_f32_16x16x32_bf16; epilogue
-//                p = SiLU(a) * u (Eq. 1, 2), rounded to bf16 for the next
-//                product.
+//                p = SiLU(a) * u (Eq. 1, 2) where the row keeps the column
+//                (every column on the base path, |SiLU(a)| >= t otherwise,
+//                Eq. 4-5) and 0 where it does not, rounded to bf16 for the
+//                next product.  For batches the group can be the whole batch:
+//                once any token takes the base path every row of the weights
+//                is read anyway, so one MFMA stream serves every token.
 // dense_down     [n_dense x d_ff] . W_down, split over d_ff chunks (partials).
 // dense_glue     sums the partials in chunk order and writes the output row
 //                of each dense token (scattered back through perm) or the
@@ -48,7 +52,9 @@ struct RouteArgs {
   uint8_t *route_out;     // optional [n]
   uint16_t *xd;           // [n][d] packed inputs of the dense group
   uint16_t *layer_in0;    // optional: inspection copy of the call input, [n][d]
+  uint8_t *gbase;         // [n] base-path flag of each group row (group order)
   int mfma;               // the call may use the MFMA path
+  int whole;              // the MFMA group is the whole batch (keep rule applied per row)
 };
 
 __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
@@ -61,18 +67,22 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     const uint64_t bal = __ballot(valid && base);
     const int nd = __popcll(bal);
     const int rank_d = __popcll(bal & ((1ull << lane) - 1ull));
-    const int on = (a.mfma && nd >= kMfmaMinTokens) ? 1 : 0;
+    // group on MFMA: the base-path tokens once there are enough of them, or the
+    // whole batch (every row then applies its own keep rule)
+    const int ng = a.whole ? a.n : nd;
+    const int on = (a.mfma && ng >= kMfmaMinTokens) ? 1 : 0;
     if (valid) {
       const int pos = base ? rank_d : nd + (tid - rank_d);
       s_perm[pos] = tid;
       a.perm[pos] = tid;
-      a.skip[tid] = (uint8_t)(on && base);
+      a.gbase[pos] = (uint8_t)base;
+      a.skip[tid] = (uint8_t)(on && (base || a.whole));
       if (a.route_out) a.route_out[tid] = (uint8_t)base;
     }
     if (tid == 0) {
-      a.ctl[0] = nd;
+      a.ctl[0] = ng;
       a.ctl[1] = on;
-      s_nd = nd;
+      s_nd = ng;
       s_on = on;
     }
   }
@@ -89,7 +99,11 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
 }
 
 struct DenseArgs {
-  const int *ctl;         // [0] n_dense, [1] MFMA path on
+  const int *ctl;         // [0] rows of the MFMA group, [1] MFMA path on
+  const uint8_t *gbase;   // [rows] base-path flag per group row
+  const int *perm;        // group row -> token of the pass
+  const float *thr;       // threshold of this layer (gate/up)
+  uint8_t *keep_out;      // optional inspection: [n][N] keep flags, rows through perm
   const uint16_t *H;      // [n_dense][K] bf16 layer input (gate/up) or p (down)
   const uint16_t *Wb;     // W_gate [K][N] or W_down [K][N] (output dim contiguous)
   const uint16_t *Wt;     // W_up_T [N][K] (gate/up only)
@@ -157,12 +171,18 @@ __global__ __launch_bounds__(kThreads) void dense_gateup_kernel(DenseArgs a) {
       }
     }
   }
+  const float thr = a.thr ? *a.thr : 0.0f;
 #pragma unroll
   for (int mt = 0; mt < 4; ++mt) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = 16 * mt + 4 * g + r;
-      if (mt < mtiles && m < nd) a.P[(size_t)m * a.N + ncol] = f32_to_bf16(silu(accg[mt][r]) * accu[mt][r]);
+      if (mt < mtiles && m < nd) {
+        const float gv = silu(accg[mt][r]);
+        const bool keep = a.gbase[m] || fabsf(gv) >= thr;  // Eq. 4-5; every column on the base path
+        a.P[(size_t)m * a.N + ncol] = keep ? f32_to_bf16(gv * accu[mt][r]) : (uint16_t)0;
+        if (a.keep_out) a.keep_out[(size_t)a.perm[m] * a.N + ncol] = (uint8_t)keep;
+      }
     }
   }
 }

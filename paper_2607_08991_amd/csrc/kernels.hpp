@@ -342,7 +342,7 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
       const bool keep = tbase[t] || (fabsf(g) >= thr);
       a.gval[((size_t)tile * NT + t) * a.d_ff + col] = g;
       mask |= (uint32_t)(keep && !tskip[t]) << t;
-      if (a.keep_out) a.keep_out[((size_t)tile * NT + t) * a.d_ff + col] = (uint8_t)keep;
+      if (a.keep_out && !tskip[t]) a.keep_out[((size_t)tile * NT + t) * a.d_ff + col] = (uint8_t)keep;
     }
   }
   const bool act = mask != 0;
@@ -604,7 +604,7 @@ __global__ __launch_bounds__(kThreads) void down_kernel(DownArgs a) {
 // Ascending list of the kept columns of one token at one layer.
 struct CompactArgs {
   const uint8_t *keep;    // [tiles][NT][d_ff] == [P'][d_ff] with P' = tiles*NT
-  const uint8_t *skip;    // optional [n]: tokens of the dense MFMA path keep every column
+  const uint8_t *skip;    // unused (the MFMA path writes its own keep flags)
   int32_t *idx;           // [n][d_ff] (this layer, offset by the pass)
   int32_t *count;         // [n]
   int n, d_ff;
@@ -616,12 +616,11 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(CompactArgs a) {
   const int tok = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const uint8_t *kp = a.keep + (size_t)tok * a.d_ff;
-  const bool all = a.skip && a.skip[tok];
   if (tid == 0) carry_s = 0;
   __syncthreads();
   for (int c0 = 0; c0 < a.d_ff; c0 += kThreads) {
     const int c = c0 + tid;
-    const bool on = c < a.d_ff && (all || kp[c]);
+    const bool on = c < a.d_ff && kp[c];
     const uint64_t bal = __ballot(on);
     const int rank = __popcll(bal & ((1ull << lane) - 1ull));
     if (lane == 0) wsum[wv] = __popcll(bal);

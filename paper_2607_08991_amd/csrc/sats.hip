@@ -140,7 +140,7 @@ struct Buffers {
   int *kcount, *kidx;     // single-token path: kept columns of each strip
   float *kg;
   int *perm, *ctl;        // batched path: token partition and dense-group control words
-  uint8_t *skip;
+  uint8_t *skip, *gbase;
   uint16_t *xd, *hnext, *pdense;  // dense group (MFMA): inputs, next inputs, p
   float *ddpart;                   // dense group down-projection partials
 };
@@ -175,6 +175,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.perm = c.take<int>(Pp);
   t.ctl = c.take<int>(64);
   t.skip = c.take<uint8_t>(Pp);
+  t.gbase = c.take<uint8_t>(Pp);
   t.xd = c.take<uint16_t>(Pp * d);
   t.hnext = c.take<uint16_t>(Pp * d);
   t.pdense = c.take<uint16_t>(Pp * d_ff);
@@ -285,7 +286,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
   const bool inspect_lists = c.active_count || c.active_idx;
 
   // routing for the pass: partition, dense-group size and whether MFMA takes it
-  const bool mfma = sizeof(T) == 2 && VEC > 1 && c.route_mode != ROUTE_SPARSE && np >= kMfmaMinTokens &&
+  const bool mfma = sizeof(T) == 2 && VEC > 1 && np >= kMfmaMinTokens &&
                     d % kDenseKT == 0 && d_ff % kDenseNT == 0 && d % kDenseNT == 0 && d <= 4096 &&
                     !getenv("SATS_NO_MFMA");
   {
@@ -302,7 +303,9 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     ra.route_out = c.route_out ? c.route_out + base : nullptr;
     ra.xd = b.xd;
     ra.layer_in0 = c.layer_in ? static_cast<uint16_t *>(c.layer_in) + base * d : nullptr;
+    ra.gbase = b.gbase;
     ra.mfma = mfma ? 1 : 0;
+    ra.whole = getenv("SATS_MFMA_BASE_GROUP_ONLY") ? 0 : 1;
     hipLaunchKernelGGL(route_kernel, dim3(1), dim3(kThreads), 0, c.stream, ra);
     HIP_TRY(hipGetLastError());
   }
@@ -312,6 +315,10 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       // base-path group on MFMA (kernels return at once when the group is small)
       DenseArgs da{};
       da.ctl = b.ctl;
+      da.gbase = b.gbase;
+      da.perm = b.perm;
+      da.thr = c.thr ? c.thr + l : nullptr;
+      da.keep_out = inspect_lists ? b.keep : nullptr;
       da.H = (l == 0) ? b.xd : b.hnext;
       da.Wb = static_cast<const uint16_t *>(c.Wg) + l * wl;
       da.Wt = static_cast<const uint16_t *>(c.Wu) + l * wl;

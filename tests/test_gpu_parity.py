@@ -147,16 +147,31 @@ def test_zero_tokens_leaves_output_untouched():
 
 
 def test_batch_rows_match_single_token_calls():
+    """Row independence: a batched call's row equals the single-token call on it.
+
+    The two calls take different kernels (batch: MFMA or compacted GEMV; one
+    token: the persistent kernel), so sums differ in order.  At layer 0 both
+    see the same input, so keep sets must agree outside the 1e-3 band around
+    the threshold; later layers see inputs that differ by rounding, so each
+    run is checked against the oracle on its own inputs; outputs agree within
+    the bf16 tolerance.
+    """
+    from harness import band_mask
     c = synth.small_case(26, 2, 256, 768, "bf16", 9, vocab=40, n_dense_ids=12, w_std=1 / 16)
     ts = case_thresholds(c, "bf16")
     full = run_gpu(c, ts, c["route_lut"], "bf16")
+    check_against_oracle(c, ts, c["route_lut"], "bf16", full)
+    wg0 = numerics.decode(c["W_gate"][0], "bf16")
     for i in range(9):
         one = dict(c, x=c["x"][i:i + 1], token_ids=c["token_ids"][i:i + 1])
         r1 = run_gpu(one, ts, c["route_lut"], "bf16")
-        for l in range(2):
-            k = r1["count"][l][0]
-            np.testing.assert_array_equal(r1["count"][l][0], full["count"][l][i])
-            np.testing.assert_array_equal(r1["idx"][l][0][:k], full["idx"][l][i][:k])
+        check_against_oracle(one, ts, c["route_lut"], "bf16", r1)
+        a1 = np.zeros(768, bool)
+        a1[r1["idx"][0][0][:r1["count"][0][0]]] = True
+        af = np.zeros(768, bool)
+        af[full["idx"][0][i][:full["count"][0][i]]] = True
+        g = mlp.silu(numerics.decode(c["x"][i], "bf16") @ wg0)
+        assert not ((a1 != af) & ~band_mask(g, float(np.float32(ts[0])))).any()
         e = rel_err(numerics.decode(full["out"][i], "bf16"), numerics.decode(r1["out"][0], "bf16"))
         assert e <= TOL["bf16"]
 
@@ -203,7 +218,12 @@ def test_config_llama_layer_full_size():
 
 @pytest.mark.parametrize("seed,L,n,n_dense_ids", [(31, 1, 20, 30), (32, 3, 40, 20), (33, 2, 64, 40)])
 def test_mfma_dense_group_matches_oracle(seed, L, n, n_dense_ids):
-    """Batches whose base-routed group has >= 8 tokens: that group runs on MFMA."""
+    """Batches of >= 8 tokens run on MFMA (whole batch, per-row keep rule); the
+    variant with only the base-path group on MFMA and the one without MFMA are
+    checked too.  Across several layers the variants may differ by more than
+    the tolerance (a column within rounding of the threshold flips and the
+    difference propagates), so each is checked against the oracle on its own
+    layer inputs."""
     c = synth.small_case(seed, L, 256, 1024, "bf16", n, vocab=40, n_dense_ids=n_dense_ids,
                          w_std=1 / 16)
     ts = case_thresholds(c, "bf16", seed=seed)
@@ -211,16 +231,29 @@ def test_mfma_dense_group_matches_oracle(seed, L, n, n_dense_ids):
     assert res["route"].sum() >= 8
     worst = check_against_oracle(c, ts, c["route_lut"], "bf16", res)
     say(f"mfma seed={seed} L={L} n={n} dense={int(res['route'].sum())} worst {worst:.3g}")
-    # same tokens with the dense group on the compacted path instead
-    os.environ["SATS_NO_MFMA"] = "1"
-    try:
-        ref = run_gpu(c, ts, c["route_lut"], "bf16")
-    finally:
-        del os.environ["SATS_NO_MFMA"]
-    for i in range(n):
-        e = rel_err(numerics.decode(res["out"][i], "bf16"), numerics.decode(ref["out"][i], "bf16"))
-        assert e <= TOL["bf16"]
-        np.testing.assert_array_equal(res["count"][:, i], ref["count"][:, i])
+    # the same tokens with only the base-path group on MFMA, and with no MFMA
+    for env in ("SATS_MFMA_BASE_GROUP_ONLY", "SATS_NO_MFMA"):
+        os.environ[env] = "1"
+        try:
+            ref = run_gpu(c, ts, c["route_lut"], "bf16")
+        finally:
+            del os.environ[env]
+        check_against_oracle(c, ts, c["route_lut"], "bf16", ref)
+        if L == 1:  # one layer: same input, so the outputs themselves must agree
+            for i in range(n):
+                e = rel_err(numerics.decode(res["out"][i], "bf16"),
+                            numerics.decode(ref["out"][i], "bf16"))
+                assert e <= TOL["bf16"]
+
+
+def test_mfma_whole_batch_without_route_table():
+    """A batch of sparse-path tokens only (no table) also runs on MFMA with per-row masks."""
+    c = synth.small_case(35, 2, 256, 1024, "bf16", 16, w_std=1 / 16)
+    ts = case_thresholds(c, "bf16", seed=35)
+    res = run_gpu(c, ts, None, "bf16")
+    check_against_oracle(c, ts, None, "bf16", res)
+    kept = res["count"].mean() / 1024
+    assert 0.3 < kept < 0.7
 
 
 def test_mfma_dense_api_batch():
