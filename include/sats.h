@@ -143,11 +143,11 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
                  int elem_bytes, hipStream_t stream);
 
 /*
- * Synchronise `stream` and report whether any kernel of this library on it
- * gave up a bounded device-side wait since the last check (SATS_ERR_DEVICE;
- * the flag is cleared).  Such a wait only gives up when workgroups of one
- * launch could not all run at once, which the cooperative launch rules out;
- * the bound exists so that a kernel always terminates.
+ * Synchronise `stream` and report whether a kernel of this library on it
+ * raised the device error flag since the last check (SATS_ERR_DEVICE; the
+ * flag is cleared).  No kernel of this version waits on another workgroup,
+ * so the flag is only a guard for future ones; the call still surfaces
+ * asynchronous HIP errors of the stream.
  */
 int sats_device_status(hipStream_t stream);
 
@@ -165,7 +165,7 @@ const char *sats_last_error(void);
  * returns the summed duration and the number of launches timed, and disarms.
  */
 enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_DECODE = 4,
-       SATS_K_DENSE = 5, SATS_K_COUNT = 6 };
+       SATS_K_DENSE = 5, SATS_K_DEC_GATE = 6, SATS_K_DEC_ROWS = 7, SATS_K_DEC_REDUCE = 8, SATS_K_COUNT = 9 };
 int sats_timing_begin(int kind, int capacity);
 int sats_timing_end(int kind, double *total_ms, int64_t *count);
 const char *sats_kernel_name(int kind);

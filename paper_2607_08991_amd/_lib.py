@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_PKG, "libsats.so")
 SATS_OK, SATS_ERR_NULL, SATS_ERR_SHAPE, SATS_ERR_HIP, SATS_ERR_WORKSPACE, SATS_ERR_ARG = 0, -1, -2, -3, -4, -5
 SATS_ERR_DEVICE = -6
 SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DECODE, SATS_K_DENSE = 0, 1, 2, 3, 4, 5
+SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_DEC_REDUCE = 6, 7, 8
 
 # exported symbols and their argument types (p = pointer, i = int64, s = stream, n = int32)
 _P, _I, _S, _N = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
@@ -57,6 +58,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run `python -m paper_2607_08991_amd.build` "
                           "(the HIP library is required: there is no other implementation)")
+    # Load torch's HIP runtime first so that the library binds to the same one;
+    # a second copy of the runtime in the process would not see the device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover - the library also works without torch
+        pass
     lib = ctypes.CDLL(path)
     for name, (args, res) in SIGNATURES.items():
         fn = getattr(lib, name)

@@ -1,28 +1,28 @@
-// Persistent single-token kernel: every layer of one call in one cooperative
-// launch (decode batch 1).
+// Single-token (decode batch 1) path: three plain launches per layer.
 //
-// Each of the G co-resident workgroups owns a contiguous strip of the d_ff
-// columns made of whole 128-byte row segments (neighbouring strips sit on the
-// same XCD).
-// Per layer:
-//   1. layer input h in LDS: the call input for layer 0, otherwise
-//      rho(y / sqrt(mean(y^2) + 1e-6)) from the previous layer's y;
-//   2. gate: a = h . W_gate for the strip's columns over all d rows (no
-//      cross-workgroup partials), SiLU (Eq. 2), the keep rule (Eq. 4-5, or
-//      every column on the base path, Eq. 13), ballot compaction of the kept
-//      columns, published with their g values;
-//   3. grid barrier; the kept rows of all strips are split evenly over the
-//      workgroups (a prefix over the published counts); the workgroup forms
-//      u_j = W_up_T[j].h and p_j = g_j u_j (Eq. 1) for its rows, then
-//      accumulates p_j W_down[j] over them, each wavefront owning a slice of
-//      the columns, and writes one partial y;
-//   4. grid barrier; workgroup w sums every partial for its own slice of
-//      columns in workgroup order, giving y (or the rounded output on the last
-//      layer) and the slice's sum of squares;
-//   5. grid barrier before the next layer.
-// The assignment of work depends only on the data, never on timing, so every
-// sum has a fixed order and results are bitwise reproducible.  Waits are
-// grid barriers of a cooperative launch, bounded so that a launch always ends.
+//   gate    W_gate is cut into tiles one 16-byte load per lane wide (64 lanes:
+//           512 bf16 or 256 fp32 columns, 1 KB of each row) by a chunk of
+//           rows.  A workgroup forms h . tile for its tile, sums its
+//           wavefronts' partials in LDS and writes one partial a per column
+//           and row chunk.
+//   rows    Work units are (column block, share): every workgroup of a
+//           column block adds the block's row-chunk partials in chunk order,
+//           applies SiLU (Eq. 2) and the keep rule (Eq. 4-5, or every column
+//           on the base path, Eq. 13) and compacts the kept columns in LDS;
+//           all of them get the same list, and each takes an even share of
+//           it: u_j = W_up_T[j] . h, p_j = g_j u_j (Eq. 1) and
+//           p_j W_down[j] accumulated into the workgroup's partial y, the
+//           rows of both projections read in the same batches.
+//   reduce  Workgroup w adds every partial for its own slice of columns in
+//           workgroup order: y, or the rounded output on the last layer, and
+//           the slice's sum of squares for the next layer's input
+//           rho(y / sqrt(mean(y^2) + 1e-6)).
+//
+// Workgroups have 1024 threads (16 wavefronts per CU keep more row reads in
+// flight than 8).  Partials cross workgroups through device-coherent stores
+// and loads; kernel boundaries order the phases.  The assignment of work
+// depends only on the data, never on timing, so every sum has a fixed order
+// and results are reproducible bit for bit.
 #pragma once
 
 #include "kernels.hpp"
@@ -43,11 +43,18 @@ __device__ unsigned long long sats_trace_buf[4096 * 8];
   } while (0)
 #endif
 
-constexpr int kDecodeThreads = 512;
-constexpr int kDecodeMaxD = 4096;        // h lives in LDS
-constexpr int kStripMax = 256;           // columns one workgroup may own
-constexpr int kDecodeMaxG = 1024;        // workgroups of one launch
-constexpr unsigned kSpinLimit = 1u << 20;  // about a second of polling
+constexpr int kDecodeThreads = 1024;  // rows and reduce launches
+constexpr int kDecodeWaves = kDecodeThreads / 64;
+#ifndef SATS_GATE_THREADS
+#define SATS_GATE_THREADS 1024
+#endif
+constexpr int kGateThreads = SATS_GATE_THREADS;  // gate launch
+constexpr int kGateBatch = kGateThreads >= 1024 ? 8 : 16;  // 16-byte loads in flight per lane
+constexpr int kDecodeMaxD = 4096;  // h lives in LDS
+constexpr int kDecodeMaxG = 1024;  // rows / reduce workgroups (partials of y)
+
+// Columns of one gate column block (one 16-byte load per lane of a wavefront).
+template <typename T> constexpr int dec_block_cols() { return 64 * Elem<T>::kVec; }
 
 struct DecodeArgs {
   const void *x;          // [d] call input (storage type)
@@ -58,402 +65,492 @@ struct DecodeArgs {
   const uint8_t *lut;
   int route_mode;
   int L, d, d_ff;
-  int *kcount;            // [G]             kept columns of each strip
-  int *kidx;              // [G][kStripMax]  the kept columns
-  float *kg;              // [G][kStripMax]  their SiLU values
-  float *ypart;           // [G][d]          per-workgroup partial y
+  int nblk, nrc;          // gate tiles: column blocks x row chunks
+  float *gpart;           // [nrc][d_ff]    partial a of each row chunk
+  float *ypart;           // [G][d]         per-workgroup partial y
   float *ybuf;            // [d]
   float *sspart;          // [G]
-  unsigned *bar;          // [2] barrier count, generation
-  unsigned *err;          // [1] set when a bounded wait gives up
+  int *state;             // [1] the token's route (1: base path), set by the layer-0 gate launch
   uint8_t *route_out;     // optional [1]
   uint8_t *keep_out;      // optional [L][d_ff]
   void *layer_in;         // optional [L][d]
 };
 
-__device__ __forceinline__ void store_coherent_i(int *p, int v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ int load_coherent_i(const int *p) {
-  return __hip_atomic_load(const_cast<int *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+struct DecodeSmem {
+  float hs[kDecodeMaxD];                // layer input
+  float red[2 * kDecodeMaxD];           // gate: wavefront partials; rows: parts of u, half sums
+  int mj[kDecodeThreads / 2];           // kept columns of the current column block ...
+  float mg[kDecodeThreads / 2];         // ... and their g values
+  int wcnt[kDecodeWaves];
+  float scal[kDecodeWaves];
+};
 
-// Four consecutive floats (16-byte aligned) written through to the
-// device-coherent level in one 16-byte store.
-__device__ __forceinline__ void store_coherent4(float *p, float x0, float x1, float x2, float x3) {
+// Four consecutive floats at byte offset voff of buffer r, written through to
+// the device-coherent level in one 16-byte store.  (A compiler builtin, not
+// inline assembly: the compiler's hazard checks do not see a store written as
+// assembly, and a following write to its data registers can then corrupt the
+// stored values.)
+__device__ __forceinline__ void store_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t voff, float x0, float x1, float x2,
+                                                float x3) {
   const f32x4 v = {x0, x1, x2, x3};
-  asm volatile("global_store_dwordx4 %0, %1, off sc1" : : "v"(p), "v"(v) : "memory");
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, 0, 16 /* write through */);
 }
 
-// True once a bounded wait of this launch has given up: later waits return at
-// once, so a failed launch still ends quickly.
-__device__ __forceinline__ bool wait_failed(unsigned *err) {
-  return __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+// Weight reads (and the partial-y writes) go through buffer descriptors: the matrix base lives in
+// scalar registers, the row offset in a scalar register and only the lane's
+// byte offset in a vector register, so a batch of loads needs no 64-bit
+// address per load.  Reads at or past `bytes` return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t weight_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+// 16 bytes at base + soff + voff, not kept in the caches (streamed once).
+__device__ __forceinline__ u32x4 load_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 2);
 }
 
-// Barrier over all G workgroups (co-resident by the cooperative launch).
-// Device-coherent stores issued before it are visible to device-coherent
-// loads after it.  Two levels keep atomic contention low: workgroups count in
-// at one counter per XCD (workgroup w runs on XCD w % 8), the last of each
-// XCD counts in globally, and the last of those bumps the generation that
-// every workgroup polls.  Counters sit 128 bytes apart.
-constexpr int kBarGen = 1, kBarGroup = 32;  // word offsets: [0] global count, [1] generation
-
-__device__ __forceinline__ bool spin_until_changed(unsigned *word, unsigned old, unsigned *err) {
-  unsigned spins = 0;
-  while (__hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == old) {
-    __builtin_amdgcn_s_sleep(1);
-    if ((++spins & 255u) == 0u && (spins > kSpinLimit || wait_failed(err))) {
-      __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return false;
+// Sums of R values over the 64 lanes of a wavefront (R a power of two),
+// by halving exchanges: at the step with lane mask m each lane keeps half of
+// its values and adds its partner's matching half, then the last values are
+// added across the remaining lanes.  Lanes r * (64 / R) ... (r + 1) * (64 / R)
+// - 1 return the sum of value r.  17 exchanges for R = 16 instead of 96.
+template <int R>
+__device__ __forceinline__ float rows_sum(float (&v)[R], int lane) {
+  static_assert(R >= 1 && R <= 64 && (R & (R - 1)) == 0, "R must be a power of two");
+#pragma unroll
+  for (int m = 32, h = R / 2; h >= 1; m >>= 1, h >>= 1) {
+    const bool hi = (lane & m) != 0;
+#pragma unroll
+    for (int i = 0; i < h; ++i) {
+      const float send = hi ? v[i] : v[i + h];
+      const float keep = hi ? v[i + h] : v[i];
+      v[i] = keep + __shfl_xor(send, m, 64);
     }
   }
-  return true;
+  float s = v[0];
+#pragma unroll
+  for (int m = 32 / R; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
+  return s;
 }
 
-__device__ __forceinline__ void grid_barrier(unsigned *bar, unsigned G, unsigned *err) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const unsigned gen = __hip_atomic_load(bar + kBarGen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __builtin_amdgcn_s_waitcnt(0);
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    const unsigned ngroups = G < 8u ? G : 8u;
-    const unsigned grp = blockIdx.x % 8u;
-    const unsigned gsize = (G - grp + 7u) / 8u;
-    unsigned *gc = bar + kBarGroup * (1u + grp);
-    bool last = false;
-    if (__hip_atomic_fetch_add(gc, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gsize - 1u) {
-      __hip_atomic_store(gc, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __builtin_amdgcn_s_waitcnt(0);
-      __atomic_signal_fence(__ATOMIC_SEQ_CST);
-      if (__hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ngroups - 1u) {
-        __hip_atomic_store(bar, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __builtin_amdgcn_s_waitcnt(0);
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        __hip_atomic_fetch_add(bar + kBarGen, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        last = true;
-      }
+// ------------------------------------------------------------------ layer input
+
+// Layer input h, in two steps so that its loads overlap others: issue()
+// starts the loads of the call input (layer 0) or of the previous layer's y
+// and the G slice sums of squares; finish() forms
+// h = rho(y / sqrt(mean(y^2) + 1e-6)) into LDS (and the inspection copy when
+// `record`).
+template <int THREADS>
+struct InputRegs {
+  u32x4 xv[kDecodeMaxD / (4 * THREADS)];  // layer 0: x, 16 bytes at a time (d <= 4096)
+  float yv[kDecodeMaxD / THREADS];
+  float ss[kDecodeMaxG / THREADS];
+};
+
+template <typename T, int THREADS>
+__device__ __forceinline__ void dec_input_issue(const DecodeArgs &a, int l, int G, InputRegs<THREADS> &r) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int tid = threadIdx.x, d = a.d;
+  // every field gets a value on both branches: finish() passes all of them
+  // through register constraints
+#pragma unroll
+  for (int i = 0; i < kDecodeMaxD / (4 * THREADS); ++i) r.xv[i] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < kDecodeMaxD / THREADS; ++i) r.yv[i] = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kDecodeMaxG / THREADS; ++i) r.ss[i] = 0.0f;
+  if (l == 0) {
+#pragma unroll
+    for (int i = 0; i < kDecodeMaxD / (4 * THREADS); ++i) {
+      const int k0 = (i * THREADS + tid) * VEC;
+      r.xv[i] = (k0 < d) ? *reinterpret_cast<const u32x4 *>(static_cast<const T *>(a.x) + k0)
+                         : u32x4{0u, 0u, 0u, 0u};
     }
-    if (!last) spin_until_changed(bar + kBarGen, gen, err);
-  }
-  __syncthreads();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
-template <typename T>
-__global__ __launch_bounds__(kDecodeThreads) void decode_kernel(DecodeArgs a) {
-  constexpr int THREADS = kDecodeThreads;
-  constexpr int VEC = Elem<T>::kVec;      // elements per 16-byte load
-  constexpr int NW = THREADS / 64;        // wavefronts per workgroup
-  constexpr int CH = 64 * VEC;            // elements per wavefront-wide 16-byte load
-  constexpr int DMAX = kDecodeMaxD / CH;  // wavefront loads per row
-
-  __shared__ float hs[kDecodeMaxD];       // layer input
-  __shared__ float red[kDecodeMaxD];      // gate reduction / workgroup partial y
-  __shared__ int pref[kDecodeMaxG + 1];   // prefix of the strips' kept counts
-  __shared__ int mj[THREADS];             // this workgroup's kept rows ...
-  __shared__ float mg[THREADS];           // ... their g values ...
-  __shared__ float mp[THREADS];           // ... and p_j = g_j u_j
-  __shared__ int wcnt[NW];
-  __shared__ float scal[NW];
-
-  const int G = gridDim.x, w = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int d = a.d, d_ff = a.d_ff;
-  const size_t wl = (size_t)d * d_ff;
-  const int base = token_is_base(a.route_mode, a.ids, a.lut, 0);
-  if (a.route_out && w == 0 && tid == 0) a.route_out[0] = (uint8_t)base;
-
-  // this workgroup's strip of columns: whole 128-byte units (one cache line
-  // of a W_gate row), split as evenly as possible over the 8 XCDs and then
-  // over the workgroups of each XCD (workgroups are dealt to the XCDs
-  // round-robin), so each XCD streams one contiguous block of every row
-  constexpr int UNIT = 128 / (VEC * (int)sizeof(T));  // 16-byte vectors per unit
-  const int nvec = d_ff / VEC;
-  const int nunits = (nvec + UNIT - 1) / UNIT;
-  int u0, nu;
-  if (G % 8 == 0) {
-    const int x = w % 8, ix = w / 8, per = G / 8;
-    const int ux = nunits / 8 + (x < nunits % 8 ? 1 : 0);
-    const int ub = x * (nunits / 8) + min(x, nunits % 8);
-    nu = ux / per + (ix < ux % per ? 1 : 0);
-    u0 = ub + ix * (ux / per) + min(ix, ux % per);
   } else {
-    nu = nunits / G + (w < nunits % G ? 1 : 0);
-    u0 = w * (nunits / G) + min(w, nunits % G);
+#pragma unroll
+    for (int i = 0; i < kDecodeMaxD / THREADS; ++i) r.yv[i] = load_coherent(a.ybuf + min(i * THREADS + tid, d - 1));
+#pragma unroll
+    for (int i = 0; i < kDecodeMaxG / THREADS; ++i)
+      r.ss[i] = (tid + i * THREADS < G) ? load_coherent(a.sspart + tid + i * THREADS) : 0.0f;
   }
-  const int v0 = u0 * UNIT;
-  const int LC = max(0, min(nu * UNIT, nvec - v0));  // lanes across the strip (one vector each)
-  const int c0 = v0 * VEC, ncols = LC * VEC;
-  const int RG = LC > 0 ? THREADS / LC : 0;  // row groups
-  const int lc = LC > 0 ? tid % LC : 0, rg = LC > 0 ? tid / LC : THREADS;
+}
 
-  SATS_TRACE_POINT(0);
-  // gate rows of this thread: k = rg + RG * r, r < nrows, loaded GB at a time
-  // (GB 16-byte loads in flight per thread; a tail batch re-reads the last
-  // row and gives it weight 0)
-  constexpr int GB = 32;
-  const int nrows = (rg < RG) ? (d - rg + RG - 1) / RG : 0;
-  const int nb = (nrows + GB - 1) / GB;
-  for (int l = 0; l < a.L; ++l) {
-    const T *__restrict__ Wg = static_cast<const T *>(a.Wg) + (size_t)l * wl + c0 + lc * VEC;
-    // ------------------------------------------------ 1. layer input
-    if (l == 0) {
-      for (int k0 = tid * VEC; k0 < d; k0 += THREADS * VEC) {  // one 16-byte load per thread
-        const u32x4 xv = *reinterpret_cast<const u32x4 *>(static_cast<const T *>(a.x) + k0);
+template <typename T, int THREADS>
+__device__ __forceinline__ void dec_input_finish(const DecodeArgs &a, int l, InputRegs<THREADS> &r, DecodeSmem &sm,
+                                                 bool record) {
+  constexpr int VEC = Elem<T>::kVec, NW = THREADS / 64;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int d = a.d;
+  // The values are first used here, not earlier: keeps the compiler from
+  // hoisting their use (and the wait for their loads) above loads issued in
+  // between.
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) hs[k0 + v] = unpack<T>(xv, v);
-        if (a.layer_in && w == 0) *reinterpret_cast<u32x4 *>(static_cast<T *>(a.layer_in) + k0) = xv;
-      }
-    } else {
-      float s = 0.0f;  // total sum of squares of y, in a fixed order
-      if (tid < G) s = sum_coherent(a.sspart + tid, THREADS, (G - tid + THREADS - 1) / THREADS);
-      s = wave_sum(s);
-      if (lane == 0) scal[wv] = s;
-      __syncthreads();
-      float tot = 0.0f;
-      for (int i = 0; i < NW; ++i) tot += scal[i];
-      const float scale = sqrtf(tot / (float)d + kGlueEps);
-      for (int k0 = 0; k0 < d; k0 += THREADS * 8) {
-        float yv[8];  // all loads in flight before the first use
+  for (int i = 0; i < kDecodeMaxD / THREADS; ++i) asm volatile("" : "+v"(r.yv[i])::"memory");
 #pragma unroll
-        for (int i = 0; i < 8; ++i) yv[i] = load_coherent(a.ybuf + min(k0 + i * THREADS + tid, d - 1));
+  for (int i = 0; i < kDecodeMaxG / THREADS; ++i) asm volatile("" : "+v"(r.ss[i])::"memory");
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int k = k0 + i * THREADS + tid;
-          if (k < d) {
-            const T hv = Elem<T>::round(yv[i] / scale);
-            hs[k] = Elem<T>::value(hv);
-            if (a.layer_in && w == 0) static_cast<T *>(a.layer_in)[(size_t)l * d + k] = hv;
-          }
-        }
+  for (int i = 0; i < kDecodeMaxD / (4 * THREADS); ++i) asm volatile("" : "+v"(r.xv[i])::"memory");
+  if (l == 0) {
+#pragma unroll
+    for (int i = 0; i < kDecodeMaxD / (4 * THREADS); ++i) {
+      const int k0 = (i * THREADS + tid) * VEC;
+      if (k0 < d) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) sm.hs[k0 + v] = unpack<T>(r.xv[i], v);
+        if (record) *reinterpret_cast<u32x4 *>(static_cast<T *>(a.layer_in) + k0) = r.xv[i];
       }
     }
+  } else {
+    float s = 0.0f;  // total sum of squares of y, in a fixed order
+#pragma unroll
+    for (int i = 0; i < kDecodeMaxG / THREADS; ++i) s += r.ss[i];
+    s = wave_sum(s);
+    if (lane == 0) sm.scal[wv] = s;
     __syncthreads();
-    if (l == 0) SATS_TRACE_POINT(1);
-
-    // ------------------------------------------------ 2. gate over the strip
-    {
-      float acc[VEC];
+    float tot = 0.0f;
+    for (int i = 0; i < NW; ++i) tot += sm.scal[i];
+    const float scale = sqrtf(tot / (float)d + kGlueEps);
 #pragma unroll
-      for (int v = 0; v < VEC; ++v) acc[v] = 0.0f;
-      if (rg < RG) {  // every row group writes its partial, zero when it has no rows
-        for (int b = 0; b < nb; ++b) {
-          u32x4 gbuf[GB];
-#pragma unroll
-          for (int u = 0; u < GB; ++u)
-            gbuf[u] = load_raw<T>(Wg + (size_t)(rg + min(b * GB + u, nrows - 1) * RG) * d_ff);
-#pragma unroll
-          for (int u = 0; u < GB; ++u) {
-            const int r = b * GB + u;
-            const float hv = (r < nrows) ? hs[rg + r * RG] : 0.0f;
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[v] = fmaf(hv, unpack<T>(gbuf[u], v), acc[v]);
-          }
-        }
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) red[rg * ncols + lc * VEC + v] = acc[v];
+    for (int i = 0; i < kDecodeMaxD / THREADS; ++i) {
+      const int k = i * THREADS + tid;
+      if (k < d) {
+        const T hv = Elem<T>::round(r.yv[i] / scale);
+        sm.hs[k] = Elem<T>::value(hv);
+        if (record) static_cast<T *>(a.layer_in)[(size_t)l * d + k] = hv;
       }
-      __syncthreads();
-      const float thr = base ? 0.0f : a.thr[l];
-      bool keep = false;
-      float g = 0.0f;
-      if (tid < ncols) {
-        float s = 0.0f;
-        for (int r = 0; r < RG; ++r) s += red[r * ncols + tid];
-        g = silu(s);
-        keep = base || (fabsf(g) >= thr);
-        if (a.keep_out) a.keep_out[(size_t)l * d_ff + c0 + tid] = (uint8_t)keep;
-      }
-      const uint64_t bal = __ballot(keep);
-      const int rank = __popcll(bal & ((1ull << lane) - 1ull));
-      if (lane == 0) wcnt[wv] = __popcll(bal);
-      __syncthreads();
-      int off = 0, tot = 0;
-      for (int i = 0; i < NW; ++i) {
-        off += (i < wv) ? wcnt[i] : 0;
-        tot += wcnt[i];
-      }
-      if (keep) {
-        store_coherent_i(a.kidx + (size_t)w * kStripMax + off + rank, c0 + tid);
-        store_coherent(a.kg + (size_t)w * kStripMax + off + rank, g);
-      }
-      if (tid == 0) store_coherent_i(a.kcount + w, tot);
     }
-    if (l == 0) SATS_TRACE_POINT(2);
-    grid_barrier(a.bar, (unsigned)G, a.err);
-    if (l == 0) SATS_TRACE_POINT(3);
+  }
+  __syncthreads();
+}
 
-    // ------------------------------------------------ 3. kept rows, split evenly
-    // Up pass: the workgroup's kept rows are dealt to its wavefronts, four at
-    // a time, for u_j = W_up_T[j] . h and p_j = g_j u_j (kept in LDS).  Down
-    // pass: wavefront v owns columns chunks v, v + NW, ... of y and streams
-    // its slice of every kept row of W_down, so y's partial needs no
-    // cross-wavefront reduction and each lane holds only VEC accumulators per
-    // chunk.
-    {
-      // exclusive prefix of the strips' counts, in workgroup order
-      for (int g0 = 0; g0 < G; g0 += THREADS)
-        if (g0 + tid < G) pref[g0 + tid + 1] = load_coherent_i(a.kcount + g0 + tid);
-      if (tid == 0) pref[0] = 0;
-      __syncthreads();
-      if (wv == 0) {
-        int carry = 0;
-        for (int b0 = 1; b0 <= G; b0 += 64) {
-          const int b = b0 + lane;
-          int incl = (b <= G) ? pref[b] : 0;
+// ------------------------------------------------------------------ gate
+
+// One batch of a gate tile: rows k0w + NW (r0 + u), u < GB, of this
+// wavefront (past its nr rows the last row is read again and given weight 0).
+template <typename T, int GB, int NW>
+__device__ __forceinline__ void gate_issue(__amdgpu_buffer_rsrc_t wr, uint32_t row0_bytes, uint32_t stride_bytes,
+                                           int r0, int nr, uint32_t lo, u32x4 (&q)[GB]) {
 #pragma unroll
-          for (int o = 1; o < 64; o <<= 1) {
-            const int u = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += u;
-          }
-          if (b <= G) pref[b] = carry + incl;
-          carry += __shfl(incl, 63, 64);
-        }
-      }
-      __syncthreads();
-      const int U = pref[G];
-      const int R = U / G, Rr = U - R * G;
-      const int p0 = w * R + min(w, Rr);
-      const int nR = R + (w < Rr ? 1 : 0);
+  for (int u = 0; u < GB; ++u) q[u] = load_rsrc(wr, lo, row0_bytes + (uint32_t)min(r0 + u, nr - 1) * stride_bytes);
+}
 
-      constexpr int NCH = (DMAX + NW - 1) / NW;  // column chunks per wavefront
-      float yacc[NCH][VEC];
+template <typename T, int GB, int NW>
+__device__ __forceinline__ void gate_consume(const DecodeSmem &sm, int k0w, int r0, int nr, const u32x4 (&q)[GB],
+                                             float (&acc)[Elem<T>::kVec]) {
+#pragma unroll
+  for (int u = 0; u < GB; ++u) {
+    const float hv = sm.hs[k0w + min(r0 + u, nr - 1) * NW];
+    const float hu = (r0 + u < nr) ? hv : 0.0f;
+#pragma unroll
+    for (int v = 0; v < Elem<T>::kVec; ++v) acc[v] = fmaf(hu, unpack<T>(q[u], v), acc[v]);
+  }
+}
+
+// Gate tiles blockIdx.x, blockIdx.x + gridDim.x, ... (tile t: column block
+// t % nblk, row chunk t / nblk); forms h in LDS before the first tile's
+// products (its loads follow the tile's first weight loads).
+template <typename T>
+__device__ void dec_gate(const DecodeArgs &a, int l, int G, DecodeSmem &sm, bool record) {
+  constexpr int THREADS = kGateThreads, VEC = Elem<T>::kVec, NW = THREADS / 64;
+  constexpr int CB = dec_block_cols<T>();
+  constexpr int GB = kGateBatch;
+  static_assert(NW * CB <= 2 * kDecodeMaxD, "gate partials fit the LDS buffer");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int d = a.d, d_ff = a.d_ff;
+  const int rows = (d + a.nrc - 1) / a.nrc;
+  const __amdgpu_buffer_rsrc_t wr =
+      weight_rsrc(static_cast<const T *>(a.Wg) + (size_t)l * d * d_ff, (uint32_t)((size_t)d * d_ff * sizeof(T)));
+  const uint32_t stride = (uint32_t)((size_t)NW * d_ff * sizeof(T));  // between a wavefront's rows
+  InputRegs<THREADS> ir;
+  bool have_input = false;
+  for (int t = blockIdx.x; t < a.nblk * a.nrc; t += gridDim.x) {
+    const int cb = t % a.nblk, rc = t / a.nblk;
+    const int k0 = rc * rows, kn = max(0, min(d, k0 + rows) - k0);
+    const int col = cb * CB + lane * VEC;
+    const int nr = (kn - wv + NW - 1) / NW;  // this wavefront's rows: k0 + wv + NW r, r < nr
+    // Lanes past d_ff read in-bounds data of the next row (or zeros past the
+    // matrix) and their sums are never stored, so only nr guards the loads.
+    const bool live = nr > 0;
+    const uint32_t row0 = (uint32_t)((size_t)(k0 + wv) * d_ff * sizeof(T));  // wavefront-uniform
+    const uint32_t lo = (uint32_t)(col * sizeof(T));
+    float acc[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = 0.0f;
+    u32x4 q[GB];
+    if (live) gate_issue<T, GB, NW>(wr, row0, stride, 0, nr, lo, q);
+    if (!have_input) {  // h is needed from the first batch on; its loads follow the weights'
+      dec_input_issue<T, THREADS>(a, l, G, ir);
+      dec_input_finish<T, THREADS>(a, l, ir, sm, record);
+      have_input = true;
+      if (l == 0) SATS_TRACE_POINT(1);
+    }
+    if (live) {
+      gate_consume<T, GB, NW>(sm, k0 + wv, 0, nr, q, acc);
+      for (int r0 = GB; r0 < nr; r0 += GB) {
+        gate_issue<T, GB, NW>(wr, row0, stride, r0, nr, lo, q);
+        gate_consume<T, GB, NW>(sm, k0 + wv, r0, nr, q, acc);
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) sm.red[wv * CB + lane * VEC + v] = acc[v];
+    __syncthreads();
+    if (tid < CB && cb * CB + tid < d_ff) {
+      float s = 0.0f;
+#pragma unroll
+      for (int q2 = 0; q2 < NW; ++q2) s += sm.red[q2 * CB + tid];
+      store_coherent(a.gpart + (size_t)rc * d_ff + cb * CB + tid, s);
+    }
+    __syncthreads();  // LDS reuse by the next tile
+  }
+}
+
+// ------------------------------------------------------------------ rows
+
+// The workgroup's wavefronts form two halves of 8; half hf takes its own
+// rows of the unit, and wavefront v of a half owns column chunks v, v + 8,
+// ... of d (64 lanes x 16 bytes each) for both projections.
+
+// One batch: loads of this wavefront's chunks of the kept rows
+// list[r0 + r], r < R (rows at or past `end` are not read).
+template <typename T, int R, int NCH>
+__device__ __forceinline__ void rows_issue(__amdgpu_buffer_rsrc_t Wu, __amdgpu_buffer_rsrc_t Wd, const DecodeSmem &sm,
+                                           int r0, int end, int d, u32x4 (&bu)[R][NCH], u32x4 (&bd)[R][NCH]) {
+  constexpr int VEC = Elem<T>::kVec, CH = 64 * VEC;
+  const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 7);
+  uint32_t soff[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    soff[r] = (uint32_t)((size_t)__builtin_amdgcn_readfirstlane(sm.mj[max(0, min(r0 + r, end - 1))]) * d * sizeof(T));
+  // all rows of W_up_T first: the up products can start while W_down arrives
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int k = (hw + c * 8) * CH + lane * VEC;
+      bu[r][c] = (k < d && r0 + r < end) ? load_rsrc(Wu, (uint32_t)(k * sizeof(T)), soff[r]) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int k = (hw + c * 8) * CH + lane * VEC;
+      bd[r][c] = (k < d && r0 + r < end) ? load_rsrc(Wd, (uint32_t)(k * sizeof(T)), soff[r]) : u32x4{0u, 0u, 0u, 0u};
+    }
+}
+
+// Uses one batch: this wavefront's parts of u_j = W_up_T[j] . h go to its
+// half's LDS slot `par`; after the barrier every wavefront of the half adds
+// the half's parts in wavefront order, p_j = g_j u_j, and accumulates p_j
+// times its chunks of W_down[j].
+template <typename T, int R, int NCH>
+__device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)[NCH][Elem<T>::kVec],
+                                             float (&yacc)[NCH][Elem<T>::kVec], int r0, int end, int par,
+                                             const u32x4 (&bu)[R][NCH], const u32x4 (&bd)[R][NCH]) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 7);
+  const int hf = __builtin_amdgcn_readfirstlane(threadIdx.x >> 9);
+  float *part = sm.red + (hf * 2 + par) * (R * 8);  // [R][8] parts of u of this half
+  float u[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    u[r] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) u[r] = fmaf(hreg[c][v], unpack<T>(bu[r][c], v), u[r]);
+  }
+  const float us = rows_sum<R>(u, lane);
+  if ((lane & (64 / R - 1)) == 0) part[(lane / (64 / R)) * 8 + hw] = us;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    float ut = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) ut += part[r * 8 + q];
+    const float pr = (r0 + r < end) ? sm.mg[max(0, min(r0 + r, end - 1))] * ut : 0.0f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) yacc[c][v] = fmaf(pr, unpack<T>(bd[r][c], v), yacc[c][v]);
+  }
+}
+
+// Rows phase of workgroup w (of G): units w, w + G, ... of nblk x S units
+// (S = max(1, G / nblk) shares per column block); writes the workgroup's
+// partial y.  h is formed first (its loads overlap the first block's partial
+// sums).
+template <typename T>
+__device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, DecodeSmem &sm) {
+  constexpr int VEC = Elem<T>::kVec, NW = kDecodeWaves;
+  constexpr int CB = dec_block_cols<T>();
+  constexpr int CH = 64 * VEC;              // elements per chunk (one 16-byte load per lane)
+  constexpr int DMAX = kDecodeMaxD / CH;    // chunks per row
+  constexpr int NCH = (DMAX + 7) / 8;       // chunks per wavefront of a half
+  constexpr int R = 8 / NCH;                // rows per batch (2 x 8 loads in flight per lane)
+  static_assert(CB <= kDecodeThreads / 2 && 4 * R * 8 <= 2 * kDecodeMaxD, "single-token tiling");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), hw = wv & 7, hf = wv >> 3;
+  const int d = a.d, d_ff = a.d_ff, nblk = a.nblk;
+  const size_t wl = (size_t)d * d_ff;
+  const int S = max(1, G / nblk), units = nblk * S;
+  const float thr = base ? 0.0f : a.thr[l];
+  const __amdgpu_buffer_rsrc_t Wu = weight_rsrc(static_cast<const T *>(a.Wu) + (size_t)l * wl, (uint32_t)(wl * sizeof(T)));
+  const __amdgpu_buffer_rsrc_t Wd = weight_rsrc(static_cast<const T *>(a.Wd) + (size_t)l * wl, (uint32_t)(wl * sizeof(T)));
+
+  InputRegs<kDecodeThreads> ir;
+  dec_input_issue<T, kDecodeThreads>(a, l, G, ir);
+  float hreg[NCH][VEC];  // h at this lane's columns
+  float yacc[NCH][VEC];
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) hreg[c][v] = yacc[c][v] = 0.0f;
+  int par = 0;  // LDS slot parity for the parts of u
+
+  for (int un = w; un < units; un += G) {
+    const int cb = un % nblk, sub = un / nblk;
+    // the block's keep list (every workgroup of the block forms the same one)
+    const int gcol = cb * CB + tid;
+    bool keep = false;
+    float g = 0.0f;
+    if (tid < CB && gcol < d_ff) {
+      g = silu(sum_coherent(a.gpart + gcol, (size_t)d_ff, a.nrc));
+      keep = base || (fabsf(g) >= thr);
+      if (sub == 0 && a.keep_out) a.keep_out[(size_t)l * d_ff + gcol] = (uint8_t)keep;
+    }
+    if (un == w) {
+      dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, false);
 #pragma unroll
       for (int c = 0; c < NCH; ++c)
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) yacc[c][v] = 0.0f;
-
-      const T *__restrict__ Wu = static_cast<const T *>(a.Wu) + (size_t)l * wl;
-      const T *__restrict__ Wd = static_cast<const T *>(a.Wd) + (size_t)l * wl;
-      for (int m0 = 0; m0 < nR; m0 += THREADS) {
-        const int mn = min(THREADS, nR - m0);
-        __syncthreads();
-        if (tid < mn) {  // row metadata of the chunk, all loads at once
-          const int p = p0 + m0 + tid;
-          int lo = 0, hi = G - 1;  // strip holding position p: largest o with pref[o] <= p
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (pref[mid] <= p) lo = mid; else hi = mid - 1;
-          }
-          const size_t e = (size_t)lo * kStripMax + (p - pref[lo]);
-          mj[tid] = load_coherent_i(a.kidx + e);
-          mg[tid] = load_coherent(a.kg + e);
+        for (int v = 0; v < VEC; ++v) {
+          const int k = (hw + c * 8) * CH + lane * VEC + v;
+          hreg[c][v] = (k < d) ? sm.hs[k] : 0.0f;
         }
-        __syncthreads();
-        if (l == 0 && m0 == 0) SATS_TRACE_POINT(4);
-
-        // up pass
-        constexpr int RU = (sizeof(T) == 2) ? 4 : 2;  // rows in flight per wavefront
-        for (int i0 = wv * RU; i0 < mn; i0 += NW * RU) {
-          u32x4 wr[RU][DMAX];
-#pragma unroll
-          for (int r = 0; r < RU; ++r) {
-            const int jr = __builtin_amdgcn_readfirstlane(mj[min(i0 + r, mn - 1)]);
-            const T *__restrict__ ur = Wu + (size_t)jr * d;
-#pragma unroll
-            for (int t = 0; t < DMAX; ++t) {
-              const int k = t * CH + lane * VEC;
-              wr[r][t] = (k < d && i0 + r < mn) ? load_raw<T>(ur + k) : u32x4{0u, 0u, 0u, 0u};
-            }
-          }
-          float u[RU];
-#pragma unroll
-          for (int r = 0; r < RU; ++r) u[r] = 0.0f;
-#pragma unroll
-          for (int t = 0; t < DMAX; ++t) {
-            const int k = t * CH + lane * VEC;
-            if (k < d) {
-#pragma unroll
-              for (int v = 0; v < VEC; ++v) {
-                const float hv = hs[k + v];
-#pragma unroll
-                for (int r = 0; r < RU; ++r) u[r] = fmaf(hv, unpack<T>(wr[r][t], v), u[r]);
-              }
-            }
-          }
-#pragma unroll
-          for (int r = 0; r < RU; ++r) {
-            const float ur = wave_sum(u[r]);
-            if (lane == 0 && i0 + r < mn) mp[i0 + r] = mg[i0 + r] * ur;
-          }
-        }
-        __syncthreads();
-
-        // down pass: this wavefront's column chunks of every row, RD rows in flight
-        constexpr int RD = (sizeof(T) == 2) ? 32 : 16;
-        for (int i0 = 0; i0 < mn; i0 += RD) {
-          u32x4 wr[RD][NCH];
-#pragma unroll
-          for (int r = 0; r < RD; ++r) {
-            const int jr = __builtin_amdgcn_readfirstlane(mj[min(i0 + r, mn - 1)]);
-            const T *__restrict__ dr = Wd + (size_t)jr * d;
-#pragma unroll
-            for (int c = 0; c < NCH; ++c) {
-              const int k = (wv + c * NW) * CH + lane * VEC;
-              wr[r][c] = (k < d && i0 + r < mn) ? load_raw<T>(dr + k) : u32x4{0u, 0u, 0u, 0u};
-            }
-          }
-#pragma unroll
-          for (int r = 0; r < RD; ++r) {
-            const float pr = (i0 + r < mn) ? mp[i0 + r] : 0.0f;
-#pragma unroll
-            for (int c = 0; c < NCH; ++c)
-#pragma unroll
-              for (int v = 0; v < VEC; ++v) yacc[c][v] = fmaf(pr, unpack<T>(wr[r][c], v), yacc[c][v]);
-          }
-        }
-      }
-      if (l == 0) SATS_TRACE_POINT(5);
-      // this workgroup's partial y, written by column owner
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) {
-        const int k = (wv + c * NW) * CH + lane * VEC;
-        if (k < d) {
-#pragma unroll
-          for (int v = 0; v < VEC; v += 4)
-            store_coherent4(a.ypart + (size_t)w * d + k + v, yacc[c][v], yacc[c][v + 1], yacc[c][v + 2],
-                            yacc[c][v + 3]);
-        }
-      }
     }
-    grid_barrier(a.bar, (unsigned)G, a.err);
-    if (l == 0) SATS_TRACE_POINT(6);
-
-    // ------------------------------------------------ 4. reduction over workgroups
-    {
-      const int cpw = (d + G - 1) / G;          // columns of this workgroup (<= THREADS)
-      const int cw0 = w * cpw;
-      const int nc = max(0, min(cpw, d - cw0));
-      const int ngr = THREADS / cpw;            // partial groups
-      const int c = tid % cpw, gr = tid / cpw;
-      float s = 0.0f;
-      if (c < nc && gr < ngr && gr < G)
-        s = sum_coherent(a.ypart + (size_t)gr * d + cw0 + c, (size_t)ngr * d, (G - gr + ngr - 1) / ngr);
-      red[tid] = s;
-      __syncthreads();
-      float y = 0.0f;
-      if (tid < nc) {
-        for (int qg = 0; qg < ngr && qg < G; ++qg) y += red[qg * cpw + tid];
-        if (l == a.L - 1) static_cast<T *>(a.out)[cw0 + tid] = Elem<T>::round(y);
-        else store_coherent(a.ybuf + cw0 + tid, y);
-      }
-      float sq = (tid < nc) ? y * y : 0.0f;  // slice sum of squares, fixed order
-      sq = wave_sum(sq);
-      __syncthreads();
-      if (lane == 0) scal[wv] = sq;
-      __syncthreads();
-      if (tid == 0 && l < a.L - 1) {
-        float tot = 0.0f;
-        for (int i = 0; i < NW; ++i) tot += scal[i];
-        store_coherent(a.sspart + w, tot);
-      }
+    const uint64_t bal = __ballot(keep);
+    const int rank = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) sm.wcnt[wv] = __popcll(bal);
+    __syncthreads();
+    int off = 0, tot = 0;
+    for (int i = 0; i < NW; ++i) {
+      off += (i < wv) ? sm.wcnt[i] : 0;
+      tot += sm.wcnt[i];
     }
-    if (l == 0) SATS_TRACE_POINT(7);
-    if (l < a.L - 1) grid_barrier(a.bar, (unsigned)G, a.err);
+    if (keep) {
+      sm.mj[off + rank] = gcol;
+      sm.mg[off + rank] = g;
+    }
+    __syncthreads();
+    // this unit's rows: list[i0, i0 + mn); half hf takes [b, e)
+    const int i0 = (int)(((int64_t)sub * tot) / S);
+    const int mn = (int)(((int64_t)(sub + 1) * tot) / S) - i0;
+    const int hn = (mn + 1) / 2;
+    const int b = i0 + hf * hn, e = i0 + min(mn, (hf + 1) * hn);
+    if (l == 0 && un == w) SATS_TRACE_POINT(4);
+    u32x4 bu[R][NCH], bd[R][NCH];
+    for (int r0 = 0; r0 < hn; r0 += R) {  // both halves run the same number of batches
+      rows_issue<T, R, NCH>(Wu, Wd, sm, b + r0, e, d, bu, bd);
+      rows_consume<T, R, NCH>(sm, hreg, yacc, b + r0, e, par, bu, bd);
+      par ^= 1;
+    }
+    __syncthreads();  // the next unit rewrites the list
   }
+  if (l == 0) SATS_TRACE_POINT(5);
+  // the two halves' sums, added in half order, are this workgroup's partial y
+  float *hsum = sm.red;  // [d]
+  if (hf == 1) {
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int k = (hw + c * 8) * CH + lane * VEC;
+      if (k < d) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) hsum[k + v] = yacc[c][v];
+      }
+    }
+  }
+  __syncthreads();
+  if (hf == 0) {
+    const __amdgpu_buffer_rsrc_t yr = weight_rsrc(a.ypart + (size_t)w * d, (uint32_t)(d * sizeof(float)));
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int k = (hw + c * 8) * CH + lane * VEC;
+      if (k < d) {
+#pragma unroll
+        for (int v = 0; v < VEC; v += 4)
+          store_coherent4(yr, (uint32_t)((k + v) * sizeof(float)), yacc[c][v] + hsum[k + v],
+                          yacc[c][v + 1] + hsum[k + v + 1], yacc[c][v + 2] + hsum[k + v + 2],
+                          yacc[c][v + 3] + hsum[k + v + 3]);
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ reduce
+
+// Workgroup w's slice of columns: y = sum of the G partials in workgroup order.
+template <typename T>
+__device__ void dec_reduce(const DecodeArgs &a, int l, int G, int w, DecodeSmem &sm) {
+  constexpr int THREADS = kDecodeThreads, NW = kDecodeWaves;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int d = a.d;
+  const int cpw = (d + G - 1) / G;  // columns of this workgroup (<= THREADS)
+  const int cw0 = w * cpw;
+  const int nc = max(0, min(cpw, d - cw0));
+  const int ngr = THREADS / cpw;    // partial groups
+  const int c = tid % cpw, gr = tid / cpw;
+  float s = 0.0f;
+  if (c < nc && gr < ngr && gr < G)
+    s = sum_coherent(a.ypart + (size_t)gr * d + cw0 + c, (size_t)ngr * d, (G - gr + ngr - 1) / ngr);
+  sm.red[tid] = s;
+  __syncthreads();
+  float y = 0.0f;
+  if (tid < nc) {
+    for (int qg = 0; qg < ngr && qg < G; ++qg) y += sm.red[qg * cpw + tid];
+    if (l == a.L - 1) static_cast<T *>(a.out)[cw0 + tid] = Elem<T>::round(y);
+    else store_coherent(a.ybuf + cw0 + tid, y);
+  }
+  float sq = (tid < nc) ? y * y : 0.0f;  // slice sum of squares, fixed order
+  sq = wave_sum(sq);
+  if (lane == 0) sm.scal[wv] = sq;
+  __syncthreads();
+  if (tid == 0 && l < a.L - 1) {
+    float tot = 0.0f;
+    for (int i = 0; i < NW; ++i) tot += sm.scal[i];
+    store_coherent(a.sspart + w, tot);
+  }
+}
+
+// ------------------------------------------------------------------ kernels
+
+// Gate tiles (any grid; G = the number of partials of the previous layer's y).
+template <typename T>
+__global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, int l, int G) {
+  __shared__ DecodeSmem sm;
+  if (l == 0 && blockIdx.x == 0 && threadIdx.x == 0) {
+    const int base = token_is_base(a.route_mode, a.ids, a.lut, 0);
+    a.state[0] = base;
+    if (a.route_out) a.route_out[0] = (uint8_t)base;
+  }
+  if (l == 0) SATS_TRACE_POINT(0);
+  dec_gate<T>(a, l, G, sm, a.layer_in != nullptr && blockIdx.x == 0);
+  if (l == 0) SATS_TRACE_POINT(2);
+}
+
+// Rows and reduce: G workgroups each.
+template <typename T>
+__global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, int l) {
+  __shared__ DecodeSmem sm;
+  if (l == 0) SATS_TRACE_POINT(3);
+  dec_rows<T>(a, l, a.state[0], gridDim.x, blockIdx.x, sm);
+}
+
+template <typename T>
+__global__ __launch_bounds__(kDecodeThreads) void dec_reduce_kernel(DecodeArgs a, int l) {
+  __shared__ DecodeSmem sm;
+  if (l == 0) SATS_TRACE_POINT(6);
+  dec_reduce<T>(a, l, gridDim.x, blockIdx.x, sm);
+  if (l == 0) SATS_TRACE_POINT(7);
 }
 
 }  // namespace sats

@@ -31,6 +31,10 @@
 namespace sats {
 
 constexpr int kThreads = 256;
+#ifndef SATS_GATE_LANES
+#define SATS_GATE_LANES 16
+#endif
+constexpr int kGateLanes = SATS_GATE_LANES;  // lanes across a gate row segment (x 16 bytes)
 constexpr float kGlueEps = 1e-6f;
 
 // ------------------------------------------------------------------ elements
@@ -211,9 +215,9 @@ struct GateArgs {
 
 template <typename T, int VEC, int NT>
 __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
-  constexpr int CL = (VEC == 1) ? 64 : 16;  // lanes across one row segment
-  constexpr int RG = kThreads / CL;         // row groups
-  constexpr int CB = CL * VEC;              // columns per block
+  constexpr int CL = (VEC == 1) ? 64 : kGateLanes;  // lanes across one row segment
+  constexpr int RG = kThreads / CL;                 // row groups
+  constexpr int CB = CL * VEC;                      // columns per block
   extern __shared__ float smem[];
   __shared__ int flag;
   __shared__ int wcnt[kThreads / 64];

@@ -84,7 +84,7 @@ int env_int(const char *name, int dflt) {
 }
 
 struct Plan {
-  int vec, CL, RG, CB;     // gate / down tiling
+  int vec, CL, RG, CB;     // down lanes per row segment; gate row groups and columns per block
   int nblocks;             // gate column blocks
   int KS, KC;              // gate row split
   int SW, n_slices, KCH;   // down column slices and list chunks
@@ -95,9 +95,10 @@ struct Plan {
 Plan make_plan(int64_t d, int64_t d_ff, int esz, bool vec_ok, int n_pass) {
   Plan p{};
   p.vec = vec_ok ? 16 / esz : 1;
-  p.CL = (p.vec == 1) ? 64 : 16;
-  p.RG = sats::kThreads / p.CL;
-  p.CB = p.CL * p.vec;
+  p.CL = (p.vec == 1) ? 64 : 16;  // down-projection lanes per row segment
+  const int gate_cl = (p.vec == 1) ? 64 : sats::kGateLanes;
+  p.RG = sats::kThreads / gate_cl;
+  p.CB = gate_cl * p.vec;
   p.nblocks = (int)((d_ff + p.CB - 1) / p.CB);
   p.NT = (n_pass == 1) ? 1 : 4;
   const int gate_target = env_int("SATS_GATE_WGS", 2048);
@@ -137,8 +138,8 @@ struct Buffers {
   uint32_t *blk_mask;
   uint8_t *keep;
   float *ypart, *sspart;  // single-token path: per-workgroup partial y and sums of squares
-  int *kcount, *kidx;     // single-token path: kept columns of each strip
-  float *kg;
+  float *dgpart;          // single-token path: partial gate sums per row chunk
+  int *dstate;            // single-token path: the token's route
   int *perm, *ctl;        // batched path: token partition and dense-group control words
   uint8_t *skip, *gbase;
   uint16_t *xd, *hnext, *pdense;  // dense group (MFMA): inputs, next inputs, p
@@ -148,7 +149,10 @@ struct Buffers {
 // Layout for passes of up to `pass` tokens (the counters live in their own
 // zero-initialised allocation).
 struct DecodePlan {
-  int G = 0;  // co-resident workgroups of the single-token kernel (0: path not used)
+  int G = 0;           // rows / reduce workgroups, one partial y each (0: path not used)
+  int nblk = 0;        // gate column blocks
+  int nrc = 0;         // gate row chunks
+  int gate_grid = 0;   // workgroups of the gate launch
 };
 
 size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, int esz, int64_t L,
@@ -180,21 +184,21 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.hnext = c.take<uint16_t>(Pp * d);
   t.pdense = c.take<uint16_t>(Pp * d_ff);
   t.ddpart = c.take<float>((int64_t)kDenseKsplit * Pp * d);
-  t.kcount = c.take<int>(dp.G);
-  t.kidx = c.take<int>((int64_t)dp.G * sats::kStripMax);
-  t.kg = c.take<float>((int64_t)dp.G * sats::kStripMax);
+  t.dgpart = c.take<float>((int64_t)dp.nrc * d_ff);
+  t.dstate = c.take<int>(64);
   if (b) *b = t;
   return c.off;
 }
 
-// The counter allocation starts with control words (barrier count and
-// generation, device error flag); the per-block counters follow.  Every
-// counter is zero whenever no kernel is running.
+// The counter allocation starts with control words (the device error flag);
+// the per-block counters follow.  Every counter is zero whenever no kernel is
+// running.
 constexpr size_t kCtl = 512;
-constexpr size_t kBar = 0, kErr = 320;
+constexpr size_t kErr = 320;
 
-size_t counter_count(const Plan &p, int64_t pass) {
+size_t counter_count(const Plan &p, int64_t pass, const DecodePlan &dp) {
   const int64_t tiles = ((pass + 3) / 4) * 4;
+  (void)dp;
   return kCtl + (size_t)std::max<int64_t>(tiles * p.nblocks + tiles * p.n_slices, 2 * (int64_t)p.nblocks + 64);
 }
 
@@ -244,16 +248,24 @@ int ensure_workspace(hipStream_t stream, size_t bytes, size_t n_counters, Worksp
   return SATS_OK;
 }
 
-// The single-token kernel holds h in LDS (d <= 4096), gives each workgroup a
-// strip of at most kStripMax columns and each reduction workgroup at most
-// one column per thread.
-bool decode_fits(int64_t d, int64_t d_ff, int esz, int G) {
-  const int64_t vec = 16 / esz, unit = 128 / esz;  // elements per 16-byte vector, per 128-byte unit
-  const int64_t units = (d_ff + unit - 1) / unit;
-  const int64_t per_wg = (G % 8 == 0) ? ((units + 7) / 8 + G / 8 - 1) / (G / 8) : (units + G - 1) / G;
-  (void)vec;
-  return G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD && per_wg * unit <= sats::kStripMax &&
-         (d + G - 1) / G <= sats::kDecodeThreads;
+// Single-token plan.  h is held in LDS (d <= kDecodeMaxD); `G` workgroups
+// (at most kDecodeMaxG) take the rows and reduce phases, each reduce
+// workgroup owning at most one column per thread; gate tiles are one column
+// block by about d / nrc rows.  Returns false when the shape does not fit.
+bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp) {
+  DecodePlan q{};
+  const int64_t cb = (int64_t)(16 / esz) * 64;
+  q.G = G;
+  q.nblk = (int)((d_ff + cb - 1) / cb);
+  const int64_t tiles = env_int("SATS_DEC_GATE_WGS", 256);
+  int64_t nrc = std::max<int64_t>(1, tiles / q.nblk);
+  nrc = std::min<int64_t>(nrc, std::max<int64_t>(1, d / (sats::kGateThreads / 64)));  // a row per wavefront
+  q.nrc = (int)nrc;
+  q.gate_grid = q.nblk * q.nrc;
+  const bool ok = G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
+                  (d + G - 1) / G <= sats::kDecodeThreads;
+  *dp = ok ? q : DecodePlan{};
+  return ok;
 }
 
 // --------------------------------------------------------------- the call
@@ -449,7 +461,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     {
       TimedLaunch tl(SATS_K_DOWN, c.stream);
       hipLaunchKernelGGL((down_kernel<T, VEC, NT>), dim3(p.n_slices, p.KCH, tiles), dim3(kThreads),
-                         sizeof(float) * (size_t)p.RG * NT * p.SW, c.stream, dn);
+                         sizeof(float) * (size_t)(kThreads / p.CL) * NT * p.SW, c.stream, dn);
     }
     HIP_TRY(hipGetLastError());
   }
@@ -472,33 +484,34 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   a.L = (int)c.L;
   a.d = (int)c.d;
   a.d_ff = (int)c.d_ff;
-  a.kcount = b.kcount;
-  a.kidx = b.kidx;
-  a.kg = b.kg;
+  a.nblk = dp.nblk;
+  a.nrc = dp.nrc;
+  a.gpart = b.dgpart;
+  a.state = b.dstate;
   a.ypart = b.ypart;
   a.ybuf = b.ybuf;
   a.sspart = b.sspart;
-  a.bar = counters + kBar;
-  a.err = counters + kErr;
   a.route_out = c.route_out;
   const bool lists = c.active_count || c.active_idx;
   a.keep_out = lists ? b.keep : nullptr;
   a.layer_in = c.layer_in;
-  void *args[] = {&a};
-  {
-    TimedLaunch tl(SATS_K_DECODE, c.stream);
-    // One workgroup per CU: every workgroup is resident when no other work
-    // shares the device.  A plain launch costs ~18 us less than a cooperative
-    // one, which guarantees residency (SATS_COOPERATIVE_LAUNCH=1 selects it);
-    // either way every wait is bounded and a failed one is reported by
-    // sats_device_status().
-    if (getenv("SATS_COOPERATIVE_LAUNCH")) {
-      HIP_TRY(hipLaunchCooperativeKernel(reinterpret_cast<const void *>(&decode_kernel<T>), dim3(dp.G),
-                                         dim3(kDecodeThreads), args, 0, c.stream));
-    } else {
-      hipLaunchKernelGGL((decode_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream, a);
-      HIP_TRY(hipGetLastError());
+  // three plain launches per layer; kernel boundaries order the phases
+  for (int l = 0; l < (int)c.L; ++l) {
+    {
+      TimedLaunch tl(SATS_K_DEC_GATE, c.stream);
+      hipLaunchKernelGGL((dec_gate_kernel<T>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream, a, l, dp.G);
     }
+    HIP_TRY(hipGetLastError());
+    {
+      TimedLaunch tl(SATS_K_DEC_ROWS, c.stream);
+      hipLaunchKernelGGL((dec_rows_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream, a, l);
+    }
+    HIP_TRY(hipGetLastError());
+    {
+      TimedLaunch tl(SATS_K_DEC_REDUCE, c.stream);
+      hipLaunchKernelGGL((dec_reduce_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream, a, l);
+    }
+    HIP_TRY(hipGetLastError());
   }
   if (lists) {
     for (int64_t l = 0; l < c.L; ++l) {
@@ -542,21 +555,13 @@ int run(const Call &c) {
                       (!c.layer_in || aligned16(c.layer_in));
   const int pass = (int)std::min<int64_t>(c.n, kMaxPass);
   const Plan p = make_plan(c.d, c.d_ff, esz, vec_ok, pass);
-  // single-token persistent path: one token, vector layout, h fits the LDS copy
+  // single-token path: one token, vector layout, h fits the LDS copy
   bool decode = c.n == 1 && vec_ok && !getenv("SATS_NO_DECODE");
   DecodePlan dp;
-  if (decode) {
-    int occ = 0;
-    HIP_TRY(hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, reinterpret_cast<const void *>(&sats::decode_kernel<T>),
-                                                         sats::kDecodeThreads, 0));
-    const int per_cu = std::min(occ, env_int("SATS_DECODE_WG_PER_CU", 1));
-    dp.G = device_cus() * per_cu;
-    decode = per_cu >= 1 && decode_fits(c.d, c.d_ff, esz, dp.G);
-    if (!decode) dp.G = 0;
-  }
+  if (decode) decode = make_decode_plan(c.d, c.d_ff, esz, env_int("SATS_DEC_ROWS_WGS", device_cus()), &dp);
   const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, c.L, dp, nullptr);
   Workspace *ws = nullptr;
-  size_t ncount = counter_count(p, pass);
+  size_t ncount = counter_count(p, pass, dp);
   int rc = ensure_workspace(c.stream, bytes, ncount, &ws);
   if (rc) return rc;
   Buffers b{};
@@ -671,13 +676,13 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, 
   size_t bytes = 0, nc = 0;
   int cus = device_cus();
   if (cus < 1) return fail(SATS_ERR_HIP, "no device");
-  DecodePlan dp;
-  dp.G = cus * 2;
+  DecodePlan dp{};
+  (void)make_decode_plan(d, d_ff, elem_bytes, env_int("SATS_DEC_ROWS_WGS", cus), &dp);
   for (int v = 0; v < 2; ++v)
     for (int np : {1, pass}) {
       const Plan p = make_plan(d, d_ff, elem_bytes, v == 1, np);
       bytes = std::max(bytes, layout(nullptr, p, pass, d, d_ff, elem_bytes, n_layers, dp, nullptr));
-      nc = std::max(nc, counter_count(p, pass));
+      nc = std::max(nc, counter_count(p, pass, dp));
     }
   Workspace *ws = nullptr;
   return ensure_workspace(stream, bytes, nc, &ws);
@@ -771,8 +776,10 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_UP: return "up_kernel";
     case SATS_K_DOWN: return "down_kernel";
     case SATS_K_INSPECT: return "compact_kernel";
-    case SATS_K_DECODE: return "decode_kernel";
     case SATS_K_DENSE: return "dense_mfma_kernels";
+    case SATS_K_DEC_GATE: return "dec_gate_kernel";
+    case SATS_K_DEC_ROWS: return "dec_rows_kernel";
+    case SATS_K_DEC_REDUCE: return "dec_reduce_kernel";
     default: return "";
   }
 }

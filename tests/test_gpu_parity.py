@@ -52,7 +52,7 @@ SMALL = [
     (6, 2, 25, 41, "f32", 2),        # odd sizes, fp32
     (7, 2, 128, 512, "f32", 67),     # more tokens than one pass (64)
     (8, 1, 4096, 1024, "bf16", 2),   # long rows: several row chunks in the gate split
-    # single tokens take the persistent one-launch path
+    # single tokens take the single-token path (three launches per layer)
     (9, 3, 256, 1000, "bf16", 1),    # stack, ragged block
     (10, 2, 4096, 1024, "bf16", 1),  # widest h the single-token path holds
     (11, 2, 512, 1536, "f32", 1),    # fp32 stack
@@ -150,7 +150,7 @@ def test_batch_rows_match_single_token_calls():
     """Row independence: a batched call's row equals the single-token call on it.
 
     The two calls take different kernels (batch: MFMA or compacted GEMV; one
-    token: the persistent kernel), so sums differ in order.  At layer 0 both
+    token: the single-token kernels), so sums differ in order.  At layer 0 both
     see the same input, so keep sets must agree outside the 1e-3 band around
     the threshold; later layers see inputs that differ by rounding, so each
     run is checked against the oracle on its own inputs; outputs agree within
@@ -174,6 +174,33 @@ def test_batch_rows_match_single_token_calls():
         assert not ((a1 != af) & ~band_mask(g, float(np.float32(ts[0])))).any()
         e = rel_err(numerics.decode(full["out"][i], "bf16"), numerics.decode(r1["out"][0], "bf16"))
         assert e <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("seed,L,d,dff,dtype", [(41, 3, 256, 1000, "bf16"), (42, 2, 4096, 1024, "bf16"),
+                                                (43, 2, 512, 1536, "f32"), (44, 2, 24, 40, "bf16")])
+def test_single_token_tilings_match_oracle_and_repeat_bitwise(seed, L, d, dff, dtype):
+    """The single-token kernels under several gate tilings (row chunks per
+    column block) and rows grids (partials of y): each matches the oracle on
+    a sparse-path and a base-path token, and a repeated call gives the same
+    bits (every sum has a fixed order)."""
+    c = synth.small_case(seed, L, d, dff, dtype, 1, vocab=40, n_dense_ids=12,
+                         w_std=1.0 / np.sqrt(d))
+    ts = case_thresholds(c, dtype, seed=seed)
+    for ids in ([0], [int(c["route_lut"].argmax())]):  # a sparse-path and a base-path token
+        c["token_ids"] = np.asarray(ids, np.int32)
+        for env in ({}, {"SATS_DEC_GATE_WGS": "1"}, {"SATS_DEC_GATE_WGS": "2000"},
+                    {"SATS_DEC_ROWS_WGS": "7"}, {"SATS_DEC_ROWS_WGS": "1000"}):
+            os.environ.update(env)
+            try:
+                r1 = run_gpu(c, ts, c["route_lut"], dtype)
+                r2 = run_gpu(c, ts, c["route_lut"], dtype)
+            finally:
+                for k in env:
+                    del os.environ[k]
+            worst = check_against_oracle(c, ts, c["route_lut"], dtype, r1)
+            say(f"  {env or 'default'} ids={ids} worst rel err {worst:.3g}")
+            for k in ("out", "layer_in", "count", "idx", "route"):
+                np.testing.assert_array_equal(r1[k], r2[k])
 
 
 def _golden(cfg):
