@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--workload", default="c2")
     p.add_argument("--copies", type=int, default=8, help="weight copies rotated to defeat the MALL")
     p.add_argument("--tokens", type=int, default=64, help="distinct decode tokens cycled over")
-    p.add_argument("--cpu-sample", type=int, default=48, help="tokens the CPU oracle is timed on")
+    p.add_argument("--cpu-sample", type=int, default=1024, help="tokens the CPU oracle is timed on")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-dense", action="store_true")
     p.add_argument("--batch", type=int, default=0, help="decode batch of a stack workload (default: its first)")
@@ -66,6 +66,29 @@ def copy_probe(mib):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 5}))
+
+
+def counter_traffic(kernel, workload_tag):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy of known
+    size), or None when there is none or the kernel source has changed since
+    the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_tag}_counters.txt")
+    src = os.path.join(ROOT, "paper_2607_08991_amd", "csrc", "decode.hpp")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            k, sep, v = line.partition(":")
+            if sep:
+                fields[k.strip()] = v.strip()
+    with open(src, "rb") as f:
+        now = hashlib.sha256(f.read()).hexdigest()
+    if fields.get("kernel_source_sha256") != now or "traffic_bytes_per_launch" not in fields:
+        return None
+    return int(float(fields["traffic_bytes_per_launch"]))
 
 
 def thresholds_for(cfg):
@@ -311,7 +334,7 @@ def main():
     cpu = None
     if not args.no_cpu:
         log(f"[bench] timing the CPU oracle on {args.cpu_sample} tokens")
-        cpu = cpu_baseline(cfg, wnp, ts, xnp, args.cpu_sample)
+        cpu = cpu_baseline(cfg, wnp, ts, synth.decode_x(cfg, args.cpu_sample), args.cpu_sample)
 
     res = {
         "metric": METRIC,
@@ -345,7 +368,7 @@ def main():
         "kernels": kern,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(dom_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": None},
+                     "traffic": counter_traffic(dom, "c2_llama_layer_bf16") if cfg.index == 1 else None},
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

@@ -1,5 +1,6 @@
 // Host side of the C ABI declared in include/sats.h: argument checks,
 // workspace management, launch planning and kernel timing.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -48,20 +49,19 @@ struct Timer {
 std::mutex g_timer_mu;
 Timer g_timer[SATS_K_COUNT];
 
+// Start and stop events of one timed launch (null when its kind is not
+// armed).  They are handed to hipExtLaunchKernelGGL, which takes the
+// timestamps from the kernel's own dispatch, so the measured span is the
+// kernel's execution and not a separate marker's.
 struct TimedLaunch {
-  Timer *t = nullptr;
-  int slot = -1;
-  hipStream_t s;
-  TimedLaunch(int kind, hipStream_t stream) : s(stream) {
+  hipEvent_t start = nullptr, stop = nullptr;
+  TimedLaunch(int kind, hipStream_t) {
     Timer &tm = g_timer[kind];
     if (tm.armed && tm.used < tm.cap) {
-      t = &tm;
-      slot = tm.used++;
-      (void)hipEventRecord(tm.start[slot], s);
+      const int slot = tm.used++;
+      start = tm.start[slot];
+      stop = tm.stop[slot];
     }
-  }
-  ~TimedLaunch() {
-    if (t) (void)hipEventRecord(t->stop[slot], s);
   }
 };
 
@@ -339,7 +339,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       da.N = (int)d_ff;
       {
         TimedLaunch tl(SATS_K_DENSE, c.stream);
-        hipLaunchKernelGGL(dense_gateup_kernel, dim3(d_ff / kDenseNT), dim3(kThreads), 0, c.stream, da);
+        hipExtLaunchKernelGGL(dense_gateup_kernel, dim3(d_ff / kDenseNT), dim3(kThreads), 0, c.stream,
+                              tl.start, tl.stop, 0, da);
       }
       HIP_TRY(hipGetLastError());
       DenseArgs dd{};
@@ -352,7 +353,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       dd.kchunk = (int)(((d_ff + kDenseKsplit - 1) / kDenseKsplit + kDenseKT - 1) / kDenseKT * kDenseKT);
       {
         TimedLaunch tl(SATS_K_DENSE, c.stream);
-        hipLaunchKernelGGL(dense_down_kernel, dim3(d / kDenseNT, kDenseKsplit), dim3(kThreads), 0, c.stream, dd);
+        hipExtLaunchKernelGGL(dense_down_kernel, dim3(d / kDenseNT, kDenseKsplit), dim3(kThreads), 0, c.stream,
+                              tl.start, tl.stop, 0, dd);
       }
       HIP_TRY(hipGetLastError());
       GlueArgs ga{};
@@ -399,8 +401,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     const size_t gate_lds = sizeof(float) * std::max<size_t>((size_t)NT * p.KC, (size_t)p.RG * NT * p.CB);
     {
       TimedLaunch tl(SATS_K_GATE, c.stream);
-      hipLaunchKernelGGL((gate_kernel<T, VEC, NT>), dim3(p.nblocks, p.KS, tiles), dim3(kThreads),
-                         gate_lds, c.stream, g);
+      hipExtLaunchKernelGGL((gate_kernel<T, VEC, NT>), dim3(p.nblocks, p.KS, tiles), dim3(kThreads), gate_lds,
+                            c.stream, tl.start, tl.stop, 0, g);
     }
     HIP_TRY(hipGetLastError());
 
@@ -413,7 +415,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       ca.n = np;
       ca.d_ff = (int)d_ff;
       TimedLaunch tl(SATS_K_INSPECT, c.stream);
-      hipLaunchKernelGGL(compact_kernel, dim3(np), dim3(kThreads), 0, c.stream, ca);
+      hipExtLaunchKernelGGL(compact_kernel, dim3(np), dim3(kThreads), 0, c.stream, tl.start, tl.stop, 0, ca);
       HIP_TRY(hipGetLastError());
     }
 
@@ -436,8 +438,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     u.CB = p.CB;
     {
       TimedLaunch tl(SATS_K_UP, c.stream);
-      hipLaunchKernelGGL((up_kernel<T, VEC, NT>), dim3(p.up_grid, tiles), dim3(kThreads),
-                         sizeof(int) * (p.nblocks + 1), c.stream, u);
+      hipExtLaunchKernelGGL((up_kernel<T, VEC, NT>), dim3(p.up_grid, tiles), dim3(kThreads),
+                            sizeof(int) * (p.nblocks + 1), c.stream, tl.start, tl.stop, 0, u);
     }
     HIP_TRY(hipGetLastError());
 
@@ -460,8 +462,9 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     dn.n_slices = p.n_slices;
     {
       TimedLaunch tl(SATS_K_DOWN, c.stream);
-      hipLaunchKernelGGL((down_kernel<T, VEC, NT>), dim3(p.n_slices, p.KCH, tiles), dim3(kThreads),
-                         sizeof(float) * (size_t)(kThreads / p.CL) * NT * p.SW, c.stream, dn);
+      hipExtLaunchKernelGGL((down_kernel<T, VEC, NT>), dim3(p.n_slices, p.KCH, tiles), dim3(kThreads),
+                            sizeof(float) * (size_t)(kThreads / p.CL) * NT * p.SW, c.stream, tl.start, tl.stop, 0,
+                            dn);
     }
     HIP_TRY(hipGetLastError());
   }
@@ -499,17 +502,20 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   for (int l = 0; l < (int)c.L; ++l) {
     {
       TimedLaunch tl(SATS_K_DEC_GATE, c.stream);
-      hipLaunchKernelGGL((dec_gate_kernel<T>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream, a, l, dp.G);
+      hipExtLaunchKernelGGL((dec_gate_kernel<T>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream,
+                            tl.start, tl.stop, 0, a, l, dp.G);
     }
     HIP_TRY(hipGetLastError());
     {
       TimedLaunch tl(SATS_K_DEC_ROWS, c.stream);
-      hipLaunchKernelGGL((dec_rows_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream, a, l);
+      hipExtLaunchKernelGGL((dec_rows_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
+                            tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
     {
       TimedLaunch tl(SATS_K_DEC_REDUCE, c.stream);
-      hipLaunchKernelGGL((dec_reduce_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream, a, l);
+      hipExtLaunchKernelGGL((dec_reduce_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
+                            tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
   }
@@ -522,7 +528,7 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
       ca.n = 1;
       ca.d_ff = (int)c.d_ff;
       TimedLaunch tl(SATS_K_INSPECT, c.stream);
-      hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(kThreads), 0, c.stream, ca);
+      hipExtLaunchKernelGGL(compact_kernel, dim3(1), dim3(kThreads), 0, c.stream, tl.start, tl.stop, 0, ca);
       HIP_TRY(hipGetLastError());
     }
   }
