@@ -55,6 +55,8 @@ constexpr int kDecodeMaxG = 1024;  // rows / reduce workgroups (partials of y)
 
 // Columns of one gate column block (one 16-byte load per lane of a wavefront).
 template <typename T> constexpr int dec_block_cols() { return 64 * Elem<T>::kVec; }
+// Gate partials of one column are stored contiguously, padded to whole 16 bytes.
+__host__ __device__ constexpr int dec_nrcp(int nrc) { return (nrc + 3) & ~3; }
 
 struct DecodeArgs {
   const void *x;          // [d] call input (storage type)
@@ -66,10 +68,11 @@ struct DecodeArgs {
   int route_mode;
   int L, d, d_ff;
   int nblk, nrc;          // gate tiles: column blocks x row chunks
-  float *gpart;           // [nrc][d_ff]    partial a of each row chunk
+  float *gpart;           // [d_ff][nrcp]   partial a of each row chunk (nrcp = nrc rounded up to 4)
   float *ypart;           // [G][d]         per-workgroup partial y
   float *ybuf;            // [d]
-  float *sspart;          // [G]
+  float *sspart;          // [RW]           per-reduce-workgroup sums of y^2
+  int G, RW;              // rows workgroups (partials of y), reduce workgroups
   int *state;             // [1] the token's route (1: base path), set by the layer-0 gate launch
   uint8_t *route_out;     // optional [1]
   uint8_t *keep_out;      // optional [L][d_ff]
@@ -103,9 +106,36 @@ __device__ __forceinline__ void store_coherent4(__amdgpu_buffer_rsrc_t r, uint32
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t weight_rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
 }
+// Byte offset that is out of range of every buffer here (all are smaller
+// than 2 GB): a buffer load at it returns zeros without a memory access.
+constexpr uint32_t kOffNone = 0x80000000u;
+
 // 16 bytes at base + soff + voff, not kept in the caches (streamed once).
 __device__ __forceinline__ u32x4 load_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 2);
+}
+
+// Sum of the nrc gate partials of column `col`, in row-chunk order: 16 bytes
+// per load, written through by the gate launch and read from the
+// device-coherent level.
+__device__ __forceinline__ float gate_sum(__amdgpu_buffer_rsrc_t gp, int col, int nrc) {
+  const int nq = dec_nrcp(nrc) / 4;
+  const uint32_t base = (uint32_t)col * (uint32_t)(nq * 16);
+  float s = 0.0f;
+  for (int q0 = 0; q0 < nq; q0 += 4) {
+    f32x4 v[4];  // up to 16 partials in flight
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t off = (q0 + i < nq) ? base + (uint32_t)((q0 + i) * 16) : kOffNone;
+      v[i] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gp, (int)off, 0, 16 /* coherent */));
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if ((q0 + i) * 4 + j < nrc) s += v[i][j];
+  }
+  return s;
 }
 
 // Sums of R values over the 64 lanes of a wavefront (R a power of two),
@@ -147,7 +177,8 @@ struct InputRegs {
 };
 
 template <typename T, int THREADS>
-__device__ __forceinline__ void dec_input_issue(const DecodeArgs &a, int l, int G, InputRegs<THREADS> &r) {
+__device__ __forceinline__ void dec_input_issue(const DecodeArgs &a, int l, InputRegs<THREADS> &r) {
+  const int G = a.RW;  // slice sums of squares of the previous layer's reduce
   constexpr int VEC = Elem<T>::kVec;
   const int tid = threadIdx.x, d = a.d;
   // every field gets a value on both branches: finish() passes all of them
@@ -249,7 +280,7 @@ __device__ __forceinline__ void gate_consume(const DecodeSmem &sm, int k0w, int 
 // t % nblk, row chunk t / nblk); forms h in LDS before the first tile's
 // products (its loads follow the tile's first weight loads).
 template <typename T>
-__device__ void dec_gate(const DecodeArgs &a, int l, int G, DecodeSmem &sm, bool record) {
+__device__ void dec_gate(const DecodeArgs &a, int l, DecodeSmem &sm, bool record) {
   constexpr int THREADS = kGateThreads, VEC = Elem<T>::kVec, NW = THREADS / 64;
   constexpr int CB = dec_block_cols<T>();
   constexpr int GB = kGateBatch;
@@ -279,7 +310,7 @@ __device__ void dec_gate(const DecodeArgs &a, int l, int G, DecodeSmem &sm, bool
     u32x4 q[GB];
     if (live) gate_issue<T, GB, NW>(wr, row0, stride, 0, nr, lo, q);
     if (!have_input) {  // h is needed from the first batch on; its loads follow the weights'
-      dec_input_issue<T, THREADS>(a, l, G, ir);
+      dec_input_issue<T, THREADS>(a, l, ir);
       dec_input_finish<T, THREADS>(a, l, ir, sm, record);
       have_input = true;
       if (l == 0) SATS_TRACE_POINT(1);
@@ -298,7 +329,7 @@ __device__ void dec_gate(const DecodeArgs &a, int l, int G, DecodeSmem &sm, bool
       float s = 0.0f;
 #pragma unroll
       for (int q2 = 0; q2 < NW; ++q2) s += sm.red[q2 * CB + tid];
-      store_coherent(a.gpart + (size_t)rc * d_ff + cb * CB + tid, s);
+      store_coherent(a.gpart + (size_t)(cb * CB + tid) * dec_nrcp(a.nrc) + rc, s);
     }
     __syncthreads();  // LDS reuse by the next tile
   }
@@ -396,9 +427,11 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
   const float thr = base ? 0.0f : a.thr[l];
   const __amdgpu_buffer_rsrc_t Wu = weight_rsrc(static_cast<const T *>(a.Wu) + (size_t)l * wl, (uint32_t)(wl * sizeof(T)));
   const __amdgpu_buffer_rsrc_t Wd = weight_rsrc(static_cast<const T *>(a.Wd) + (size_t)l * wl, (uint32_t)(wl * sizeof(T)));
+  const __amdgpu_buffer_rsrc_t gp =
+      weight_rsrc(a.gpart, (uint32_t)((size_t)d_ff * dec_nrcp(a.nrc) * sizeof(float)));
 
   InputRegs<kDecodeThreads> ir;
-  dec_input_issue<T, kDecodeThreads>(a, l, G, ir);
+  dec_input_issue<T, kDecodeThreads>(a, l, ir);
   float hreg[NCH][VEC];  // h at this lane's columns
   float yacc[NCH][VEC];
 #pragma unroll
@@ -414,7 +447,7 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
     bool keep = false;
     float g = 0.0f;
     if (tid < CB && gcol < d_ff) {
-      g = silu(sum_coherent(a.gpart + gcol, (size_t)d_ff, a.nrc));
+      g = silu(gate_sum(gp, gcol, a.nrc));
       keep = base || (fabsf(g) >= thr);
       if (sub == 0 && a.keep_out) a.keep_out[(size_t)l * d_ff + gcol] = (uint8_t)keep;
     }
@@ -488,13 +521,14 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
 
 // ------------------------------------------------------------------ reduce
 
-// Workgroup w's slice of columns: y = sum of the G partials in workgroup order.
+// Workgroup w (of RW) and its slice of columns: y = sum of the G partials
+// in workgroup order.
 template <typename T>
-__device__ void dec_reduce(const DecodeArgs &a, int l, int G, int w, DecodeSmem &sm) {
+__device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm) {
   constexpr int THREADS = kDecodeThreads, NW = kDecodeWaves;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int d = a.d;
-  const int cpw = (d + G - 1) / G;  // columns of this workgroup (<= THREADS)
+  const int d = a.d, G = a.G;
+  const int cpw = (d + a.RW - 1) / a.RW;  // columns of this workgroup (<= THREADS)
   const int cw0 = w * cpw;
   const int nc = max(0, min(cpw, d - cw0));
   const int ngr = THREADS / cpw;    // partial groups
@@ -523,9 +557,9 @@ __device__ void dec_reduce(const DecodeArgs &a, int l, int G, int w, DecodeSmem 
 
 // ------------------------------------------------------------------ kernels
 
-// Gate tiles (any grid; G = the number of partials of the previous layer's y).
+// Gate tiles (any grid).
 template <typename T>
-__global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, int l, int G) {
+__global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
   if (l == 0 && blockIdx.x == 0 && threadIdx.x == 0) {
     const int base = token_is_base(a.route_mode, a.ids, a.lut, 0);
@@ -533,23 +567,23 @@ __global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, in
     if (a.route_out) a.route_out[0] = (uint8_t)base;
   }
   if (l == 0) SATS_TRACE_POINT(0);
-  dec_gate<T>(a, l, G, sm, a.layer_in != nullptr && blockIdx.x == 0);
+  dec_gate<T>(a, l, sm, a.layer_in != nullptr && blockIdx.x == 0);
   if (l == 0) SATS_TRACE_POINT(2);
 }
 
-// Rows and reduce: G workgroups each.
+// Rows: G workgroups; reduce: RW workgroups.
 template <typename T>
 __global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
   if (l == 0) SATS_TRACE_POINT(3);
-  dec_rows<T>(a, l, a.state[0], gridDim.x, blockIdx.x, sm);
+  dec_rows<T>(a, l, a.state[0], a.G, blockIdx.x, sm);
 }
 
 template <typename T>
 __global__ __launch_bounds__(kDecodeThreads) void dec_reduce_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
   if (l == 0) SATS_TRACE_POINT(6);
-  dec_reduce<T>(a, l, gridDim.x, blockIdx.x, sm);
+  dec_reduce<T>(a, l, blockIdx.x, sm);
   if (l == 0) SATS_TRACE_POINT(7);
 }
 

@@ -149,7 +149,8 @@ struct Buffers {
 // Layout for passes of up to `pass` tokens (the counters live in their own
 // zero-initialised allocation).
 struct DecodePlan {
-  int G = 0;           // rows / reduce workgroups, one partial y each (0: path not used)
+  int G = 0;           // rows workgroups, one partial y each (0: path not used)
+  int RW = 0;          // reduce workgroups (128-byte column slices where d allows)
   int nblk = 0;        // gate column blocks
   int nrc = 0;         // gate row chunks
   int gate_grid = 0;   // workgroups of the gate launch
@@ -175,7 +176,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.blk_mask = c.take<uint32_t>(tiles * d_ff);
   t.keep = c.take<uint8_t>(std::max(Pp, L) * d_ff);
   t.ypart = c.take<float>((int64_t)dp.G * d);
-  t.sspart = c.take<float>(dp.G);
+  t.sspart = c.take<float>(std::max(dp.G, dp.RW));
   t.perm = c.take<int>(Pp);
   t.ctl = c.take<int>(64);
   t.skip = c.take<uint8_t>(Pp);
@@ -184,7 +185,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.hnext = c.take<uint16_t>(Pp * d);
   t.pdense = c.take<uint16_t>(Pp * d_ff);
   t.ddpart = c.take<float>((int64_t)kDenseKsplit * Pp * d);
-  t.dgpart = c.take<float>((int64_t)dp.nrc * d_ff);
+  t.dgpart = c.take<float>((int64_t)sats::dec_nrcp(dp.nrc) * d_ff);
   t.dstate = c.take<int>(64);
   if (b) *b = t;
   return c.off;
@@ -262,8 +263,10 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp) {
   nrc = std::min<int64_t>(nrc, std::max<int64_t>(1, d / (sats::kGateThreads / 64)));  // a row per wavefront
   q.nrc = (int)nrc;
   q.gate_grid = q.nblk * q.nrc;
+  // reduce: 32 columns (128 bytes of each partial) per workgroup
+  q.RW = (int)std::min<int64_t>(sats::kDecodeMaxG, std::max<int64_t>(1, (d + 31) / 32));
   const bool ok = G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
-                  (d + G - 1) / G <= sats::kDecodeThreads;
+                  (d + q.RW - 1) / q.RW <= sats::kDecodeThreads;
   *dp = ok ? q : DecodePlan{};
   return ok;
 }
@@ -491,6 +494,8 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   a.nrc = dp.nrc;
   a.gpart = b.dgpart;
   a.state = b.dstate;
+  a.G = dp.G;
+  a.RW = dp.RW;
   a.ypart = b.ypart;
   a.ybuf = b.ybuf;
   a.sspart = b.sspart;
@@ -503,7 +508,7 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
     {
       TimedLaunch tl(SATS_K_DEC_GATE, c.stream);
       hipExtLaunchKernelGGL((dec_gate_kernel<T>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream,
-                            tl.start, tl.stop, 0, a, l, dp.G);
+                            tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
     {
@@ -514,7 +519,7 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
     HIP_TRY(hipGetLastError());
     {
       TimedLaunch tl(SATS_K_DEC_REDUCE, c.stream);
-      hipExtLaunchKernelGGL((dec_reduce_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
+      hipExtLaunchKernelGGL((dec_reduce_kernel<T>), dim3(dp.RW), dim3(kDecodeThreads), 0, c.stream,
                             tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
