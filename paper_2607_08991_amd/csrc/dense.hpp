@@ -24,8 +24,8 @@
 // MFMA operand layout of v_mfma_f32_16x16x32_bf16 (wavefront of 64 lanes):
 // lane l supplies A[l % 16][8 (l / 16) + e] and B[8 (l / 16) + e][l % 16],
 // e = 0..7, and receives C[4 (l / 16) + r][l % 16], r = 0..3.  W_gate and
-// W_down are stored with the output dimension contiguous, so their tiles are
-// staged through LDS and read back k-major; W_up_T rows are already k-major.
+// W_down are stored with the output dimension contiguous, so their operands
+// are read from LDS transposed; W_up_T and H rows are already k-major.
 #pragma once
 
 #include "kernels.hpp"
@@ -35,8 +35,6 @@ namespace sats {
 constexpr int kMfmaMinTokens = 8;   // dense group size from which MFMA is used
 constexpr int kDenseMaxTokens = 64; // tokens of one pass (four 16-row MFMA tiles)
 constexpr int kDenseNT = 64;        // output columns per workgroup
-constexpr int kDenseKT = 32;        // k per MFMA step
-constexpr int kLdsPitch = 66;       // bf16 per staged row (132 bytes: conflict-free k-major reads)
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
@@ -112,120 +110,238 @@ struct DenseArgs {
   int K, N, kchunk;       // reduction length, output columns, k per split (down)
 };
 
-// One 32 x 64 tile of a row-major [K][N] bf16 matrix, staged into LDS with a
-// 132-byte row pitch.  Thread t copies row t / 8, columns 8 (t % 8) .. + 8.
-__device__ __forceinline__ u32x4 tile_load(const uint16_t *W, int N, int k0, int n0) {
-  const int t = threadIdx.x;
-  return __builtin_nontemporal_load(
-      reinterpret_cast<const u32x4 *>(W + (size_t)(k0 + t / 8) * N + n0 + 8 * (t % 8)));
+// ---------------------------------------------------------------- MFMA GEMMs
+//
+// Both products stream a weight matrix once and reuse each weight over the
+// rows of the group, so they are bound by HBM, not by the matrix cores: what
+// matters is how many bytes each workgroup keeps in flight.  A workgroup of
+// 512 threads owns 64 output columns and walks its k range in stages of 64
+// rows.  Every thread issues 16-byte buffer loads for kDenseStages stages
+// ahead into registers (weights streamed past the caches, the small left
+// operand H cached), and each stage is copied into one of two LDS buffers,
+// one barrier per stage, before the wavefronts read their MFMA operands.
+//
+// LDS tiles are 64 rows of 128 bytes (eight 16-byte chunks per row):
+//   k-row tile   W_gate / W_down rows k0..k0+63, columns n0..n0+63
+//   row tile     W_up_T rows n0..n0+63 or H rows 0..63, entries k0..k0+63
+// Chunks are stored at a swizzled position so that the operand reads below
+// touch 64 distinct banks: chunk q of row r sits at q ^ (2 ((r >> 3) & 3)) in
+// a k-row tile and at q ^ ((r >> 1) & 7) in a row tile.
+
+constexpr int kDenseThreads = 512;            // 8 wavefronts
+constexpr int kDenseKC = 64;                  // k rows per stage
+constexpr int kDenseTileBytes = 64 * 128;     // one LDS tile
+constexpr int kDenseXPitch = 68;              // floats per row of the epilogue exchange tile
+
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t dense_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
 }
-__device__ __forceinline__ void tile_store(uint32_t *lds, const u32x4 &v) {
-  const int t = threadIdx.x;
-  uint32_t *p = lds + (t / 8) * (kLdsPitch / 2) + 4 * (t % 8);
-  p[0] = v.x;
-  p[1] = v.y;
-  p[2] = v.z;
-  p[3] = v.w;
+constexpr uint32_t kDenseOffNone = 0x80000000u;  // past every buffer: the load returns zeros
+// 16 bytes streamed once (weights) / kept in the caches (H, read by every workgroup)
+__device__ __forceinline__ u32x4 dense_load_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2);
 }
-// k-major operand of column c (0..63) of the staged tile: rows 8 g .. 8 g + 7
-__device__ __forceinline__ bf16x8 tile_operand(const uint32_t *lds, int c, int g) {
-  const uint16_t *p = reinterpret_cast<const uint16_t *>(lds);
+__device__ __forceinline__ u32x4 dense_load_cached(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+}
+
+__device__ __forceinline__ int krow_pos(int r, int q) { return q ^ (2 * ((r >> 3) & 3)); }
+__device__ __forceinline__ int row_pos(int r, int q) { return q ^ ((r >> 1) & 7); }
+
+__device__ __forceinline__ void lds_put16(uint8_t *tile, int r, int pos, const u32x4 &v) {
+  *reinterpret_cast<u32x4 *>(tile + r * 128 + pos * 16) = v;
+}
+
+// MFMA operand from a row tile: row `r`, k = 32 j + 8 g .. + 7 of the stage
+__device__ __forceinline__ bf16x8 row_operand(const uint8_t *tile, int r, int j, int g) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(tile + r * 128 + row_pos(r, 4 * j + g) * 16));
+}
+// MFMA operand from a k-row tile: column c, k = 32 j + 8 g .. + 7 (a transposed
+// read, one 16-bit entry per row)
+__device__ __forceinline__ bf16x8 krow_operand(const uint8_t *tile, int c, int j, int g) {
+  const uint16_t *p = reinterpret_cast<const uint16_t *>(tile);
   bf16x8 b;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) b[e] = __builtin_bit_cast(__bf16, p[(8 * g + e) * kLdsPitch + c]);
+  for (int e = 0; e < 8; ++e) {
+    const int r = 32 * j + 8 * g + e;
+    b[e] = __builtin_bit_cast(__bf16, p[r * 64 + krow_pos(r, c >> 3) * 8 + (c & 7)]);
+  }
   return b;
 }
-__device__ __forceinline__ bf16x8 load_k8(const uint16_t *p) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
+
+// p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every row of
+// the group.  Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
+// MT 16-row tiles cover the group (rows past it are read as zeros).
+template <int STAGES, int MT>
+__global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a) {
+  static_assert(STAGES % 2 == 0, "stage buffers alternate");
+  if (!a.ctl[1]) return;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * 3 * kDenseTileBytes];
+  const int nd = min(a.ctl[0], 16 * MT);
+  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int mat = wv >> 2, c = 16 * (wv & 3) + (lane & 15), g = lane >> 4;
+  const int n0 = blockIdx.x * kDenseNT;
+  const int K = a.K, N = a.N;
+  const int S = K / kDenseKC;
+  const __amdgpu_buffer_rsrc_t rg = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t ru = dense_rsrc(a.Wt, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t rh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
+  // this thread's 16-byte piece of each tile: row lr, chunk lq
+  const int lr = tid >> 3, lq = tid & 7;
+  const uint32_t og = (uint32_t)(((size_t)lr * N + n0 + 8 * lq) * 2);
+  const uint32_t ou = (uint32_t)(((size_t)(n0 + lr) * K + 8 * lq) * 2);
+  const uint32_t oh = (uint32_t)(((size_t)lr * K + 8 * lq) * 2);
+  const uint32_t sg = (uint32_t)kDenseKC * N * 2, sk = (uint32_t)kDenseKC * 2;  // per stage
+  const bool hrow = lr < nd;
+  u32x4 bw[STAGES], bu[STAGES], bh[STAGES];
+#pragma unroll
+  for (int p = 0; p < STAGES; ++p) {
+    const bool v = p < S;
+    bw[p] = dense_load_stream(rg, v ? og + p * sg : kDenseOffNone);
+    bu[p] = dense_load_stream(ru, v ? ou + p * sk : kDenseOffNone);
+    bh[p] = dense_load_cached(rh, v && hrow ? oh + p * sk : kDenseOffNone);
+    __builtin_amdgcn_sched_barrier(0);  // issue in stage order: the waits below count on it
+  }
+  f32x4v acc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  const int SR = (S + STAGES - 1) / STAGES * STAGES;
+  for (int s0 = 0; s0 < SR; s0 += STAGES) {
+#pragma unroll
+    for (int p = 0; p < STAGES; ++p) {
+      uint8_t *tg = lds + (p & 1) * 3 * kDenseTileBytes, *tu = tg + kDenseTileBytes, *th = tu + kDenseTileBytes;
+      lds_put16(tg, lr, krow_pos(lr, lq), bw[p]);
+      lds_put16(tu, lr, row_pos(lr, lq), bu[p]);
+      lds_put16(th, lr, row_pos(lr, lq), bh[p]);
+      const int sn = s0 + p + STAGES;
+      const bool v = sn < S;
+      bw[p] = dense_load_stream(rg, v ? og + (uint32_t)sn * sg : kDenseOffNone);
+      bu[p] = dense_load_stream(ru, v ? ou + (uint32_t)sn * sk : kDenseOffNone);
+      bh[p] = dense_load_cached(rh, v && hrow ? oh + (uint32_t)sn * sk : kDenseOffNone);
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const bf16x8 b = mat == 0 ? krow_operand(tg, c, j, g) : row_operand(tu, c, j, g);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(row_operand(th, 16 * mt + (lane & 15), j, g), b, acc[mt],
+                                                            0, 0, 0);
+      }
+    }
+  }
+  // epilogue: SiLU(a) through LDS to the W_up wavefronts, p through LDS to
+  // 16-byte row stores
+  __syncthreads();
+  float *xs = reinterpret_cast<float *>(lds);
+  uint16_t *pt = reinterpret_cast<uint16_t *>(lds + 64 * kDenseXPitch * 4);
+  if (mat == 0) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * kDenseXPitch + c] = silu(acc[mt][r]);
+  }
+  __syncthreads();
+  if (mat == 1) {
+    const float thr = a.thr ? *a.thr : 0.0f;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = 16 * mt + 4 * g + r;
+        if (m < nd) {
+          const float gv = xs[m * kDenseXPitch + c];
+          const bool keep = a.gbase[m] || fabsf(gv) >= thr;  // Eq. 4-5; every column on the base path
+          pt[m * 64 + c] = keep ? f32_to_bf16(gv * acc[mt][r]) : (uint16_t)0;
+          if (a.keep_out) a.keep_out[(size_t)a.perm[m] * N + n0 + c] = (uint8_t)keep;
+        }
+      }
+  }
+  __syncthreads();
+  if (lr < nd)
+    *reinterpret_cast<u32x4 *>(a.P + (size_t)lr * N + n0 + 8 * lq) = *reinterpret_cast<const u32x4 *>(pt + lr * 64 + 8 * lq);
 }
 
-// p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every dense token
-__global__ __launch_bounds__(kThreads) void dense_gateup_kernel(DenseArgs a) {
+// partial y over k chunk blockIdx.y for 64 output columns (blockIdx.x).
+// Wavefronts w and w + 4 take the two 32-row halves of each stage for the
+// same 16 columns; their sums are added in LDS at the end.
+template <int STAGES, int MT>
+__global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) {
+  static_assert(STAGES % 2 == 0, "stage buffers alternate");
   if (!a.ctl[1]) return;
-  __shared__ uint32_t lds[kDenseKT * kLdsPitch / 2];
-  const int nd = a.ctl[0];
-  const int mtiles = (nd + 15) / 16;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, g = lane / 16;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * 2 * kDenseTileBytes];
+  const int nd = min(a.ctl[0], 16 * MT);
+  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int jh = wv >> 2, c = 16 * (wv & 3) + (lane & 15), g = lane >> 4;
   const int n0 = blockIdx.x * kDenseNT;
-  const int ncol = n0 + 16 * wv + (lane % 16);
-  typedef float f4 __attribute__((ext_vector_type(4)));
-  f4 accg[4], accu[4];
+  const int K = a.K, N = a.N;
+  const int kb = blockIdx.y * a.kchunk, ke = min(K, kb + a.kchunk);
+  const int S = ke > kb ? (ke - kb) / kDenseKC : 0;
+  const __amdgpu_buffer_rsrc_t rw = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t rh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
+  const int lr = tid >> 3, lq = tid & 7;
+  const uint32_t ow = (uint32_t)(((size_t)(kb + lr) * N + n0 + 8 * lq) * 2);
+  const uint32_t oh = (uint32_t)(((size_t)lr * K + kb + 8 * lq) * 2);
+  const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = (uint32_t)kDenseKC * 2;
+  const bool hrow = lr < nd;
+  u32x4 bw[STAGES], bh[STAGES];
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) accg[mt] = accu[mt] = f4{0.f, 0.f, 0.f, 0.f};
-  u32x4 next = tile_load(a.Wb, a.N, 0, n0);
-  for (int k0 = 0; k0 < a.K; k0 += kDenseKT) {
-    __syncthreads();
-    tile_store(lds, next);
-    __syncthreads();
-    if (k0 + kDenseKT < a.K) next = tile_load(a.Wb, a.N, k0 + kDenseKT, n0);
-    const bf16x8 bg = tile_operand(lds, 16 * wv + (lane % 16), g);
-    const bf16x8 bu = load_k8(a.Wt + (size_t)ncol * a.K + k0 + 8 * g);
+  for (int p = 0; p < STAGES; ++p) {
+    const bool v = p < S;
+    bw[p] = dense_load_stream(rw, v ? ow + p * sw : kDenseOffNone);
+    bh[p] = dense_load_cached(rh, v && hrow ? oh + p * sk : kDenseOffNone);
+    __builtin_amdgcn_sched_barrier(0);  // issue in stage order: the waits below count on it
+  }
+  f32x4v acc[MT];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      if (mt < mtiles) {
-        const int m = 16 * mt + (lane % 16);
-        bf16x8 av = load_k8(a.H + (size_t)min(m, nd - 1) * a.K + k0 + 8 * g);
-        if (m >= nd) av = bf16x8{};
-        accg[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bg, accg[mt], 0, 0, 0);
-        accu[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bu, accu[mt], 0, 0, 0);
-      }
+  for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  const int SR = (S + STAGES - 1) / STAGES * STAGES;
+  for (int s0 = 0; s0 < SR; s0 += STAGES) {
+#pragma unroll
+    for (int p = 0; p < STAGES; ++p) {
+      uint8_t *tw = lds + (p & 1) * 2 * kDenseTileBytes, *th = tw + kDenseTileBytes;
+      lds_put16(tw, lr, krow_pos(lr, lq), bw[p]);
+      lds_put16(th, lr, row_pos(lr, lq), bh[p]);
+      const int sn = s0 + p + STAGES;
+      const bool v = sn < S;
+      bw[p] = dense_load_stream(rw, v ? ow + (uint32_t)sn * sw : kDenseOffNone);
+      bh[p] = dense_load_cached(rh, v && hrow ? oh + (uint32_t)sn * sk : kDenseOffNone);
+      __syncthreads();
+      const bf16x8 b = krow_operand(tw, c, jh, g);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(row_operand(th, 16 * mt + (lane & 15), jh, g), b, acc[mt],
+                                                          0, 0, 0);
     }
   }
-  const float thr = a.thr ? *a.thr : 0.0f;
+  __syncthreads();
+  float *xs = reinterpret_cast<float *>(lds);
+  if (jh == 1) {
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * mt + 4 * g + r;
-      if (mt < mtiles && m < nd) {
-        const float gv = silu(accg[mt][r]);
-        const bool keep = a.gbase[m] || fabsf(gv) >= thr;  // Eq. 4-5; every column on the base path
-        a.P[(size_t)m * a.N + ncol] = keep ? f32_to_bf16(gv * accu[mt][r]) : (uint16_t)0;
-        if (a.keep_out) a.keep_out[(size_t)a.perm[m] * a.N + ncol] = (uint8_t)keep;
-      }
-    }
+      for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * kDenseXPitch + c] = acc[mt][r];
   }
-}
-
-// partial y over k chunk blockIdx.y for 64 output columns (blockIdx.x)
-__global__ __launch_bounds__(kThreads) void dense_down_kernel(DenseArgs a) {
-  if (!a.ctl[1]) return;
-  __shared__ uint32_t lds[kDenseKT * kLdsPitch / 2];
-  const int nd = a.ctl[0];
-  const int mtiles = (nd + 15) / 16;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, g = lane / 16;
-  const int n0 = blockIdx.x * kDenseNT;
-  const int ncol = n0 + 16 * wv + (lane % 16);
-  const int kb = blockIdx.y * a.kchunk, ke = min(a.K, kb + a.kchunk);
-  typedef float f4 __attribute__((ext_vector_type(4)));
-  f4 acc[4];
+  __syncthreads();
+  if (jh == 0) {
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) acc[mt] = f4{0.f, 0.f, 0.f, 0.f};
-  u32x4 next = u32x4{0u, 0u, 0u, 0u};
-  if (kb < ke) next = tile_load(a.Wb, a.N, kb, n0);
-  for (int k0 = kb; k0 < ke; k0 += kDenseKT) {
-    __syncthreads();
-    tile_store(lds, next);
-    __syncthreads();
-    if (k0 + kDenseKT < ke) next = tile_load(a.Wb, a.N, k0 + kDenseKT, n0);
-    const bf16x8 b = tile_operand(lds, 16 * wv + (lane % 16), g);
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      if (mt < mtiles) {
-        const int m = 16 * mt + (lane % 16);
-        bf16x8 av = load_k8(a.H + (size_t)min(m, nd - 1) * a.K + k0 + 8 * g);
-        if (m >= nd) av = bf16x8{};
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, b, acc[mt], 0, 0, 0);
+      for (int r = 0; r < 4; ++r) {
+        float *q = xs + (16 * mt + 4 * g + r) * kDenseXPitch + c;
+        *q = acc[mt][r] + *q;
       }
-    }
   }
+  __syncthreads();
+  // 16 MT rows x 16 chunks of 4 floats
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = 16 * mt + 4 * g + r;
-      if (mt < mtiles && m < nd) a.part[((size_t)blockIdx.y * nd + m) * a.N + ncol] = acc[mt][r];
-    }
+  for (int i = 0; i < (MT + 1) / 2; ++i) {
+    const int e = tid + i * kDenseThreads, m = e >> 4, q = e & 15;
+    if (m < nd)
+      *reinterpret_cast<f32x4v *>(a.part + ((size_t)blockIdx.y * nd + m) * N + n0 + 4 * q) =
+          *reinterpret_cast<const f32x4v *>(xs + m * kDenseXPitch + 4 * q);
+  }
 }
 
 struct GlueArgs {

@@ -69,6 +69,27 @@ struct TimedLaunch {
 
 constexpr int kMaxPass = 64;  // tokens per pass through the layers
 constexpr int kDenseKsplit = 4;  // d_ff chunks of the dense group's down-projection
+constexpr int kDenseGateUpStages = 8;  // stages in flight per thread: 3 loads each
+constexpr int kDenseDownStages = 12;   // 2 loads each
+
+// MFMA kernels specialised on the 16-row tiles that cover a pass of np tokens
+typedef void (*DenseKernel)(sats::DenseArgs);
+DenseKernel dense_gateup_fn(int np) {
+  using namespace sats;
+  const int mt = (np + 15) / 16;
+  return mt <= 1 ? dense_gateup_kernel<kDenseGateUpStages, 1>
+         : mt == 2 ? dense_gateup_kernel<kDenseGateUpStages, 2>
+         : mt == 3 ? dense_gateup_kernel<kDenseGateUpStages, 3>
+                   : dense_gateup_kernel<kDenseGateUpStages, 4>;
+}
+DenseKernel dense_down_fn(int np) {
+  using namespace sats;
+  const int mt = (np + 15) / 16;
+  return mt <= 1 ? dense_down_kernel<kDenseDownStages, 1>
+         : mt == 2 ? dense_down_kernel<kDenseDownStages, 2>
+         : mt == 3 ? dense_down_kernel<kDenseDownStages, 3>
+                   : dense_down_kernel<kDenseDownStages, 4>;
+}
 
 int round_pow2_down(int v) {
   int p = 1;
@@ -302,8 +323,13 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
 
   // routing for the pass: partition, dense-group size and whether MFMA takes it
   const bool mfma = sizeof(T) == 2 && VEC > 1 && np >= kMfmaMinTokens &&
-                    d % kDenseKT == 0 && d_ff % kDenseNT == 0 && d % kDenseNT == 0 && d <= 4096 &&
+                    d % kDenseKC == 0 && d_ff % kDenseKC == 0 && d <= 4096 &&
+                    (uint64_t)d * d_ff * 2 < (1ull << 31) &&
                     !getenv("SATS_NO_MFMA");
+  // whole batch on MFMA (each row applies its own keep rule): known here, so
+  // the compacted sparse-path launches are left out
+  const bool whole = !getenv("SATS_MFMA_BASE_GROUP_ONLY");
+  const bool all_mfma = mfma && whole;
   {
     RouteArgs ra{};
     ra.ids = c.ids ? c.ids + base : nullptr;
@@ -320,7 +346,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     ra.layer_in0 = c.layer_in ? static_cast<uint16_t *>(c.layer_in) + base * d : nullptr;
     ra.gbase = b.gbase;
     ra.mfma = mfma ? 1 : 0;
-    ra.whole = getenv("SATS_MFMA_BASE_GROUP_ONLY") ? 0 : 1;
+    ra.whole = whole ? 1 : 0;
     hipLaunchKernelGGL(route_kernel, dim3(1), dim3(kThreads), 0, c.stream, ra);
     HIP_TRY(hipGetLastError());
   }
@@ -342,7 +368,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       da.N = (int)d_ff;
       {
         TimedLaunch tl(SATS_K_DENSE, c.stream);
-        hipExtLaunchKernelGGL(dense_gateup_kernel, dim3(d_ff / kDenseNT), dim3(kThreads), 0, c.stream,
+        hipExtLaunchKernelGGL(dense_gateup_fn(np), dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, c.stream,
                               tl.start, tl.stop, 0, da);
       }
       HIP_TRY(hipGetLastError());
@@ -353,10 +379,10 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       dd.part = b.ddpart;
       dd.K = (int)d_ff;
       dd.N = (int)d;
-      dd.kchunk = (int)(((d_ff + kDenseKsplit - 1) / kDenseKsplit + kDenseKT - 1) / kDenseKT * kDenseKT);
+      dd.kchunk = (int)(((d_ff + kDenseKsplit - 1) / kDenseKsplit + kDenseKC - 1) / kDenseKC * kDenseKC);
       {
         TimedLaunch tl(SATS_K_DENSE, c.stream);
-        hipExtLaunchKernelGGL(dense_down_kernel, dim3(d / kDenseNT, kDenseKsplit), dim3(kThreads), 0, c.stream,
+        hipExtLaunchKernelGGL(dense_down_fn(np), dim3(d / kDenseNT, kDenseKsplit), dim3(kDenseThreads), 0, c.stream,
                               tl.start, tl.stop, 0, dd);
       }
       HIP_TRY(hipGetLastError());
@@ -372,6 +398,23 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
                                                  : nullptr;
       hipLaunchKernelGGL(dense_glue_kernel, dim3(np), dim3(kThreads), 0, c.stream, ga);
       HIP_TRY(hipGetLastError());
+    }
+    auto compact = [&]() -> int {
+      CompactArgs ca{};
+      ca.keep = b.keep;
+      ca.skip = b.skip;
+      ca.idx = c.active_idx ? c.active_idx + (l * c.n + base) * d_ff : nullptr;
+      ca.count = c.active_count ? c.active_count + l * c.n + base : nullptr;
+      ca.n = np;
+      ca.d_ff = (int)d_ff;
+      TimedLaunch tl(SATS_K_INSPECT, c.stream);
+      hipExtLaunchKernelGGL(compact_kernel, dim3(np), dim3(kThreads), 0, c.stream, tl.start, tl.stop, 0, ca);
+      HIP_TRY(hipGetLastError());
+      return SATS_OK;
+    };
+    if (all_mfma) {
+      if (inspect_lists && compact() != SATS_OK) return SATS_ERR_HIP;
+      continue;
     }
     GateArgs g{};
     g.W = static_cast<const T *>(c.Wg) + l * wl;
@@ -409,18 +452,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     }
     HIP_TRY(hipGetLastError());
 
-    if (inspect_lists) {
-      CompactArgs ca{};
-      ca.keep = b.keep;
-      ca.skip = b.skip;
-      ca.idx = c.active_idx ? c.active_idx + (l * c.n + base) * d_ff : nullptr;
-      ca.count = c.active_count ? c.active_count + l * c.n + base : nullptr;
-      ca.n = np;
-      ca.d_ff = (int)d_ff;
-      TimedLaunch tl(SATS_K_INSPECT, c.stream);
-      hipExtLaunchKernelGGL(compact_kernel, dim3(np), dim3(kThreads), 0, c.stream, tl.start, tl.stop, 0, ca);
-      HIP_TRY(hipGetLastError());
-    }
+    if (inspect_lists && compact() != SATS_OK) return SATS_ERR_HIP;
 
     UpArgs u{};
     u.W = static_cast<const T *>(c.Wu) + l * wl;
