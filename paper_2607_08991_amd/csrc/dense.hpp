@@ -34,7 +34,9 @@ namespace sats {
 
 constexpr int kMfmaMinTokens = 8;   // dense group size from which MFMA is used
 constexpr int kDenseMaxTokens = 64; // tokens of one pass (four 16-row MFMA tiles)
-constexpr int kDenseNT = 64;        // output columns per workgroup
+constexpr int kDenseNT = 64;        // output columns per workgroup (gate/up)
+constexpr int kDenseDownNT = 128;   // output columns per workgroup (down)
+constexpr int kDenseMaxKsplit = 16; // d_ff chunks of the down-projection, at most
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
@@ -171,6 +173,18 @@ __device__ __forceinline__ bf16x8 krow_operand(const uint8_t *tile, int c, int j
   return b;
 }
 
+// the same from a k-row tile of `pitch` bytes per row
+__device__ __forceinline__ bf16x8 krow_operand_w(const uint8_t *tile, int pitch, int c, int j, int g) {
+  const uint16_t *p = reinterpret_cast<const uint16_t *>(tile);
+  bf16x8 b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int r = 32 * j + 8 * g + e;
+    b[e] = __builtin_bit_cast(__bf16, p[r * (pitch / 2) + krow_pos(r, c >> 3) * 8 + (c & 7)]);
+  }
+  return b;
+}
+
 // p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every row of
 // the group.  Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
 // MT 16-row tiles cover the group (rows past it are read as zeros).
@@ -263,33 +277,37 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
     *reinterpret_cast<u32x4 *>(a.P + (size_t)lr * N + n0 + 8 * lq) = *reinterpret_cast<const u32x4 *>(pt + lr * 64 + 8 * lq);
 }
 
-// partial y over k chunk blockIdx.y for 64 output columns (blockIdx.x).
-// Wavefronts w and w + 4 take the two 32-row halves of each stage for the
-// same 16 columns; their sums are added in LDS at the end.
+// partial y over k chunk blockIdx.y for 128 output columns (blockIdx.x).
+// The wider tile halves the re-reads of p per weight byte; wavefront w takes
+// columns 16 w .. 16 w + 15.  The W_down tile rows are 256 bytes (16 chunks).
 template <int STAGES, int MT>
 __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) {
   static_assert(STAGES % 2 == 0, "stage buffers alternate");
+  constexpr int WT = 2 * kDenseTileBytes;  // 64 rows x 256 bytes
   if (!a.ctl[1]) return;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * 2 * kDenseTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * (WT + kDenseTileBytes)];
   const int nd = min(a.ctl[0], 16 * MT);
   const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int jh = wv >> 2, c = 16 * (wv & 3) + (lane & 15), g = lane >> 4;
-  const int n0 = blockIdx.x * kDenseNT;
+  const int c = 16 * wv + (lane & 15), g = lane >> 4;
+  const int n0 = blockIdx.x * kDenseDownNT;
   const int K = a.K, N = a.N;
   const int kb = blockIdx.y * a.kchunk, ke = min(K, kb + a.kchunk);
   const int S = ke > kb ? (ke - kb) / kDenseKC : 0;
   const __amdgpu_buffer_rsrc_t rw = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
   const __amdgpu_buffer_rsrc_t rh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
-  const int lr = tid >> 3, lq = tid & 7;
-  const uint32_t ow = (uint32_t)(((size_t)(kb + lr) * N + n0 + 8 * lq) * 2);
+  // W tile: rows wr and wr + 32, chunk wq; H tile: row lr, chunk lq
+  const int wr = tid >> 4, wq = tid & 15, lr = tid >> 3, lq = tid & 7;
+  const uint32_t ow = (uint32_t)(((size_t)(kb + wr) * N + n0 + 8 * wq) * 2);
+  const uint32_t ow2 = ow + 32u * N * 2;
   const uint32_t oh = (uint32_t)(((size_t)lr * K + kb + 8 * lq) * 2);
   const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = (uint32_t)kDenseKC * 2;
   const bool hrow = lr < nd;
-  u32x4 bw[STAGES], bh[STAGES];
+  u32x4 bw[STAGES], bw2[STAGES], bh[STAGES];
 #pragma unroll
   for (int p = 0; p < STAGES; ++p) {
     const bool v = p < S;
     bw[p] = dense_load_stream(rw, v ? ow + p * sw : kDenseOffNone);
+    bw2[p] = dense_load_stream(rw, v ? ow2 + p * sw : kDenseOffNone);
     bh[p] = dense_load_cached(rh, v && hrow ? oh + p * sk : kDenseOffNone);
     __builtin_amdgcn_sched_barrier(0);  // issue in stage order: the waits below count on it
   }
@@ -300,47 +318,42 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   for (int s0 = 0; s0 < SR; s0 += STAGES) {
 #pragma unroll
     for (int p = 0; p < STAGES; ++p) {
-      uint8_t *tw = lds + (p & 1) * 2 * kDenseTileBytes, *th = tw + kDenseTileBytes;
-      lds_put16(tw, lr, krow_pos(lr, lq), bw[p]);
+      uint8_t *tw = lds + (p & 1) * (WT + kDenseTileBytes), *th = tw + WT;
+      *reinterpret_cast<u32x4 *>(tw + wr * 256 + krow_pos(wr, wq) * 16) = bw[p];
+      *reinterpret_cast<u32x4 *>(tw + (wr + 32) * 256 + krow_pos(wr + 32, wq) * 16) = bw2[p];
       lds_put16(th, lr, row_pos(lr, lq), bh[p]);
       const int sn = s0 + p + STAGES;
       const bool v = sn < S;
       bw[p] = dense_load_stream(rw, v ? ow + (uint32_t)sn * sw : kDenseOffNone);
+      bw2[p] = dense_load_stream(rw, v ? ow2 + (uint32_t)sn * sw : kDenseOffNone);
       bh[p] = dense_load_cached(rh, v && hrow ? oh + (uint32_t)sn * sk : kDenseOffNone);
       __syncthreads();
-      const bf16x8 b = krow_operand(tw, c, jh, g);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(row_operand(th, 16 * mt + (lane & 15), jh, g), b, acc[mt],
-                                                          0, 0, 0);
+      for (int j = 0; j < 2; ++j) {
+        const bf16x8 b = krow_operand_w(tw, 256, c, j, g);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(row_operand(th, 16 * mt + (lane & 15), j, g), b, acc[mt],
+                                                            0, 0, 0);
+      }
     }
   }
+  // through LDS to 16-byte row stores of the partial
   __syncthreads();
   float *xs = reinterpret_cast<float *>(lds);
-  if (jh == 1) {
+  constexpr int XP = 132;  // floats per row
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * kDenseXPitch + c] = acc[mt][r];
-  }
+    for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * XP + c] = acc[mt][r];
   __syncthreads();
-  if (jh == 0) {
+  // 16 MT rows x 32 chunks of 4 floats
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float *q = xs + (16 * mt + 4 * g + r) * kDenseXPitch + c;
-        *q = acc[mt][r] + *q;
-      }
-  }
-  __syncthreads();
-  // 16 MT rows x 16 chunks of 4 floats
-#pragma unroll
-  for (int i = 0; i < (MT + 1) / 2; ++i) {
-    const int e = tid + i * kDenseThreads, m = e >> 4, q = e & 15;
+  for (int i = 0; i < MT; ++i) {
+    const int e = tid + i * kDenseThreads, m = e >> 5, q = e & 31;
     if (m < nd)
       *reinterpret_cast<f32x4v *>(a.part + ((size_t)blockIdx.y * nd + m) * N + n0 + 4 * q) =
-          *reinterpret_cast<const f32x4v *>(xs + m * kDenseXPitch + 4 * q);
+          *reinterpret_cast<const f32x4v *>(xs + m * XP + 4 * q);
   }
 }
 
@@ -354,49 +367,54 @@ struct GlueArgs {
   uint16_t *layer_in;     // optional: inspection copy of the next layer input, rows through perm
 };
 
-// one workgroup per dense token (blockIdx.x)
-__global__ __launch_bounds__(kThreads) void dense_glue_kernel(GlueArgs a) {
+// one workgroup per dense token (blockIdx.x); thread t owns columns
+// 4 t .. 4 t + 3 and issues its loads of every partial at once
+constexpr int kGlueThreads = 1024;
+__global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
   if (!a.ctl[1]) return;
   const int m = blockIdx.x;
-  if (m >= a.ctl[0]) return;
   const int nd = a.ctl[0];
-  __shared__ float ssw[kThreads / 64];
+  if (m >= nd) return;
+  __shared__ float ssw[kGlueThreads / 64];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  constexpr int PT = 16;  // columns per thread (d <= 4096)
-  float y[PT];
-  float sq = 0.0f;
+  const int c = 4 * tid;  // d <= 4096
+  const bool on = c < a.d;
+  f32x4v v[kDenseMaxKsplit];
 #pragma unroll
-  for (int i = 0; i < PT; ++i) {
-    const int c = tid + i * kThreads;
-    float s = 0.0f;
-    if (c < a.d)
-      for (int q = 0; q < a.ksplit; ++q) s += a.part[((size_t)q * nd + m) * a.d + c];
-    y[i] = s;
-    sq = fmaf(s, s, sq);
-  }
+  for (int q = 0; q < kDenseMaxKsplit; ++q)
+    v[q] = (on && q < a.ksplit) ? *reinterpret_cast<const f32x4v *>(a.part + ((size_t)q * nd + m) * a.d + c)
+                                : f32x4v{0.f, 0.f, 0.f, 0.f};
+  f32x4v y = v[0];
+#pragma unroll
+  for (int q = 1; q < kDenseMaxKsplit; ++q) y += v[q];  // chunk order
   const int row = a.perm[m];
   if (a.out) {
-#pragma unroll
-    for (int i = 0; i < PT; ++i) {
-      const int c = tid + i * kThreads;
-      if (c < a.d) a.out[(size_t)row * a.d + c] = f32_to_bf16(y[i]);
+    if (on) {
+      uint16_t *o = a.out + (size_t)row * a.d + c;
+      o[0] = f32_to_bf16(y[0]);
+      o[1] = f32_to_bf16(y[1]);
+      o[2] = f32_to_bf16(y[2]);
+      o[3] = f32_to_bf16(y[3]);
     }
     return;
   }
+  float sq = y[0] * y[0];
+  sq = fmaf(y[1], y[1], sq);
+  sq = fmaf(y[2], y[2], sq);
+  sq = fmaf(y[3], y[3], sq);
   sq = wave_sum(sq);
   if (lane == 0) ssw[wv] = sq;
   __syncthreads();
   float tot = 0.0f;
-  for (int i = 0; i < kThreads / 64; ++i) tot += ssw[i];
+  for (int i = 0; i < kGlueThreads / 64; ++i) tot += ssw[i];
   const float scale = sqrtf(tot / (float)a.d + kGlueEps);
+  if (on) {
+    uint16_t h[4];
 #pragma unroll
-  for (int i = 0; i < PT; ++i) {
-    const int c = tid + i * kThreads;
-    if (c < a.d) {
-      const uint16_t hv = f32_to_bf16(y[i] / scale);
-      a.hnext[(size_t)m * a.d + c] = hv;
-      if (a.layer_in) a.layer_in[(size_t)row * a.d + c] = hv;
-    }
+    for (int i = 0; i < 4; ++i) h[i] = f32_to_bf16(y[i] / scale);
+    const uint2 hv = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+    *reinterpret_cast<uint2 *>(a.hnext + (size_t)m * a.d + c) = hv;
+    if (a.layer_in) *reinterpret_cast<uint2 *>(a.layer_in + (size_t)row * a.d + c) = hv;
   }
 }
 

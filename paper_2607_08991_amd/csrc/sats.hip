@@ -68,9 +68,17 @@ struct TimedLaunch {
 // --------------------------------------------------------------- planning
 
 constexpr int kMaxPass = 64;  // tokens per pass through the layers
-constexpr int kDenseKsplit = 4;  // d_ff chunks of the dense group's down-projection
 constexpr int kDenseGateUpStages = 8;  // stages in flight per thread: 3 loads each
-constexpr int kDenseDownStages = 12;   // 2 loads each
+constexpr int kDenseDownStages = 8;    // 3 loads each
+
+// d_ff chunks of the dense group's down-projection: about 256 workgroups,
+// each chunk a whole number of 64-row stages
+int dense_ksplit(int64_t d, int64_t d_ff) {
+  const int64_t tiles = d / sats::kDenseDownNT;
+  int64_t ks = std::max<int64_t>(1, (256 + tiles - 1) / tiles);
+  ks = std::min<int64_t>(ks, std::min<int64_t>(sats::kDenseMaxKsplit, std::max<int64_t>(1, d_ff / sats::kDenseKC)));
+  return (int)ks;
+}
 
 // MFMA kernels specialised on the 16-row tiles that cover a pass of np tokens
 typedef void (*DenseKernel)(sats::DenseArgs);
@@ -205,7 +213,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.xd = c.take<uint16_t>(Pp * d);
   t.hnext = c.take<uint16_t>(Pp * d);
   t.pdense = c.take<uint16_t>(Pp * d_ff);
-  t.ddpart = c.take<float>((int64_t)kDenseKsplit * Pp * d);
+  t.ddpart = c.take<float>((int64_t)sats::kDenseMaxKsplit * Pp * d);
   t.dgpart = c.take<float>((int64_t)sats::dec_nrcp(dp.nrc) * d_ff);
   t.dstate = c.take<int>(64);
   if (b) *b = t;
@@ -323,7 +331,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
 
   // routing for the pass: partition, dense-group size and whether MFMA takes it
   const bool mfma = sizeof(T) == 2 && VEC > 1 && np >= kMfmaMinTokens &&
-                    d % kDenseKC == 0 && d_ff % kDenseKC == 0 && d <= 4096 &&
+                    d % kDenseDownNT == 0 && d_ff % kDenseKC == 0 && d <= 4096 &&
                     (uint64_t)d * d_ff * 2 < (1ull << 31) &&
                     !getenv("SATS_NO_MFMA");
   // whole batch on MFMA (each row applies its own keep rule): known here, so
@@ -379,10 +387,11 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       dd.part = b.ddpart;
       dd.K = (int)d_ff;
       dd.N = (int)d;
-      dd.kchunk = (int)(((d_ff + kDenseKsplit - 1) / kDenseKsplit + kDenseKC - 1) / kDenseKC * kDenseKC);
+      const int ks = dense_ksplit(d, d_ff);
+      dd.kchunk = (int)(((d_ff + ks - 1) / ks + kDenseKC - 1) / kDenseKC * kDenseKC);
       {
         TimedLaunch tl(SATS_K_DENSE, c.stream);
-        hipExtLaunchKernelGGL(dense_down_fn(np), dim3(d / kDenseNT, kDenseKsplit), dim3(kDenseThreads), 0, c.stream,
+        hipExtLaunchKernelGGL(dense_down_fn(np), dim3(d / kDenseDownNT, ks), dim3(kDenseThreads), 0, c.stream,
                               tl.start, tl.stop, 0, dd);
       }
       HIP_TRY(hipGetLastError());
@@ -390,13 +399,13 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       ga.ctl = b.ctl;
       ga.perm = b.perm;
       ga.part = b.ddpart;
-      ga.ksplit = kDenseKsplit;
+      ga.ksplit = ks;
       ga.d = (int)d;
       ga.out = (l == c.L - 1) ? static_cast<uint16_t *>(c.out) + base * d : nullptr;
       ga.hnext = b.hnext;
       ga.layer_in = (c.layer_in && l + 1 < c.L) ? static_cast<uint16_t *>(c.layer_in) + ((l + 1) * c.n + base) * d
                                                  : nullptr;
-      hipLaunchKernelGGL(dense_glue_kernel, dim3(np), dim3(kThreads), 0, c.stream, ga);
+      hipLaunchKernelGGL(dense_glue_kernel, dim3(np), dim3(kGlueThreads), 0, c.stream, ga);
       HIP_TRY(hipGetLastError());
     }
     auto compact = [&]() -> int {
