@@ -116,65 +116,67 @@ struct DenseArgs {
 //
 // Both products stream a weight matrix once and reuse each weight over the
 // rows of the group, so they are bound by HBM, not by the matrix cores: what
-// matters is how many bytes each workgroup keeps in flight.  A workgroup of
-// 512 threads owns 64 output columns and walks its k range in stages of 64
-// rows.  Every thread issues 16-byte buffer loads for kDenseStages stages
-// ahead into registers (weights streamed past the caches, the small left
-// operand H cached), and each stage is copied into one of two LDS buffers,
-// one barrier per stage, before the wavefronts read their MFMA operands.
+// matters is how many bytes stay in flight and how little work each byte
+// costs on its way to the MFMA.  A workgroup of 512 threads owns a tile of
+// output columns and walks its k range in stages of 64 rows.  Each stage
+// (24 KB) is loaded straight into LDS with buffer loads that write LDS
+// (no register staging, no LDS store instructions) into a ring of six stage
+// buffers: five stages are in flight while the wavefronts read the MFMA
+// operands of the sixth.  One barrier per stage; before it every wavefront
+// waits until its own loads of that stage have landed.
 //
-// LDS tiles are 64 rows of 128 bytes (eight 16-byte chunks per row):
-//   k-row tile   W_gate / W_down rows k0..k0+63, columns n0..n0+63
-//   row tile     W_up_T rows n0..n0+63 or H rows 0..63, entries k0..k0+63
-// Chunks are stored at a swizzled position so that the operand reads below
-// touch 64 distinct banks: chunk q of row r sits at q ^ (2 ((r >> 3) & 3)) in
-// a k-row tile and at q ^ ((r >> 1) & 7) in a row tile.
+// A buffer load into LDS writes 16 bytes per lane at consecutive addresses,
+// so the tile layout is chosen through the global address each lane reads.
+// LDS tiles:
+//   k-row tile  W_gate rows (128 bytes each) or W_down rows (256 bytes each)
+//               of the stage; chunk q (16 bytes) of row r sits at position
+//               q ^ (2 ((r >> 3) & 3)), so that the transposed operand reads
+//               of a wavefront touch distinct banks
+//   row tile    W_up_T rows n0..n0+63 or H rows, 128 bytes (64 k) each;
+//               chunk q of row r sits at q ^ ((r >> 1) & 7)
 
-constexpr int kDenseThreads = 512;            // 8 wavefronts
-constexpr int kDenseKC = 64;                  // k rows per stage
-constexpr int kDenseTileBytes = 64 * 128;     // one LDS tile
-constexpr int kDenseXPitch = 68;              // floats per row of the epilogue exchange tile
+constexpr int kDenseThreads = 512;             // 8 wavefronts
+constexpr int kDenseKC = 64;                   // k rows per stage
+constexpr int kDenseStageBytes = 24 * 1024;    // one stage buffer
+constexpr int kDenseXP = 68;                   // floats per row of the gate/up exchange tile
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t dense_rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
 }
 constexpr uint32_t kDenseOffNone = 0x80000000u;  // past every buffer: the load returns zeros
-// 16 bytes streamed once (weights) / kept in the caches (H, read by every workgroup)
-__device__ __forceinline__ u32x4 dense_load_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 2);
+// offset of a load that is skipped when !v; the skipped loads of one stage
+// get distinct offsets so that they stay separate loads
+__device__ __forceinline__ uint32_t dense_off(bool v, uint32_t off, int tag) {
+  return v ? off : kDenseOffNone + 16u * (uint32_t)tag;
 }
-__device__ __forceinline__ u32x4 dense_load_cached(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+// 16 bytes per lane from the buffer into LDS at dst + 16 * lane (dst is the
+// same for the whole wavefront); aux 2 streams past the caches
+template <int AUX>
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint8_t *dst, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)dst, 16, (int)off, 0, 0, AUX);
+}
+// wait until at most `vm` buffer loads of this wavefront are outstanding and
+// its LDS reads are done, then meet the other wavefronts
+template <int VM>
+__device__ __forceinline__ void dense_stage_barrier() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (0 << 8) | ((VM >> 4) << 14));
+  __builtin_amdgcn_s_barrier();
 }
 
 __device__ __forceinline__ int krow_pos(int r, int q) { return q ^ (2 * ((r >> 3) & 3)); }
 __device__ __forceinline__ int row_pos(int r, int q) { return q ^ ((r >> 1) & 7); }
 
-__device__ __forceinline__ void lds_put16(uint8_t *tile, int r, int pos, const u32x4 &v) {
-  *reinterpret_cast<u32x4 *>(tile + r * 128 + pos * 16) = v;
-}
-
-// MFMA operand from a row tile: row `r`, k = 32 j + 8 g .. + 7 of the stage
+// MFMA operand from a row tile: row r, k = 32 j + 8 g .. + 7 of the stage
 __device__ __forceinline__ bf16x8 row_operand(const uint8_t *tile, int r, int j, int g) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(tile + r * 128 + row_pos(r, 4 * j + g) * 16));
 }
-// MFMA operand from a k-row tile: column c, k = 32 j + 8 g .. + 7 (a transposed
-// read, one 16-bit entry per row)
-__device__ __forceinline__ bf16x8 krow_operand(const uint8_t *tile, int c, int j, int g) {
-  const uint16_t *p = reinterpret_cast<const uint16_t *>(tile);
-  bf16x8 b;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int r = 32 * j + 8 * g + e;
-    b[e] = __builtin_bit_cast(__bf16, p[r * 64 + krow_pos(r, c >> 3) * 8 + (c & 7)]);
-  }
-  return b;
-}
-
-// the same from a k-row tile of `pitch` bytes per row
-__device__ __forceinline__ bf16x8 krow_operand_w(const uint8_t *tile, int pitch, int c, int j, int g) {
+// transposed MFMA operand from a k-row tile of `pitch` bytes per row:
+// column c, rows 32 j + 8 g .. + 7
+__device__ __forceinline__ bf16x8 krow_operand(const uint8_t *tile, int pitch, int c, int j, int g) {
   const uint16_t *p = reinterpret_cast<const uint16_t *>(tile);
   bf16x8 b;
 #pragma unroll
@@ -184,77 +186,98 @@ __device__ __forceinline__ bf16x8 krow_operand_w(const uint8_t *tile, int pitch,
   }
   return b;
 }
+__device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const f32x4v &c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// The stage loop shared by both products: stage s lives in ring buffer
+// s % 6; `issue(buf, s)` starts three buffer loads per lane for stage s
+// (loads past the k range read zeros) and `compute(buf)` consumes a stage.
+#define SATS_DENSE_RING(S, ISSUE, COMPUTE)                                                   \
+  {                                                                                          \
+    uint8_t *const rb_[6] = {rg0, rg1, rg2, rg3, rg4, rg5};                                  \
+    (void)rb_;                                                                               \
+    ISSUE(rg0, 0);                                                                           \
+    ISSUE(rg1, 1);                                                                           \
+    ISSUE(rg2, 2);                                                                           \
+    ISSUE(rg3, 3);                                                                           \
+    ISSUE(rg4, 4);                                                                           \
+    for (int s0 = 0; s0 < (S); s0 += 6) {                                                    \
+      SATS_DENSE_STEP(S, ISSUE, COMPUTE, rg0, rg5, 0)                                        \
+      SATS_DENSE_STEP(S, ISSUE, COMPUTE, rg1, rg0, 1)                                        \
+      SATS_DENSE_STEP(S, ISSUE, COMPUTE, rg2, rg1, 2)                                        \
+      SATS_DENSE_STEP(S, ISSUE, COMPUTE, rg3, rg2, 3)                                        \
+      SATS_DENSE_STEP(S, ISSUE, COMPUTE, rg4, rg3, 4)                                        \
+      SATS_DENSE_STEP(S, ISSUE, COMPUTE, rg5, rg4, 5)                                        \
+    }                                                                                        \
+    __builtin_amdgcn_s_waitcnt(0); /* the zero-filling loads past the range land too */     \
+  }
+// stage s: its loads are the oldest of the five stages in flight (three
+// loads each), so at most 12 may still be outstanding
+#define SATS_DENSE_STEP(S, ISSUE, COMPUTE, CUR, NXT, P)                                      \
+  {                                                                                          \
+    const int s_ = s0 + (P);                                                                 \
+    dense_stage_barrier<12>();                                                               \
+    if (s_ < (S)) COMPUTE(CUR);                                                              \
+    ISSUE(NXT, s_ + 5);                                                                      \
+  }
 
 // p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every row of
-// the group.  Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
-// MT 16-row tiles cover the group (rows past it are read as zeros).
-template <int STAGES, int MT>
+// the group (MT 16-row tiles; rows past the group are read as zeros).
+// Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
+template <int MT>
 __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a) {
-  static_assert(STAGES % 2 == 0, "stage buffers alternate");
+  __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
+      rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
   if (!a.ctl[1]) return;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * 3 * kDenseTileBytes];
   const int nd = min(a.ctl[0], 16 * MT);
-  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int mat = wv >> 2, c = 16 * (wv & 3) + (lane & 15), g = lane >> 4;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int mat = w >> 2, g = lane >> 4, l16 = lane & 15, c = 16 * (w & 3) + l16;
   const int n0 = blockIdx.x * kDenseNT;
   const int K = a.K, N = a.N;
   const int S = K / kDenseKC;
-  const __amdgpu_buffer_rsrc_t rg = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
-  const __amdgpu_buffer_rsrc_t ru = dense_rsrc(a.Wt, (uint32_t)((size_t)K * N * 2));
-  const __amdgpu_buffer_rsrc_t rh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
-  // this thread's 16-byte piece of each tile: row lr, chunk lq
-  const int lr = tid >> 3, lq = tid & 7;
-  const uint32_t og = (uint32_t)(((size_t)lr * N + n0 + 8 * lq) * 2);
-  const uint32_t ou = (uint32_t)(((size_t)(n0 + lr) * K + 8 * lq) * 2);
-  const uint32_t oh = (uint32_t)(((size_t)lr * K + 8 * lq) * 2);
-  const uint32_t sg = (uint32_t)kDenseKC * N * 2, sk = (uint32_t)kDenseKC * 2;  // per stage
-  const bool hrow = lr < nd;
-  u32x4 bw[STAGES], bu[STAGES], bh[STAGES];
-#pragma unroll
-  for (int p = 0; p < STAGES; ++p) {
-    const bool v = p < S;
-    bw[p] = dense_load_stream(rg, v ? og + p * sg : kDenseOffNone);
-    bu[p] = dense_load_stream(ru, v ? ou + p * sk : kDenseOffNone);
-    bh[p] = dense_load_cached(rh, v && hrow ? oh + p * sk : kDenseOffNone);
-    __builtin_amdgcn_sched_barrier(0);  // issue in stage order: the waits below count on it
-  }
+  const __amdgpu_buffer_rsrc_t rsg = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t rsu = dense_rsrc(a.Wt, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
+  // wavefront w loads rows 8 w .. 8 w + 7 of each tile (1 KB); lane: row dr, slot dp
+  const int dr = 8 * w + (lane >> 3), dp = lane & 7;
+  const uint32_t og = (uint32_t)(((size_t)dr * N + n0 + 8 * krow_pos(dr, dp)) * 2);
+  const uint32_t ou = (uint32_t)(((size_t)(n0 + dr) * K + 8 * row_pos(dr, dp)) * 2);
+  const uint32_t oh = (uint32_t)(((size_t)dr * K + 8 * row_pos(dr, dp)) * 2);
+  const bool hv = dr < nd;
+  const uint32_t sg = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;  // per stage
   f32x4v acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4v{0.f, 0.f, 0.f, 0.f};
-  const int SR = (S + STAGES - 1) / STAGES * STAGES;
-  for (int s0 = 0; s0 < SR; s0 += STAGES) {
-#pragma unroll
-    for (int p = 0; p < STAGES; ++p) {
-      uint8_t *tg = lds + (p & 1) * 3 * kDenseTileBytes, *tu = tg + kDenseTileBytes, *th = tu + kDenseTileBytes;
-      lds_put16(tg, lr, krow_pos(lr, lq), bw[p]);
-      lds_put16(tu, lr, row_pos(lr, lq), bu[p]);
-      lds_put16(th, lr, row_pos(lr, lq), bh[p]);
-      const int sn = s0 + p + STAGES;
-      const bool v = sn < S;
-      bw[p] = dense_load_stream(rg, v ? og + (uint32_t)sn * sg : kDenseOffNone);
-      bu[p] = dense_load_stream(ru, v ? ou + (uint32_t)sn * sk : kDenseOffNone);
-      bh[p] = dense_load_cached(rh, v && hrow ? oh + (uint32_t)sn * sk : kDenseOffNone);
-      __syncthreads();
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const bf16x8 b = mat == 0 ? krow_operand(tg, c, j, g) : row_operand(tu, c, j, g);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(row_operand(th, 16 * mt + (lane & 15), j, g), b, acc[mt],
-                                                            0, 0, 0);
-      }
-    }
+#define SATS_GU_ISSUE(BUF, SN)                                                               \
+  {                                                                                          \
+    const bool v_ = (SN) < S;                                                                \
+    const uint32_t ss_ = (uint32_t)(SN);                                                     \
+    dma16<2>(rsg, (BUF) + w * 1024, dense_off(v_, og + ss_ * sg, 0));                        \
+    dma16<2>(rsu, (BUF) + 8192 + w * 1024, dense_off(v_, ou + ss_ * sk, 1));                 \
+    dma16<0>(rsh, (BUF) + 16384 + w * 1024, dense_off(v_ && hv, oh + ss_ * sk, 2));          \
   }
+#define SATS_GU_COMPUTE(BUF)                                                                 \
+  {                                                                                          \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                          \
+      const bf16x8 b_ = mat == 0 ? krow_operand((BUF), 128, c, j, g) : row_operand((BUF) + 8192, c, j, g); \
+      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt)                                      \
+        acc[mt] = mfma16(row_operand((BUF) + 16384, 16 * mt + l16, j, g), b_, acc[mt]);      \
+    }                                                                                        \
+  }
+  SATS_DENSE_RING(S, SATS_GU_ISSUE, SATS_GU_COMPUTE)
+#undef SATS_GU_ISSUE
+#undef SATS_GU_COMPUTE
   // epilogue: SiLU(a) through LDS to the W_up wavefronts, p through LDS to
   // 16-byte row stores
   __syncthreads();
-  float *xs = reinterpret_cast<float *>(lds);
-  uint16_t *pt = reinterpret_cast<uint16_t *>(lds + 64 * kDenseXPitch * 4);
+  float *xs = reinterpret_cast<float *>(rg0);
+  uint16_t *pt = reinterpret_cast<uint16_t *>(rg1);
   if (mat == 0) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * kDenseXPitch + c] = silu(acc[mt][r]);
+      for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * kDenseXP + c] = silu(acc[mt][r]);
   }
   __syncthreads();
   if (mat == 1) {
@@ -265,7 +288,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
       for (int r = 0; r < 4; ++r) {
         const int m = 16 * mt + 4 * g + r;
         if (m < nd) {
-          const float gv = xs[m * kDenseXPitch + c];
+          const float gv = xs[m * kDenseXP + c];
           const bool keep = a.gbase[m] || fabsf(gv) >= thr;  // Eq. 4-5; every column on the base path
           pt[m * 64 + c] = keep ? f32_to_bf16(gv * acc[mt][r]) : (uint16_t)0;
           if (a.keep_out) a.keep_out[(size_t)a.perm[m] * N + n0 + c] = (uint8_t)keep;
@@ -273,89 +296,78 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
       }
   }
   __syncthreads();
+  const int lr = threadIdx.x >> 3, lq = threadIdx.x & 7;
   if (lr < nd)
     *reinterpret_cast<u32x4 *>(a.P + (size_t)lr * N + n0 + 8 * lq) = *reinterpret_cast<const u32x4 *>(pt + lr * 64 + 8 * lq);
 }
 
-// partial y over k chunk blockIdx.y for 128 output columns (blockIdx.x).
-// The wider tile halves the re-reads of p per weight byte; wavefront w takes
-// columns 16 w .. 16 w + 15.  The W_down tile rows are 256 bytes (16 chunks).
-template <int STAGES, int MT>
+// partial y over k chunk blockIdx.y for 128 output columns (blockIdx.x);
+// wavefront w takes columns 16 w .. 16 w + 15.  A stage holds 64 W_down
+// rows of 256 bytes (16 KB) and the matching 64 entries of p rows (8 KB).
+template <int MT>
 __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) {
-  static_assert(STAGES % 2 == 0, "stage buffers alternate");
-  constexpr int WT = 2 * kDenseTileBytes;  // 64 rows x 256 bytes
+  __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
+      rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
   if (!a.ctl[1]) return;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * (WT + kDenseTileBytes)];
   const int nd = min(a.ctl[0], 16 * MT);
-  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int c = 16 * wv + (lane & 15), g = lane >> 4;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, l16 = lane & 15, c = 16 * w + l16;
   const int n0 = blockIdx.x * kDenseDownNT;
   const int K = a.K, N = a.N;
   const int kb = blockIdx.y * a.kchunk, ke = min(K, kb + a.kchunk);
   const int S = ke > kb ? (ke - kb) / kDenseKC : 0;
-  const __amdgpu_buffer_rsrc_t rw = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
-  const __amdgpu_buffer_rsrc_t rh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
-  // W tile: rows wr and wr + 32, chunk wq; H tile: row lr, chunk lq
-  const int wr = tid >> 4, wq = tid & 15, lr = tid >> 3, lq = tid & 7;
-  const uint32_t ow = (uint32_t)(((size_t)(kb + wr) * N + n0 + 8 * wq) * 2);
-  const uint32_t ow2 = ow + 32u * N * 2;
-  const uint32_t oh = (uint32_t)(((size_t)lr * K + kb + 8 * lq) * 2);
-  const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = (uint32_t)kDenseKC * 2;
-  const bool hrow = lr < nd;
-  u32x4 bw[STAGES], bw2[STAGES], bh[STAGES];
-#pragma unroll
-  for (int p = 0; p < STAGES; ++p) {
-    const bool v = p < S;
-    bw[p] = dense_load_stream(rw, v ? ow + p * sw : kDenseOffNone);
-    bw2[p] = dense_load_stream(rw, v ? ow2 + p * sw : kDenseOffNone);
-    bh[p] = dense_load_cached(rh, v && hrow ? oh + p * sk : kDenseOffNone);
-    __builtin_amdgcn_sched_barrier(0);  // issue in stage order: the waits below count on it
-  }
+  const __amdgpu_buffer_rsrc_t rsw = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
+  // wavefront w loads W_down rows 8 w .. 8 w + 7 (two loads of 4 rows) and
+  // p rows 8 w .. 8 w + 7
+  const int wr = 8 * w + (lane >> 4), wp = lane & 15;
+  const uint32_t ow0 = (uint32_t)(((size_t)(kb + wr) * N + n0 + 8 * krow_pos(wr, wp)) * 2);
+  const uint32_t ow1 = (uint32_t)(((size_t)(kb + wr + 4) * N + n0 + 8 * krow_pos(wr + 4, wp)) * 2);
+  const int hr = 8 * w + (lane >> 3), hp = lane & 7;
+  const uint32_t oh = (uint32_t)(((size_t)hr * K + kb + 8 * row_pos(hr, hp)) * 2);
+  const bool hv = hr < nd;
+  const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;
   f32x4v acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4v{0.f, 0.f, 0.f, 0.f};
-  const int SR = (S + STAGES - 1) / STAGES * STAGES;
-  for (int s0 = 0; s0 < SR; s0 += STAGES) {
-#pragma unroll
-    for (int p = 0; p < STAGES; ++p) {
-      uint8_t *tw = lds + (p & 1) * (WT + kDenseTileBytes), *th = tw + WT;
-      *reinterpret_cast<u32x4 *>(tw + wr * 256 + krow_pos(wr, wq) * 16) = bw[p];
-      *reinterpret_cast<u32x4 *>(tw + (wr + 32) * 256 + krow_pos(wr + 32, wq) * 16) = bw2[p];
-      lds_put16(th, lr, row_pos(lr, lq), bh[p]);
-      const int sn = s0 + p + STAGES;
-      const bool v = sn < S;
-      bw[p] = dense_load_stream(rw, v ? ow + (uint32_t)sn * sw : kDenseOffNone);
-      bw2[p] = dense_load_stream(rw, v ? ow2 + (uint32_t)sn * sw : kDenseOffNone);
-      bh[p] = dense_load_cached(rh, v && hrow ? oh + (uint32_t)sn * sk : kDenseOffNone);
-      __syncthreads();
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const bf16x8 b = krow_operand_w(tw, 256, c, j, g);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(row_operand(th, 16 * mt + (lane & 15), j, g), b, acc[mt],
-                                                            0, 0, 0);
-      }
-    }
+#define SATS_DN_ISSUE(BUF, SN)                                                               \
+  {                                                                                          \
+    const bool v_ = (SN) < S;                                                                \
+    const uint32_t ss_ = (uint32_t)(SN);                                                     \
+    dma16<2>(rsw, (BUF) + w * 2048, dense_off(v_, ow0 + ss_ * sw, 0));                       \
+    dma16<2>(rsw, (BUF) + w * 2048 + 1024, dense_off(v_, ow1 + ss_ * sw, 1));                \
+    dma16<0>(rsh, (BUF) + 16384 + w * 1024, dense_off(v_ && hv, oh + ss_ * sk, 2));          \
   }
-  // through LDS to 16-byte row stores of the partial
+#define SATS_DN_COMPUTE(BUF)                                                                 \
+  {                                                                                          \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                          \
+      const bf16x8 b_ = krow_operand((BUF), 256, c, j, g);                                   \
+      _Pragma("unroll") for (int mt = 0; mt < MT; ++mt)                                      \
+        acc[mt] = mfma16(row_operand((BUF) + 16384, 16 * mt + l16, j, g), b_, acc[mt]);      \
+    }                                                                                        \
+  }
+  SATS_DENSE_RING(S, SATS_DN_ISSUE, SATS_DN_COMPUTE)
+#undef SATS_DN_ISSUE
+#undef SATS_DN_COMPUTE
+  // through LDS to 16-byte row stores: rows 0-31 in one stage buffer, 32-63 in the next
   __syncthreads();
-  float *xs = reinterpret_cast<float *>(lds);
-  constexpr int XP = 132;  // floats per row
+  constexpr int XP = 132;
+  float *x0 = reinterpret_cast<float *>(rg0), *x1 = reinterpret_cast<float *>(rg1);
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * XP + c] = acc[mt][r];
+    for (int r = 0; r < 4; ++r) (mt < 2 ? x0 : x1)[(16 * (mt & 1) + 4 * g + r) * XP + c] = acc[mt][r];
   __syncthreads();
-  // 16 MT rows x 32 chunks of 4 floats
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    const int e = tid + i * kDenseThreads, m = e >> 5, q = e & 31;
+    const int e = threadIdx.x + i * kDenseThreads, m = e >> 5, q = e & 31;
     if (m < nd)
       *reinterpret_cast<f32x4v *>(a.part + ((size_t)blockIdx.y * nd + m) * N + n0 + 4 * q) =
-          *reinterpret_cast<const f32x4v *>(xs + m * XP + 4 * q);
+          *reinterpret_cast<const f32x4v *>((m < 32 ? x0 : x1) + (m & 31) * XP + 4 * q);
   }
 }
+#undef SATS_DENSE_RING
+#undef SATS_DENSE_STEP
 
 struct GlueArgs {
   const int *ctl;

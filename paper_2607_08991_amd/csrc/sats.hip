@@ -68,8 +68,6 @@ struct TimedLaunch {
 // --------------------------------------------------------------- planning
 
 constexpr int kMaxPass = 64;  // tokens per pass through the layers
-constexpr int kDenseGateUpStages = 8;  // stages in flight per thread: 3 loads each
-constexpr int kDenseDownStages = 8;    // 3 loads each
 
 // d_ff chunks of the dense group's down-projection: about 256 workgroups,
 // each chunk a whole number of 64-row stages
@@ -85,18 +83,14 @@ typedef void (*DenseKernel)(sats::DenseArgs);
 DenseKernel dense_gateup_fn(int np) {
   using namespace sats;
   const int mt = (np + 15) / 16;
-  return mt <= 1 ? dense_gateup_kernel<kDenseGateUpStages, 1>
-         : mt == 2 ? dense_gateup_kernel<kDenseGateUpStages, 2>
-         : mt == 3 ? dense_gateup_kernel<kDenseGateUpStages, 3>
-                   : dense_gateup_kernel<kDenseGateUpStages, 4>;
+  return mt <= 1 ? dense_gateup_kernel<1> : mt == 2 ? dense_gateup_kernel<2> : mt == 3 ? dense_gateup_kernel<3>
+                                                                                        : dense_gateup_kernel<4>;
 }
 DenseKernel dense_down_fn(int np) {
   using namespace sats;
   const int mt = (np + 15) / 16;
-  return mt <= 1 ? dense_down_kernel<kDenseDownStages, 1>
-         : mt == 2 ? dense_down_kernel<kDenseDownStages, 2>
-         : mt == 3 ? dense_down_kernel<kDenseDownStages, 3>
-                   : dense_down_kernel<kDenseDownStages, 4>;
+  return mt <= 1 ? dense_down_kernel<1> : mt == 2 ? dense_down_kernel<2> : mt == 3 ? dense_down_kernel<3>
+                                                                                    : dense_down_kernel<4>;
 }
 
 int round_pow2_down(int v) {
