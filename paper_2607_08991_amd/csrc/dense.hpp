@@ -213,13 +213,14 @@ __device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const
     __builtin_amdgcn_s_waitcnt(0); /* the zero-filling loads past the range land too */     \
   }
 // stage s: its loads are the oldest of the five stages in flight (three
-// loads each), so at most 12 may still be outstanding
+// loads each), so at most 12 may still be outstanding.  After the barrier
+// every wavefront is done with stage s - 1, whose buffer takes stage s + 5.
 #define SATS_DENSE_STEP(S, ISSUE, COMPUTE, CUR, NXT, P)                                      \
   {                                                                                          \
     const int s_ = s0 + (P);                                                                 \
     dense_stage_barrier<12>();                                                               \
-    if (s_ < (S)) COMPUTE(CUR);                                                              \
     ISSUE(NXT, s_ + 5);                                                                      \
+    if (s_ < (S)) COMPUTE(CUR);                                                              \
   }
 
 // p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every row of
