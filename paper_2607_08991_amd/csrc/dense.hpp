@@ -32,7 +32,7 @@
 
 namespace sats {
 
-constexpr int kMfmaMinTokens = 8;   // dense group size from which MFMA is used
+constexpr int kMfmaMinTokens = 2;   // group size from which MFMA is used
 constexpr int kDenseMaxTokens = 64; // tokens of one pass (four 16-row MFMA tiles)
 constexpr int kDenseNT = 64;        // output columns per workgroup (gate/up)
 constexpr int kDenseDownNT = 128;   // output columns per workgroup (down)
@@ -57,10 +57,14 @@ struct RouteArgs {
   int whole;              // the MFMA group is the whole batch (keep rule applied per row)
 };
 
+// One workgroup per token of the pass: every workgroup forms the same
+// partition (64 table reads), workgroup 0 publishes it, and workgroup b
+// gathers row b of the dense group's inputs.
 __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
   __shared__ int s_perm[kDenseMaxTokens];
   __shared__ int s_nd, s_on;
   const int tid = threadIdx.x, lane = tid & 63;
+  const bool pub = blockIdx.x == 0;
   if (tid < 64) {
     const bool valid = tid < a.n;
     const int base = valid ? token_is_base(a.route_mode, a.ids, a.lut, tid) : 0;
@@ -74,27 +78,32 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     if (valid) {
       const int pos = base ? rank_d : nd + (tid - rank_d);
       s_perm[pos] = tid;
-      a.perm[pos] = tid;
-      a.gbase[pos] = (uint8_t)base;
-      a.skip[tid] = (uint8_t)(on && (base || a.whole));
-      if (a.route_out) a.route_out[tid] = (uint8_t)base;
+      if (pub) {
+        a.perm[pos] = tid;
+        a.gbase[pos] = (uint8_t)base;
+        a.skip[tid] = (uint8_t)(on && (base || a.whole));
+        if (a.route_out) a.route_out[tid] = (uint8_t)base;
+      }
     }
     if (tid == 0) {
-      a.ctl[0] = ng;
-      a.ctl[1] = on;
+      if (pub) {
+        a.ctl[0] = ng;
+        a.ctl[1] = on;
+      }
       s_nd = ng;
       s_on = on;
     }
   }
   __syncthreads();
-  if (!s_on) return;
-  // gather the dense group's inputs, 16 bytes per thread and step
+  const int m = blockIdx.x;
+  if (!s_on || m >= s_nd) return;
+  // row m of the dense group, 16 bytes per thread and step
   const int vpr = a.d / 8;  // 16-byte vectors per row (d % 32 == 0 on this path)
-  for (int i = tid; i < s_nd * vpr; i += kThreads) {
-    const int m = i / vpr, v = i - m * vpr;
-    const u32x4 q = *reinterpret_cast<const u32x4 *>(a.x + (size_t)s_perm[m] * a.d + v * 8);
+  const int src = s_perm[m];
+  for (int v = tid; v < vpr; v += kThreads) {
+    const u32x4 q = *reinterpret_cast<const u32x4 *>(a.x + (size_t)src * a.d + v * 8);
     *reinterpret_cast<u32x4 *>(a.xd + (size_t)m * a.d + v * 8) = q;
-    if (a.layer_in0) *reinterpret_cast<u32x4 *>(a.layer_in0 + (size_t)s_perm[m] * a.d + v * 8) = q;
+    if (a.layer_in0) *reinterpret_cast<u32x4 *>(a.layer_in0 + (size_t)src * a.d + v * 8) = q;
   }
 }
 

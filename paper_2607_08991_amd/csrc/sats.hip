@@ -349,7 +349,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     ra.gbase = b.gbase;
     ra.mfma = mfma ? 1 : 0;
     ra.whole = whole ? 1 : 0;
-    hipLaunchKernelGGL(route_kernel, dim3(1), dim3(kThreads), 0, c.stream, ra);
+    hipLaunchKernelGGL(route_kernel, dim3(np), dim3(kThreads), 0, c.stream, ra);
     HIP_TRY(hipGetLastError());
   }
 

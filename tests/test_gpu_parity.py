@@ -243,19 +243,21 @@ def test_config_llama_layer_full_size():
 
 # ------------------------------------------------------------ dense group on MFMA
 
-@pytest.mark.parametrize("seed,L,n,n_dense_ids", [(31, 1, 20, 30), (32, 3, 40, 20), (33, 2, 64, 40)])
+@pytest.mark.parametrize("seed,L,n,n_dense_ids", [(31, 1, 20, 30), (32, 3, 40, 20), (33, 2, 64, 40),
+                                                 (36, 1, 2, 12), (37, 2, 3, 12), (38, 1, 7, 20)])
 def test_mfma_dense_group_matches_oracle(seed, L, n, n_dense_ids):
-    """Batches of >= 8 tokens run on MFMA (whole batch, per-row keep rule); the
-    variant with only the base-path group on MFMA and the one without MFMA are
-    checked too.  Across several layers the variants may differ by more than
-    the tolerance (a column within rounding of the threshold flips and the
-    difference propagates), so each is checked against the oracle on its own
-    layer inputs."""
+    """Batches of >= 2 tokens run on MFMA (whole batch, per-row keep rule; one
+    to four 16-row tiles, ragged); the variant with only the base-path group
+    on MFMA and the one without MFMA are checked too.  Across several layers
+    the variants may differ by more than the tolerance (a column within
+    rounding of the threshold flips and the difference propagates), so each
+    is checked against the oracle on its own layer inputs."""
     c = synth.small_case(seed, L, 256, 1024, "bf16", n, vocab=40, n_dense_ids=n_dense_ids,
                          w_std=1 / 16)
     ts = case_thresholds(c, "bf16", seed=seed)
     res = run_gpu(c, ts, c["route_lut"], "bf16")
-    assert res["route"].sum() >= 8
+    if n >= 16:
+        assert res["route"].sum() >= 2
     worst = check_against_oracle(c, ts, c["route_lut"], "bf16", res)
     say(f"mfma seed={seed} L={L} n={n} dense={int(res['route'].sum())} worst {worst:.3g}")
     # the same tokens with only the base-path group on MFMA, and with no MFMA
