@@ -291,3 +291,32 @@ def test_mfma_dense_api_batch():
     ref = mlp.forward_dense(c["x"], c["W_gate"], c["W_up_T"], c["W_down"], "bf16")
     for i in range(24):
         assert rel_err(numerics.decode(res["out"][i], "bf16"), ref[i]) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("n,env", [(20, None), (5, None), (5, "SATS_NO_MFMA")])
+def test_batch_rows_are_permutation_equivariant_bitwise(n, env):
+    """Permuting the tokens of a batch permutes the output rows bit for bit:
+    a row's sums do not depend on its position in the batch or in the
+    dense/sparse partition (MFMA path and compacted path)."""
+    c = synth.small_case(39, 2, 256, 1024, "bf16", n, vocab=40, n_dense_ids=12, w_std=1 / 16)
+    ts = case_thresholds(c, "bf16", seed=39)
+    perm = np.random.default_rng(5).permutation(n)
+    cp = dict(c, x=c["x"][perm], token_ids=c["token_ids"][perm])
+    if env:
+        os.environ[env] = "1"
+    try:
+        a = run_gpu(c, ts, c["route_lut"], "bf16", inspect=False)
+        b = run_gpu(cp, ts, c["route_lut"], "bf16", inspect=False)
+    finally:
+        if env:
+            del os.environ[env]
+    np.testing.assert_array_equal(a["out"][perm], b["out"])
+
+
+def test_256_tokens_span_four_passes():
+    """256 tokens: four passes of 64 through the layers, mixed routes."""
+    c = synth.small_case(40, 2, 256, 1024, "bf16", 256, vocab=40, n_dense_ids=12, w_std=1 / 16)
+    ts = case_thresholds(c, "bf16", seed=40)
+    res = run_gpu(c, ts, c["route_lut"], "bf16")
+    worst = check_against_oracle(c, ts, c["route_lut"], "bf16", res)
+    say(f"256 tokens worst rel err {worst:.3g}; dense tokens {int(res['route'].sum())}")
