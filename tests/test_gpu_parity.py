@@ -224,20 +224,23 @@ def test_config_small_fp32_layer():
     assert 0 < res["route"].sum() < n
 
 
-def test_config_llama_layer_full_size():
-    """Llama-3.1-8B-shaped layer (4096 x 14336, bf16), all tokens sparse, batch 1 and 4."""
-    cfg = get_config(1)
+@pytest.mark.parametrize("cfg_name", ["c2_llama8b_layer_bf16", "c2_llama8b_layer_f32"])
+def test_config_llama_layer_full_size(cfg_name):
+    """Llama-3.1-8B-shaped layer (4096 x 14336), bf16 and fp32 weights, all tokens
+    sparse, batch 1 (single-token kernels) and 4 (MFMA for bf16, the compacted
+    batch kernels for fp32)."""
+    cfg = get_config(cfg_name)
     ts = _golden(cfg)
-    say("generating c2 weights")
+    say(f"generating {cfg.name} weights")
     wg, wu, wd = synth.layer_weights(cfg.seed, 0, cfg.d, cfg.d_ff, cfg.dtype)
-    dec = [numerics.decode(w, "bf16") for w in (wg, wu, wd)]
+    dec = [numerics.decode(w, cfg.dtype) for w in (wg, wu, wd)]
     for n in (1, 4):
         c = dict(x=synth.decode_x(cfg, n), token_ids=np.zeros(n, np.int32), W_gate=wg[None],
                  W_up_T=wu[None], W_down=wd[None])
         res = run_gpu(c, ts, None, cfg.dtype)
         worst = check_against_oracle(c, ts, None, cfg.dtype, res, weights=lambda l: dec)
         sp = 1 - res["count"].mean() / cfg.d_ff
-        say(f"c2 n={n}: worst rel err {worst:.3g}, realized sparsity {sp:.4f}")
+        say(f"{cfg.name} n={n}: worst rel err {worst:.3g}, realized sparsity {sp:.4f}")
         assert 0.4 < sp < 0.6
 
 

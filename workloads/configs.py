@@ -1,4 +1,4 @@
-"""The five workloads the path is specified on.
+"""The workloads the path is specified on: five, and an fp32 twin of the second.
 
 Shapes follow the models the paper evaluates (Section 4, "Base Models"):
 Llama-3.1-8B (d=4096, d_ff=14336, 32 MLP layers) and Qwen3-8B (d=4096,
@@ -52,6 +52,10 @@ CONFIGS = (
            128256, 32064, "zipf", 1.1, (1, 4, 16)),
     Config(4, "c5_llama8b_stack32_b64_bf16", 32, 4096, 14336, "bf16", 1024, 0.60, None,
            128256, 51302, "zipf", 1.1, (64,)),
+    # the second workload with fp32 weights and activations: the precision the
+    # paper's own throughput figures are measured in (Section 4)
+    Config(5, "c2_llama8b_layer_f32", 1, 4096, 14336, "f32", 1024, 0.50, None,
+           None, 0, None, 0.0, (1,)),
 )
 
 
