@@ -74,6 +74,8 @@ struct DecodeArgs {
   float *sspart;          // [RW]           per-reduce-workgroup sums of y^2
   int G, RW;              // rows workgroups (partials of y), reduce workgroups
   int *state;             // [1] the token's route (1: base path), set by the layer-0 gate launch
+  unsigned *done;         // [1] rows workgroups whose partial y is written (cleared by the gate launch)
+  unsigned *err;          // device error flag (a bounded wait gave up)
   uint8_t *route_out;     // optional [1]
   uint8_t *keep_out;      // optional [L][d_ff]
   void *layer_in;         // optional [L][d]
@@ -86,6 +88,7 @@ struct DecodeSmem {
   float mg[kDecodeThreads / 2];         // ... and their g values
   int wcnt[kDecodeWaves];
   float scal[kDecodeWaves];
+  int flag;
 };
 
 // Four consecutive floats at byte offset voff of buffer r, written through to
@@ -417,7 +420,8 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
   constexpr int CH = 64 * VEC;              // elements per chunk (one 16-byte load per lane)
   constexpr int DMAX = kDecodeMaxD / CH;    // chunks per row
   constexpr int NCH = (DMAX + 7) / 8;       // chunks per wavefront of a half
-  constexpr int R = 8 / NCH;                // rows per batch (2 x 8 loads in flight per lane)
+  constexpr int R = 8 / NCH;                // rows of two batches (2 x 8 loads in flight per lane)
+  constexpr int RB = R > 2 ? R / 4 : 1;     // rows per batch
   static_assert(CB <= kDecodeThreads / 2 && 4 * R * 8 <= 2 * kDecodeMaxD, "single-token tiling");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), hw = wv & 7, hf = wv >> 3;
@@ -431,7 +435,6 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
       weight_rsrc(a.gpart, (uint32_t)((size_t)d_ff * dec_nrcp(a.nrc) * sizeof(float)));
 
   InputRegs<kDecodeThreads> ir;
-  dec_input_issue<T, kDecodeThreads>(a, l, ir);
   float hreg[NCH][VEC];  // h at this lane's columns
   float yacc[NCH][VEC];
 #pragma unroll
@@ -451,16 +454,9 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
       keep = base || (fabsf(g) >= thr);
       if (sub == 0 && a.keep_out) a.keep_out[(size_t)l * d_ff + gcol] = (uint8_t)keep;
     }
-    if (un == w) {
-      dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, false);
-#pragma unroll
-      for (int c = 0; c < NCH; ++c)
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-          const int k = (hw + c * 8) * CH + lane * VEC + v;
-          hreg[c][v] = (k < d) ? sm.hs[k] : 0.0f;
-        }
-    }
+    // h's loads follow the partials' (the keep list is on the critical path)
+    // and are waited for only after the first rows are issued
+    if (un == w) dec_input_issue<T, kDecodeThreads>(a, l, ir);
     const uint64_t bal = __ballot(keep);
     const int rank = __popcll(bal & ((1ull << lane) - 1ull));
     if (lane == 0) sm.wcnt[wv] = __popcll(bal);
@@ -481,11 +477,31 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
     const int hn = (mn + 1) / 2;
     const int b = i0 + hf * hn, e = i0 + min(mn, (hf + 1) * hn);
     if (l == 0 && un == w) SATS_TRACE_POINT(4);
-    u32x4 bu[R][NCH], bd[R][NCH];
-    for (int r0 = 0; r0 < hn; r0 += R) {  // both halves run the same number of batches
-      rows_issue<T, R, NCH>(Wu, Wd, sm, b + r0, e, d, bu, bd);
-      rows_consume<T, R, NCH>(sm, hreg, yacc, b + r0, e, par, bu, bd);
+    // batches of RB rows in two register sets: the next batch is always in
+    // flight while one is used (both halves run the same number of batches)
+    const int nbt = (hn + RB - 1) / RB;
+    u32x4 au[RB][NCH], ad[RB][NCH], cu[RB][NCH], cd[RB][NCH];
+    if (nbt > 0) rows_issue<T, RB, NCH>(Wu, Wd, sm, b, e, d, au, ad);
+    if (nbt > 1) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + RB, e, d, cu, cd);
+    if (un == w) {
+      dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, false);
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+          const int k = (hw + c * 8) * CH + lane * VEC + v;
+          hreg[c][v] = (k < d) ? sm.hs[k] : 0.0f;
+        }
+    }
+    for (int i = 0; i < nbt; i += 2) {
+      rows_consume<T, RB, NCH>(sm, hreg, yacc, b + i * RB, e, par, au, ad);
       par ^= 1;
+      if (i + 2 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
+      if (i + 1 < nbt) {
+        rows_consume<T, RB, NCH>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd);
+        par ^= 1;
+        if (i + 3 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
+      }
     }
     __syncthreads();  // the next unit rewrites the list
   }
@@ -561,6 +577,8 @@ __device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm) {
 template <typename T>
 __global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
+  if (blockIdx.x == 0 && threadIdx.x == 0)  // the previous rows launch has finished
+    __hip_atomic_store(a.done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (l == 0 && blockIdx.x == 0 && threadIdx.x == 0) {
     const int base = token_is_base(a.route_mode, a.ids, a.lut, 0);
     a.state[0] = base;
@@ -571,20 +589,43 @@ __global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, in
   if (l == 0) SATS_TRACE_POINT(2);
 }
 
-// Rows: G workgroups; reduce: RW workgroups.
+// Rows: G workgroups, then the second reduction stage: the last RW of them
+// to finish each sum one slice of y over every partial (workgroup order).
+// They wait only for workgroups that are running or done, with nothing of
+// their own in flight; the wait is bounded (it raises the device error
+// flag instead of hanging).  The count goes back to zero at the start of the
+// next gate launch (which always comes before the next rows launch).
+constexpr int kSpinLimit = 1 << 20;  // polls of one wait (each a device-coherent load)
+
 template <typename T>
 __global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
   if (l == 0) SATS_TRACE_POINT(3);
   dec_rows<T>(a, l, a.state[0], a.G, blockIdx.x, sm);
-}
-
-template <typename T>
-__global__ __launch_bounds__(kDecodeThreads) void dec_reduce_kernel(DecodeArgs a, int l) {
-  __shared__ DecodeSmem sm;
+  const int tid = threadIdx.x, G = a.G;
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial-y stores have completed
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __syncthreads();
+  if (tid == 0) sm.flag = (int)__hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  const int ticket = sm.flag;
+  if (ticket < G - a.RW) return;
+  if (tid == 0) {
+    int polls = 0;
+    while (__hip_atomic_load(a.done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (unsigned)G) {
+      if (++polls >= kSpinLimit) {
+        __hip_atomic_store(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __syncthreads();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
   if (l == 0) SATS_TRACE_POINT(6);
-  dec_reduce<T>(a, l, blockIdx.x, sm);
+  dec_reduce<T>(a, l, ticket - (G - a.RW), sm);
   if (l == 0) SATS_TRACE_POINT(7);
 }
+
 
 }  // namespace sats

@@ -219,6 +219,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
 // running.
 constexpr size_t kCtl = 512;
 constexpr size_t kErr = 320;
+constexpr size_t kDone = 322;  // single-token rows launch: partials written (second-stage reduction)
 
 size_t counter_count(const Plan &p, int64_t pass, const DecodePlan &dp) {
   const int64_t tiles = ((pass + 3) / 4) * 4;
@@ -286,8 +287,12 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp) {
   nrc = std::min<int64_t>(nrc, std::max<int64_t>(1, d / (sats::kGateThreads / 64)));  // a row per wavefront
   q.nrc = (int)nrc;
   q.gate_grid = q.nblk * q.nrc;
-  // reduce: 32 columns (128 bytes of each partial) per workgroup
-  q.RW = (int)std::min<int64_t>(sats::kDecodeMaxG, std::max<int64_t>(1, (d + 31) / 32));
+  // second reduction stage: the last RW rows workgroups to finish take one
+  // slice of y each, 32 columns (128 bytes of each partial) or more; RW is
+  // kept to a quarter of the CUs so that the reducers, which wait for the
+  // others, never fill the device
+  q.RW = (int)std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32), std::max(1, device_cus() / 4));
+  q.RW = std::min(q.RW, G);
   const bool ok = G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
                   (d + q.RW - 1) / q.RW <= sats::kDecodeThreads;
   *dp = ok ? q : DecodePlan{};
@@ -532,13 +537,16 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   a.G = dp.G;
   a.RW = dp.RW;
   a.ypart = b.ypart;
+  a.done = counters + kDone;
+  a.err = counters + kErr;
   a.ybuf = b.ybuf;
   a.sspart = b.sspart;
   a.route_out = c.route_out;
   const bool lists = c.active_count || c.active_idx;
   a.keep_out = lists ? b.keep : nullptr;
   a.layer_in = c.layer_in;
-  // three plain launches per layer; kernel boundaries order the phases
+  // two plain launches per layer (the rows launch ends with the second
+  // reduction stage); kernel boundaries order the phases
   for (int l = 0; l < (int)c.L; ++l) {
     {
       TimedLaunch tl(SATS_K_DEC_GATE, c.stream);
@@ -549,12 +557,6 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
     {
       TimedLaunch tl(SATS_K_DEC_ROWS, c.stream);
       hipExtLaunchKernelGGL((dec_rows_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
-                            tl.start, tl.stop, 0, a, l);
-    }
-    HIP_TRY(hipGetLastError());
-    {
-      TimedLaunch tl(SATS_K_DEC_REDUCE, c.stream);
-      hipExtLaunchKernelGGL((dec_reduce_kernel<T>), dim3(dp.RW), dim3(kDecodeThreads), 0, c.stream,
                             tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
@@ -825,7 +827,6 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_DENSE: return "dense_mfma_kernels";
     case SATS_K_DEC_GATE: return "dec_gate_kernel";
     case SATS_K_DEC_ROWS: return "dec_rows_kernel";
-    case SATS_K_DEC_REDUCE: return "dec_reduce_kernel";
     default: return "";
   }
 }
