@@ -22,4 +22,4 @@ glue of a stack (``mlp.glue``) is a convention of this library, not something
 the paper defines: parity unpinned by the paper (pinned only by its own
 invariants).
 """
-from . import numerics, mlp, calibrate  # noqa: F401
+from . import numerics, mlp, calibrate, sats  # noqa: F401
