@@ -151,6 +151,52 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
  */
 int sats_device_status(hipStream_t stream);
 
+/*
+ * SATS calibration (Section 3.1, Eq. 6-10): the offline step that produces
+ * the per-layer thresholds the forward calls take.  Unlike the forward
+ * calls, these take and return their small arrays in HOST memory, allocate
+ * device buffers of their own, and synchronise `stream` before returning.
+ *
+ * sats_calibration_curves -- one layer.  h [n][d] holds the layer's inputs
+ * for n calibration rows (device, bf16; the base-path inputs in a stack),
+ * W_gate [d][d_ff], W_up_T [d_ff][d], W_down [d_ff][d] (device, bf16).  For
+ * each level q_k of levels[n_levels] (host, ascending in [0, 1]) the
+ * candidate threshold t_k is the Eq. 3 order statistic v_(ceil(q_k N)) of the
+ * N = n d_ff post-gate magnitudes |SiLU(h W_gate)| (q_k = 0 gives t_k = 0;
+ * q_k is taken to 1e-6), and
+ *   err_out[k] = Err(t_k) = mean over rows of ||y - y_t|| / (||y|| + 1e-6)   (Eq. 6)
+ *   sp_out[k]  = #{|g| < t_k} / N                      (the layer sparsity at t_k)
+ * with y the dense MLP output of the row and y_t the output with the neurons
+ * of |g| < t_k removed.  t_out, err_out, sp_out: host arrays [n_levels];
+ * err_rows (device float [n][n_levels], or NULL) receives the per-row terms.
+ * g and u accumulate in float32; p = g u enters the error product as two
+ * bf16 terms (about 16 bits of p); the sums have a fixed order.
+ * Shapes: d a multiple of 128 up to 4096, d_ff a multiple of 64.
+ *
+ * sats_calibrate_sats -- a stack.  The n_cal rows of x_cal (device bf16
+ * [n_cal][d]) run through the base path of the n_layers-layer stack (the
+ * forward calls' own inter-layer normalisation); every layer's curves are
+ * measured on its inputs at the candidate levels 0, coarse_step,
+ * 2 coarse_step, ... (Eq. 3 percentiles); for a budget b each layer takes
+ * its largest candidate with Err <= b (Eq. 7), S(b) is the mean layer
+ * sparsity (Eq. 9), and b* minimises |S(b) - s_tar| over every distinct
+ * error value (Eq. 10; the smallest b on ties).  Then, per layer, levels
+ * fine_step apart between the coarse levels around its choice are added
+ * and b* is chosen again.  With guardrail != 0 (and n_layers > 1) the last
+ * layer keeps its CATS threshold at level s_tar (its sparsity counts in S).
+ * thresholds_out: host float [n_layers]; budget_out, realized_out: host
+ * doubles (may be NULL) receiving b* and S(b*).
+ */
+int sats_calibration_curves(const sats_bf16 *h, const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                            const sats_bf16 *W_down, int64_t n, int64_t d, int64_t d_ff,
+                            const double *levels, int64_t n_levels, float *t_out, double *err_out,
+                            double *sp_out, float *err_rows, hipStream_t stream);
+int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *W_gate,
+                        const sats_bf16 *W_up_T, const sats_bf16 *W_down, int64_t d, int64_t d_ff,
+                        int64_t n_layers, double s_tar, double coarse_step, double fine_step,
+                        int guardrail, float *thresholds_out, double *budget_out,
+                        double *realized_out, hipStream_t stream);
+
 /* Free every workspace of the calling process (synchronises each device). */
 int sats_release(void);
 

@@ -141,11 +141,13 @@ def fine_levels(q, coarse, fine_step):
 
 
 def calibrate(x_cal, W_gate, W_up_T, W_down, s_tar, dtype, coarse_step=0.05, fine_step=0.005,
-              guardrail=True, eps=ERR_EPS):
+              guardrail=True, eps=ERR_EPS, layer_inputs=None):
     """SATS thresholds for a stack (coarse-to-fine search of Eq. 7-10).
 
     Calibration tokens run through the base stack with the inter-layer glue;
-    at every layer the candidate curves are measured on that layer's inputs.
+    at every layer the candidate curves are measured on that layer's inputs
+    (or on layer_inputs[l], stored values, when given: lets a comparison use
+    another implementation's own layer inputs).
     Returns a dict: thresholds (float32 [L]), budget b*, realized S(b*), and
     the per-layer candidate sets, error and sparsity curves of both stages.
     """
@@ -154,6 +156,8 @@ def calibrate(x_cal, W_gate, W_up_T, W_down, s_tar, dtype, coarse_step=0.05, fin
     coarse = coarse_levels(coarse_step)
     layers = []
     for l in range(L):
+        if layer_inputs is not None:
+            H = decode(layer_inputs[l], dtype)
         wg, wu, wd = (decode(w[l], dtype) for w in (W_gate, W_up_T, W_down))
         g, p, y = layer_terms(H, wg, wu, wd)
         absg = np.abs(g)

@@ -38,6 +38,8 @@ SIGNATURES = {
     "sats_timing_begin": ([_N, _N], _N),
     "sats_timing_end": ([_N, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], _N),
     "sats_kernel_name": ([_N], ctypes.c_char_p),
+    "sats_calibration_curves": ([_P] * 4 + [_I] * 3 + [_P, _I] + [_P] * 4 + [_S], _N),
+    "sats_calibrate_sats": ([_P, _I] + [_P] * 3 + [_I] * 3 + [ctypes.c_double] * 3 + [_N] + [_P] * 3 + [_S], _N),
 }
 
 
@@ -167,3 +169,41 @@ def _is_f32(x) -> bool:
     if x.dtype == torch.bfloat16:
         return False
     raise ValueError(f"x must be bfloat16 or float32, got {x.dtype}")
+
+
+def _host(a, dtype):
+    import numpy as np
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def sats_calibration_curves(h, W_gate, W_up_T, W_down, n, d, d_ff, levels, err_rows=None, stream=None):
+    """SATS curves of one layer (Eq. 3 candidates at `levels`, Eq. 6 errors, sparsities).
+
+    h and the weights are device tensors (bf16); levels is a host sequence.
+    Returns host arrays (t float32, err float64, sp float64); synchronises.
+    """
+    import numpy as np
+    lv = _host(levels, np.float64)
+    t = np.zeros(len(lv), np.float32)
+    err = np.zeros(len(lv), np.float64)
+    sp = np.zeros(len(lv), np.float64)
+    _call("sats_calibration_curves", _ptr(h), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down), n, d, d_ff,
+          lv.ctypes.data, len(lv), t.ctypes.data, err.ctypes.data, sp.ctypes.data, _ptr(err_rows),
+          _stream(stream))
+    return t, err, sp
+
+
+def sats_calibrate_sats(x_cal, n_cal, W_gate, W_up_T, W_down, d, d_ff, n_layers, s_tar,
+                        coarse_step=0.05, fine_step=0.005, guardrail=True, stream=None):
+    """SATS thresholds of a stack (Eq. 7-10, coarse to fine, final-layer guardrail).
+
+    Returns (thresholds float32 [n_layers], budget b*, realized sparsity S(b*)); synchronises.
+    """
+    import numpy as np
+    ts = np.zeros(n_layers, np.float32)
+    b = ctypes.c_double(0.0)
+    s = ctypes.c_double(0.0)
+    _call("sats_calibrate_sats", _ptr(x_cal), n_cal, _ptr(W_gate), _ptr(W_up_T), _ptr(W_down), d, d_ff,
+          n_layers, float(s_tar), float(coarse_step), float(fine_step), int(bool(guardrail)),
+          ts.ctypes.data, ctypes.addressof(b), ctypes.addressof(s), _stream(stream))
+    return ts, b.value, s.value

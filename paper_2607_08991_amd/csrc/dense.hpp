@@ -119,6 +119,8 @@ struct DenseArgs {
   uint16_t *P;            // gate/up output p, [n_dense][N] bf16
   float *part;            // down output partials, [KSPLIT][n_dense][N]
   int K, N, kchunk;       // reduction length, output columns, k per split (down)
+  float *cal_g;           // calibration (gate/up): g = SiLU(a) in float32, [rows][N] (P unused) ...
+  uint16_t *cal_ph, *cal_pl;  // ... and p = g u as two bf16 terms, hi = rne(p), lo = rne(p - hi)
 };
 
 // ---------------------------------------------------------------- MFMA GEMMs
@@ -290,6 +292,26 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
       for (int r = 0; r < 4; ++r) xs[(16 * mt + 4 * g + r) * kDenseXP + c] = silu(acc[mt][r]);
   }
   __syncthreads();
+  if (a.cal_g) {  // calibration: g and p = g u (float32, no keep rule), p split into bf16 hi + lo
+    if (mat == 1) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = 16 * mt + 4 * g + r;
+          if (m < nd) {
+            const float gv = xs[m * kDenseXP + c];
+            const float pv = gv * acc[mt][r];
+            const uint16_t hi = f32_to_bf16(pv);
+            const size_t o = (size_t)m * N + n0 + c;
+            a.cal_g[o] = gv;
+            a.cal_ph[o] = hi;
+            a.cal_pl[o] = f32_to_bf16(pv - bf16_to_f32(hi));
+          }
+        }
+    }
+    return;
+  }
   if (mat == 1) {
     const float thr = a.thr ? *a.thr : 0.0f;
 #pragma unroll
@@ -376,6 +398,126 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
           *reinterpret_cast<const f32x4v *>((m < 32 ? x0 : x1) + (m & 31) * XP + 4 * q);
   }
 }
+// ---------------------------------------------------------------- SATS error curves
+//
+// Eq. 6 for one layer and up to 15 candidate thresholds t_0 <= ... <= t_14
+// (missing ones +inf).  For calibration row m, y - y_t = sum over the
+// neurons removed at t (|g_j| < t) of p_j W_down[j]; every candidate is one
+// row of a product with W_down: row (m, r) of A is p_m masked to the
+// neurons removed at t_r, and row (m, 15) is p_m itself (y).  The removed
+// test is an integer compare: c[m][j] = #{r : t_r <= |g_mj|} counts the
+// candidates at or below the neuron's magnitude, and neuron j is removed at
+// t_r exactly when c <= r.  p enters as two bf16 terms (p = hi + lo, lo the
+// rounded remainder), so that hi W + lo W carries about 16 bits of p into
+// float32 accumulation.  Each workgroup takes 16 calibration rows and 128
+// output columns (wavefront w: columns 16 w .. 16 w + 15, one 16 x 16 MFMA
+// tile per calibration row), walks all of d_ff in stages of 64 rows (W_down
+// 16 KB, hi and lo 2 KB each, c 1 KB), and writes, per row (m, r), the sum of
+// the squares of its 128 outputs: the partial of ||y - y_t||^2 (and ||y||^2)
+// for that column tile.  The row norms are finished by cal_reduce_kernel.
+
+struct CalErrArgs {
+  const uint16_t *ph, *pl;  // [n][d_ff] bf16 hi and lo terms of p
+  const uint8_t *cnt;       // [n][d_ff] candidates at or below |g|
+  const uint16_t *Wd;       // W_down of the layer, [d_ff][d]
+  float *part;              // [d / 128][n][16] column-tile sums of squares
+  int n, d, d_ff;
+};
+
+constexpr int kCalRows = 16;  // calibration rows per workgroup
+
+__global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
+  __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
+      rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
+  constexpr int TT = kCalRows;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, l16 = lane & 15, c = 16 * w + l16;
+  const int n0 = blockIdx.x * kDenseDownNT, m0 = blockIdx.y * TT;
+  const int K = a.d_ff, N = a.d;
+  const int S = K / kDenseKC;
+  const __amdgpu_buffer_rsrc_t rsw = dense_rsrc(a.Wd, (uint32_t)((size_t)K * N * 2));
+  const uint32_t pbytes = (uint32_t)((size_t)a.n * K * 2);
+  const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.ph, pbytes), rsl = dense_rsrc(a.pl, pbytes);
+  const __amdgpu_buffer_rsrc_t rsc = dense_rsrc(a.cnt, (uint32_t)((size_t)a.n * K));
+  // W_down rows as in dense_down_kernel: wavefront w loads rows 8 w .. 8 w + 7
+  const int wr = 8 * w + (lane >> 4), wp = lane & 15;
+  const uint32_t ow0 = (uint32_t)(((size_t)wr * N + n0 + 8 * krow_pos(wr, wp)) * 2);
+  const uint32_t ow1 = (uint32_t)(((size_t)(wr + 4) * N + n0 + 8 * krow_pos(wr + 4, wp)) * 2);
+  // hi and lo: wavefronts 0-1 and 2-3, 16 rows x 128 bytes each (lane: row, 16-byte chunk);
+  // c: wavefront 4, 16 rows x 64 bytes
+  const int ar = 8 * (w & 1) + (lane >> 3), aq = lane & 7;
+  const bool arv = m0 + ar < a.n;
+  const uint32_t oa = (uint32_t)(((size_t)(m0 + ar) * K + 8 * aq) * 2);
+  const int cr = lane >> 2, cq = lane & 3;
+  const bool crv = m0 + cr < a.n;
+  const uint32_t oc = (uint32_t)((size_t)(m0 + cr) * K + 16 * cq);
+  const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;
+  f32x4v acc[TT];
+#pragma unroll
+  for (int t = 0; t < TT; ++t) acc[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
+#define SATS_CE_ISSUE(BUF, SN)                                                               \
+  {                                                                                          \
+    const bool v_ = (SN) < S;                                                                \
+    const uint32_t ss_ = (uint32_t)(SN);                                                     \
+    dma16<2>(rsw, (BUF) + w * 2048, dense_off(v_, ow0 + ss_ * sw, 0));                       \
+    dma16<2>(rsw, (BUF) + w * 2048 + 1024, dense_off(v_, ow1 + ss_ * sw, 1));                \
+    if (w < 4)                                                                               \
+      dma16<0>(w < 2 ? rsh : rsl, (BUF) + 16384 + w * 1024, dense_off(v_ && arv, oa + ss_ * sk, 2)); \
+    else if (w == 4)                                                                         \
+      dma16<0>(rsc, (BUF) + 20480, dense_off(v_ && crv, oc + ss_ * kDenseKC, 2));            \
+    else                                                                                     \
+      dma16<0>(rsc, (BUF) + 21504 + (w - 5) * 1024, kDenseOffNone + 48u);                    \
+  }
+  // A operand of candidate row l16 for calibration row t: k = 32 j + 8 g .. + 7
+  // of the stage; hi or lo, zero where the neuron is kept at t_l16 (row 15: p itself)
+#define SATS_CE_COMPUTE(BUF)                                                                 \
+  {                                                                                          \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                          \
+      const bf16x8 b_ = krow_operand((BUF), 256, c, j, g);                                   \
+      _Pragma("unroll") for (int t = 0; t < TT; ++t) {                                       \
+        const int k_ = 32 * j + 8 * g;                                                       \
+        const u32x4 hv_ = *reinterpret_cast<const u32x4 *>((BUF) + 16384 + t * 128 + 2 * k_); \
+        const u32x4 lv_ = *reinterpret_cast<const u32x4 *>((BUF) + 18432 + t * 128 + 2 * k_); \
+        const uint2 cv_ = *reinterpret_cast<const uint2 *>((BUF) + 20480 + t * 64 + k_);      \
+        u32x4 mh_, ml_;                                                                      \
+        _Pragma("unroll") for (int q = 0; q < 4; ++q) {                                      \
+          const uint32_t cw_ = q < 2 ? cv_.x : cv_.y;                                        \
+          const uint32_t c0_ = (cw_ >> (16 * (q & 1))) & 0xffu, c1_ = (cw_ >> (16 * (q & 1) + 8)) & 0xffu; \
+          const uint32_t keep_ = (c0_ <= (uint32_t)l16 ? 0x0000ffffu : 0u) | (c1_ <= (uint32_t)l16 ? 0xffff0000u : 0u); \
+          mh_[q] = hv_[q] & keep_;                                                           \
+          ml_[q] = lv_[q] & keep_;                                                           \
+        }                                                                                    \
+        acc[t] = mfma16(__builtin_bit_cast(bf16x8, mh_), b_, acc[t]);                        \
+        acc[t] = mfma16(__builtin_bit_cast(bf16x8, ml_), b_, acc[t]);                        \
+      }                                                                                      \
+    }                                                                                        \
+  }
+  SATS_DENSE_RING(S, SATS_CE_ISSUE, SATS_CE_COMPUTE)
+#undef SATS_CE_ISSUE
+#undef SATS_CE_COMPUTE
+  // sums of squares over the tile's 128 columns: 16 columns per wavefront by
+  // lane exchange, then the 8 wavefronts in order through LDS
+  __syncthreads();
+  float *xs = reinterpret_cast<float *>(rg0);  // [8 wavefronts][TT][16 rows]
+#pragma unroll
+  for (int t = 0; t < TT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v = acc[t][r] * acc[t][r];
+#pragma unroll
+      for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 16);
+      if (l16 == 0) xs[(w * TT + t) * 16 + 4 * g + r] = v;
+    }
+  __syncthreads();
+  if (threadIdx.x < TT * 16) {
+    const int t = threadIdx.x >> 4, r = threadIdx.x & 15;
+    float s = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += xs[(q * TT + t) * 16 + r];
+    if (m0 + t < a.n) a.part[((size_t)blockIdx.x * a.n + m0 + t) * 16 + r] = s;
+  }
+}
+
 #undef SATS_DENSE_RING
 #undef SATS_DENSE_STEP
 

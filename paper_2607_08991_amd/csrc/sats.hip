@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -18,6 +19,7 @@
 #include "kernels.hpp"
 #include "decode.hpp"
 #include "dense.hpp"
+#include "calib.hpp"
 
 namespace {
 
@@ -643,6 +645,318 @@ Call make_call(const void *x, const int32_t *ids, const void *Wg, const void *Wu
 
 int route_mode_of(const uint8_t *lut) { return lut ? sats::ROUTE_LUT : sats::ROUTE_SPARSE; }
 
+
+// --------------------------------------------------------------- SATS calibration
+
+// Device buffers of one calibration call (allocated per call: calibration is
+// an offline step, and its buffers are sized by the calibration set).
+struct CalBuffers {
+  float *G = nullptr;              // [n][d_ff] g
+  uint16_t *ph = nullptr, *pl = nullptr;  // [n][d_ff] p as bf16 hi + lo
+  uint8_t *cnt = nullptr;          // [n][d_ff] candidates at or below |g|
+  float *part = nullptr;           // [d / 128][n][16]
+  uint32_t *hist0 = nullptr, *hist1 = nullptr, *hist2 = nullptr, *prefix = nullptr, *rank = nullptr;
+  float *tk = nullptr, *thr15 = nullptr;
+  unsigned long long *hist16 = nullptr;
+  double *errsum = nullptr;
+  int *ctl = nullptr;              // [passes][2] rows of each gate/up pass, MFMA on
+  ~CalBuffers() {
+    for (void *q : {(void *)G, (void *)ph, (void *)pl, (void *)cnt, (void *)part, (void *)hist0, (void *)hist1,
+                    (void *)hist2, (void *)prefix, (void *)rank, (void *)tk, (void *)thr15, (void *)hist16,
+                    (void *)errsum, (void *)ctl})
+      if (q) (void)hipFree(q);
+  }
+};
+
+template <typename P> int cal_alloc(P **p, size_t count) {
+  if (hipMalloc((void **)p, std::max<size_t>(count, 1) * sizeof(P)) != hipSuccess)
+    return fail(SATS_ERR_WORKSPACE, "calibration buffer of %zu bytes failed", count * sizeof(P));
+  return SATS_OK;
+}
+
+// Rank m = ceil(q N) of the Eq. 3 order statistic at level q (q taken to 1e-6).
+uint64_t level_rank(double q, uint64_t N) {
+  if (!(q > 0.0)) return 0;
+  const uint64_t qi = (uint64_t)std::llround(std::min(q, 1.0) * 1e6);
+  const unsigned __int128 num = (unsigned __int128)qi * N + 999999u;
+  const uint64_t m = (uint64_t)(num / 1000000u);
+  return std::max<uint64_t>(1, std::min<uint64_t>(m, N));
+}
+
+int cal_check_shape(int64_t n, int64_t d, int64_t d_ff) {
+  if (n < 1 || d < 1 || d_ff < 1)
+    return fail(SATS_ERR_SHAPE, "calibration needs n, d, d_ff >= 1");
+  if (d % sats::kDenseDownNT || d % sats::kDenseKC || d_ff % sats::kDenseNT || d_ff % sats::kDenseKC || d > 4096)
+    return fail(SATS_ERR_SHAPE, "calibration needs d a multiple of 128 (at most 4096) and d_ff of 64");
+  if ((uint64_t)d * d_ff * 2 >= (1ull << 31) || (uint64_t)n * d_ff * 2 >= (1ull << 31))
+    return fail(SATS_ERR_SHAPE, "calibration buffers past 2 GB");
+  return SATS_OK;
+}
+
+// g and p of n calibration rows (MFMA, 64 rows per pass) into G, ph, pl.
+int cal_gate_up(const uint16_t *h, const uint16_t *Wg, const uint16_t *Wu, int64_t n, int64_t d, int64_t d_ff,
+                CalBuffers &cb, hipStream_t s) {
+  using namespace sats;
+  const int64_t passes = (n + kDenseMaxTokens - 1) / kDenseMaxTokens;
+  std::vector<int> ctl(2 * passes);
+  for (int64_t i = 0; i < passes; ++i) {
+    ctl[2 * i] = (int)std::min<int64_t>(kDenseMaxTokens, n - i * kDenseMaxTokens);
+    ctl[2 * i + 1] = 1;
+  }
+  HIP_TRY(hipMemcpyAsync(cb.ctl, ctl.data(), ctl.size() * sizeof(int), hipMemcpyHostToDevice, s));
+  for (int64_t i = 0; i < passes; ++i) {
+    DenseArgs da{};
+    da.ctl = cb.ctl + 2 * i;
+    da.H = h + i * kDenseMaxTokens * d;
+    da.Wb = Wg;
+    da.Wt = Wu;
+    da.K = (int)d;
+    da.N = (int)d_ff;
+    const size_t o = (size_t)i * kDenseMaxTokens * d_ff;
+    da.cal_g = cb.G + o;
+    da.cal_ph = cb.ph + o;
+    da.cal_pl = cb.pl + o;
+    hipLaunchKernelGGL(dense_gateup_kernel<4>, dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, s, da);
+    HIP_TRY(hipGetLastError());
+  }
+  return SATS_OK;
+}
+
+// Eq. 3 order statistics of |g| at `levels` (up to kCalMaxLevels) into t (host).
+int cal_quantiles(CalBuffers &cb, uint64_t N, const double *levels, int K, float *t, hipStream_t s) {
+  using namespace sats;
+  std::vector<uint32_t> rank(K), zero(K, 0u);
+  for (int k = 0; k < K; ++k) rank[k] = (uint32_t)level_rank(levels[k], N);
+  HIP_TRY(hipMemcpyAsync(cb.rank, rank.data(), K * sizeof(uint32_t), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemcpyAsync(cb.prefix, zero.data(), K * sizeof(uint32_t), hipMemcpyHostToDevice, s));
+  const int grid = (int)std::min<uint64_t>(2048, (N + kCalThreads - 1) / kCalThreads);
+  HIP_TRY(hipMemsetAsync(cb.hist0, 0, 4096 * sizeof(uint32_t), s));
+  hipLaunchKernelGGL(cal_hist0_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.hist0);
+  hipLaunchKernelGGL(cal_select_kernel, dim3(1), dim3(kCalMaxLevels), 0, s, cb.hist0, (size_t)0, 4096, 12,
+                     cb.prefix, cb.rank, K, (float *)nullptr);
+  HIP_TRY(hipMemsetAsync(cb.hist1, 0, (size_t)K * 4096 * sizeof(uint32_t), s));
+  hipLaunchKernelGGL(cal_histk_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.prefix, K, 8, 4096,
+                     cb.hist1);
+  hipLaunchKernelGGL(cal_select_kernel, dim3(1), dim3(kCalMaxLevels), 0, s, cb.hist1, (size_t)4096, 4096, 12,
+                     cb.prefix, cb.rank, K, (float *)nullptr);
+  HIP_TRY(hipMemsetAsync(cb.hist2, 0, (size_t)K * 256 * sizeof(uint32_t), s));
+  hipLaunchKernelGGL(cal_histk_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.prefix, K, 0, 256,
+                     cb.hist2);
+  hipLaunchKernelGGL(cal_select_kernel, dim3(1), dim3(kCalMaxLevels), 0, s, cb.hist2, (size_t)256, 256, 8,
+                     cb.prefix, cb.rank, K, cb.tk);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync(t, cb.tk, K * sizeof(float), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return SATS_OK;
+}
+
+// Eq. 6 error and sparsity of ascending candidates t[0..K) (any K), 15 per
+// product.  err_rows (device, [n][K]) is optional.
+int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t d_ff, const float *t, int K,
+               double *err, double *sp, float *err_rows, hipStream_t s) {
+  using namespace sats;
+  const uint64_t N = (uint64_t)n * d_ff;
+  const int grid = (int)std::min<uint64_t>(2048, (N + kCalThreads - 1) / kCalThreads);
+  for (int k0 = 0; k0 < K; k0 += kCalCand) {
+    const int kc = std::min(kCalCand, K - k0);
+    float thr[kCalCand];
+    for (int r = 0; r < kCalCand; ++r) thr[r] = r < kc ? t[k0 + r] : INFINITY;
+    HIP_TRY(hipMemcpyAsync(cb.thr15, thr, sizeof thr, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemsetAsync(cb.hist16, 0, 16 * sizeof(unsigned long long), s));
+    hipLaunchKernelGGL(cal_bucket_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.thr15, cb.cnt,
+                       cb.hist16);
+    CalErrArgs ce{};
+    ce.ph = cb.ph;
+    ce.pl = cb.pl;
+    ce.cnt = cb.cnt;
+    ce.Wd = Wd;
+    ce.part = cb.part;
+    ce.n = (int)n;
+    ce.d = (int)d;
+    ce.d_ff = (int)d_ff;
+    hipLaunchKernelGGL(cal_err_kernel, dim3(d / kDenseDownNT, (n + kCalRows - 1) / kCalRows), dim3(kDenseThreads), 0,
+                       s, ce);
+    hipLaunchKernelGGL(cal_reduce_kernel, dim3(1), dim3(kCalReduceThreads), 0, s, cb.part,
+                       (int)(d / kDenseDownNT), (int)n, kc, err_rows ? err_rows + k0 : (float *)nullptr, K,
+                       cb.errsum);
+    HIP_TRY(hipGetLastError());
+    double es[kCalCand];
+    unsigned long long h16[16];
+    HIP_TRY(hipMemcpyAsync(es, cb.errsum, kc * sizeof(double), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(h16, cb.hist16, sizeof h16, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    unsigned long long below = 0;
+    for (int r = 0; r < kc; ++r) {
+      below += h16[r];  // #{c <= r} = #{|g| < t_r}
+      err[k0 + r] = es[r] / (double)n;
+      sp[k0 + r] = (double)below / (double)N;
+    }
+  }
+  return SATS_OK;
+}
+
+int cal_buffers(CalBuffers &cb, int64_t n, int64_t d, int64_t d_ff) {
+  const size_t N = (size_t)n * d_ff;
+  int rc = 0;
+  if ((rc = cal_alloc(&cb.G, N)) || (rc = cal_alloc(&cb.ph, N)) || (rc = cal_alloc(&cb.pl, N)) ||
+      (rc = cal_alloc(&cb.cnt, N)) || (rc = cal_alloc(&cb.part, (size_t)(d / sats::kDenseDownNT) * n * 16)) ||
+      (rc = cal_alloc(&cb.hist0, 4096)) || (rc = cal_alloc(&cb.hist1, (size_t)sats::kCalMaxLevels * 4096)) ||
+      (rc = cal_alloc(&cb.hist2, (size_t)sats::kCalMaxLevels * 256)) || (rc = cal_alloc(&cb.prefix, sats::kCalMaxLevels)) ||
+      (rc = cal_alloc(&cb.rank, sats::kCalMaxLevels)) || (rc = cal_alloc(&cb.tk, sats::kCalMaxLevels)) ||
+      (rc = cal_alloc(&cb.thr15, sats::kCalCand)) || (rc = cal_alloc(&cb.hist16, 16)) ||
+      (rc = cal_alloc(&cb.errsum, sats::kCalCand)) ||
+      (rc = cal_alloc(&cb.ctl, 2 * ((n + sats::kDenseMaxTokens - 1) / sats::kDenseMaxTokens))))
+    return rc;
+  return SATS_OK;
+}
+
+// One layer: candidates at `levels` and their curves (host outputs).
+int cal_layer(CalBuffers &cb, const uint16_t *h, const uint16_t *Wg, const uint16_t *Wu, const uint16_t *Wd, int64_t n,
+              int64_t d, int64_t d_ff, const double *levels, int K, float *t, double *err, double *sp, float *err_rows,
+              hipStream_t s, bool gate_up = true) {
+  int rc = 0;
+  if (gate_up && (rc = cal_gate_up(h, Wg, Wu, n, d, d_ff, cb, s))) return rc;
+  for (int k0 = 0; k0 < K; k0 += sats::kCalMaxLevels)
+    if ((rc = cal_quantiles(cb, (uint64_t)n * d_ff, levels + k0, std::min(sats::kCalMaxLevels, K - k0), t + k0, s)))
+      return rc;
+  return cal_curves(cb, Wd, n, d, d_ff, t, K, err, sp, err_rows, s);
+}
+
+struct CalCurve {
+  std::vector<double> level, t, err, sp;
+};
+
+// b* over the breakpoints of S(b) (Eq. 7-10): for each distinct error value
+// b (and 0), every free layer takes its largest candidate with Err <= b; S
+// is the mean sparsity over all layers (fixed ones at their own); the
+// budget whose S is nearest the target wins, the smallest on ties.
+void cal_select(const std::vector<CalCurve> &cv, const std::vector<int> &fixed, const std::vector<double> &fixed_sp,
+                double s_tar, double *b_out, std::vector<int> *idx_out, double *s_out) {
+  const size_t L = cv.size();
+  std::vector<double> budgets{0.0};
+  for (size_t l = 0; l < L; ++l)
+    if (!fixed[l]) budgets.insert(budgets.end(), cv[l].err.begin(), cv[l].err.end());
+  std::sort(budgets.begin(), budgets.end());
+  budgets.erase(std::unique(budgets.begin(), budgets.end()), budgets.end());
+  bool have = false;
+  for (double b : budgets) {
+    std::vector<int> idx(L, -1);
+    double S = 0.0;
+    for (size_t l = 0; l < L; ++l) {
+      if (fixed[l]) {
+        S += fixed_sp[l];
+        continue;
+      }
+      int best = -1;  // the largest admissible threshold (t = 0, Err = 0, is always admissible)
+      for (size_t k = 0; k < cv[l].t.size(); ++k)
+        if (cv[l].err[k] <= b && (best < 0 || cv[l].t[k] > cv[l].t[best])) best = (int)k;
+      best = std::max(best, 0);
+      idx[l] = best;
+      S += cv[l].sp[best];
+    }
+    S /= (double)L;
+    if (!have || std::fabs(S - s_tar) < std::fabs(*s_out - s_tar)) {
+      have = true;
+      *b_out = b;
+      *idx_out = idx;
+      *s_out = S;
+    }
+  }
+}
+
+// candidate levels: 0 and step, 2 step, ... below 1
+std::vector<double> cal_coarse(double step) {
+  std::vector<double> v{0.0};
+  const int n = (int)std::lround(1.0 / step);
+  for (int i = 1; i < n; ++i) v.push_back(std::round(i * step * 1e10) / 1e10);
+  return v;
+}
+// levels fine apart strictly between the coarse neighbours of q
+std::vector<double> cal_fine(double q, const std::vector<double> &coarse, double fine) {
+  double lo = 0.0, hi = 1.0;
+  for (double c : coarse) {
+    if (c > 0.0 && c < q - 1e-12) lo = std::max(lo, c);
+    if (c > q + 1e-12) hi = std::min(hi, c);
+  }
+  std::vector<double> v;
+  for (int i = 1; lo + i * fine < hi - 1e-9; ++i) v.push_back(std::round((lo + i * fine) * 1e10) / 1e10);
+  return v;
+}
+
+int cal_stack(const uint16_t *x, int64_t n, const uint16_t *Wg, const uint16_t *Wu, const uint16_t *Wd, int64_t d,
+              int64_t d_ff, int64_t L, double s_tar, double coarse_step, double fine_step, int guardrail,
+              float *thresholds, double *budget, double *realized, hipStream_t s) {
+  int rc = cal_check_shape(n, d, d_ff);
+  if (rc) return rc;
+  if (L < 1 || !(coarse_step > 0.0 && coarse_step < 1.0) || !(fine_step > 0.0) || !(s_tar >= 0.0 && s_tar <= 1.0))
+    return fail(SATS_ERR_ARG, "calibration needs L >= 1, 0 < coarse_step < 1, fine_step > 0, 0 <= s_tar <= 1");
+  const size_t wl = (size_t)d * d_ff;
+  // every layer's input on the base path (the stack's own forward, inputs exported)
+  uint16_t *hin = nullptr, *out = nullptr;
+  if ((rc = cal_alloc(&hin, (size_t)L * n * d)) || (rc = cal_alloc(&out, (size_t)n * d))) {
+    if (hin) (void)hipFree(hin);
+    return rc;
+  }
+  struct Free {
+    uint16_t *a, *b;
+    ~Free() { (void)hipFree(a); (void)hipFree(b); }
+  } fr{hin, out};
+  Call c = make_call(x, nullptr, Wg, Wu, Wd, nullptr, nullptr, out, n, d, d_ff, L, s, sats::ROUTE_BASE);
+  c.layer_in = hin;
+  if ((rc = run<uint16_t>(c))) return rc;
+  CalBuffers cb;
+  if ((rc = cal_buffers(cb, n, d, d_ff))) return rc;
+  const std::vector<double> coarse = cal_coarse(coarse_step);
+  std::vector<CalCurve> cv(L);
+  std::vector<int> fixed(L, 0);
+  std::vector<double> fixed_sp(L, 0.0);
+  std::vector<float> fixed_t(L, 0.0f);
+  auto layer_curves = [&](int64_t l, const std::vector<double> &lv, CalCurve &out_c, bool gate_up) -> int {
+    const int K = (int)lv.size();
+    std::vector<float> t(K);
+    std::vector<double> err(K), sp(K);
+    const int r = cal_layer(cb, hin + (size_t)l * n * d, Wg + l * wl, Wu + l * wl, Wd + l * wl, n, d, d_ff, lv.data(),
+                            K, t.data(), err.data(), sp.data(), nullptr, s, gate_up);
+    if (r) return r;
+    for (int k = 0; k < K; ++k) {
+      out_c.level.push_back(lv[k]);
+      out_c.t.push_back(t[k]);
+      out_c.err.push_back(err[k]);
+      out_c.sp.push_back(sp[k]);
+    }
+    return SATS_OK;
+  };
+  // stage 1: the coarse grid on every layer; the guardrail layer keeps its
+  // CATS threshold at the target sparsity
+  for (int64_t l = 0; l < L; ++l) {
+    if ((rc = layer_curves(l, coarse, cv[l], true))) return rc;
+    if (guardrail && L > 1 && l == L - 1) {
+      CalCurve g1;
+      if ((rc = layer_curves(l, {s_tar}, g1, false))) return rc;
+      fixed[l] = 1;
+      fixed_sp[l] = g1.sp[0];
+      fixed_t[l] = (float)g1.t[0];
+    }
+  }
+  double b1 = 0.0, s1 = 0.0;
+  std::vector<int> idx1;
+  cal_select(cv, fixed, fixed_sp, s_tar, &b1, &idx1, &s1);
+  // stage 2: finer levels around each free layer's choice, added to its candidates
+  for (int64_t l = 0; l < L; ++l) {
+    if (fixed[l]) continue;
+    const double q = cv[l].sp[idx1[l]];
+    const std::vector<double> fl = cal_fine(q, coarse, fine_step);
+    if (fl.empty()) continue;
+    if ((rc = layer_curves(l, fl, cv[l], true))) return rc;
+  }
+  double b2 = 0.0, s2 = 0.0;
+  std::vector<int> idx2;
+  cal_select(cv, fixed, fixed_sp, s_tar, &b2, &idx2, &s2);
+  for (int64_t l = 0; l < L; ++l) thresholds[l] = fixed[l] ? fixed_t[l] : (float)cv[l].t[idx2[l]];
+  if (budget) *budget = b2;
+  if (realized) *realized = s2;
+  return SATS_OK;
+}
 }  // namespace
 
 // =============================================================== C ABI
@@ -750,6 +1064,40 @@ int sats_release(void) {
   g_ws.clear();
   HIP_TRY(hipSetDevice(cur));
   return SATS_OK;
+}
+
+int sats_calibration_curves(const sats_bf16 *h, const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                            const sats_bf16 *W_down, int64_t n, int64_t d, int64_t d_ff, const double *levels,
+                            int64_t n_levels, float *t_out, double *err_out, double *sp_out, float *err_rows,
+                            hipStream_t stream) {
+  g_err.clear();
+  if (!h || !W_gate || !W_up_T || !W_down || !levels || !t_out || !err_out || !sp_out)
+    return fail(SATS_ERR_NULL, "h, weights, levels and the outputs must be non-null");
+  if (n_levels < 1 || n_levels > 4096) return fail(SATS_ERR_ARG, "1 <= n_levels <= 4096");
+  for (int64_t k = 0; k < n_levels; ++k)
+    if (!(levels[k] >= 0.0 && levels[k] <= 1.0) || (k && levels[k] < levels[k - 1]))
+      return fail(SATS_ERR_ARG, "levels must be ascending in [0, 1]");
+  int rc = cal_check_shape(n, d, d_ff);
+  if (rc) return rc;
+  CalBuffers cb;
+  if ((rc = cal_buffers(cb, n, d, d_ff))) return rc;
+  rc = cal_layer(cb, h, W_gate, W_up_T, W_down, n, d, d_ff, levels, (int)n_levels, t_out, err_out, sp_out, err_rows,
+                 stream);
+  if (!rc) HIP_TRY(hipStreamSynchronize(stream));
+  return rc;
+}
+
+int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                        const sats_bf16 *W_down, int64_t d, int64_t d_ff, int64_t n_layers, double s_tar,
+                        double coarse_step, double fine_step, int guardrail, float *thresholds_out,
+                        double *budget_out, double *realized_out, hipStream_t stream) {
+  g_err.clear();
+  if (!x_cal || !W_gate || !W_up_T || !W_down || !thresholds_out)
+    return fail(SATS_ERR_NULL, "x_cal, weights and thresholds_out must be non-null");
+  const int rc = cal_stack(x_cal, n_cal, W_gate, W_up_T, W_down, d, d_ff, n_layers, s_tar, coarse_step, fine_step,
+                           guardrail, thresholds_out, budget_out, realized_out, stream);
+  if (!rc) HIP_TRY(hipStreamSynchronize(stream));
+  return rc;
 }
 
 const char *sats_last_error(void) { return g_err.c_str(); }

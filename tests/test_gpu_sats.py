@@ -1,0 +1,147 @@
+"""GPU parity of SATS calibration (Section 3.1, Eq. 6-10) through the C ABI.
+
+Comparison rules (the GPU accumulates g and u in float32 and enters p as
+two bf16 terms; the oracle is float64 on the same stored values):
+  * candidate thresholds: the Eq. 3 order statistics agree to 1e-4 relative
+    (an order statistic of nearly identical values);
+  * errors and sparsities are compared at the GPU's own thresholds.  A
+    candidate is a sample magnitude, so at least one neuron sits exactly on
+    it, and neurons within float32 rounding of a threshold (1e-5 relative)
+    may be removed on one side and kept on the other: per row, the GPU's
+    error must lie (to 1e-4 relative) between the oracle's errors with those
+    neurons kept and with them removed, and the sparsity within their count;
+  * a stack: the oracle runs on the GPU's own layer inputs (exported by the
+    forward call), and the GPU's choice must be the oracle's, or one the
+    oracle scores equally close to the target sparsity.
+"""
+import numpy as np
+import pytest
+
+from harness import from_dev, to_dev
+from oracle import calibrate, numerics, sats as osats
+from workloads import synth
+
+pytestmark = pytest.mark.gpu
+
+LEVELS = sorted([0.0] + [round(0.05 * i, 4) for i in range(1, 20)] + [0.33, 0.5001, 0.999])
+
+
+def _layer(seed, d, dff, n, w_std=None):
+    c = synth.small_case(seed, 1, d, dff, "bf16", n, w_std=w_std or 1.0 / np.sqrt(d))
+    return c["x"], c["W_gate"][0], c["W_up_T"][0], c["W_down"][0]
+
+
+def _bounds(H, W, ts, rel=1e-5):
+    """Per row and candidate, the oracle's Eq. 6 term with the neurons within
+    `rel` of the threshold kept and with them removed (low, high), and the
+    number of such neurons per candidate."""
+    g, p, y = osats.layer_terms(H, *W)
+    a = np.abs(g)
+    ny = np.linalg.norm(y, axis=1)
+    lo = np.zeros((len(H), len(ts)))
+    hi = np.zeros_like(lo)
+    nnear = np.zeros(len(ts), int)
+    for k, t in enumerate(ts):
+        near = np.abs(a - t) <= rel * t
+        nnear[k] = near.sum()
+        sure = (a < t) & ~near
+        e1 = np.linalg.norm(np.where(sure, p, 0.0) @ W[2], axis=1) / (ny + 1e-6)
+        e2 = np.linalg.norm(np.where(sure | near, p, 0.0) @ W[2], axis=1) / (ny + 1e-6)
+        lo[:, k], hi[:, k] = np.minimum(e1, e2), np.maximum(e1, e2)
+    return lo, hi, nnear, g
+
+
+def _within(got, lo, hi, rel=1e-4, atol=1e-6):
+    slack = rel * np.maximum(np.abs(lo), np.abs(hi)) + atol
+    return (got >= lo - slack) & (got <= hi + slack)
+
+
+def _gpu_curves(x, wg, wu, wd, levels, rows=True):
+    import torch
+    import paper_2607_08991_amd as sats
+    n, d = x.shape
+    dff = wg.shape[1]
+    er = torch.zeros((n, len(levels)), dtype=torch.float32, device="cuda") if rows else None
+    t, err, sp = sats.sats_calibration_curves(to_dev(x, "bf16"), to_dev(wg, "bf16"), to_dev(wu, "bf16"),
+                                              to_dev(wd, "bf16"), n, d, dff, levels, err_rows=er)
+    return t, err, sp, (er.cpu().numpy() if rows else None)
+
+
+@pytest.mark.parametrize("seed,d,dff,n", [(61, 256, 1024, 40), (62, 128, 512, 17), (63, 512, 1536, 64)])
+def test_curves_match_oracle(seed, d, dff, n):
+    x, wg, wu, wd = _layer(seed, d, dff, n)
+    t, err, sp, er = _gpu_curves(x, wg, wu, wd, LEVELS)
+    H = numerics.decode(x, "bf16")
+    W = [numerics.decode(w, "bf16") for w in (wg, wu, wd)]
+    g = osats.layer_terms(H, *W)[0]
+    absg = np.abs(g)
+    # candidates: Eq. 3 order statistics
+    for k, q in enumerate(LEVELS):
+        ref = calibrate.percentile_threshold(absg, q)
+        assert t[k] == pytest.approx(ref, rel=1e-4, abs=1e-30), (k, q)
+    assert t[0] == 0.0 and np.all(np.diff(t) >= 0)
+    # errors and sparsities at the GPU's thresholds
+    ts = t.astype(np.float64)
+    lo, hi, nnear, _ = _bounds(H, W, ts)
+    assert err[0] == 0.0
+    assert _within(er, lo, hi).all()
+    assert _within(err, lo.mean(0), hi.mean(0)).all()
+    sp_ref = osats.sparsity_curve(g, ts)
+    assert np.all(np.abs(sp - sp_ref) <= (nnear + 0.5) / absg.size)
+
+
+def test_curves_llama_layer_sampled():
+    """One Llama-3.1-8B-shaped layer (4096 x 14336), 48 calibration rows: all
+    candidates on the GPU; the oracle recomputes 16 rows at 5 candidates."""
+    from workloads import get_config
+    cfg = get_config(1)
+    wg, wu, wd = synth.layer_weights(cfg.seed, 0, cfg.d, cfg.d_ff, cfg.dtype)
+    x = synth.activations(cfg.seed, synth.S_CAL, 48, cfg.d, cfg.dtype)
+    t, err, sp, er = _gpu_curves(x, wg, wu, wd, LEVELS)
+    H = numerics.decode(x[:16], "bf16")
+    W = [numerics.decode(w, "bf16") for w in (wg, wu, wd)]
+    pick = [0, 5, 9, 14, 20]
+    lo, hi, _, _ = _bounds(H, W, t[pick].astype(np.float64))
+    got = er[:16][:, pick]
+    assert _within(got, lo, hi).all()
+    # the realized sparsity of each candidate on the calibration set is its level
+    N = 48 * cfg.d_ff
+    for k, q in enumerate(LEVELS):
+        if 0 < q < 1:
+            assert abs(sp[k] - (np.ceil(q * N) - 1) / N) <= 4.0 / N
+
+
+def test_calibrate_stack_matches_oracle():
+    import torch
+    import paper_2607_08991_amd as sats
+    L, d, dff, n = 3, 256, 1024, 96
+    c = synth.small_case(71, L, d, dff, "bf16", n, w_std=1.0 / np.sqrt(d))
+    x = c["x"]
+    dw = [to_dev(c[k], "bf16") for k in ("W_gate", "W_up_T", "W_down")]
+    ts, b, s = sats.sats_calibrate_sats(to_dev(x, "bf16"), n, *dw, d, dff, L, 0.5,
+                                        coarse_step=0.1, fine_step=0.02, guardrail=True)
+    # the GPU's own layer inputs on the base path
+    lin = torch.empty((L, n, d), dtype=torch.bfloat16, device="cuda")
+    out = torch.empty((n, d), dtype=torch.bfloat16, device="cuda")
+    lut = torch.ones(1, dtype=torch.uint8, device="cuda")
+    ids = torch.zeros(n, dtype=torch.int32, device="cuda")
+    thr = torch.zeros(L, dtype=torch.float32, device="cuda")
+    sats.sats_mlp_forward_inspect(to_dev(x, "bf16"), ids, *dw, thr, lut, out, n, d, dff, L, layer_in=lin)
+    torch.cuda.synchronize()
+    H = from_dev(lin)
+    r = osats.calibrate(x, c["W_gate"], c["W_up_T"], c["W_down"], 0.5, "bf16", coarse_step=0.1, fine_step=0.02,
+                        layer_inputs=H)
+    # guardrail layer: its CATS threshold
+    assert ts[L - 1] == pytest.approx(float(r["thresholds"][L - 1]), rel=1e-4)
+    # free layers: each GPU threshold is an oracle candidate of the refined stage (same level)
+    b2, idx2, s2, c2 = r["fine"]
+    S = r["guardrail"][L - 1]
+    for l in range(L - 1):
+        tsl, errl, spl = c2[l]
+        k = int(np.argmin(np.abs(tsl - ts[l])))
+        assert tsl[k] == pytest.approx(float(ts[l]), rel=1e-4)
+        S += spl[k]
+    S /= L
+    # the GPU's choice is as close to the target as the oracle's (same breakpoints)
+    assert abs(S - 0.5) <= abs(s2 - 0.5) + 2e-3
+    assert abs(s - S) <= 2e-3
