@@ -51,6 +51,7 @@ def parse():
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--no-dense", action="store_true")
     p.add_argument("--batch", type=int, default=0, help="decode batch of a stack workload (default: its first)")
+    p.add_argument("--cal-rows", type=int, default=1024, help="calibration rows (sats-calib workload)")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
@@ -209,6 +210,89 @@ def bench_stack(args, cfg):
     print(json.dumps(res), flush=True)
 
 
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+
+
+def bench_calib(args):
+    """SATS calibration of one Llama-3.1-8B-shaped layer (Eq. 6 curves at the
+    coarse grid of 20 Eq. 3 levels over `--cal-rows` calibration rows): one
+    step is one sats_calibration_curves call."""
+    import torch
+    import paper_2607_08991_amd as sats
+    from workloads import get_config, synth
+    from oracle import sats as osats, numerics  # test infrastructure: the cpu_baseline leg only
+
+    cfg = get_config(1)
+    d, d_ff, n = cfg.d, cfg.d_ff, args.cal_rows
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    log(f"[bench] generating {cfg.name} weights and {n} calibration rows")
+    wnp = synth.layer_weights(cfg.seed, 0, d, d_ff, cfg.dtype)
+    W = [torch.from_numpy(w.view(np.int16)).view(torch.bfloat16).to(dev) for w in wnp]
+    xnp = synth.activations(cfg.seed, synth.S_CAL, n, d, cfg.dtype)
+    X = torch.from_numpy(xnp.view(np.int16)).view(torch.bfloat16).to(dev)
+    levels = [0.0] + [round(0.05 * i, 4) for i in range(1, 20)]
+    K = len(levels)
+    stream = torch.cuda.current_stream()
+    for _ in range(max(1, args.warmup)):
+        sats.sats_calibration_curves(X, *W, n, d, d_ff, levels)
+    steps = max(1, args.steps)
+    kinds = (sats.SATS_K_CAL_ERR, sats.SATS_K_CAL_GATEUP)
+    for k in kinds:
+        sats.sats_timing_begin(k, 64 * steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        t, err, sp = sats.sats_calibration_curves(X, *W, n, d, d_ff, levels)
+    dt = (time.perf_counter() - t0) / steps
+    kern = {}
+    products = (K + 14) // 15
+    for k in kinds:
+        tot, c = sats.sats_timing_end(k)
+        kern[sats.sats_kernel_name(k)] = {"avg_us": round(tot / c * 1e3, 2), "launches_per_step": c // steps}
+    # algorithmic flops of the error products of one step: per product of kc
+    # candidates, kc masked products and y itself per calibration row, each
+    # over d_ff x d; executed: hi and lo terms, and 16 MFMA rows per
+    # calibration row (8 when at most 7 candidates share a tile)
+    kcs = [min(15, K - k0) for k0 in range(0, K, 15)]
+    alg_flops = sum(2.0 * n * (kc + 1) * d_ff * d for kc in kcs)
+    exe_flops = sum(2.0 * 2 * n * (8 if kc <= 7 else 16) * d_ff * d for kc in kcs)
+    e = kern["cal_err_kernel"]
+    e_step_us = e["avg_us"] * e["launches_per_step"]
+    achieved = alg_flops / (e_step_us * 1e-6) / 1e12
+    e.update(candidates_per_launch=kcs, algorithmic_flops_per_step=alg_flops, achieved_tflops=round(achieved, 1),
+             executed_flops_per_step=exe_flops, executed_tflops=round(exe_flops / (e_step_us * 1e-6) / 1e12, 1))
+    cpu = None
+    if not args.no_cpu:
+        rows = 4
+        H = numerics.decode(xnp[:rows], cfg.dtype)
+        Wd = [numerics.decode(w, cfg.dtype) for w in wnp]
+        c0 = time.perf_counter()
+        osats.err_curve(H, *Wd, t.astype(np.float64))
+        cdt = time.perf_counter() - c0
+        cores = len(os.sched_getaffinity(0))
+        cpu = {"value": round(rows / cdt, 4), "unit": "calibration rows/s (20 candidates)", "cores": cores,
+               "kind": "oracle",
+               "sample": f"{rows} calibration rows x {K} candidates through the float64 oracle (Eq. 6 by "
+                         f"masking), {cdt:.1f} s"}
+    res = {
+        "metric": "SATS calibration: Eq. 6 error curves of one layer", "value": round(n / dt, 1),
+        "unit": "calibration rows/s (20 candidates)", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 (fp32 accumulate, p as bf16 hi + lo)", "data": "synthetic",
+        "config": {"workload": f"sats_calib_{cfg.name}", "d": d, "d_ff": d_ff, "calibration_rows": n,
+                   "candidates": K, "error_products": products},
+        "kernels": kern,
+        "roofline": {"kernel": "cal_err_kernel", "bound": "mfma", "achieved": round(achieved, 1),
+                     "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None},
+        "cpu_baseline": cpu,
+        "realized_sparsity_at_candidates": [round(float(v), 5) for v in sp],
+        "err_at_candidates": [round(float(v), 6) for v in err],
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -225,6 +309,8 @@ def main():
     from workloads import get_config, synth
 
     sats.load()
+    if args.workload == "sats-calib":
+        return bench_calib(args)
     cfg = get_config(args.workload)
     if cfg.n_layers != 1:
         return bench_stack(args, cfg)

@@ -8,5 +8,6 @@ from ._lib import (  # noqa: F401
     SatsError, load, sats_mlp_forward, sats_mlp_dense, sats_mlp_forward_inspect,
     sats_reserve, sats_release, sats_device_status, sats_last_error, sats_timing_begin, sats_timing_end,
     sats_kernel_name, SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DENSE, LIB_PATH,
-    SATS_K_DEC_GATE, SATS_K_DEC_ROWS, sats_calibration_curves, sats_calibrate_sats,
+    SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, sats_calibration_curves,
+    sats_calibrate_sats,
 )

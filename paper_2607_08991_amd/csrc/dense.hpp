@@ -409,40 +409,63 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
 // candidates at or below the neuron's magnitude, and neuron j is removed at
 // t_r exactly when c <= r.  p enters as two bf16 terms (p = hi + lo, lo the
 // rounded remainder), so that hi W + lo W carries about 16 bits of p into
-// float32 accumulation.  Each workgroup takes 16 calibration rows and 128
-// output columns (wavefront w: columns 16 w .. 16 w + 15, one 16 x 16 MFMA
-// tile per calibration row), walks all of d_ff in stages of 64 rows (W_down
-// 16 KB, hi and lo 2 KB each, c 1 KB), and writes, per row (m, r), the sum of
-// the squares of its 128 outputs: the partial of ||y - y_t||^2 (and ||y||^2)
-// for that column tile.  The row norms are finished by cal_reduce_kernel.
+// float32 accumulation.
+//
+// Each workgroup takes 16 calibration rows and 128 output columns and walks
+// all of d_ff in stages of 64 k (W_down^T rows of the 128 columns 16 KB, hi
+// and lo 2 KB each, c 1 KB) through a ring of 6 LDS stages.  Wavefront w
+// owns calibration rows 2 w and 2 w + 1 over all 128 columns: it builds the
+// masked A operands of its rows once per stage and multiplies them with the
+// 8 column tiles of W_down^T, so that no two wavefronts build the same
+// operand.  With PACK = 1 an A tile holds the 16 rows (15 candidates and y)
+// of one calibration row; with PACK = 2 (at most 7 candidates) it holds two
+// calibration rows of 8 (7 candidates and y), halving the MFMA work.
+// W_down enters transposed (W_down^T, [d][d_ff], made by
+// cal_transpose_kernel) so that each MFMA B operand is one 16-byte LDS read;
+// chunk q of tile row r sits at q ^ (r & 7), so the eight rows read by eight
+// consecutive lanes fall in distinct banks.  The operands of the first half
+// of stage s + 1 are read and masked at the end of stage s (the stage
+// barrier waits for two stages), so every stage starts with MFMAs.
+// Per row (m, r) the kernel writes the sum of the squares of its 128
+// outputs, the partial of ||y - y_t||^2 (and ||y||^2, slot 15) for the
+// column tile; cal_reduce_kernel finishes the norms.
 
 struct CalErrArgs {
   const uint16_t *ph, *pl;  // [n][d_ff] bf16 hi and lo terms of p
   const uint8_t *cnt;       // [n][d_ff] candidates at or below |g|
-  const uint16_t *Wd;       // W_down of the layer, [d_ff][d]
+  const uint16_t *WdT;      // W_down^T of the layer, [d][d_ff]
   float *part;              // [d / 128][n][16] column-tile sums of squares
   int n, d, d_ff;
 };
 
-constexpr int kCalRows = 16;  // calibration rows per workgroup
+constexpr int kCalRows = 16;  // calibration rows per workgroup (2 per wavefront)
 
+__device__ __forceinline__ int ct_pos(int r, int q) { return q ^ (r & 7); }
+
+template <int PACK>
 __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
+  static_assert(PACK == 1 || PACK == 2, "one or two calibration rows per A tile");
   __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
       rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
-  constexpr int TT = kCalRows;
+  constexpr int CT = kDenseDownNT / 16;  // column tiles of 16
+  constexpr int NA = 2 / PACK;           // A tiles per wavefront
+  constexpr int RPT = 16 / PACK;         // A rows per calibration row
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 4, l16 = lane & 15, c = 16 * w + l16;
-  const int n0 = blockIdx.x * kDenseDownNT, m0 = blockIdx.y * TT;
-  const int K = a.d_ff, N = a.d;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int n0 = blockIdx.x * kDenseDownNT, m0 = blockIdx.y * kCalRows;
+  const int K = a.d_ff;
   const int S = K / kDenseKC;
-  const __amdgpu_buffer_rsrc_t rsw = dense_rsrc(a.Wd, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t rsw = dense_rsrc(a.WdT, (uint32_t)((size_t)K * a.d * 2));
   const uint32_t pbytes = (uint32_t)((size_t)a.n * K * 2);
   const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.ph, pbytes), rsl = dense_rsrc(a.pl, pbytes);
   const __amdgpu_buffer_rsrc_t rsc = dense_rsrc(a.cnt, (uint32_t)((size_t)a.n * K));
-  // W_down rows as in dense_down_kernel: wavefront w loads rows 8 w .. 8 w + 7
-  const int wr = 8 * w + (lane >> 4), wp = lane & 15;
-  const uint32_t ow0 = (uint32_t)(((size_t)wr * N + n0 + 8 * krow_pos(wr, wp)) * 2);
-  const uint32_t ow1 = (uint32_t)(((size_t)(wr + 4) * N + n0 + 8 * krow_pos(wr + 4, wp)) * 2);
+  // W_down^T row tile (128 rows of 128 bytes): wavefront w fills LDS slots
+  // 128 w + 64 i + lane (i = 0, 1); slot s holds, at position s & 7 of tile
+  // row s >> 3, the chunk whose position is ct_pos
+  const int s0 = 128 * w + lane, s1 = s0 + 64;
+  const int r0 = s0 >> 3, r1 = s1 >> 3;
+  const uint32_t ow0 = (uint32_t)(((size_t)(n0 + r0) * K + 8 * ct_pos(r0, s0 & 7)) * 2);
+  const uint32_t ow1 = (uint32_t)(((size_t)(n0 + r1) * K + 8 * ct_pos(r1, s1 & 7)) * 2);
   // hi and lo: wavefronts 0-1 and 2-3, 16 rows x 128 bytes each (lane: row, 16-byte chunk);
   // c: wavefront 4, 16 rows x 64 bytes
   const int ar = 8 * (w & 1) + (lane >> 3), aq = lane & 7;
@@ -451,71 +474,122 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
   const int cr = lane >> 2, cq = lane & 3;
   const bool crv = m0 + cr < a.n;
   const uint32_t oc = (uint32_t)((size_t)(m0 + cr) * K + 16 * cq);
-  const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;
-  f32x4v acc[TT];
+  const uint32_t sk = kDenseKC * 2;
+  // the third load of every wavefront, chosen without branches (wavefronts
+  // 5-7 read zeros past the range into the stage's last 3 KB): a branch
+  // around the loads would cost the compiler its record of which LDS buffer
+  // each pending load writes, and with it waits on loads of later stages
+  const __amdgpu_buffer_rsrc_t r3 = w < 2 ? rsh : (w < 4 ? rsl : rsc);
+  const int d3 = w < 4 ? 16384 + w * 1024 : 20480 + (w - 4) * 1024;
+  const bool v3 = w < 4 ? arv : (w == 4 && crv);
+  const uint32_t o3 = w < 4 ? oa : oc, st3 = w < 4 ? sk : (uint32_t)kDenseKC;
+  // A row of this lane: calibration row 2 w + t (tile t), candidate lim; the
+  // last row of a calibration row is y (lim 15: every neuron)
+  const int rr = l16 % RPT;
+  const uint32_t lim = rr == RPT - 1 ? 15u : (uint32_t)rr;
+  f32x4v acc[NA][CT];
 #pragma unroll
-  for (int t = 0; t < TT; ++t) acc[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < NA; ++t)
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) acc[t][ct] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  bf16x8 ah[NA], al[NA], bq[CT];
+  // stage buffer BUF, half j: this lane's masked A operands and the B operands
+  auto load_ops = [&](const uint8_t *buf, int j) {
+    const int k = 32 * j + 8 * g;
+#pragma unroll
+    for (int t = 0; t < NA; ++t) {
+      const int row = 2 * w + (PACK == 1 ? t : l16 / RPT);
+      const u32x4 hv = *reinterpret_cast<const u32x4 *>(buf + 16384 + row * 128 + 2 * k);
+      const u32x4 lv = *reinterpret_cast<const u32x4 *>(buf + 18432 + row * 128 + 2 * k);
+      const uint2 cv = *reinterpret_cast<const uint2 *>(buf + 20480 + row * 64 + k);
+      u32x4 mh, ml;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t cw = q < 2 ? cv.x : cv.y;
+        const uint32_t c0 = (cw >> (16 * (q & 1))) & 0xffu, c1 = (cw >> (16 * (q & 1) + 8)) & 0xffu;
+        const uint32_t keep = (c0 <= lim ? 0x0000ffffu : 0u) | (c1 <= lim ? 0xffff0000u : 0u);
+        mh[q] = hv[q] & keep;
+        ml[q] = lv[q] & keep;
+      }
+      ah[t] = __builtin_bit_cast(bf16x8, mh);
+      al[t] = __builtin_bit_cast(bf16x8, ml);
+    }
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct) {
+      const int r = 16 * ct + l16;
+      bq[ct] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(buf + r * 128 + ct_pos(r, 4 * j + g) * 16));
+    }
+  };
+  auto mma = [&]() {
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int t = 0; t < NA; ++t) acc[t][ct] = mfma16(ah[t], bq[ct], acc[t][ct]);
+#pragma unroll
+    for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+      for (int t = 0; t < NA; ++t) acc[t][ct] = mfma16(al[t], bq[ct], acc[t][ct]);
+  };
 #define SATS_CE_ISSUE(BUF, SN)                                                               \
   {                                                                                          \
     const bool v_ = (SN) < S;                                                                \
     const uint32_t ss_ = (uint32_t)(SN);                                                     \
-    dma16<2>(rsw, (BUF) + w * 2048, dense_off(v_, ow0 + ss_ * sw, 0));                       \
-    dma16<2>(rsw, (BUF) + w * 2048 + 1024, dense_off(v_, ow1 + ss_ * sw, 1));                \
-    if (w < 4)                                                                               \
-      dma16<0>(w < 2 ? rsh : rsl, (BUF) + 16384 + w * 1024, dense_off(v_ && arv, oa + ss_ * sk, 2)); \
-    else if (w == 4)                                                                         \
-      dma16<0>(rsc, (BUF) + 20480, dense_off(v_ && crv, oc + ss_ * kDenseKC, 2));            \
-    else                                                                                     \
-      dma16<0>(rsc, (BUF) + 21504 + (w - 5) * 1024, kDenseOffNone + 48u);                    \
+    dma16<0>(rsw, (BUF) + w * 2048, dense_off(v_, ow0 + ss_ * sk, 0));                       \
+    dma16<0>(rsw, (BUF) + w * 2048 + 1024, dense_off(v_, ow1 + ss_ * sk, 1));                \
+    dma16<0>(r3, (BUF) + d3, dense_off(v_ && v3, o3 + ss_ * st3, 2));                        \
   }
-  // A operand of candidate row l16 for calibration row t: k = 32 j + 8 g .. + 7
-  // of the stage; hi or lo, zero where the neuron is kept at t_l16 (row 15: p itself)
-#define SATS_CE_COMPUTE(BUF)                                                                 \
+  // step s: wait until stage s + 1 has landed (the loads of s + 2 .. s + 4,
+  // nine, may be outstanding) and every wavefront is done with stage s - 1,
+  // whose buffer takes stage s + 5; then stage s, whose first-half operands
+  // are already in registers, and the first-half operands of stage s + 1
+#define SATS_CE_STEP(CUR, NXT, FREE, P)                                                      \
   {                                                                                          \
-    _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                          \
-      const bf16x8 b_ = krow_operand((BUF), 256, c, j, g);                                   \
-      _Pragma("unroll") for (int t = 0; t < TT; ++t) {                                       \
-        const int k_ = 32 * j + 8 * g;                                                       \
-        const u32x4 hv_ = *reinterpret_cast<const u32x4 *>((BUF) + 16384 + t * 128 + 2 * k_); \
-        const u32x4 lv_ = *reinterpret_cast<const u32x4 *>((BUF) + 18432 + t * 128 + 2 * k_); \
-        const uint2 cv_ = *reinterpret_cast<const uint2 *>((BUF) + 20480 + t * 64 + k_);      \
-        u32x4 mh_, ml_;                                                                      \
-        _Pragma("unroll") for (int q = 0; q < 4; ++q) {                                      \
-          const uint32_t cw_ = q < 2 ? cv_.x : cv_.y;                                        \
-          const uint32_t c0_ = (cw_ >> (16 * (q & 1))) & 0xffu, c1_ = (cw_ >> (16 * (q & 1) + 8)) & 0xffu; \
-          const uint32_t keep_ = (c0_ <= (uint32_t)l16 ? 0x0000ffffu : 0u) | (c1_ <= (uint32_t)l16 ? 0xffff0000u : 0u); \
-          mh_[q] = hv_[q] & keep_;                                                           \
-          ml_[q] = lv_[q] & keep_;                                                           \
-        }                                                                                    \
-        acc[t] = mfma16(__builtin_bit_cast(bf16x8, mh_), b_, acc[t]);                        \
-        acc[t] = mfma16(__builtin_bit_cast(bf16x8, ml_), b_, acc[t]);                        \
-      }                                                                                      \
+    const int s_ = s0_ + (P);                                                                \
+    dense_stage_barrier<9>();                                                                \
+    SATS_CE_ISSUE(FREE, s_ + 5);                                                             \
+    if (s_ < S) {                                                                            \
+      mma();                                                                                 \
+      load_ops((CUR), 1);                                                                    \
+      mma();                                                                                 \
+      if (s_ + 1 < S) load_ops((NXT), 0);                                                    \
     }                                                                                        \
   }
-  SATS_DENSE_RING(S, SATS_CE_ISSUE, SATS_CE_COMPUTE)
+  SATS_CE_ISSUE(rg0, 0);
+  SATS_CE_ISSUE(rg1, 1);
+  SATS_CE_ISSUE(rg2, 2);
+  SATS_CE_ISSUE(rg3, 3);
+  SATS_CE_ISSUE(rg4, 4);
+  dense_stage_barrier<12>();  // stage 0 has landed
+  load_ops(rg0, 0);
+  for (int s0_ = 0; s0_ < S; s0_ += 6) {
+    SATS_CE_STEP(rg0, rg1, rg5, 0)
+    SATS_CE_STEP(rg1, rg2, rg0, 1)
+    SATS_CE_STEP(rg2, rg3, rg1, 2)
+    SATS_CE_STEP(rg3, rg4, rg2, 3)
+    SATS_CE_STEP(rg4, rg5, rg3, 4)
+    SATS_CE_STEP(rg5, rg0, rg4, 5)
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // the zero-filling loads past the range land too
+#undef SATS_CE_STEP
 #undef SATS_CE_ISSUE
-#undef SATS_CE_COMPUTE
-  // sums of squares over the tile's 128 columns: 16 columns per wavefront by
-  // lane exchange, then the 8 wavefronts in order through LDS
-  __syncthreads();
-  float *xs = reinterpret_cast<float *>(rg0);  // [8 wavefronts][TT][16 rows]
+  // sums of squares over the tile's 128 columns: the 8 column tiles in order
+  // within the lane, then the 16 columns of a tile by lane exchange.  Lane
+  // (g, l16) of tile t holds A rows 4 g .. 4 g + 3.
 #pragma unroll
-  for (int t = 0; t < TT; ++t)
+  for (int t = 0; t < NA; ++t)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      float v = acc[t][r] * acc[t][r];
+      float v = 0.0f;
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) v += acc[t][ct][r] * acc[t][ct][r];
 #pragma unroll
       for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 16);
-      if (l16 == 0) xs[(w * TT + t) * 16 + 4 * g + r] = v;
+      const int arow = 4 * g + r;
+      const int m = m0 + 2 * w + (PACK == 1 ? t : arow / RPT);
+      const int cand = arow % RPT;
+      const int slot = cand == RPT - 1 ? 15 : cand;
+      if (l16 == 0 && m < a.n) a.part[((size_t)blockIdx.x * a.n + m) * 16 + slot] = v;
     }
-  __syncthreads();
-  if (threadIdx.x < TT * 16) {
-    const int t = threadIdx.x >> 4, r = threadIdx.x & 15;
-    float s = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) s += xs[(q * TT + t) * 16 + r];
-    if (m0 + t < a.n) a.part[((size_t)blockIdx.x * a.n + m0 + t) * 16 + r] = s;
-  }
 }
 
 #undef SATS_DENSE_RING

@@ -654,15 +654,16 @@ struct CalBuffers {
   float *G = nullptr;              // [n][d_ff] g
   uint16_t *ph = nullptr, *pl = nullptr;  // [n][d_ff] p as bf16 hi + lo
   uint8_t *cnt = nullptr;          // [n][d_ff] candidates at or below |g|
+  uint16_t *WdT = nullptr;         // [d][d_ff] W_down^T of the layer
   float *part = nullptr;           // [d / 128][n][16]
-  uint32_t *hist0 = nullptr, *hist1 = nullptr, *hist2 = nullptr, *prefix = nullptr, *rank = nullptr;
+  uint32_t *hpart = nullptr, *hist = nullptr, *prefix = nullptr, *rank = nullptr;
   float *tk = nullptr, *thr15 = nullptr;
   unsigned long long *hist16 = nullptr;
   double *errsum = nullptr;
   int *ctl = nullptr;              // [passes][2] rows of each gate/up pass, MFMA on
   ~CalBuffers() {
-    for (void *q : {(void *)G, (void *)ph, (void *)pl, (void *)cnt, (void *)part, (void *)hist0, (void *)hist1,
-                    (void *)hist2, (void *)prefix, (void *)rank, (void *)tk, (void *)thr15, (void *)hist16,
+    for (void *q : {(void *)G, (void *)ph, (void *)pl, (void *)cnt, (void *)WdT, (void *)part, (void *)hpart, (void *)hist,
+                    (void *)prefix, (void *)rank, (void *)tk, (void *)thr15, (void *)hist16,
                     (void *)errsum, (void *)ctl})
       if (q) (void)hipFree(q);
   }
@@ -673,6 +674,8 @@ template <typename P> int cal_alloc(P **p, size_t count) {
     return fail(SATS_ERR_WORKSPACE, "calibration buffer of %zu bytes failed", count * sizeof(P));
   return SATS_OK;
 }
+
+constexpr int kCalHistParts = 256;  // workgroups of a radix pass (each writes its own histogram)
 
 // Rank m = ceil(q N) of the Eq. 3 order statistic at level q (q taken to 1e-6).
 uint64_t level_rank(double q, uint64_t N) {
@@ -716,7 +719,9 @@ int cal_gate_up(const uint16_t *h, const uint16_t *Wg, const uint16_t *Wu, int64
     da.cal_g = cb.G + o;
     da.cal_ph = cb.ph + o;
     da.cal_pl = cb.pl + o;
-    hipLaunchKernelGGL(dense_gateup_kernel<4>, dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, s, da);
+    TimedLaunch tl(SATS_K_CAL_GATEUP, s);
+    hipExtLaunchKernelGGL(dense_gateup_kernel<4>, dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, s, tl.start,
+                          tl.stop, 0, da);
     HIP_TRY(hipGetLastError());
   }
   return SATS_OK;
@@ -729,21 +734,18 @@ int cal_quantiles(CalBuffers &cb, uint64_t N, const double *levels, int K, float
   for (int k = 0; k < K; ++k) rank[k] = (uint32_t)level_rank(levels[k], N);
   HIP_TRY(hipMemcpyAsync(cb.rank, rank.data(), K * sizeof(uint32_t), hipMemcpyHostToDevice, s));
   HIP_TRY(hipMemcpyAsync(cb.prefix, zero.data(), K * sizeof(uint32_t), hipMemcpyHostToDevice, s));
-  const int grid = (int)std::min<uint64_t>(2048, (N + kCalThreads - 1) / kCalThreads);
-  HIP_TRY(hipMemsetAsync(cb.hist0, 0, 4096 * sizeof(uint32_t), s));
-  hipLaunchKernelGGL(cal_hist0_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.hist0);
-  hipLaunchKernelGGL(cal_select_kernel, dim3(1), dim3(kCalMaxLevels), 0, s, cb.hist0, (size_t)0, 4096, 12,
-                     cb.prefix, cb.rank, K, (float *)nullptr);
-  HIP_TRY(hipMemsetAsync(cb.hist1, 0, (size_t)K * 4096 * sizeof(uint32_t), s));
-  hipLaunchKernelGGL(cal_histk_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.prefix, K, 8, 4096,
-                     cb.hist1);
-  hipLaunchKernelGGL(cal_select_kernel, dim3(1), dim3(kCalMaxLevels), 0, s, cb.hist1, (size_t)4096, 4096, 12,
-                     cb.prefix, cb.rank, K, (float *)nullptr);
-  HIP_TRY(hipMemsetAsync(cb.hist2, 0, (size_t)K * 256 * sizeof(uint32_t), s));
-  hipLaunchKernelGGL(cal_histk_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.prefix, K, 0, 256,
-                     cb.hist2);
-  hipLaunchKernelGGL(cal_select_kernel, dim3(1), dim3(kCalMaxLevels), 0, s, cb.hist2, (size_t)256, 256, 8,
-                     cb.prefix, cb.rank, K, cb.tk);
+  // passes: bits 31..20 (one histogram for every level), 19..12, 11..4, 3..0
+  static const int kShift[4] = {20, 12, 4, 0}, kBits[4] = {12, 8, 8, 4};
+  for (int pass = 0; pass < 4; ++pass) {
+    const int kh = pass == 0 ? 1 : K, nh = kh << kBits[pass];
+    hipLaunchKernelGGL(cal_hist_kernel, dim3(kCalHistParts), dim3(kCalHistThreads), 0, s, cb.G, (size_t)N,
+                       cb.prefix, kh, kShift[pass], kBits[pass], cb.hpart);
+    hipLaunchKernelGGL(cal_hist_reduce_kernel, dim3((nh + kCalThreads - 1) / kCalThreads), dim3(kCalThreads), 0, s,
+                       cb.hpart, kCalHistParts, nh, cb.hist);
+    hipLaunchKernelGGL(cal_select_kernel, dim3(K), dim3(kCalSelThreads), 0, s, cb.hist,
+                       pass == 0 ? (size_t)0 : ((size_t)1 << kBits[pass]), 1 << kBits[pass], kBits[pass], cb.prefix,
+                       cb.rank, pass == 3 ? cb.tk : (float *)nullptr);
+  }
   HIP_TRY(hipGetLastError());
   HIP_TRY(hipMemcpyAsync(t, cb.tk, K * sizeof(float), hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
@@ -751,12 +753,18 @@ int cal_quantiles(CalBuffers &cb, uint64_t N, const double *levels, int K, float
 }
 
 // Eq. 6 error and sparsity of ascending candidates t[0..K) (any K), 15 per
-// product.  err_rows (device, [n][K]) is optional.
+// product.  err_rows (device, [n][K]) is optional; without err only the
+// sparsities are computed.
 int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t d_ff, const float *t, int K,
                double *err, double *sp, float *err_rows, hipStream_t s) {
   using namespace sats;
   const uint64_t N = (uint64_t)n * d_ff;
   const int grid = (int)std::min<uint64_t>(2048, (N + kCalThreads - 1) / kCalThreads);
+  if (err) {
+    hipLaunchKernelGGL(cal_transpose_kernel, dim3(d / 64, d_ff / 64), dim3(kCalThreads), 0, s, Wd, (int)d_ff,
+                       (int)d, cb.WdT);
+    HIP_TRY(hipGetLastError());
+  }
   for (int k0 = 0; k0 < K; k0 += kCalCand) {
     const int kc = std::min(kCalCand, K - k0);
     float thr[kCalCand];
@@ -765,30 +773,40 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
     HIP_TRY(hipMemsetAsync(cb.hist16, 0, 16 * sizeof(unsigned long long), s));
     hipLaunchKernelGGL(cal_bucket_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.thr15, cb.cnt,
                        cb.hist16);
-    CalErrArgs ce{};
-    ce.ph = cb.ph;
-    ce.pl = cb.pl;
-    ce.cnt = cb.cnt;
-    ce.Wd = Wd;
-    ce.part = cb.part;
-    ce.n = (int)n;
-    ce.d = (int)d;
-    ce.d_ff = (int)d_ff;
-    hipLaunchKernelGGL(cal_err_kernel, dim3(d / kDenseDownNT, (n + kCalRows - 1) / kCalRows), dim3(kDenseThreads), 0,
-                       s, ce);
-    hipLaunchKernelGGL(cal_reduce_kernel, dim3(1), dim3(kCalReduceThreads), 0, s, cb.part,
-                       (int)(d / kDenseDownNT), (int)n, kc, err_rows ? err_rows + k0 : (float *)nullptr, K,
-                       cb.errsum);
+    if (err) {
+      CalErrArgs ce{};
+      ce.ph = cb.ph;
+      ce.pl = cb.pl;
+      ce.cnt = cb.cnt;
+      ce.WdT = cb.WdT;
+      ce.part = cb.part;
+      ce.n = (int)n;
+      ce.d = (int)d;
+      ce.d_ff = (int)d_ff;
+      {
+        TimedLaunch tl(SATS_K_CAL_ERR, s);
+        // at most 7 candidates: two calibration rows per MFMA tile
+        if (kc <= 7)
+          hipExtLaunchKernelGGL(cal_err_kernel<2>, dim3(d / kDenseDownNT, (n + kCalRows - 1) / kCalRows),
+                                dim3(kDenseThreads), 0, s, tl.start, tl.stop, 0, ce);
+        else
+          hipExtLaunchKernelGGL(cal_err_kernel<1>, dim3(d / kDenseDownNT, (n + kCalRows - 1) / kCalRows),
+                                dim3(kDenseThreads), 0, s, tl.start, tl.stop, 0, ce);
+      }
+      hipLaunchKernelGGL(cal_reduce_kernel, dim3(1), dim3(kCalReduceThreads), 0, s, cb.part,
+                         (int)(d / kDenseDownNT), (int)n, kc, err_rows ? err_rows + k0 : (float *)nullptr, K,
+                         cb.errsum);
+    }
     HIP_TRY(hipGetLastError());
     double es[kCalCand];
     unsigned long long h16[16];
-    HIP_TRY(hipMemcpyAsync(es, cb.errsum, kc * sizeof(double), hipMemcpyDeviceToHost, s));
+    if (err) HIP_TRY(hipMemcpyAsync(es, cb.errsum, kc * sizeof(double), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipMemcpyAsync(h16, cb.hist16, sizeof h16, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     unsigned long long below = 0;
     for (int r = 0; r < kc; ++r) {
       below += h16[r];  // #{c <= r} = #{|g| < t_r}
-      err[k0 + r] = es[r] / (double)n;
+      if (err) err[k0 + r] = es[r] / (double)n;
       sp[k0 + r] = (double)below / (double)N;
     }
   }
@@ -799,9 +817,10 @@ int cal_buffers(CalBuffers &cb, int64_t n, int64_t d, int64_t d_ff) {
   const size_t N = (size_t)n * d_ff;
   int rc = 0;
   if ((rc = cal_alloc(&cb.G, N)) || (rc = cal_alloc(&cb.ph, N)) || (rc = cal_alloc(&cb.pl, N)) ||
-      (rc = cal_alloc(&cb.cnt, N)) || (rc = cal_alloc(&cb.part, (size_t)(d / sats::kDenseDownNT) * n * 16)) ||
-      (rc = cal_alloc(&cb.hist0, 4096)) || (rc = cal_alloc(&cb.hist1, (size_t)sats::kCalMaxLevels * 4096)) ||
-      (rc = cal_alloc(&cb.hist2, (size_t)sats::kCalMaxLevels * 256)) || (rc = cal_alloc(&cb.prefix, sats::kCalMaxLevels)) ||
+      (rc = cal_alloc(&cb.cnt, N)) || (rc = cal_alloc(&cb.WdT, (size_t)d * d_ff)) ||
+      (rc = cal_alloc(&cb.part, (size_t)(d / sats::kDenseDownNT) * n * 16)) ||
+      (rc = cal_alloc(&cb.hpart, (size_t)kCalHistParts * sats::kCalHistLds)) ||
+      (rc = cal_alloc(&cb.hist, sats::kCalHistLds)) || (rc = cal_alloc(&cb.prefix, sats::kCalMaxLevels)) ||
       (rc = cal_alloc(&cb.rank, sats::kCalMaxLevels)) || (rc = cal_alloc(&cb.tk, sats::kCalMaxLevels)) ||
       (rc = cal_alloc(&cb.thr15, sats::kCalCand)) || (rc = cal_alloc(&cb.hist16, 16)) ||
       (rc = cal_alloc(&cb.errsum, sats::kCalCand)) ||
@@ -911,12 +930,14 @@ int cal_stack(const uint16_t *x, int64_t n, const uint16_t *Wg, const uint16_t *
   std::vector<int> fixed(L, 0);
   std::vector<double> fixed_sp(L, 0.0);
   std::vector<float> fixed_t(L, 0.0f);
-  auto layer_curves = [&](int64_t l, const std::vector<double> &lv, CalCurve &out_c, bool gate_up) -> int {
+  // with_err false: thresholds and sparsities only (the guardrail layer)
+  auto layer_curves = [&](int64_t l, const std::vector<double> &lv, CalCurve &out_c, bool gate_up,
+                          bool with_err = true) -> int {
     const int K = (int)lv.size();
     std::vector<float> t(K);
-    std::vector<double> err(K), sp(K);
+    std::vector<double> err(K, 0.0), sp(K);
     const int r = cal_layer(cb, hin + (size_t)l * n * d, Wg + l * wl, Wu + l * wl, Wd + l * wl, n, d, d_ff, lv.data(),
-                            K, t.data(), err.data(), sp.data(), nullptr, s, gate_up);
+                            K, t.data(), with_err ? err.data() : nullptr, sp.data(), nullptr, s, gate_up);
     if (r) return r;
     for (int k = 0; k < K; ++k) {
       out_c.level.push_back(lv[k]);
@@ -932,7 +953,7 @@ int cal_stack(const uint16_t *x, int64_t n, const uint16_t *Wg, const uint16_t *
     if ((rc = layer_curves(l, coarse, cv[l], true))) return rc;
     if (guardrail && L > 1 && l == L - 1) {
       CalCurve g1;
-      if ((rc = layer_curves(l, {s_tar}, g1, false))) return rc;
+      if ((rc = layer_curves(l, {s_tar}, g1, false, false))) return rc;
       fixed[l] = 1;
       fixed_sp[l] = g1.sp[0];
       fixed_t[l] = (float)g1.t[0];
@@ -1175,6 +1196,8 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_DENSE: return "dense_mfma_kernels";
     case SATS_K_DEC_GATE: return "dec_gate_kernel";
     case SATS_K_DEC_ROWS: return "dec_rows_kernel";
+    case SATS_K_CAL_ERR: return "cal_err_kernel";
+    case SATS_K_CAL_GATEUP: return "dense_gateup_kernel (calibration)";
     default: return "";
   }
 }
