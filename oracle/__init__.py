@@ -16,10 +16,12 @@ Modules
                routing by table lookup (Eq. 13), multi-layer forward
   calibrate -- CATS percentile threshold (Eq. 3) and per-layer calibration of
                a stack on dense-propagated calibration tokens
+  sats      -- SATS calibration (Eq. 6-10)
+  lora      -- LoRA-aware routed sparse MLP (Section 5, fine-tuned models)
 
 Parity status of each function is stated in its docstring.  The inter-layer
 glue of a stack (``mlp.glue``) is a convention of this library, not something
 the paper defines: parity unpinned by the paper (pinned only by its own
 invariants).
 """
-from . import numerics, mlp, calibrate, sats  # noqa: F401
+from . import numerics, mlp, calibrate, sats, lora  # noqa: F401
