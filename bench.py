@@ -52,6 +52,9 @@ def parse():
     p.add_argument("--no-dense", action="store_true")
     p.add_argument("--batch", type=int, default=0, help="decode batch of a stack workload (default: its first)")
     p.add_argument("--cal-rows", type=int, default=1024, help="calibration rows (sats-calib workload)")
+    p.add_argument("--lora-rank", type=int, default=0,
+                   help="single-layer workloads: run the LoRA-aware sparse path with adapters of this rank")
+    p.add_argument("--lora-scale", type=float, default=2.0)
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
@@ -97,9 +100,10 @@ def thresholds_for(cfg):
         return np.asarray(json.load(f)[cfg.name]["thresholds"], np.float32)
 
 
-def cpu_baseline(cfg, weights_np, ts, x_np, n_sample):
-    """The CPU oracle, as it is, on the first n_sample decode tokens."""
-    from oracle import mlp  # test infrastructure: only this leg of the benchmark uses it
+def cpu_baseline(cfg, weights_np, ts, x_np, n_sample, adapters=None, scale=0.0):
+    """The CPU oracle, as it is, on the first n_sample decode tokens (the
+    LoRA-aware oracle when adapters are given)."""
+    from oracle import lora, mlp  # test infrastructure: only this leg of the benchmark uses it
     try:
         from threadpoolctl import threadpool_info
         blas = [(i.get("internal_api"), i.get("num_threads")) for i in threadpool_info()]
@@ -110,7 +114,11 @@ def cpu_baseline(cfg, weights_np, ts, x_np, n_sample):
     wg, wu, wd = weights_np
     x = x_np[:n_sample]
     t0 = time.perf_counter()
-    mlp.forward(x, np.zeros(len(x), np.int32), wg[None], wu[None], wd[None], ts, None, cfg.dtype)
+    if adapters is None:
+        mlp.forward(x, np.zeros(len(x), np.int32), wg[None], wu[None], wd[None], ts, None, cfg.dtype)
+    else:
+        lora.forward_lora(x, np.zeros(len(x), np.int32), wg[None], wu[None], wd[None],
+                          tuple(m[None] for m in adapters), scale, ts, None, cfg.dtype)
     dt = time.perf_counter() - t0
     return {"value": round(len(x) / dt, 3), "unit": "tok/s", "cores": int(min(threads, cores)),
             "kind": "oracle",
@@ -330,6 +338,9 @@ def main():
         return t.view(tdt).to(dev) if a.dtype == np.uint16 else t.to(dev)
 
     base = [up(w) for w in wnp]
+    R = args.lora_rank
+    if R:  # the adapters travel with each weight copy
+        base += [up(m) for m in synth.lora_adapters(cfg.seed, 0, d, d_ff, R, cfg.dtype)]
     copies = [base] + [[w.clone() for w in base] for _ in range(args.copies - 1)]
     xnp = synth.decode_x(cfg, args.tokens)
     X = up(xnp)
@@ -345,18 +356,31 @@ def main():
     cnt = torch.zeros((L, args.tokens), dtype=torch.int32, device=dev)
     route = torch.zeros(args.tokens, dtype=torch.uint8, device=dev)
     for i in range(args.tokens):
-        sats.sats_mlp_forward_inspect(X[i:i + 1], ids[i:i + 1] if dlut is not None else None,
-                                      *base, thr, dlut, out[i:i + 1], 1, d, d_ff, L,
-                                      route_out=route[i:i + 1], active_count=cnt[:, i:i + 1])
+        if R:
+            sats.sats_mlp_forward_lora(X[i:i + 1], ids[i:i + 1] if dlut is not None else None, *base[:3],
+                                       base[3:], R, args.lora_scale, thr, dlut, out[i:i + 1], 1, d, d_ff, L,
+                                       route_out=route[i:i + 1], active_count=cnt[:, i:i + 1])
+        else:
+            sats.sats_mlp_forward_inspect(X[i:i + 1], ids[i:i + 1] if dlut is not None else None,
+                                          *base, thr, dlut, out[i:i + 1], 1, d, d_ff, L,
+                                          route_out=route[i:i + 1], active_count=cnt[:, i:i + 1])
     torch.cuda.synchronize()
     kept = cnt.cpu().numpy().astype(np.float64)
     routed_base = route.cpu().numpy()
 
-    def step_fwd(s):
+    def step_plain(s):
         i = s % args.tokens
         w = copies[s % args.copies]
         sats.sats_mlp_forward(X[i:i + 1], ids[i:i + 1] if dlut is not None else None, w[0], w[1],
                               w[2], thr, dlut, out[i:i + 1], n, d, d_ff, L, stream)
+
+    def step_lora(s):
+        i = s % args.tokens
+        w = copies[s % args.copies]
+        sats.sats_mlp_forward_lora(X[i:i + 1], ids[i:i + 1] if dlut is not None else None, w[0], w[1], w[2],
+                                   w[3:], R, args.lora_scale, thr, dlut, out[i:i + 1], n, d, d_ff, L, stream)
+
+    step_fwd = step_lora if R else step_plain
 
     def step_dense(s):
         i = s % args.tokens
@@ -394,6 +418,7 @@ def main():
     dense_ms = None
     if not args.no_dense:
         dense_ms, _ = timed(step_dense)
+    plain_ms = timed(step_plain)[0] if R else None
 
     # algorithmic bytes: all of W_gate, the kept rows of W_up_T and W_down, x and out
     steps_idx = (args.warmup + np.arange(args.steps)) % args.tokens
@@ -401,14 +426,20 @@ def main():
     gate_bytes = d * d_ff * esz + n * d * esz
     updown_row = d * esz
     touched = L * d * d_ff * esz + 2 * updown_row * a_mean + 2 * n * d * esz
+    # LoRA: A_gate, B_gate, A_up and B_down whole, the kept rows of B_up_T and A_down
+    lora_bytes = L * (2 * d * R + R * d_ff + R * d) * esz + 2 * R * esz * a_mean if R else 0
+    touched += lora_bytes
     gbps = touched / (ms * 1e-3) / 1e9
     sparsity = 1.0 - a_mean / (L * d_ff)
 
     up_bytes = updown_row * a_mean / L
     kern = {}
+    gate_lora = (2 * d * R + R * d_ff) * esz if R else 0
+    rows_lora = (2 * R * esz * a_mean / L + R * d * esz) if R else 0
     for name, (kms, c) in kt.items():
         b = {"gate_kernel": gate_bytes, "up_kernel": up_bytes, "down_kernel": up_bytes,
-             "dec_gate_kernel": gate_bytes, "dec_rows_kernel": 2 * up_bytes + n * d * esz}[name]
+             "dec_gate_kernel": gate_bytes + gate_lora,
+             "dec_rows_kernel": 2 * up_bytes + n * d * esz + rows_lora}[name]
         kern[name] = {"avg_us": round(kms * 1e3, 3), "launches": c,
                       "algorithmic_bytes": int(b), "achieved_gbps": round(b / (kms * 1e-3) / 1e9, 1)}
     dom = max(kern, key=lambda k: kern[k]["avg_us"])
@@ -418,7 +449,9 @@ def main():
     cpu = None
     if not args.no_cpu:
         log(f"[bench] timing the CPU oracle on {args.cpu_sample} tokens")
-        cpu = cpu_baseline(cfg, wnp, ts, synth.decode_x(cfg, args.cpu_sample), args.cpu_sample)
+        ns = min(args.cpu_sample, 128) if R else args.cpu_sample  # the adapted oracle merges weights per token
+        cpu = cpu_baseline(cfg, wnp, ts, synth.decode_x(cfg, ns), ns,
+                           synth.lora_adapters(cfg.seed, 0, d, d_ff, R, cfg.dtype) if R else None, args.lora_scale)
 
     res = {
         "metric": METRIC,
@@ -433,8 +466,8 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: one Llama-3.1-8B-shaped gated-MLP layer" if cfg.index == 1
-                   else cfg.name,
+        "config": {"workload": (f"{cfg.name}: one Llama-3.1-8B-shaped gated-MLP layer" if cfg.index == 1
+                                else cfg.name) + (f", LoRA rank {R} on the sparse path" if R else ""),
                    "d": d, "d_ff": d_ff, "n_layers": L, "decode_batch": n,
                    "route": "all tokens sparse" if lut is None else "route_lut",
                    "threshold": [float(t) for t in ts], "target_sparsity": cfg.k_fixed,
@@ -452,9 +485,14 @@ def main():
         "kernels": kern,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(dom_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
-                     "traffic": counter_traffic(dom, "c2_llama_layer_bf16") if cfg.index == 1 else None},
+                     "traffic": counter_traffic(dom, "c2_llama_layer_bf16") if cfg.index == 1 and not R
+                     else None},
         "cpu_baseline": cpu,
     }
+    if R:
+        res["lora"] = {"rank": R, "scale": args.lora_scale, "adapter_bytes_per_step": int(lora_bytes),
+                       "plain_sparse_ms_per_step": round(plain_ms, 6),
+                       "overhead_vs_plain_sparse": round(ms / plain_ms, 4)}
     print(json.dumps(res), flush=True)
 
 

@@ -135,6 +135,42 @@ int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids,
                                  float *layer_in);
 
 /*
+ * LoRA-aware routed sparse forward (Section 5, the fine-tuned routed
+ * models): sparse-path tokens run the base weights plus rank-r adapters on
+ * the three projections,
+ *   W_gate + scale A_gate B_gate,  W_up + scale A_up B_up,  W_down + scale A_down B_down,
+ * and base-path tokens run the base weights alone (both paths share them, so
+ * the adapters are not merged in).  The CATS threshold applies to
+ * |SiLU(h (W_gate + scale A_gate B_gate))|.  Device arrays in the activation
+ * type, stacked over n_layers like the weights, row-major:
+ *   A_gate [d][rank], B_gate [rank][d_ff], A_up [d][rank],
+ *   B_up_T [d_ff][rank] (B_up transposed, like W_up_T),
+ *   A_down [d_ff][rank], B_down [rank][d].
+ * The adapters run inside the same launches as the base computation: the up
+ * adapter only for kept columns, the down adapter's first factor only over
+ * kept rows.  rank is 8, 16, 32 or 64; the adapter arrays must be 16-byte
+ * aligned; the shapes must fit the single-token path (d <= 4096, d and d_ff
+ * multiples of 16 bytes' worth of elements) -- tokens are processed one
+ * after another, each on its own route.  Other arguments and the optional
+ * inspection outputs as in sats_mlp_forward_inspect.  Errors: SATS_ERR_NULL
+ * (a required array), SATS_ERR_SHAPE (rank or shape), SATS_ERR_ARG
+ * (alignment, non-finite scale), and those of sats_mlp_forward.
+ */
+int sats_mlp_forward_lora(const sats_bf16 *x, const int32_t *token_ids, const sats_bf16 *W_gate,
+                          const sats_bf16 *W_up_T, const sats_bf16 *W_down, const sats_bf16 *A_gate,
+                          const sats_bf16 *B_gate, const sats_bf16 *A_up, const sats_bf16 *B_up_T,
+                          const sats_bf16 *A_down, const sats_bf16 *B_down, int64_t rank, float scale,
+                          const float *thresholds, const uint8_t *route_lut, sats_bf16 *out, int64_t n_tokens,
+                          int64_t d, int64_t d_ff, int64_t n_layers, hipStream_t stream, uint8_t *route_out,
+                          int32_t *active_count, int32_t *active_idx, sats_bf16 *layer_in);
+int sats_mlp_forward_lora_f32(const float *x, const int32_t *token_ids, const float *W_gate, const float *W_up_T,
+                              const float *W_down, const float *A_gate, const float *B_gate, const float *A_up,
+                              const float *B_up_T, const float *A_down, const float *B_down, int64_t rank,
+                              float scale, const float *thresholds, const uint8_t *route_lut, float *out,
+                              int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers, hipStream_t stream,
+                              uint8_t *route_out, int32_t *active_count, int32_t *active_idx, float *layer_in);
+
+/*
  * Allocate the workspace of (current device, stream) for calls of up to
  * max_tokens tokens at this d, d_ff, n_layers and element size (2 = bf16,
  * 4 = f32), so that later calls of that size or smaller allocate nothing.
@@ -145,9 +181,10 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
 /*
  * Synchronise `stream` and report whether a kernel of this library on it
  * raised the device error flag since the last check (SATS_ERR_DEVICE; the
- * flag is cleared).  No kernel of this version waits on another workgroup,
- * so the flag is only a guard for future ones; the call still surfaces
- * asynchronous HIP errors of the stream.
+ * flag is cleared).  The single-token path's second reduction stage waits
+ * for the other workgroups of its launch with a bounded wait that raises
+ * the flag instead of hanging; the call also surfaces asynchronous HIP
+ * errors of the stream.
  */
 int sats_device_status(hipStream_t stream);
 

@@ -38,6 +38,8 @@ SIGNATURES = {
     "sats_timing_begin": ([_N, _N], _N),
     "sats_timing_end": ([_N, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)], _N),
     "sats_kernel_name": ([_N], ctypes.c_char_p),
+    "sats_mlp_forward_lora": ([_P] * 11 + [_I, ctypes.c_float] + [_P] * 3 + [_I] * 4 + [_S] + [_P] * 4, _N),
+    "sats_mlp_forward_lora_f32": ([_P] * 11 + [_I, ctypes.c_float] + [_P] * 3 + [_I] * 4 + [_S] + [_P] * 4, _N),
     "sats_calibration_curves": ([_P] * 4 + [_I] * 3 + [_P, _I] + [_P] * 4 + [_S], _N),
     "sats_calibrate_sats": ([_P, _I] + [_P] * 3 + [_I] * 3 + [ctypes.c_double] * 3 + [_N] + [_P] * 3 + [_S], _N),
 }
@@ -125,6 +127,19 @@ def sats_mlp_forward_inspect(x, token_ids, W_gate, W_up_T, W_down, thresholds, r
     _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
           _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers,
           _stream(stream), _ptr(route_out), _ptr(active_count), _ptr(active_idx), _ptr(layer_in))
+
+
+def sats_mlp_forward_lora(x, token_ids, W_gate, W_up_T, W_down, adapters, rank, scale, thresholds, route_lut,
+                          out, n_tokens, d, d_ff, n_layers, stream=None, route_out=None, active_count=None,
+                          active_idx=None, layer_in=None):
+    """LoRA-aware routed sparse forward; adapters = (A_gate, B_gate, A_up, B_up_T, A_down, B_down)."""
+    name = "sats_mlp_forward_lora_f32" if _is_f32(x) else "sats_mlp_forward_lora"
+    if len(adapters) != 6:
+        raise ValueError("adapters = (A_gate, B_gate, A_up, B_up_T, A_down, B_down)")
+    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+          *(_ptr(m) for m in adapters), int(rank), float(scale), _ptr(thresholds), _ptr(route_lut), _ptr(out),
+          n_tokens, d, d_ff, n_layers, _stream(stream), _ptr(route_out), _ptr(active_count), _ptr(active_idx),
+          _ptr(layer_in))
 
 
 def sats_reserve(max_tokens, d, d_ff, n_layers, elem_bytes, stream=None):

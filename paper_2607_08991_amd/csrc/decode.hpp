@@ -32,10 +32,10 @@ namespace sats {
 // Optional phase timestamps (build with -DSATS_TRACE): per workgroup, wall
 // clock at fixed points of the first layer, read back with sats_trace_read().
 #ifdef SATS_TRACE
-__device__ unsigned long long sats_trace_buf[4096 * 8];
+__device__ unsigned long long sats_trace_buf[4096 * 16];
 #define SATS_TRACE_POINT(i)                                                               \
   do {                                                                                    \
-    if (threadIdx.x == 0 && blockIdx.x < 4096) sats_trace_buf[blockIdx.x * 8 + (i)] = wall_clock64(); \
+    if (threadIdx.x == 0 && blockIdx.x < 4096) sats_trace_buf[blockIdx.x * 16 + (i)] = wall_clock64(); \
   } while (0)
 #else
 #define SATS_TRACE_POINT(i) \
@@ -78,8 +78,19 @@ struct DecodeArgs {
   unsigned *err;          // device error flag (a bounded wait gave up)
   uint8_t *route_out;     // optional [1]
   uint8_t *keep_out;      // optional [L][d_ff]
-  void *layer_in;         // optional [L][d]
+  void *layer_in;         // optional [L][...]: layer l's input at layer_in + l * in_stride
+  int64_t in_stride;      // elements between the layers' inputs in layer_in
+  // LoRA adapters of the sparse path (Ag null: none), stacked per layer like
+  // the weights: Ag, Au [d][rank], Bg [rank][d_ff], BuT, Ad [d_ff][rank],
+  // Bd [rank][d]; lscale multiplies every adapter product
+  const void *Ag, *Bg, *Au, *BuT, *Ad, *Bd;
+  int rank;
+  float lscale;
+  float *vpart;           // [nrc][rank] per gate row chunk: partial h . A_up
+  float *zpart;           // [G][rank]   per rows workgroup: sum of p_j A_down[j] over its kept rows
 };
+
+constexpr int kLoraMaxRank = 64;  // ranks 8, 16, 32, 64
 
 struct DecodeSmem {
   float hs[kDecodeMaxD];                // layer input
@@ -89,6 +100,16 @@ struct DecodeSmem {
   int wcnt[kDecodeWaves];
   float scal[kDecodeWaves];
   int flag;
+  float lv[2][kDecodeWaves][kLoraMaxRank];  // LoRA: wavefront partials of h . A (gate, up)
+  float lz[kLoraMaxRank];                    // LoRA: h . A_up (rows) or z (reduce)
+};
+
+// LoRA operands of a rows workgroup's kept rows (list position i): the up
+// adapter's contribution w_i = s (h A_up) . B_up_T[j] and A_down[j].
+template <typename T>
+struct LoraRows {
+  float lw[kDecodeThreads / 2];
+  T lad[64 * Elem<T>::kVec * kLoraMaxRank];  // [list position][rank]: one column block's list at most
 };
 
 // Four consecutive floats at byte offset voff of buffer r, written through to
@@ -249,11 +270,111 @@ __device__ __forceinline__ void dec_input_finish(const DecodeArgs &a, int l, Inp
       if (k < d) {
         const T hv = Elem<T>::round(r.yv[i] / scale);
         sm.hs[k] = Elem<T>::value(hv);
-        if (record) static_cast<T *>(a.layer_in)[(size_t)l * d + k] = hv;
+        if (record) static_cast<T *>(a.layer_in)[(size_t)l * a.in_stride + k] = hv;
       }
     }
   }
   __syncthreads();
+}
+
+// ------------------------------------------------------------------ LoRA adapters
+//
+// The sparse path of a fine-tuned routed model adds s A B to each projection
+// (Section 5).  Every product splits over the gate's row chunks: a gate tile
+// over rows k0 .. k0 + kn adds s (h[k0..] A_gate[k0..]) B_gate to its partial
+// of a, so the row-chunk sums give h (W_gate + s A_gate B_gate) with no step
+// of its own; the tiles of column block 0 also write h[k0..] A_up[k0..], whose
+// sum the rows launch uses for the up adapter of its kept rows.  The down
+// adapter's first factor is summed over the kept rows (z = sum p_j A_down[j])
+// next to each rows workgroup's partial y, and the second reduction stage
+// adds s z B_down.
+
+constexpr int kLoraPieces = 2;  // 16-byte pieces of an A matrix per thread and pass
+
+template <typename T>
+struct LoraGateRegs {
+  u32x4 ag[kLoraPieces], au[kLoraPieces];  // A_gate / A_up pieces of one pass over the tile's rows
+};
+
+// B_gate rows at the tile's columns, staged in LDS by loads that write LDS
+// (no registers held across the tile): row r at lb[r], 16 bytes per lane.
+struct LoraGateSmem {
+  uint8_t lb[kLoraMaxRank][1024];
+};
+
+// One pass of A loads: pieces p0 + tid, p0 + tid + THREADS (16 bytes each) of
+// rows k0 .. k0 + kn of A_gate (and of A_up when `up`).
+template <typename T>
+__device__ __forceinline__ void lora_a_issue(const DecodeArgs &a, int l, int k0, int kn, bool up, int p0,
+                                             LoraGateRegs<T> &lr) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int R = a.rank, tid = threadIdx.x;
+  const uint32_t abytes = (uint32_t)((size_t)a.d * R * sizeof(T));
+  const __amdgpu_buffer_rsrc_t rg = weight_rsrc(static_cast<const T *>(a.Ag) + (size_t)l * a.d * R, abytes);
+  const __amdgpu_buffer_rsrc_t ru = weight_rsrc(static_cast<const T *>(a.Au) + (size_t)l * a.d * R, abytes);
+  const int np = kn * R / VEC;
+  const uint32_t abase = (uint32_t)((size_t)k0 * R * sizeof(T));
+#pragma unroll
+  for (int m = 0; m < kLoraPieces; ++m) {
+    const int pc = p0 + tid + m * kGateThreads;
+    const uint32_t off = pc < np ? abase + (uint32_t)pc * 16u : kOffNone;
+    lr.ag[m] = __builtin_amdgcn_raw_buffer_load_b128(rg, (int)off, 0, 0);
+    lr.au[m] = up ? __builtin_amdgcn_raw_buffer_load_b128(ru, (int)off, 0, 0) : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// This wavefront's rows of B_gate (wv, wv + NW, ...) at the lane's columns,
+// straight into LDS.
+template <typename T>
+__device__ __forceinline__ void lora_b_issue(const DecodeArgs &a, int l, int col, LoraGateSmem &ls) {
+  constexpr int NW = kGateThreads / 64;
+  const int R = a.rank, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const __amdgpu_buffer_rsrc_t rb = weight_rsrc(static_cast<const T *>(a.Bg) + (size_t)l * R * a.d_ff,
+                                                (uint32_t)((size_t)R * a.d_ff * sizeof(T)));
+  // every row slot is loaded, past the rank from past the buffer (zeros): a
+  // branch around these loads would cost the compiler its record of which
+  // LDS bytes they write, and with it waits on every load before LDS reads
+#pragma unroll
+  for (int m = 0; m < kLoraMaxRank / NW; ++m) {
+    const int row = wv + m * NW;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (__attribute__((address_space(3))) void *)ls.lb[row], 16,
+                                             row < R ? (int)(col * sizeof(T)) : (int)kOffNone,
+                                             row < R ? (int)((size_t)row * a.d_ff * sizeof(T)) : 0, 0, 0);
+  }
+}
+
+// h . A over the tile's rows: each lane adds its pieces of one pass to sv
+// (every piece of a thread covers the same rank indices: THREADS pieces
+// span whole rows); lora_v_reduce then adds the lanes of equal index by
+// halving exchanges, and lanes 0 .. R / VEC - 1 write the wavefront's sums.
+template <typename T>
+__device__ __forceinline__ void lora_a_acc(const DecodeArgs &a, int k0, int kn, int p0, const u32x4 (&pc)[kLoraPieces],
+                                           float (&sv)[Elem<T>::kVec], const DecodeSmem &sm) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int R = a.rank, np = kn * R / VEC;
+#pragma unroll
+  for (int m = 0; m < kLoraPieces; ++m) {
+    const int p = p0 + threadIdx.x + m * kGateThreads;
+    if (p < np) {
+      const float hv = sm.hs[k0 + p * VEC / R];
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) sv[v] = fmaf(hv, unpack<T>(pc[m], v), sv[v]);
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void lora_v_reduce(const DecodeArgs &a, float (&sv)[Elem<T>::kVec],
+                                              float (&out)[kLoraMaxRank]) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int RQ = a.rank / VEC, lane = threadIdx.x & 63;
+  for (int msk = 32; msk >= max(RQ, 1); msk >>= 1)
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) sv[v] += __shfl_xor(sv[v], msk, 64);
+  if (lane < RQ) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) out[lane * VEC + v] = sv[v];
+  }
 }
 
 // ------------------------------------------------------------------ gate
@@ -282,8 +403,8 @@ __device__ __forceinline__ void gate_consume(const DecodeSmem &sm, int k0w, int 
 // Gate tiles blockIdx.x, blockIdx.x + gridDim.x, ... (tile t: column block
 // t % nblk, row chunk t / nblk); forms h in LDS before the first tile's
 // products (its loads follow the tile's first weight loads).
-template <typename T>
-__device__ void dec_gate(const DecodeArgs &a, int l, DecodeSmem &sm, bool record) {
+template <typename T, bool LORA>
+__device__ void dec_gate(const DecodeArgs &a, int l, DecodeSmem &sm, LoraGateSmem &ls, bool record) {
   constexpr int THREADS = kGateThreads, VEC = Elem<T>::kVec, NW = THREADS / 64;
   constexpr int CB = dec_block_cols<T>();
   constexpr int GB = kGateBatch;
@@ -297,6 +418,10 @@ __device__ void dec_gate(const DecodeArgs &a, int l, DecodeSmem &sm, bool record
   const uint32_t stride = (uint32_t)((size_t)NW * d_ff * sizeof(T));  // between a wavefront's rows
   InputRegs<THREADS> ir;
   bool have_input = false;
+  // LoRA: the token's route (base-path tokens use the base weights only)
+  constexpr bool lora = LORA;
+  const float lsc = !lora ? 0.0f
+                          : ((l == 0 ? token_is_base(a.route_mode, a.ids, a.lut, 0) : a.state[0]) ? 0.0f : a.lscale);
   for (int t = blockIdx.x; t < a.nblk * a.nrc; t += gridDim.x) {
     const int cb = t % a.nblk, rc = t / a.nblk;
     const int k0 = rc * rows, kn = max(0, min(d, k0 + rows) - k0);
@@ -311,6 +436,15 @@ __device__ void dec_gate(const DecodeArgs &a, int l, DecodeSmem &sm, bool record
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] = 0.0f;
     u32x4 q[GB];
+    // LoRA: B_gate rows go to LDS now; the A pieces are loaded with the
+    // wavefront's last weight batch and used after it (a wait for them
+    // earlier would also wait for the weight loads issued before them)
+    LoraGateRegs<T> lr;
+    const bool a_early = !live || nr <= GB;
+    if constexpr (LORA) {
+      lora_b_issue<T>(a, l, col, ls);
+      if (a_early) lora_a_issue<T>(a, l, k0, kn, cb == 0, 0, lr);
+    }
     if (live) gate_issue<T, GB, NW>(wr, row0, stride, 0, nr, lo, q);
     if (!have_input) {  // h is needed from the first batch on; its loads follow the weights'
       dec_input_issue<T, THREADS>(a, l, ir);
@@ -321,8 +455,45 @@ __device__ void dec_gate(const DecodeArgs &a, int l, DecodeSmem &sm, bool record
     if (live) {
       gate_consume<T, GB, NW>(sm, k0 + wv, 0, nr, q, acc);
       for (int r0 = GB; r0 < nr; r0 += GB) {
+        if (LORA && r0 + GB >= nr) lora_a_issue<T>(a, l, k0, kn, cb == 0, 0, lr);
         gate_issue<T, GB, NW>(wr, row0, stride, r0, nr, lo, q);
         gate_consume<T, GB, NW>(sm, k0 + wv, r0, nr, q, acc);
+      }
+    }
+    if constexpr (LORA) {  // this tile's h . A_gate (and h . A_up on column block 0)
+      float sg[VEC], su[VEC];
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) sg[v] = su[v] = 0.0f;
+      const int np = kn * a.rank / VEC, pp = kLoraPieces * kGateThreads;
+      for (int p0 = 0; p0 < np; p0 += pp) {
+        if (p0 > 0) lora_a_issue<T>(a, l, k0, kn, cb == 0, p0, lr);
+        lora_a_acc<T>(a, k0, kn, p0, lr.ag, sg, sm);
+        if (cb == 0) lora_a_acc<T>(a, k0, kn, p0, lr.au, su, sm);
+      }
+      lora_v_reduce<T>(a, sg, sm.lv[0][wv]);
+      if (cb == 0) lora_v_reduce<T>(a, su, sm.lv[1][wv]);
+      __syncthreads();
+      if (l == 0) SATS_TRACE_POINT(13);
+      if (cb == 0 && tid < a.rank) {
+        float v = 0.0f;
+#pragma unroll
+        for (int q2 = 0; q2 < NW; ++q2) v += sm.lv[1][q2][tid];
+        store_coherent(a.vpart + (size_t)rc * a.rank + tid, v);
+      }
+    }
+    if (LORA && lsc != 0.0f) {  // s (h[k0..] A_gate[k0..]) B_gate: this wavefront's rows of B_gate
+#pragma unroll
+      for (int m = 0; m < kLoraMaxRank / NW; ++m) {
+        const int row = wv + m * NW;
+        if (row < a.rank) {
+          float vg = 0.0f;
+#pragma unroll
+          for (int q2 = 0; q2 < NW; ++q2) vg += sm.lv[0][q2][row];
+          vg *= lsc;
+          const u32x4 bq = *reinterpret_cast<const u32x4 *>(&ls.lb[row][lane * 16]);
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc[v] = fmaf(vg, unpack<T>(bq, v), acc[v]);
+        }
       }
     }
 #pragma unroll
@@ -379,7 +550,8 @@ __device__ __forceinline__ void rows_issue(__amdgpu_buffer_rsrc_t Wu, __amdgpu_b
 template <typename T, int R, int NCH>
 __device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)[NCH][Elem<T>::kVec],
                                              float (&yacc)[NCH][Elem<T>::kVec], int r0, int end, int par,
-                                             const u32x4 (&bu)[R][NCH], const u32x4 (&bd)[R][NCH]) {
+                                             const u32x4 (&bu)[R][NCH], const u32x4 (&bd)[R][NCH], bool lora,
+                                             const LoraRows<T> &lr, int rank, float &zh) {
   constexpr int VEC = Elem<T>::kVec;
   const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 7);
   const int hf = __builtin_amdgcn_readfirstlane(threadIdx.x >> 9);
@@ -401,7 +573,11 @@ __device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)
     float ut = 0.0f;
 #pragma unroll
     for (int q = 0; q < 8; ++q) ut += part[r * 8 + q];
-    const float pr = (r0 + r < end) ? sm.mg[max(0, min(r0 + r, end - 1))] * ut : 0.0f;
+    const int li = max(0, min(r0 + r, end - 1));
+    if (lora) ut += lr.lw[li];  // the up adapter's term of this kept row
+    const float pr = (r0 + r < end) ? sm.mg[li] * ut : 0.0f;
+    if (lora && hw == 0 && lane < rank && r0 + r < end)  // z_lane += p_j A_down[j][lane], this half's rows in order
+      zh = fmaf(pr, Elem<T>::value(lr.lad[(size_t)li * rank + lane]), zh);
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
 #pragma unroll
@@ -409,12 +585,89 @@ __device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)
   }
 }
 
+// LoRA: h . A_up from the gate launch's row-chunk partials, in a fixed
+// order: thread (q, i) adds chunks q, q + 8, ... (its first loads are issued
+// at the start of the rows launch, ahead of every streaming load of its
+// wavefront, since loads complete in issue order), then thread i adds the 8
+// groups, into sm.lz.
+constexpr int kLoraVG = 8, kLoraVQ = 4;
+__device__ __forceinline__ void lora_vu_issue(const DecodeArgs &a, float (&vq)[kLoraVQ]) {
+  const int R = a.rank, tid = threadIdx.x, i = tid % R, q = tid / R;
+#pragma unroll
+  for (int k = 0; k < kLoraVQ; ++k) {
+    const int rc = q + kLoraVG * k;
+    vq[k] = (q < kLoraVG && rc < a.nrc) ? load_coherent(a.vpart + (size_t)rc * R + i) : 0.0f;
+  }
+}
+__device__ __forceinline__ void lora_vu_finish(const DecodeArgs &a, const float (&vq)[kLoraVQ], DecodeSmem &sm) {
+  const int R = a.rank, tid = threadIdx.x, i = tid % R, q = tid / R;
+  float *flat = &sm.lv[0][0][0];
+  float v = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kLoraVQ; ++k) v += vq[k];
+  const int rest = a.nrc - q - kLoraVG * kLoraVQ;  // chunks past the first loads
+  if (q < kLoraVG && rest > 0)
+    v += sum_coherent(a.vpart + (size_t)(q + kLoraVG * kLoraVQ) * R + i, (size_t)kLoraVG * R,
+                      (rest + kLoraVG - 1) / kLoraVG);
+  flat[tid] = v;
+  __syncthreads();
+  if (tid < R) {
+    float u = 0.0f;
+#pragma unroll
+    for (int g = 0; g < kLoraVG; ++g) u += flat[g * R + tid];
+    sm.lz[tid] = u;
+  }
+}
+
+// LoRA: for the kept rows list[i0 .. i0 + mn) of a unit, w_i = s (h A_up) .
+// B_up_T[j] into lr.lw and A_down[j] into lr.lad (R / VEC adjacent threads
+// per row, 16 bytes each).  The loads of the first pass are issued before
+// the unit's first row batches (loads complete in issue order) and used
+// after them; further passes (more than THREADS / (R / VEC) rows) follow.
+template <typename T>
+struct LoraPrepRegs {
+  u32x4 bu, ad;
+};
+
+template <typename T>
+__device__ __forceinline__ void lora_prep_load(const DecodeArgs &a, int l, const DecodeSmem &sm, int i0, int mn, int b0,
+                                               LoraPrepRegs<T> &pr) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int R = a.rank, RQ = R / VEC, idx = b0 + (int)threadIdx.x;
+  const size_t rl = (size_t)a.d_ff * R;
+  const uint32_t bytes = (uint32_t)(rl * sizeof(T));
+  const __amdgpu_buffer_rsrc_t rb = weight_rsrc(static_cast<const T *>(a.BuT) + (size_t)l * rl, bytes);
+  const __amdgpu_buffer_rsrc_t rd = weight_rsrc(static_cast<const T *>(a.Ad) + (size_t)l * rl, bytes);
+  const bool on = idx < mn * RQ;
+  const int m = i0 + (on ? idx / RQ : 0), q = idx % RQ;
+  const uint32_t off = on ? (uint32_t)(((size_t)sm.mj[m] * R + q * VEC) * sizeof(T)) : kOffNone;
+  pr.bu = __builtin_amdgcn_raw_buffer_load_b128(rb, (int)off, 0, 0);
+  pr.ad = __builtin_amdgcn_raw_buffer_load_b128(rd, (int)off, 0, 0);
+}
+
+template <typename T>
+__device__ __forceinline__ void lora_prep_use(const DecodeArgs &a, const DecodeSmem &sm, LoraRows<T> &lr, int i0,
+                                              int mn, int b0, const LoraPrepRegs<T> &pr) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int R = a.rank, RQ = R / VEC, idx = b0 + (int)threadIdx.x;
+  const bool on = idx < mn * RQ;
+  const int m = i0 + (on ? idx / RQ : 0), q = idx % RQ;
+  float w = 0.0f;
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) w = fmaf(sm.lz[q * VEC + v], unpack<T>(pr.bu, v), w);
+  for (int msk = 1; msk < RQ; msk <<= 1) w += __shfl_xor(w, msk, 64);
+  if (on) {
+    if (q == 0) lr.lw[m] = a.lscale * w;
+    *reinterpret_cast<u32x4 *>(&lr.lad[(size_t)m * R + q * VEC]) = pr.ad;
+  }
+}
+
 // Rows phase of workgroup w (of G): units w, w + G, ... of nblk x S units
 // (S = max(1, G / nblk) shares per column block); writes the workgroup's
 // partial y.  h is formed first (its loads overlap the first block's partial
 // sums).
-template <typename T>
-__device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, DecodeSmem &sm) {
+template <typename T, bool LORA>
+__device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, DecodeSmem &sm, LoraRows<T> &lr) {
   constexpr int VEC = Elem<T>::kVec, NW = kDecodeWaves;
   constexpr int CB = dec_block_cols<T>();
   constexpr int CH = 64 * VEC;              // elements per chunk (one 16-byte load per lane)
@@ -442,6 +695,13 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
 #pragma unroll
     for (int v = 0; v < VEC; ++v) hreg[c][v] = yacc[c][v] = 0.0f;
   int par = 0;  // LDS slot parity for the parts of u
+  const bool lora = LORA && !base;
+  float zh = 0.0f;  // LoRA, lane i < rank of wavefront 0 of each half: z_i over the half's kept rows
+  float vq[kLoraVQ];
+  if (lora) {
+    lora_vu_issue(a, vq);
+    asm volatile("" ::: "memory");  // keeps these loads ahead of the partial sums' and the rows'
+  }
 
   for (int un = w; un < units; un += G) {
     const int cb = un % nblk, sub = un / nblk;
@@ -477,10 +737,13 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
     const int hn = (mn + 1) / 2;
     const int b = i0 + hf * hn, e = i0 + min(mn, (hf + 1) * hn);
     if (l == 0 && un == w) SATS_TRACE_POINT(4);
+    if (lora && un == w) lora_vu_finish(a, vq, sm);
     // batches of RB rows in two register sets: the next batch is always in
     // flight while one is used (both halves run the same number of batches)
     const int nbt = (hn + RB - 1) / RB;
     u32x4 au[RB][NCH], ad[RB][NCH], cu[RB][NCH], cd[RB][NCH];
+    LoraPrepRegs<T> lp;
+    if (lora) lora_prep_load<T>(a, l, sm, i0, mn, 0, lp);
     if (nbt > 0) rows_issue<T, RB, NCH>(Wu, Wd, sm, b, e, d, au, ad);
     if (nbt > 1) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + RB, e, d, cu, cd);
     if (un == w) {
@@ -493,17 +756,34 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
           hreg[c][v] = (k < d) ? sm.hs[k] : 0.0f;
         }
     }
+    if (lora) {  // the up adapter's terms and A_down of this unit's rows
+      if (l == 0 && un == w) SATS_TRACE_POINT(8);
+      const int rq = a.rank / VEC;
+      lora_prep_use<T>(a, sm, lr, i0, mn, 0, lp);
+      for (int b0 = kDecodeThreads; b0 < mn * rq; b0 += kDecodeThreads) {
+        lora_prep_load<T>(a, l, sm, i0, mn, b0, lp);
+        lora_prep_use<T>(a, sm, lr, i0, mn, b0, lp);
+      }
+      __syncthreads();
+      if (l == 0 && un == w) SATS_TRACE_POINT(9);
+    }
     for (int i = 0; i < nbt; i += 2) {
-      rows_consume<T, RB, NCH>(sm, hreg, yacc, b + i * RB, e, par, au, ad);
+      rows_consume<T, RB, NCH>(sm, hreg, yacc, b + i * RB, e, par, au, ad, lora, lr, a.rank, zh);
       par ^= 1;
       if (i + 2 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
       if (i + 1 < nbt) {
-        rows_consume<T, RB, NCH>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd);
+        rows_consume<T, RB, NCH>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
         par ^= 1;
         if (i + 3 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
       }
     }
     __syncthreads();  // the next unit rewrites the list
+  }
+  if (lora) {  // z = half 0's sum + half 1's
+    if (wv == 8 && lane < a.rank) lr.lw[lane] = zh;
+    __syncthreads();
+    if (wv == 0 && lane < a.rank) store_coherent(a.zpart + (size_t)w * a.rank + lane, zh + lr.lw[lane]);
+    if (l == 0) SATS_TRACE_POINT(10);
   }
   if (l == 0) SATS_TRACE_POINT(5);
   // the two halves' sums, added in half order, are this workgroup's partial y
@@ -539,8 +819,9 @@ __device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, Dec
 
 // Workgroup w (of RW) and its slice of columns: y = sum of the G partials
 // in workgroup order.
-template <typename T>
-__device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm) {
+template <typename T, bool LORA>
+__device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm, bool base) {
+  const bool lora = LORA && !base;
   constexpr int THREADS = kDecodeThreads, NW = kDecodeWaves;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int d = a.d, G = a.G;
@@ -555,8 +836,51 @@ __device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm) {
   sm.red[tid] = s;
   __syncthreads();
   float y = 0.0f;
-  if (tid < nc) {
+  if (tid < nc)
     for (int qg = 0; qg < ngr && qg < G; ++qg) y += sm.red[qg * cpw + tid];
+  if (lora) {  // + s z B_down, z summed over the G partials in workgroup order
+    const int R = a.rank, Q = THREADS / R;
+    // B_down[i][cw0 + c] for every (i, c) of the slice, one element per thread
+    // and pass (every load of a pass issued before any is used), into LDS
+    float *bsl = sm.red + THREADS;  // [R][cpw] (the partial-group sums use the first THREADS)
+    {
+      const T *bd = static_cast<const T *>(a.Bd) + (size_t)l * R * d + cw0;
+      const int per = max(1, cpw), tot = R * per;
+      float bv[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = tid + k * THREADS, i = min(e / per, R - 1), c = min(e % per, max(nc - 1, 0));
+        bv[k] = Elem<T>::get(bd + (size_t)i * d + c);
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (tid + k * THREADS < tot) bsl[tid + k * THREADS] = bv[k];
+      for (int e = tid + 4 * THREADS; e < tot; e += THREADS) bsl[e] = Elem<T>::get(bd + (size_t)(e / per) * d + min(e % per, max(nc - 1, 0)));
+    }
+    float *flat = &sm.lv[0][0][0];
+    float zs = 0.0f;
+    {
+      const int i = tid % R, q = tid / R;
+      if (q < G) zs = sum_coherent(a.zpart + (size_t)q * R + i, (size_t)Q * R, (G - q + Q - 1) / Q);
+    }
+    if (l == 0) SATS_TRACE_POINT(12);
+    flat[tid] = zs;
+    __syncthreads();
+    if (l == 0) SATS_TRACE_POINT(14);
+    if (tid < R) {
+      float z = 0.0f;
+      for (int q = 0; q < Q; ++q) z += flat[q * R + tid];
+      sm.lz[tid] = a.lscale * z;
+    }
+    __syncthreads();
+    if (l == 0) SATS_TRACE_POINT(11);
+    if (tid < nc) {
+      float t = 0.0f;
+      for (int i = 0; i < R; ++i) t = fmaf(sm.lz[i], bsl[i * cpw + tid], t);
+      y += t;
+    }
+  }
+  if (tid < nc) {
     if (l == a.L - 1) static_cast<T *>(a.out)[cw0 + tid] = Elem<T>::round(y);
     else store_coherent(a.ybuf + cw0 + tid, y);
   }
@@ -573,10 +897,11 @@ __device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm) {
 
 // ------------------------------------------------------------------ kernels
 
-// Gate tiles (any grid).
-template <typename T>
+// Gate tiles (any grid); LORA: with the adapters of the sparse path.
+template <typename T, bool LORA>
 __global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
+  __shared__ LoraGateSmem ls;
   if (blockIdx.x == 0 && threadIdx.x == 0)  // the previous rows launch has finished
     __hip_atomic_store(a.done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (l == 0 && blockIdx.x == 0 && threadIdx.x == 0) {
@@ -585,7 +910,7 @@ __global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, in
     if (a.route_out) a.route_out[0] = (uint8_t)base;
   }
   if (l == 0) SATS_TRACE_POINT(0);
-  dec_gate<T>(a, l, sm, a.layer_in != nullptr && blockIdx.x == 0);
+  dec_gate<T, LORA>(a, l, sm, ls, a.layer_in != nullptr && blockIdx.x == 0);
   if (l == 0) SATS_TRACE_POINT(2);
 }
 
@@ -597,11 +922,13 @@ __global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, in
 // next gate launch (which always comes before the next rows launch).
 constexpr int kSpinLimit = 1 << 20;  // polls of one wait (each a device-coherent load)
 
-template <typename T>
+template <typename T, bool LORA>
 __global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
+  __shared__ LoraRows<T> lr;
   if (l == 0) SATS_TRACE_POINT(3);
-  dec_rows<T>(a, l, a.state[0], a.G, blockIdx.x, sm);
+  const int base = a.state[0];
+  dec_rows<T, LORA>(a, l, base, a.G, blockIdx.x, sm, lr);
   const int tid = threadIdx.x, G = a.G;
   __builtin_amdgcn_s_waitcnt(0);  // this thread's partial-y stores have completed
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -623,7 +950,7 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, 
   __syncthreads();
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   if (l == 0) SATS_TRACE_POINT(6);
-  dec_reduce<T>(a, l, ticket - (G - a.RW), sm);
+  dec_reduce<T, LORA>(a, l, ticket - (G - a.RW), sm, base);
   if (l == 0) SATS_TRACE_POINT(7);
 }
 

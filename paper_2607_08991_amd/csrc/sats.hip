@@ -164,6 +164,7 @@ struct Buffers {
   uint8_t *keep;
   float *ypart, *sspart;  // single-token path: per-workgroup partial y and sums of squares
   float *dgpart;          // single-token path: partial gate sums per row chunk
+  float *dvpart, *dzpart; // single-token path, LoRA: partial h . A_up per row chunk, z per rows workgroup
   int *dstate;            // single-token path: the token's route
   int *perm, *ctl;        // batched path: token partition and dense-group control words
   uint8_t *skip, *gbase;
@@ -211,6 +212,8 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.pdense = c.take<uint16_t>(Pp * d_ff);
   t.ddpart = c.take<float>((int64_t)sats::kDenseMaxKsplit * Pp * d);
   t.dgpart = c.take<float>((int64_t)sats::dec_nrcp(dp.nrc) * d_ff);
+  t.dvpart = c.take<float>((int64_t)dp.nrc * sats::kLoraMaxRank);
+  t.dzpart = c.take<float>((int64_t)dp.G * sats::kLoraMaxRank);
   t.dstate = c.take<int>(64);
   if (b) *b = t;
   return c.off;
@@ -279,7 +282,7 @@ int ensure_workspace(hipStream_t stream, size_t bytes, size_t n_counters, Worksp
 // (at most kDecodeMaxG) take the rows and reduce phases, each reduce
 // workgroup owning at most one column per thread; gate tiles are one column
 // block by about d / nrc rows.  Returns false when the shape does not fit.
-bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp) {
+bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, int lora_rank = 0) {
   DecodePlan q{};
   const int64_t cb = (int64_t)(16 / esz) * 64;
   q.G = G;
@@ -287,6 +290,7 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp) {
   const int64_t tiles = env_int("SATS_DEC_GATE_WGS", 256);
   int64_t nrc = std::max<int64_t>(1, tiles / q.nblk);
   nrc = std::min<int64_t>(nrc, std::max<int64_t>(1, d / (sats::kGateThreads / 64)));  // a row per wavefront
+  (void)lora_rank;
   q.nrc = (int)nrc;
   q.gate_grid = q.nblk * q.nrc;
   // second reduction stage: the last RW rows workgroups to finish take one
@@ -317,6 +321,12 @@ struct Call {
   uint8_t *route_out;
   int32_t *active_count, *active_idx;
   void *layer_in;
+  // LoRA adapters of the sparse path (Ag null: none)
+  const void *Ag, *Bg, *Au, *BuT, *Ad, *Bd;
+  int64_t rank;
+  float lscale;
+  // token tok of ntot: the single-token path's offsets into the inspection arrays
+  int64_t tok, ntot;
 };
 
 
@@ -547,28 +557,48 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   const bool lists = c.active_count || c.active_idx;
   a.keep_out = lists ? b.keep : nullptr;
   a.layer_in = c.layer_in;
+  a.in_stride = std::max<int64_t>(1, c.ntot) * c.d;
+  a.Ag = c.Ag;
+  a.Bg = c.Bg;
+  a.Au = c.Au;
+  a.BuT = c.BuT;
+  a.Ad = c.Ad;
+  a.Bd = c.Bd;
+  a.rank = (int)c.rank;
+  a.lscale = c.lscale;
+  a.vpart = b.dvpart;
+  a.zpart = b.dzpart;
   // two plain launches per layer (the rows launch ends with the second
   // reduction stage); kernel boundaries order the phases
   for (int l = 0; l < (int)c.L; ++l) {
     {
       TimedLaunch tl(SATS_K_DEC_GATE, c.stream);
-      hipExtLaunchKernelGGL((dec_gate_kernel<T>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream,
-                            tl.start, tl.stop, 0, a, l);
+      if (c.Ag)
+        hipExtLaunchKernelGGL((dec_gate_kernel<T, true>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream,
+                              tl.start, tl.stop, 0, a, l);
+      else
+        hipExtLaunchKernelGGL((dec_gate_kernel<T, false>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream,
+                              tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
     {
       TimedLaunch tl(SATS_K_DEC_ROWS, c.stream);
-      hipExtLaunchKernelGGL((dec_rows_kernel<T>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
-                            tl.start, tl.stop, 0, a, l);
+      if (c.Ag)
+        hipExtLaunchKernelGGL((dec_rows_kernel<T, true>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
+                              tl.start, tl.stop, 0, a, l);
+      else
+        hipExtLaunchKernelGGL((dec_rows_kernel<T, false>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
+                              tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
   }
   if (lists) {
     for (int64_t l = 0; l < c.L; ++l) {
       CompactArgs ca{};
+      const int64_t nt = std::max<int64_t>(1, c.ntot);
       ca.keep = b.keep + l * c.d_ff;
-      ca.idx = c.active_idx ? c.active_idx + l * c.d_ff : nullptr;
-      ca.count = c.active_count ? c.active_count + l : nullptr;
+      ca.idx = c.active_idx ? c.active_idx + (l * nt + c.tok) * c.d_ff : nullptr;
+      ca.count = c.active_count ? c.active_count + l * nt + c.tok : nullptr;
       ca.n = 1;
       ca.d_ff = (int)c.d_ff;
       TimedLaunch tl(SATS_K_INSPECT, c.stream);
@@ -580,6 +610,49 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// LoRA calls run the single-token path, token after token (each token takes
+// its own route; the inspection outputs are written at the token's offsets).
+template <typename T>
+int run_lora(const Call &c, bool vec_ok) {
+  const int esz = (int)sizeof(T);
+  if (!c.Bg || !c.Au || !c.BuT || !c.Ad || !c.Bd) return fail(SATS_ERR_NULL, "all six adapter matrices are required");
+  if (c.rank != 8 && c.rank != 16 && c.rank != 32 && c.rank != 64)
+    return fail(SATS_ERR_SHAPE, "LoRA rank must be 8, 16, 32 or 64 (got %lld)", (long long)c.rank);
+  for (const void *q : {c.Ag, c.Bg, c.Au, c.BuT, c.Ad, c.Bd})
+    if (!aligned16(q)) return fail(SATS_ERR_ARG, "adapter matrices must be 16-byte aligned");
+  if (!std::isfinite(c.lscale)) return fail(SATS_ERR_ARG, "LoRA scale must be finite");
+  DecodePlan dp;
+  if (!vec_ok || getenv("SATS_NO_DECODE") ||
+      !make_decode_plan(c.d, c.d_ff, esz, env_int("SATS_DEC_ROWS_WGS", device_cus()), &dp, (int)c.rank))
+    return fail(SATS_ERR_SHAPE,
+                "LoRA calls need the single-token layout: d <= %d, d and d_ff multiples of %d, 16-byte aligned arrays",
+                sats::kDecodeMaxD, 16 / esz);
+  if ((uint64_t)c.d_ff * c.rank * esz >= (1ull << 31) || (uint64_t)c.d * c.rank * esz >= (1ull << 31))
+    return fail(SATS_ERR_SHAPE, "adapter matrices past 2 GB");
+  if (c.rank * ((c.d + dp.RW - 1) / dp.RW) > 2 * sats::kDecodeMaxD - sats::kDecodeThreads)
+    return fail(SATS_ERR_SHAPE, "LoRA: B_down slices of the second reduction stage do not fit LDS");
+  const Plan p = make_plan(c.d, c.d_ff, esz, vec_ok, 1);
+  const size_t bytes = layout(nullptr, p, 1, c.d, c.d_ff, esz, c.L, dp, nullptr);
+  Workspace *ws = nullptr;
+  int rc = ensure_workspace(c.stream, bytes, counter_count(p, 1, dp), &ws);
+  if (rc) return rc;
+  Buffers b{};
+  layout(ws->mem, p, 1, c.d, c.d_ff, esz, c.L, dp, &b);
+  for (int64_t i = 0; i < c.n; ++i) {
+    Call ci = c;
+    ci.x = static_cast<const T *>(c.x) + i * c.d;
+    ci.out = static_cast<T *>(c.out) + i * c.d;
+    ci.ids = c.ids ? c.ids + i : nullptr;
+    ci.route_out = c.route_out ? c.route_out + i : nullptr;
+    ci.layer_in = c.layer_in ? static_cast<void *>(static_cast<T *>(c.layer_in) + i * c.d) : nullptr;
+    ci.n = 1;
+    ci.tok = i;
+    ci.ntot = c.n;
+    if ((rc = run_decode<T>(ci, dp, b, ws->counters))) return rc;
+  }
+  return SATS_OK;
+}
 
 template <typename T>
 int run(const Call &c) {
@@ -605,6 +678,7 @@ int run(const Call &c) {
                       (!c.layer_in || aligned16(c.layer_in));
   const int pass = (int)std::min<int64_t>(c.n, kMaxPass);
   const Plan p = make_plan(c.d, c.d_ff, esz, vec_ok, pass);
+  if (c.Ag) return run_lora<T>(c, vec_ok);
   // single-token path: one token, vector layout, h fits the LDS copy
   bool decode = c.n == 1 && vec_ok && !getenv("SATS_NO_DECODE");
   DecodePlan dp;
@@ -978,6 +1052,31 @@ int cal_stack(const uint16_t *x, int64_t n, const uint16_t *Wg, const uint16_t *
   if (realized) *realized = s2;
   return SATS_OK;
 }
+
+template <typename T>
+int forward_lora(const T *x, const int32_t *token_ids, const T *W_gate, const T *W_up_T, const T *W_down,
+                 const T *A_gate, const T *B_gate, const T *A_up, const T *B_up_T, const T *A_down, const T *B_down,
+                 int64_t rank, float scale, const float *thresholds, const uint8_t *route_lut, T *out,
+                 int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers, hipStream_t stream,
+                 uint8_t *route_out, int32_t *active_count, int32_t *active_idx, T *layer_in) {
+  g_err.clear();
+  if (!A_gate) return fail(SATS_ERR_NULL, "all six adapter matrices are required");
+  Call c = make_call(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out, n_tokens, d,
+                     d_ff, n_layers, stream, route_mode_of(route_lut));
+  c.route_out = route_out;
+  c.active_count = active_count;
+  c.active_idx = active_idx;
+  c.layer_in = layer_in;
+  c.Ag = A_gate;
+  c.Bg = B_gate;
+  c.Au = A_up;
+  c.BuT = B_up_T;
+  c.Ad = A_down;
+  c.Bd = B_down;
+  c.rank = rank;
+  c.lscale = scale;
+  return run<T>(c);
+}
 }  // namespace
 
 // =============================================================== C ABI
@@ -1049,6 +1148,30 @@ int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids, const
   return run<float>(c);
 }
 
+
+int sats_mlp_forward_lora(const sats_bf16 *x, const int32_t *token_ids, const sats_bf16 *W_gate,
+                          const sats_bf16 *W_up_T, const sats_bf16 *W_down, const sats_bf16 *A_gate,
+                          const sats_bf16 *B_gate, const sats_bf16 *A_up, const sats_bf16 *B_up_T,
+                          const sats_bf16 *A_down, const sats_bf16 *B_down, int64_t rank, float scale,
+                          const float *thresholds, const uint8_t *route_lut, sats_bf16 *out, int64_t n_tokens,
+                          int64_t d, int64_t d_ff, int64_t n_layers, hipStream_t stream, uint8_t *route_out,
+                          int32_t *active_count, int32_t *active_idx, sats_bf16 *layer_in) {
+  return forward_lora<uint16_t>(x, token_ids, W_gate, W_up_T, W_down, A_gate, B_gate, A_up, B_up_T, A_down, B_down,
+                                rank, scale, thresholds, route_lut, out, n_tokens, d, d_ff, n_layers, stream,
+                                route_out, active_count, active_idx, layer_in);
+}
+
+int sats_mlp_forward_lora_f32(const float *x, const int32_t *token_ids, const float *W_gate, const float *W_up_T,
+                              const float *W_down, const float *A_gate, const float *B_gate, const float *A_up,
+                              const float *B_up_T, const float *A_down, const float *B_down, int64_t rank,
+                              float scale, const float *thresholds, const uint8_t *route_lut, float *out,
+                              int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers, hipStream_t stream,
+                              uint8_t *route_out, int32_t *active_count, int32_t *active_idx, float *layer_in) {
+  return forward_lora<float>(x, token_ids, W_gate, W_up_T, W_down, A_gate, B_gate, A_up, B_up_T, A_down, B_down,
+                             rank, scale, thresholds, route_lut, out, n_tokens, d, d_ff, n_layers, stream,
+                             route_out, active_count, active_idx, layer_in);
+}
+
 int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, int elem_bytes,
                  hipStream_t stream) {
   g_err.clear();
@@ -1059,14 +1182,16 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, 
   size_t bytes = 0, nc = 0;
   int cus = device_cus();
   if (cus < 1) return fail(SATS_ERR_HIP, "no device");
-  DecodePlan dp{};
-  (void)make_decode_plan(d, d_ff, elem_bytes, env_int("SATS_DEC_ROWS_WGS", cus), &dp);
-  for (int v = 0; v < 2; ++v)
-    for (int np : {1, pass}) {
-      const Plan p = make_plan(d, d_ff, elem_bytes, v == 1, np);
-      bytes = std::max(bytes, layout(nullptr, p, pass, d, d_ff, elem_bytes, n_layers, dp, nullptr));
-      nc = std::max(nc, counter_count(p, pass, dp));
-    }
+  DecodePlan dps[2]{};  // the plain single-token plan and the one of LoRA calls at the largest rank
+  (void)make_decode_plan(d, d_ff, elem_bytes, env_int("SATS_DEC_ROWS_WGS", cus), &dps[0]);
+  (void)make_decode_plan(d, d_ff, elem_bytes, env_int("SATS_DEC_ROWS_WGS", cus), &dps[1], sats::kLoraMaxRank);
+  for (const DecodePlan &dp : dps)
+    for (int v = 0; v < 2; ++v)
+      for (int np : {1, pass}) {
+        const Plan p = make_plan(d, d_ff, elem_bytes, v == 1, np);
+        bytes = std::max(bytes, layout(nullptr, p, pass, d, d_ff, elem_bytes, n_layers, dp, nullptr));
+        nc = std::max(nc, counter_count(p, pass, dp));
+      }
   Workspace *ws = nullptr;
   return ensure_workspace(stream, bytes, nc, &ws);
 }
@@ -1182,7 +1307,7 @@ int sats_timing_end(int kind, double *total_ms, int64_t *count) {
 int sats_trace_read(unsigned long long *host, int64_t count) {
   HIP_TRY(hipDeviceSynchronize());
   HIP_TRY(hipMemcpyFromSymbol(host, HIP_SYMBOL(sats::sats_trace_buf),
-                              sizeof(unsigned long long) * (size_t)std::min<int64_t>(count, 4096 * 8)));
+                              sizeof(unsigned long long) * (size_t)std::min<int64_t>(count, 4096 * 16)));
   return SATS_OK;
 }
 #endif

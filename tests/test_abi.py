@@ -87,3 +87,32 @@ def test_dense_needs_no_thresholds_but_checks_weights():
 
 def test_reserve_rejects_bad_element_size():
     assert sats.load().sats_reserve(4, 8, 8, 1, 3, None) == _lib.SATS_ERR_ARG
+
+
+def fwd_lora(rank=16, scale=0.5, **kw):
+    ad = dict(ag=FAKE, bg=FAKE, au=FAKE, bu=FAKE, adn=FAKE, bd=FAKE)
+    ad.update({k: kw.pop(k) for k in list(kw) if k in ad})
+    a = dict(x=FAKE, ids=FAKE, wg=FAKE, wu=FAKE, wd=FAKE, thr=FAKE, lut=FAKE, out=FAKE * 16, n=1, d=8, dff=8, L=1)
+    a.update(kw)
+    return sats.load().sats_mlp_forward_lora(a["x"], a["ids"], a["wg"], a["wu"], a["wd"], ad["ag"], ad["bg"],
+                                             ad["au"], ad["bu"], ad["adn"], ad["bd"], rank, scale, a["thr"],
+                                             a["lut"], a["out"], a["n"], a["d"], a["dff"], a["L"], None, None,
+                                             None, None, None)
+
+
+@pytest.mark.parametrize("field", ["ag", "bg", "au", "bu", "adn", "bd"])
+def test_lora_needs_every_adapter(field):
+    assert fwd_lora(**{field: None}) == _lib.SATS_ERR_NULL
+    assert "adapter" in sats.sats_last_error()
+
+
+@pytest.mark.parametrize("rank", [0, 4, 12, 128])
+def test_lora_rank_rejected(rank):
+    assert fwd_lora(rank=rank) == _lib.SATS_ERR_SHAPE
+    assert "rank" in sats.sats_last_error()
+
+
+def test_lora_alignment_and_scale_rejected():
+    assert fwd_lora(bd=FAKE + 2) == _lib.SATS_ERR_ARG
+    assert fwd_lora(scale=float("nan")) == _lib.SATS_ERR_ARG
+    assert fwd_lora(rank=12, n=0) == _lib.SATS_OK  # zero tokens: nothing to do

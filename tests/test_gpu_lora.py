@@ -1,0 +1,204 @@
+"""GPU parity of the LoRA-aware routed sparse forward (Section 5, fine-tuned
+routed models) through the C ABI, against oracle/lora.py.
+
+Comparison rules as in tests/harness.py: routes exact; keep sets exact
+outside the 1e-3 band around the threshold (the oracle's adapted gate value
+decides the band); each layer recomputed from the GPU's own input with the
+GPU's decisions inside the band; outputs within 2e-2 (bf16) / 1e-5 (f32) of
+the per-token max.  Adapters: workloads.synth.lora_adapters, scaled so that
+each adapter product is about a quarter of its weight matrix.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import calibrate, lora, mlp, numerics
+from workloads import get_config, synth
+
+from harness import BAND, TOL, act_torch_dtype, band_mask, from_dev, rel_err, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    import paper_2607_08991_amd as sats
+    sats.load()
+
+
+def scale_for(w_std, rank):
+    # adapter product entries ~ 0.02 * 0.1 / sqrt(r) * sqrt(r) = 0.002 per unit scale
+    return 0.25 * w_std / 0.002
+
+
+def run_lora(case, adapters, rank, scale, thresholds, lut, dtype, inspect=True):
+    import torch
+    import paper_2607_08991_amd as sats
+    x = case["x"]
+    n, d = x.shape
+    L, _, d_ff = case["W_gate"].shape
+    dx = to_dev(x, dtype)
+    wg, wu, wd = (to_dev(case[k], dtype) for k in ("W_gate", "W_up_T", "W_down"))
+    ad = tuple(to_dev(m, dtype) for m in adapters)
+    ids = to_dev(np.asarray(case["token_ids"], np.int32), dtype)
+    thr = torch.tensor(np.asarray(thresholds, np.float32)).cuda()
+    dl = to_dev(lut, dtype) if lut is not None else None
+    out = torch.empty((n, d), dtype=act_torch_dtype(dtype), device="cuda")
+    res = {}
+    if inspect:
+        route = torch.full((n,), 7, dtype=torch.uint8, device="cuda")
+        cnt = torch.full((L, n), -1, dtype=torch.int32, device="cuda")
+        idx = torch.full((L, n, d_ff), -1, dtype=torch.int32, device="cuda")
+        lin = torch.empty((L, n, d), dtype=act_torch_dtype(dtype), device="cuda")
+        sats.sats_mlp_forward_lora(dx, ids if lut is not None else None, wg, wu, wd, ad, rank, scale, thr, dl, out,
+                                   n, d, d_ff, L, route_out=route, active_count=cnt, active_idx=idx, layer_in=lin)
+        torch.cuda.synchronize()
+        res.update(route=route.cpu().numpy(), count=cnt.cpu().numpy(), idx=idx.cpu().numpy(),
+                   layer_in=from_dev(lin))
+    else:
+        sats.sats_mlp_forward_lora(dx, ids if lut is not None else None, wg, wu, wd, ad, rank, scale, thr, dl, out,
+                                   n, d, d_ff, L)
+    torch.cuda.synchronize()
+    sats.sats_device_status()
+    res["out"] = from_dev(out)
+    return res
+
+
+def check_lora(case, adapters, scale, thresholds, lut, dtype, res, layers=None):
+    """Layer by layer from the GPU's own inputs; returns the worst relative error."""
+    x = case["x"]
+    n = x.shape[0]
+    L = len(thresholds)
+    tol = TOL[dtype]
+    r = mlp.route(case["token_ids"], lut)
+    np.testing.assert_array_equal(res["route"], r)
+    np.testing.assert_array_equal(res["layer_in"][0], x)
+    worst = 0.0
+    for l in (range(L) if layers is None else layers):
+        wg, wu, wd = (numerics.decode(case[k][l], dtype) for k in ("W_gate", "W_up_T", "W_down"))
+        ad_l = tuple(numerics.decode(m[l], dtype) for m in adapters)
+        t = float(np.float32(thresholds[l]))
+        for i in range(n):
+            h = numerics.decode(res["layer_in"][l][i], dtype)
+            base = bool(r[i])
+            y, a, g, keep = lora.layer_lora(h, wg, wu, wd, ad_l, scale, t, base)
+            d_ff = g.size
+            cnt = int(res["count"][l][i])
+            lst = np.asarray(res["idx"][l][i][:cnt])
+            assert 0 <= cnt <= d_ff and np.all(np.diff(lst) > 0)
+            gk = np.zeros(d_ff, dtype=bool)
+            gk[lst] = True
+            band = np.zeros(d_ff, dtype=bool) if base else band_mask(g, t)
+            bad = (gk != keep) & ~band
+            assert not bad.any(), f"layer {l} token {i}: keep set differs outside the band at {np.nonzero(bad)[0][:10]}"
+            if (gk != keep).any():
+                y = lora.layer_lora(h, wg, wu, wd, ad_l, scale, t, base, mask=gk)[0]
+            if l < L - 1:
+                ref, got = mlp.glue(y, dtype), numerics.decode(res["layer_in"][l + 1][i], dtype)
+            else:
+                ref, got = numerics.rho(y, dtype), numerics.decode(res["out"][i], dtype)
+            e = rel_err(got, ref)
+            assert e <= tol, f"layer {l} token {i}: relative error {e:.3g} > {tol}"
+            worst = max(worst, e)
+    return worst
+
+
+def thresholds_for(case, dtype, seed, k=0.5):
+    L, d, _ = case["W_gate"].shape
+    xcal = synth.activations(900 + seed, synth.S_CAL, 24, d, dtype)
+    return calibrate.calibrate_stack(xcal, case["W_gate"], case["W_up_T"], case["W_down"], [k] * L, dtype)
+
+
+CASES = [
+    # seed, layers, d, d_ff, dtype, tokens, rank
+    (31, 1, 256, 1000, "bf16", 1, 16),    # ragged last column block
+    (32, 3, 256, 1000, "bf16", 4, 8),     # stack; the table mixes the routes
+    (33, 2, 512, 1536, "f32", 1, 32),     # the small fp32 shape
+    (34, 1, 4096, 1024, "bf16", 1, 64),   # wide rows: more row chunks for the adapters
+    (35, 2, 64, 4096, "bf16", 2, 16),     # many short rows
+    (36, 2, 24, 40, "bf16", 1, 8),        # tiny: one gate tile
+    (37, 2, 512, 1536, "f32", 3, 64),     # fp32, largest rank, several tokens
+]
+
+
+@pytest.mark.parametrize("seed,L,d,dff,dtype,n,rank", CASES)
+def test_lora_cases_match_oracle(seed, L, d, dff, dtype, n, rank):
+    say(f"lora case seed={seed} L={L} d={d} d_ff={dff} {dtype} n={n} rank={rank}")
+    w_std = 1.0 / np.sqrt(d)
+    c = synth.small_case(seed, L, d, dff, dtype, n, vocab=40, n_dense_ids=12, w_std=w_std)
+    ad = synth.stack_lora_adapters(seed, L, d, dff, rank, dtype)
+    s = scale_for(w_std, rank)
+    ts = thresholds_for(c, dtype, seed)
+    for lut in (None, c["route_lut"]):
+        res = run_lora(c, ad, rank, s, ts, lut, dtype)
+        worst = check_lora(c, ad, s, ts, lut, dtype, res)
+        say(f"  lut={'yes' if lut is not None else 'no'} worst rel err {worst:.3g}")
+    # the adapters matter: the output moves by much more than the tolerance
+    plain = mlp.forward(c["x"], c["token_ids"], c["W_gate"], c["W_up_T"], c["W_down"], ts, None, dtype)
+    adapted = lora.forward_lora(c["x"], c["token_ids"], c["W_gate"], c["W_up_T"], c["W_down"], ad, s, ts, None,
+                                dtype)
+    assert max(rel_err(plain[i], adapted[i]) for i in range(n)) > 10 * TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_zero_scale_and_base_routes_equal_the_plain_calls(dtype):
+    import torch
+    import paper_2607_08991_amd as sats
+    from harness import run_gpu
+    L, d, dff, n, rank = 2, 128, 512, 3, 16
+    c = synth.small_case(41, L, d, dff, dtype, n, vocab=40, n_dense_ids=12, w_std=1 / 11)
+    ad = synth.stack_lora_adapters(41, L, d, dff, rank, dtype)
+    ts = thresholds_for(c, dtype, 41)
+    plain = run_gpu(c, ts, None, dtype, inspect=False)
+    # one token at a time is the plain single-token path
+    for i in range(n):
+        one = dict(c, x=c["x"][i:i + 1], token_ids=c["token_ids"][i:i + 1])
+        z = run_lora(one, ad, rank, 0.0, ts, None, dtype, inspect=False)
+        p1 = run_gpu(one, ts, None, dtype, inspect=False)
+        np.testing.assert_array_equal(numerics.decode(z["out"], dtype), numerics.decode(p1["out"], dtype))
+    # every token on the base path: the adapters are not applied
+    allb = np.ones(40, np.uint8)
+    b = run_lora(c, ad, rank, 5.0, ts, allb, dtype, inspect=False)
+    dn = run_gpu(c, ts, None, dtype, dense=True)
+    np.testing.assert_allclose(numerics.decode(b["out"], dtype), numerics.decode(dn["out"], dtype),
+                               rtol=TOL[dtype], atol=TOL[dtype] * np.abs(numerics.decode(dn["out"], dtype)).max())
+    del plain
+
+
+def test_lora_is_deterministic():
+    c = synth.small_case(42, 2, 256, 1024, "bf16", 2, vocab=40, n_dense_ids=12, w_std=1 / 16)
+    ad = synth.stack_lora_adapters(42, 2, 256, 1024, 32, "bf16")
+    ts = thresholds_for(c, "bf16", 42)
+    a = run_lora(c, ad, 32, 4.0, ts, c["route_lut"], "bf16", inspect=False)
+    b = run_lora(c, ad, 32, 4.0, ts, c["route_lut"], "bf16", inspect=False)
+    r = run_lora(c, ad, 32, 4.0, ts, c["route_lut"], "bf16", inspect=True)
+    np.testing.assert_array_equal(a["out"], b["out"])
+    np.testing.assert_array_equal(a["out"], r["out"])
+
+
+def test_lora_llama_layer():
+    """One Llama-3.1-8B-shaped layer (d = 4096, d_ff = 14336, bf16), rank 16,
+    scale 2, CATS threshold at 50 % on the base model: one sparse token."""
+    cfg = get_config(1)
+    d, dff, rank, s = cfg.d, cfg.d_ff, 16, 2.0
+    wg, wu, wd = synth.layer_weights(cfg.seed, 0, d, dff, "bf16")
+    ad = tuple(m[None] for m in synth.lora_adapters(cfg.seed, 0, d, dff, rank, "bf16"))
+    x = synth.activations(cfg.seed, synth.S_TEST, 1, d, "bf16")
+    c = dict(x=x, token_ids=np.zeros(1, np.int32), W_gate=wg[None], W_up_T=wu[None], W_down=wd[None])
+    xcal = synth.activations(cfg.seed, synth.S_CAL, 64, d, "bf16")
+    t = calibrate.calibrate_stack(xcal, c["W_gate"], c["W_up_T"], c["W_down"], [0.5], "bf16")
+    say(f"llama layer, t = {float(t[0]):.4g}")
+    res = run_lora(c, ad, rank, s, t, None, "bf16")
+    worst = check_lora(c, ad, s, t, None, "bf16", res)
+    kept = int(res["count"][0][0]) / dff
+    say(f"  kept {kept:.3f}, worst rel err {worst:.3g}")
+    assert 0.3 < kept < 0.7

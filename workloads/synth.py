@@ -21,6 +21,10 @@ import numpy as np
 S_WEIGHTS, S_CAL, S_DECODE, S_IDS, S_LUT, S_KLEVEL, S_TEST = 0, 1, 2, 3, 4, 5, 6
 # matrix ids inside the weight stream
 M_GATE, M_UP_T, M_DOWN = 0, 1, 2
+# LoRA adapter stream and its matrix ids
+S_LORA = 7
+M_A_GATE, M_B_GATE, M_A_UP, M_B_UP_T, M_A_DOWN, M_B_DOWN = 0, 1, 2, 3, 4, 5
+LORA_A_STD = 0.02
 
 WEIGHT_STD = 0.02
 _ROW_CHUNK = 256
@@ -91,6 +95,26 @@ def stack_weights(seed: int, n_layers: int, d: int, d_ff: int, dtype: str):
     for l in range(n_layers):
         wg[l], wu[l], wd[l] = layer_weights(seed, l, d, d_ff, dtype)
     return wg, wu, wd
+
+
+def lora_adapters(seed: int, layer: int, d: int, d_ff: int, rank: int, dtype: str):
+    """(A_gate [d][r], B_gate [r][d_ff], A_up [d][r], B_up_T [d_ff][r], A_down [d_ff][r],
+    B_down [r][d]) of one layer: A entries N(0, 0.02^2), B entries N(0, (0.1 / sqrt(r))^2),
+    so that with scale 2 each adapter product is about a fifth of its weight matrix."""
+    base = (seed, S_LORA, layer)
+    b_std = 0.1 / float(np.sqrt(rank))
+    return (normal_matrix(d, rank, LORA_A_STD, base + (M_A_GATE,), dtype),
+            normal_matrix(rank, d_ff, b_std, base + (M_B_GATE,), dtype),
+            normal_matrix(d, rank, LORA_A_STD, base + (M_A_UP,), dtype),
+            normal_matrix(d_ff, rank, b_std, base + (M_B_UP_T,), dtype),
+            normal_matrix(d_ff, rank, LORA_A_STD, base + (M_A_DOWN,), dtype),
+            normal_matrix(rank, d, b_std, base + (M_B_DOWN,), dtype))
+
+
+def stack_lora_adapters(seed: int, n_layers: int, d: int, d_ff: int, rank: int, dtype: str):
+    """The six adapter matrices stacked [L][...]; layer l equals ``lora_adapters(seed, l, ...)``."""
+    per = [lora_adapters(seed, l, d, d_ff, rank, dtype) for l in range(n_layers)]
+    return tuple(np.stack([p[k] for p in per]) for k in range(6))
 
 
 def activations(seed: int, stream: int, n: int, d: int, dtype: str, idx: int = 0) -> np.ndarray:
