@@ -18,10 +18,11 @@ Modules
                a stack on dense-propagated calibration tokens
   sats      -- SATS calibration (Eq. 6-10)
   lora      -- LoRA-aware routed sparse MLP (Section 5, fine-tuned models)
+  route     -- routing-table construction (Eq. 11-14)
 
 Parity status of each function is stated in its docstring.  The inter-layer
 glue of a stack (``mlp.glue``) is a convention of this library, not something
 the paper defines: parity unpinned by the paper (pinned only by its own
 invariants).
 """
-from . import numerics, mlp, calibrate, sats, lora  # noqa: F401
+from . import numerics, mlp, calibrate, sats, lora, route  # noqa: F401
