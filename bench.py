@@ -301,6 +301,63 @@ def bench_calib(args):
     print(json.dumps(res), flush=True)
 
 
+def bench_route(args):
+    """Routing-table construction (Eq. 11-14) at the Llama-3.1 vocabulary (128256 ids):
+    2^22 routing-corpus occurrences with base and sparse losses, 2^20 held-out ids,
+    Zipf(1.1) ids, target routed fraction 0.5.  One step is one sats_route_table call."""
+    import torch
+    import paper_2607_08991_amd as sats
+    from workloads import synth
+    from oracle import route  # test infrastructure: the cpu_baseline leg only
+
+    V, n, nh, r_tar = 128256, 1 << 22, 1 << 20, 0.5
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    log(f"[bench] generating a routing corpus of {n} occurrences")
+    ids, lb, ls = synth.routing_corpus(11, n, V)
+    held = synth.routing_corpus(11, nh, V, split=1)[0]
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    dids, dlb, dls, dheld = up(ids), up(lb), up(ls), up(held)
+    table = torch.empty(V, dtype=torch.uint8, device=dev)
+    for _ in range(max(1, args.warmup)):
+        sats.sats_route_table(dlb, dls, dids, dheld, V, r_tar, table)
+    steps = max(1, args.steps)
+    sats.sats_timing_begin(sats.SATS_K_ROUTE_ACCUM, steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        tau, r = sats.sats_route_table(dlb, dls, dids, dheld, V, r_tar, table)
+    dt = (time.perf_counter() - t0) / steps
+    tot, c = sats.sats_timing_end(sats.SATS_K_ROUTE_ACCUM)
+    k_us = tot / c * 1e3
+    alg = 12 * n  # one id and two float32 losses per occurrence
+    gbps = alg / (k_us * 1e-6) / 1e9
+    cpu = None
+    if not args.no_cpu:
+        ns, nhs = 1 << 22, 1 << 17  # the whole routing split; the oracle's candidate loop is quadratic
+        c0 = time.perf_counter()
+        route.build(ids[:ns], lb[:ns], ls[:ns], held[:nhs], V, r_tar)
+        cdt = time.perf_counter() - c0
+        cpu = {"value": round(ns / cdt, 1), "unit": "routing occurrences/s", "cores": 1, "kind": "oracle",
+               "sample": f"{ns} routing occurrences and {nhs} held-out ids through the oracle (Python loops "
+                         f"over occurrences and candidate thresholds), {cdt:.1f} s"}
+    res = {
+        "metric": "routing-table construction (Eq. 11-14)", "value": round(n / dt, 1),
+        "unit": "routing occurrences/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32 losses, exact integer sums, f64 scores", "data": "synthetic",
+        "config": {"workload": "route_table_llama_vocab", "vocab": V, "routing_occurrences": n,
+                   "heldout_occurrences": nh, "ids": "Zipf(1.1)", "r_tar": r_tar},
+        "tau": tau, "realized_routed_fraction": r,
+        "kernels": {"route_accum_kernel": {"avg_us": round(k_us, 2), "algorithmic_bytes": alg,
+                                           "achieved_gbps": round(gbps, 1)}},
+        "roofline": {"kernel": "route_accum_kernel", "bound": "hbm", "achieved": round(gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -319,6 +376,8 @@ def main():
     sats.load()
     if args.workload == "sats-calib":
         return bench_calib(args)
+    if args.workload == "route-lut":
+        return bench_route(args)
     cfg = get_config(args.workload)
     if cfg.n_layers != 1:
         return bench_stack(args, cfg)

@@ -234,6 +234,30 @@ int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *
                         int guardrail, float *thresholds_out, double *budget_out,
                         double *realized_out, hipStream_t stream);
 
+/*
+ * Routing-table construction (Section 3.2, Eq. 11-14), the offline step that
+ * produces route_lut.  token_ids [n_tokens] with loss_base and loss_sparse
+ * [n_tokens] (device, float32: the next-token cross-entropy of each
+ * occurrence of the routing corpus on the base and the sparse path) give
+ * each id x the score s(x) = mean over its occurrences of
+ * d = max(0, loss_sparse - loss_base) (Eq. 11-12; d taken in float32 and
+ * rounded to a multiple of 2^-32, so that the per-id sums are exact;
+ * s = +inf for an id without occurrences).  heldout_ids [n_heldout] (device)
+ * calibrate the threshold: tau* minimises |R(tau) - r_tar| over the distinct
+ * finite scores of the held-out ids and +inf (Eq. 14; the smallest on ties),
+ * R(tau) being the fraction of held-out occurrences whose id scores below
+ * tau.  route_lut [vocab] (device) receives 0 (sparse path) where
+ * s(x) < tau*, else 1 (base path) -- the table the forward calls take.
+ * scores [vocab] (device double, or NULL) receives s; tau_out and
+ * realized_out (host, or NULL) receive tau* and R(tau*).  Synchronises the
+ * stream; allocates its own buffers.  Errors: SATS_ERR_NULL, SATS_ERR_SHAPE,
+ * SATS_ERR_ARG (r_tar outside [0, 1], an id outside [0, vocab), a loss
+ * difference NaN or >= 2^31).  The per-id sums of d must stay below 2^32.
+ */
+int sats_route_table(const float *loss_base, const float *loss_sparse, const int32_t *token_ids, int64_t n_tokens,
+                     const int32_t *heldout_ids, int64_t n_heldout, int64_t vocab, double r_tar,
+                     uint8_t *route_lut, double *scores, double *tau_out, double *realized_out, hipStream_t stream);
+
 /* Free every workspace of the calling process (synchronises each device). */
 int sats_release(void);
 
@@ -249,7 +273,7 @@ const char *sats_last_error(void);
  */
 enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_DENSE = 4,
        SATS_K_DEC_GATE = 5, SATS_K_DEC_ROWS = 6, SATS_K_CAL_ERR = 7, SATS_K_CAL_GATEUP = 8,
-       SATS_K_COUNT = 9 };
+       SATS_K_ROUTE_ACCUM = 9, SATS_K_COUNT = 10 };
 int sats_timing_begin(int kind, int capacity);
 int sats_timing_end(int kind, double *total_ms, int64_t *count);
 const char *sats_kernel_name(int kind);

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_PKG, "libsats.so")
 SATS_OK, SATS_ERR_NULL, SATS_ERR_SHAPE, SATS_ERR_HIP, SATS_ERR_WORKSPACE, SATS_ERR_ARG = 0, -1, -2, -3, -4, -5
 SATS_ERR_DEVICE = -6
 SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DENSE = 0, 1, 2, 3, 4
-SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP = 5, 6, 7, 8
+SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, SATS_K_ROUTE_ACCUM = 5, 6, 7, 8, 9
 
 # exported symbols and their argument types (p = pointer, i = int64, s = stream, n = int32)
 _P, _I, _S, _N = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
@@ -40,6 +40,7 @@ SIGNATURES = {
     "sats_kernel_name": ([_N], ctypes.c_char_p),
     "sats_mlp_forward_lora": ([_P] * 11 + [_I, ctypes.c_float] + [_P] * 3 + [_I] * 4 + [_S] + [_P] * 4, _N),
     "sats_mlp_forward_lora_f32": ([_P] * 11 + [_I, ctypes.c_float] + [_P] * 3 + [_I] * 4 + [_S] + [_P] * 4, _N),
+    "sats_route_table": ([_P] * 3 + [_I, _P, _I, _I, ctypes.c_double] + [_P] * 4 + [_S], _N),
     "sats_calibration_curves": ([_P] * 4 + [_I] * 3 + [_P, _I] + [_P] * 4 + [_S], _N),
     "sats_calibrate_sats": ([_P, _I] + [_P] * 3 + [_I] * 3 + [ctypes.c_double] * 3 + [_N] + [_P] * 3 + [_S], _N),
 }
@@ -222,3 +223,19 @@ def sats_calibrate_sats(x_cal, n_cal, W_gate, W_up_T, W_down, d, d_ff, n_layers,
           n_layers, float(s_tar), float(coarse_step), float(fine_step), int(bool(guardrail)),
           ts.ctypes.data, ctypes.addressof(b), ctypes.addressof(s), _stream(stream))
     return ts, b.value, s.value
+
+
+def sats_route_table(loss_base, loss_sparse, token_ids, heldout_ids, vocab, r_tar, route_lut, scores=None,
+                     stream=None):
+    """Routing table of Eq. 11-14 into route_lut (device uint8 [vocab]); returns (tau*, R(tau*)).
+
+    Synchronises.  Empty splits may be passed as None.
+    """
+    tau = ctypes.c_double(0.0)
+    r = ctypes.c_double(0.0)
+    n = 0 if token_ids is None else token_ids.numel()
+    nh = 0 if heldout_ids is None else heldout_ids.numel()
+    _call("sats_route_table", _ptr(loss_base), _ptr(loss_sparse), _ptr(token_ids), n, _ptr(heldout_ids), nh,
+          int(vocab), float(r_tar), _ptr(route_lut), _ptr(scores), ctypes.addressof(tau), ctypes.addressof(r),
+          _stream(stream))
+    return tau.value, r.value

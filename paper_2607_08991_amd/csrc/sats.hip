@@ -20,6 +20,7 @@
 #include "decode.hpp"
 #include "dense.hpp"
 #include "calib.hpp"
+#include "route.hpp"
 
 namespace {
 
@@ -1077,6 +1078,171 @@ int forward_lora(const T *x, const int32_t *token_ids, const T *W_gate, const T 
   c.lscale = scale;
   return run<T>(c);
 }
+// --------------------------------------------------------------- routing table
+
+// tau* of Eq. 14 over the candidates (distinct values of cs, weights cw =
+// held-out occurrences, and +inf).  R(tau) = W(tau) / n_heldout with W(tau)
+// the weight of the scores below tau grows strictly from candidate to
+// candidate, so |R - r_tar| falls and then rises: the best candidate is the
+// first one with R >= r_tar or the one before it (the earlier on ties).  The
+// first one is found through the weighted order statistic o of rank T' (the
+// least weight with R >= r_tar): it is the least score above o (+inf if
+// none), and o is the candidate before it.  The order statistic is a radix
+// select on the bit patterns of the scores (non-negative doubles order like
+// their patterns), 8 bits per pass.
+void route_select(const std::vector<double> &cs, const std::vector<unsigned> &cw, int64_t nh, double r_tar,
+                  double *tau, double *r) {
+  const size_t n = cs.size();
+  uint64_t F = 0;
+  for (unsigned w : cw) F += w;
+  auto R = [&](uint64_t c) { return nh ? (double)c / (double)nh : 0.0; };
+  // T': the least c in [0, F] with R(c) >= r_tar (F + 1 if none)
+  uint64_t lo = 0, hi = F + 1;
+  while (lo < hi) {
+    const uint64_t mid = lo + (hi - lo) / 2;
+    if (R(mid) >= r_tar) hi = mid;
+    else lo = mid + 1;
+  }
+  const uint64_t T = lo;
+  if (T > F) {  // every candidate falls short of r_tar: the largest, +inf
+    *tau = INFINITY;
+    *r = R(F);
+    return;
+  }
+  double vstar = INFINITY, pred = 0.0;
+  bool has_pred = false;
+  uint64_t wstar = F, wpred = 0;
+  if (T == 0) {
+    for (double v : cs) vstar = std::min(vstar, v);
+    wstar = 0;
+  } else {
+    // o = the T-th smallest occurrence score (weighted radix select)
+    std::vector<uint32_t> idx(n);
+    for (size_t i = 0; i < n; ++i) idx[i] = (uint32_t)i;
+    uint64_t prefix = 0, rank = T;
+    for (int shift = 56; shift >= 0; shift -= 8) {
+      uint64_t hist[256] = {0};
+      for (uint32_t i : idx) {
+        uint64_t bits;
+        std::memcpy(&bits, &cs[i], 8);
+        hist[(bits >> shift) & 255u] += cw[i];
+      }
+      unsigned b = 0;
+      for (; b < 255 && hist[b] < rank; ++b) rank -= hist[b];
+      prefix |= (uint64_t)b << shift;
+      std::vector<uint32_t> keep;
+      for (uint32_t i : idx) {
+        uint64_t bits;
+        std::memcpy(&bits, &cs[i], 8);
+        if (((bits >> shift) & 255u) == b) keep.push_back(i);
+      }
+      idx.swap(keep);
+    }
+    double o;
+    std::memcpy(&o, &prefix, 8);
+    has_pred = true;
+    pred = o;
+    wstar = 0;
+    for (size_t i = 0; i < n; ++i) {
+      if (cs[i] > o) vstar = std::min(vstar, cs[i]);
+      else wstar += cw[i];                   // scores <= o lie below vstar
+      if (cs[i] < o) wpred += cw[i];
+    }
+    if (vstar == INFINITY) wstar = F;
+  }
+  if (has_pred && std::fabs(R(wpred) - r_tar) <= std::fabs(R(wstar) - r_tar)) {
+    *tau = pred;
+    *r = R(wpred);
+  } else {
+    *tau = vstar;
+    *r = R(wstar);
+  }
+}
+
+// The routing-table construction of Eq. 11-14 (synchronous; buffers of its
+// own, like calibration).
+int route_build(const float *lb, const float *ls, const int32_t *ids, int64_t n, const int32_t *hids, int64_t nh,
+                int64_t vocab, double r_tar, uint8_t *table, double *score_out, double *tau_out,
+                double *realized_out, hipStream_t s) {
+  using namespace sats;
+  if (!table || (n > 0 && (!lb || !ls || !ids)) || (nh > 0 && !hids))
+    return fail(SATS_ERR_NULL, "route_lut, and the losses and ids of a non-empty split, must be non-null");
+  if (n < 0 || nh < 0 || vocab < 1 || vocab > (1ll << 31) - 1 || n > (1ll << 40) || nh > (1ll << 40))
+    return fail(SATS_ERR_SHAPE, "need n_tokens, n_heldout >= 0 and 1 <= vocab < 2^31");
+  if (!(r_tar >= 0.0 && r_tar <= 1.0)) return fail(SATS_ERR_ARG, "r_tar must be in [0, 1]");
+  const size_t V = (size_t)vocab;
+  unsigned long long *sum = nullptr;
+  unsigned *cnt = nullptr, *hcnt = nullptr, *htot = nullptr, *err = nullptr;
+  double *score = score_out;
+  struct Free {
+    void *p[6] = {};
+    ~Free() {
+      for (void *q : p)
+        if (q) (void)hipFree(q);
+    }
+  } fr;
+  int rc = 0;
+  const size_t VC = V * kRouteCopies;
+  if ((rc = cal_alloc(&sum, VC)) || (rc = cal_alloc(&cnt, VC)) || (rc = cal_alloc(&hcnt, VC)) ||
+      (rc = cal_alloc(&htot, V)) || (rc = cal_alloc(&err, 1)))
+    return rc;
+  fr.p[0] = sum;
+  fr.p[1] = cnt;
+  fr.p[2] = hcnt;
+  fr.p[3] = err;
+  fr.p[5] = htot;
+  if (!score) {
+    if ((rc = cal_alloc(&score, V))) return rc;
+    fr.p[4] = score;
+  }
+  HIP_TRY(hipMemsetAsync(sum, 0, VC * sizeof(unsigned long long), s));
+  HIP_TRY(hipMemsetAsync(cnt, 0, VC * sizeof(unsigned), s));
+  HIP_TRY(hipMemsetAsync(hcnt, 0, VC * sizeof(unsigned), s));
+  HIP_TRY(hipMemsetAsync(err, 0, sizeof(unsigned), s));
+  if (n > 0) {
+    RouteAccumArgs ra{ids, lb, ls, n, (int)vocab, sum, cnt, err};
+    TimedLaunch tl(SATS_K_ROUTE_ACCUM, s);
+    hipExtLaunchKernelGGL(route_accum_kernel<true>, dim3((unsigned)((n + kRouteChunk - 1) / kRouteChunk)),
+                          dim3(kRouteThreads), 0, s, tl.start, tl.stop, 0, ra);
+  }
+  if (nh > 0) {
+    RouteAccumArgs ra{hids, nullptr, nullptr, nh, (int)vocab, nullptr, hcnt, err};
+    hipLaunchKernelGGL(route_accum_kernel<false>, dim3((unsigned)((nh + kRouteChunk - 1) / kRouteChunk)),
+                       dim3(kRouteThreads), 0, s, ra);
+  }
+  hipLaunchKernelGGL(route_score_kernel, dim3((unsigned)((V + 255) / 256)), dim3(256), 0, s, sum, cnt, hcnt,
+                     (int)vocab, score, htot);
+  HIP_TRY(hipGetLastError());
+  std::vector<double> hs(V);
+  std::vector<unsigned> hh(V);
+  unsigned herr = 0;
+  HIP_TRY(hipMemcpyAsync(hs.data(), score, V * sizeof(double), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(hh.data(), htot, V * sizeof(unsigned), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(&herr, err, sizeof(unsigned), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (herr == 1) return fail(SATS_ERR_ARG, "a token id is outside [0, vocab)");
+  if (herr == 2) return fail(SATS_ERR_ARG, "a loss difference is NaN or at least 2^31");
+  if (herr) return fail(SATS_ERR_DEVICE, "routing table: a chunk's id table overflowed");
+  // Eq. 14: candidates are the distinct finite scores of the held-out ids and
+  // +inf; R(tau) = (held-out occurrences with s < tau) / n_heldout; the
+  // nearest to r_tar wins, the smallest tau on ties.
+  std::vector<double> cs;
+  std::vector<unsigned> cw;
+  for (size_t x = 0; x < V; ++x)
+    if (hh[x] && std::isfinite(hs[x])) {
+      cs.push_back(hs[x]);
+      cw.push_back(hh[x]);
+    }
+  double best_tau = 0.0, best_r = 0.0;
+  route_select(cs, cw, nh, r_tar, &best_tau, &best_r);
+  hipLaunchKernelGGL(route_table_kernel, dim3((unsigned)((V + 255) / 256)), dim3(256), 0, s, score, (int)vocab,
+                     best_tau, table);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipStreamSynchronize(s));
+  if (tau_out) *tau_out = best_tau;
+  if (realized_out) *realized_out = best_r;
+  return SATS_OK;
+}
 }  // namespace
 
 // =============================================================== C ABI
@@ -1170,6 +1336,14 @@ int sats_mlp_forward_lora_f32(const float *x, const int32_t *token_ids, const fl
   return forward_lora<float>(x, token_ids, W_gate, W_up_T, W_down, A_gate, B_gate, A_up, B_up_T, A_down, B_down,
                              rank, scale, thresholds, route_lut, out, n_tokens, d, d_ff, n_layers, stream,
                              route_out, active_count, active_idx, layer_in);
+}
+
+int sats_route_table(const float *loss_base, const float *loss_sparse, const int32_t *token_ids, int64_t n_tokens,
+                     const int32_t *heldout_ids, int64_t n_heldout, int64_t vocab, double r_tar,
+                     uint8_t *route_lut, double *scores, double *tau_out, double *realized_out, hipStream_t stream) {
+  g_err.clear();
+  return route_build(loss_base, loss_sparse, token_ids, n_tokens, heldout_ids, n_heldout, vocab, r_tar, route_lut,
+                     scores, tau_out, realized_out, stream);
 }
 
 int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, int elem_bytes,
@@ -1319,6 +1493,7 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_DOWN: return "down_kernel";
     case SATS_K_INSPECT: return "compact_kernel";
     case SATS_K_DENSE: return "dense_mfma_kernels";
+    case SATS_K_ROUTE_ACCUM: return "route_accum_kernel";
     case SATS_K_DEC_GATE: return "dec_gate_kernel";
     case SATS_K_DEC_ROWS: return "dec_rows_kernel";
     case SATS_K_CAL_ERR: return "cal_err_kernel";

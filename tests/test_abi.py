@@ -116,3 +116,16 @@ def test_lora_alignment_and_scale_rejected():
     assert fwd_lora(bd=FAKE + 2) == _lib.SATS_ERR_ARG
     assert fwd_lora(scale=float("nan")) == _lib.SATS_ERR_ARG
     assert fwd_lora(rank=12, n=0) == _lib.SATS_OK  # zero tokens: nothing to do
+
+
+def test_route_table_arguments_rejected():
+    lib = sats.load()
+
+    def call(table=FAKE, n=10, nh=10, vocab=100, r_tar=0.5, ids=FAKE):
+        return lib.sats_route_table(FAKE, FAKE, ids, n, FAKE, nh, vocab, r_tar, table, None, None, None, None)
+    assert call(table=None) == _lib.SATS_ERR_NULL
+    assert call(ids=None) == _lib.SATS_ERR_NULL
+    assert call(vocab=0) == _lib.SATS_ERR_SHAPE
+    assert call(n=-1) == _lib.SATS_ERR_SHAPE
+    assert call(r_tar=1.5) == _lib.SATS_ERR_ARG
+    assert call(r_tar=float("nan")) == _lib.SATS_ERR_ARG

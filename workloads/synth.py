@@ -23,6 +23,8 @@ S_WEIGHTS, S_CAL, S_DECODE, S_IDS, S_LUT, S_KLEVEL, S_TEST = 0, 1, 2, 3, 4, 5, 6
 M_GATE, M_UP_T, M_DOWN = 0, 1, 2
 # LoRA adapter stream and its matrix ids
 S_LORA = 7
+# routing-corpus stream
+S_ROUTE = 8
 M_A_GATE, M_B_GATE, M_A_UP, M_B_UP_T, M_A_DOWN, M_B_DOWN = 0, 1, 2, 3, 4, 5
 LORA_A_STD = 0.02
 
@@ -147,6 +149,20 @@ def zipf_ids(n: int, vocab: int, s: float, key) -> np.ndarray:
     u = gen(*key).random(n)
     ids = np.searchsorted(cdf, u, side="right")
     return np.minimum(ids, vocab - 1).astype(np.int32)
+
+
+def routing_corpus(seed: int, n: int, vocab: int, s: float = 1.1, split: int = 0):
+    """A synthetic routing corpus (stand-in for per-occurrence next-token losses of a
+    language model on the base and sparse paths): ids Zipf(s) over the vocabulary; each
+    id a sensitivity k_x ~ Exp(mean 0.15) (shared by every split of one seed); base
+    loss ~ Gamma(2, 1.2) nats; sparse loss = base + k_x + N(0, 0.3^2); float32.
+    Returns (ids int32 [n], loss_base float32 [n], loss_sparse float32 [n])."""
+    kappa = gen(seed, S_ROUTE, 0).exponential(0.15, vocab)
+    ids = zipf_ids(n, vocab, s, (seed, S_ROUTE, 1, split))
+    g = gen(seed, S_ROUTE, 2, split)
+    lb = g.gamma(2.0, 1.2, n).astype(np.float32)
+    ls = (lb + kappa[ids] + g.normal(0.0, 0.3, n)).astype(np.float32)
+    return ids, lb, ls
 
 
 def uniform_ids(n: int, vocab: int, key) -> np.ndarray:
