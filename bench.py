@@ -152,6 +152,19 @@ def bench_stack(args, cfg):
     thr = torch.from_numpy(ts).to(dev)
     out = torch.empty((slots, batch, d), dtype=torch.bfloat16, device=dev)
     stream = torch.cuda.current_stream()
+    R = args.lora_rank
+    AD = None
+    if R:  # rank-R adapters of every layer on the sparse path
+        AD = [torch.from_numpy(m.view(np.int16)).view(torch.bfloat16).to(dev)
+              for m in synth.stack_lora_adapters(cfg.seed, L, d, d_ff, R, cfg.dtype)]
+
+    def forward(k, lora, **inspect):
+        if lora:
+            sats.sats_mlp_forward_lora(X[k], ids[k], *W, AD, R, args.lora_scale, thr, dlut, out[k], batch, d, d_ff,
+                                       L, stream, **inspect)
+        else:
+            fn = sats.sats_mlp_forward_inspect if inspect else sats.sats_mlp_forward
+            fn(X[k], ids[k], *W, thr, dlut, out[k], batch, d, d_ff, L, stream, **inspect)
 
     # per slot: routes and the union of kept columns per layer (algorithmic bytes)
     union = np.zeros((slots, L))
@@ -162,8 +175,7 @@ def bench_stack(args, cfg):
     route = torch.empty(batch, dtype=torch.uint8, device=dev)
     ar = torch.arange(d_ff, device=dev)
     for s in range(slots):
-        sats.sats_mlp_forward_inspect(X[s], ids[s], *W, thr, dlut, out[s], batch, d, d_ff, L,
-                                      route_out=route, active_count=cnt, active_idx=idx)
+        forward(s, bool(R), route_out=route, active_count=cnt, active_idx=idx)
         valid = ar[None, None, :] < cnt[:, :, None].long()
         m = torch.zeros((L, d_ff), dtype=torch.bool, device=dev)
         for l in range(L):
@@ -175,29 +187,44 @@ def bench_stack(args, cfg):
     routes = np.array(routes)
     kept = np.array(kept, dtype=np.float64)  # [slots][L][batch]
 
-    def step(s, dense=False):
+    def step(s, dense=False, lora=bool(R)):
         k = s % slots
         if dense:
             sats.sats_mlp_dense(X[k], *W, out[k], batch, d, d_ff, L, stream)
         else:
-            sats.sats_mlp_forward(X[k], ids[k], *W, thr, dlut, out[k], batch, d, d_ff, L, stream)
+            forward(k, lora)
 
-    def timed(dense=False):
-        for s in range(args.warmup):
-            step(s, dense)
+    def timed(dense=False, lora=bool(R), steps=args.steps, warmup=args.warmup):
+        for s in range(warmup):
+            step(s, dense, lora)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for s in range(args.steps):
-            step(args.warmup + s, dense)
+        for s in range(steps):
+            step(warmup + s, dense, lora)
         e1.record(stream)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / args.steps
+        return e0.elapsed_time(e1) / steps
 
     ms = timed()
     dense_ms = None if args.no_dense else timed(True)
+    lora_res = None
+    if R:
+        plain_ms = timed(lora=False)
+        per_token_ms = None
+        if batch > 1:  # the same batch token after token on the single-token path (a few steps: it is slow)
+            os.environ["SATS_LORA_PER_TOKEN"] = "1"
+            per_token_ms = timed(steps=min(args.steps, 3), warmup=1)
+            del os.environ["SATS_LORA_PER_TOKEN"]
+        lora_res = {"rank": R, "scale": args.lora_scale, "plain_sparse_ms_per_step": round(plain_ms, 5),
+                    "overhead_vs_plain_sparse": round(ms / plain_ms, 4),
+                    "token_by_token_ms_per_step": None if per_token_ms is None else round(per_token_ms, 5),
+                    "speedup_vs_token_by_token": None if per_token_ms is None else round(per_token_ms / ms, 3)}
     sl = (args.warmup + np.arange(args.steps)) % slots
     alg = (L * d * d_ff * esz + 2 * d * esz * union[sl].sum(axis=1)).mean() + 2 * batch * d * esz
+    if R:  # the adapters: A_gate, A_up, B_gate and B_down whole; B_up_T and A_down whole on the batched path
+        alg += L * (2 * d * R + 3 * d_ff * R + R * d) * esz if batch > 1 else \
+            L * (2 * d * R + R * d_ff + R * d) * esz + 2 * R * esz * union[sl].sum(axis=1).mean()
     sparse_mask = routes[sl] == 0
     sp = 1.0 - (kept[sl].transpose(0, 2, 1)[sparse_mask].mean() / d_ff) if sparse_mask.any() else None
     res = {
@@ -205,7 +232,8 @@ def bench_stack(args, cfg):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": cfg.name, "d": d, "d_ff": d_ff, "n_layers": L, "decode_batch": batch,
+        "config": {"workload": cfg.name + (f", LoRA rank {R} on the sparse path" if R else ""),
+                   "d": d, "d_ff": d_ff, "n_layers": L, "decode_batch": batch,
                    "route": "route_lut", "base_routed_ids": cfg.n_dense_ids, "vocab": cfg.vocab},
         "algorithmic_bytes_per_step": int(alg),
         "hbm_gbps_algorithmic": round(alg / (ms * 1e-3) / 1e9, 1),
@@ -215,6 +243,8 @@ def bench_stack(args, cfg):
         "dense_ms_per_step": None if dense_ms is None else round(dense_ms, 5),
         "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 4),
     }
+    if lora_res:
+        res["lora"] = lora_res
     print(json.dumps(res), flush=True)
 
 

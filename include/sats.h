@@ -149,9 +149,15 @@ int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids,
  * The adapters run inside the same launches as the base computation: the up
  * adapter only for kept columns, the down adapter's first factor only over
  * kept rows.  rank is 8, 16, 32 or 64; the adapter arrays must be 16-byte
- * aligned; the shapes must fit the single-token path (d <= 4096, d and d_ff
- * multiples of 16 bytes' worth of elements) -- tokens are processed one
- * after another, each on its own route.  Other arguments and the optional
+ * aligned.  Batches of two or more bf16 tokens whose shapes fit the matrix-core
+ * path (d a multiple of 128 and at most 4096, d_ff a multiple of 64) run in
+ * passes of up to 64 tokens with every row on the matrix cores: each row
+ * applies its own route and keep rule, the gate and up adapter terms are
+ * added in float32 before SiLU and the keep rule, z = p A_down is summed per
+ * 64-column tile and scale z B_down is added with the output.  Otherwise the
+ * shapes must fit the single-token path (d <= 4096, d and d_ff multiples of
+ * 16 bytes' worth of elements) and tokens are processed one after another,
+ * each on its own route.  Other arguments and the optional
  * inspection outputs as in sats_mlp_forward_inspect.  Errors: SATS_ERR_NULL
  * (a required array), SATS_ERR_SHAPE (rank or shape), SATS_ERR_ARG
  * (alignment, non-finite scale), and those of sats_mlp_forward.
@@ -273,7 +279,7 @@ const char *sats_last_error(void);
  */
 enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_DENSE = 4,
        SATS_K_DEC_GATE = 5, SATS_K_DEC_ROWS = 6, SATS_K_CAL_ERR = 7, SATS_K_CAL_GATEUP = 8,
-       SATS_K_ROUTE_ACCUM = 9, SATS_K_COUNT = 10 };
+       SATS_K_ROUTE_ACCUM = 9, SATS_K_LORA_V = 10, SATS_K_COUNT = 11 };
 int sats_timing_begin(int kind, int capacity);
 int sats_timing_end(int kind, double *total_ms, int64_t *count);
 const char *sats_kernel_name(int kind);

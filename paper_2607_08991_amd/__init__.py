@@ -9,5 +9,5 @@ from ._lib import (  # noqa: F401
     sats_reserve, sats_release, sats_device_status, sats_last_error, sats_timing_begin, sats_timing_end,
     sats_kernel_name, SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DENSE, LIB_PATH,
     SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, sats_calibration_curves,
-    sats_calibrate_sats, sats_mlp_forward_lora, sats_route_table, SATS_K_ROUTE_ACCUM,
+    sats_calibrate_sats, sats_mlp_forward_lora, sats_route_table, SATS_K_ROUTE_ACCUM, SATS_K_LORA_V,
 )

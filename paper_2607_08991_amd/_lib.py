@@ -18,6 +18,7 @@ SATS_OK, SATS_ERR_NULL, SATS_ERR_SHAPE, SATS_ERR_HIP, SATS_ERR_WORKSPACE, SATS_E
 SATS_ERR_DEVICE = -6
 SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DENSE = 0, 1, 2, 3, 4
 SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, SATS_K_ROUTE_ACCUM = 5, 6, 7, 8, 9
+SATS_K_LORA_V = 10
 
 # exported symbols and their argument types (p = pointer, i = int64, s = stream, n = int32)
 _P, _I, _S, _N = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int

@@ -55,6 +55,7 @@ struct RouteArgs {
   uint8_t *gbase;         // [n] base-path flag of each group row (group order)
   int mfma;               // the call may use the MFMA path
   int whole;              // the MFMA group is the whole batch (keep rule applied per row)
+  int min_group;          // smallest group the MFMA path takes (kMfmaMinTokens; 1 for LoRA passes)
 };
 
 // One workgroup per token of the pass: every workgroup forms the same
@@ -74,7 +75,7 @@ __global__ __launch_bounds__(kThreads) void route_kernel(RouteArgs a) {
     // group on MFMA: the base-path tokens once there are enough of them, or the
     // whole batch (every row then applies its own keep rule)
     const int ng = a.whole ? a.n : nd;
-    const int on = (a.mfma && ng >= kMfmaMinTokens) ? 1 : 0;
+    const int on = (a.mfma && ng >= a.min_group) ? 1 : 0;
     if (valid) {
       const int pos = base ? rank_d : nd + (tid - rank_d);
       s_perm[pos] = tid;
@@ -121,6 +122,14 @@ struct DenseArgs {
   int K, N, kchunk;       // reduction length, output columns, k per split (down)
   float *cal_g;           // calibration (gate/up): g = SiLU(a) in float32, [rows][N] (P unused) ...
   uint16_t *cal_ph, *cal_pl;  // ... and p = g u as two bf16 terms, hi = rne(p), lo = rne(p - hi)
+  // LoRA adapters of the sparse path (gate/up with LORA): lv [2][kDenseMaxTokens][rank]
+  // = s (h A_gate), s (h A_up) per group row; B_gate [rank][N], B_up_T [N][rank] and
+  // A_down [N][rank] of the layer; zpart [N / 64][kDenseMaxTokens][rank]: per column
+  // tile, sum of p_j A_down[j] over its columns (zero for base-path rows)
+  const float *lv;
+  const uint16_t *Bg, *BuT, *Ad;
+  float *zpart;
+  int rank;
 };
 
 // ---------------------------------------------------------------- MFMA GEMMs
@@ -237,7 +246,7 @@ __device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const
 // p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every row of
 // the group (MT 16-row tiles; rows past the group are read as zeros).
 // Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
-template <int MT>
+template <int MT, bool LORA = false>
 __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
       rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
@@ -277,6 +286,24 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
         acc[mt] = mfma16(row_operand((BUF) + 16384, 16 * mt + l16, j, g), b_, acc[mt]);      \
     }                                                                                        \
   }
+  // LoRA: this tile's adapter operands are loaded before the stream (16 bytes
+  // per load: one each of B_gate[:, tile], B_up_T[tile] and A_down[tile] for
+  // the first 8 R threads, up to four of s (h A)) and written to LDS after it
+  const int R = LORA ? a.rank : 0;
+  u32x4 pbg = {0u, 0u, 0u, 0u}, pbu = {0u, 0u, 0u, 0u}, pad = {0u, 0u, 0u, 0u}, plv[4];
+  if (LORA) {
+    const int t = threadIdx.x;
+    if (t < 8 * R) {
+      pbg = *reinterpret_cast<const u32x4 *>(a.Bg + (size_t)(t >> 3) * N + n0 + 8 * (t & 7));
+      pbu = *reinterpret_cast<const u32x4 *>(a.BuT + (size_t)n0 * R + 8 * t);  // rows n0 .. n0 + 63: contiguous
+      pad = *reinterpret_cast<const u32x4 *>(a.Ad + (size_t)n0 * R + 8 * t);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = t + kDenseThreads * j;  // 4 floats of lv [2][kDenseMaxTokens][R]
+      plv[j] = (e < 32 * R) ? *reinterpret_cast<const u32x4 *>(a.lv + 4 * e) : u32x4{0u, 0u, 0u, 0u};
+    }
+  }
   SATS_DENSE_RING(S, SATS_GU_ISSUE, SATS_GU_COMPUTE)
 #undef SATS_GU_ISSUE
 #undef SATS_GU_COMPUTE
@@ -285,6 +312,65 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   __syncthreads();
   float *xs = reinterpret_cast<float *>(rg0);
   uint16_t *pt = reinterpret_cast<uint16_t *>(rg1);
+  // LoRA: the adapter terms are small products on the same MFMA tiles.  The
+  // gate term s (h A_gate) B_gate is added into the gate accumulators as a
+  // product with K = 2 R: s (h A_gate) enters as two bf16 terms (hi, then the
+  // rounded remainder lo) against B_gate twice, so it keeps about 16 bits;
+  // the up term likewise with B_up_T.  K is padded to a whole MFMA step (32)
+  // with zeros.  LDS (bf16):
+  //   lvh [rows][KP]  hi | lo of s (h A) per group row (zero rows past the group)
+  //   lbt [64][R]     B_gate^T / B_up_T of the tile's columns, ranks contiguous
+  //   ladT [R][64]    A_down^T of the tile's columns, columns contiguous
+  const int KP = R >= 16 ? 2 * R : 32;
+  uint16_t *lvhg = reinterpret_cast<uint16_t *>(rg2), *lvhu = reinterpret_cast<uint16_t *>(rg3);
+  uint16_t *lbgt = reinterpret_cast<uint16_t *>(rg4), *lbut = reinterpret_cast<uint16_t *>(rg5);
+  uint16_t *ladt = reinterpret_cast<uint16_t *>(rg1 + 8192);
+  if (LORA) {
+    const int t = threadIdx.x;
+    if (t < 8 * R) {
+      const int i = t >> 3, q = t & 7;  // B_gate[i][n0 + 8 q .. + 7]
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        lbgt[(8 * q + k) * R + i] = (uint16_t)((k & 1) ? (pbg[k >> 1] >> 16) : (pbg[k >> 1] & 0xffffu));
+      *reinterpret_cast<u32x4 *>(lbut + 8 * t) = pbu;  // B_up_T rows n0 .. n0 + 63 as they are
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {  // element 8 t + k of A_down rows n0 ..: column (8 t + k) / R, rank (8 t + k) % R
+        const int e = 8 * t + k;
+        ladt[(e % R) * 64 + e / R] = (uint16_t)((k & 1) ? (pad[k >> 1] >> 16) : (pad[k >> 1] & 0xffffu));
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = t + kDenseThreads * j;
+      if (e < 32 * R)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int fi = 4 * e + u, half = fi / (kDenseMaxTokens * R), rem = fi % (kDenseMaxTokens * R);
+          const int m = rem / R, i = rem % R;
+          const float v = m < nd ? __uint_as_float(plv[j][u]) : 0.0f;
+          const uint16_t hi = f32_to_bf16(v);
+          uint16_t *row = (half ? lvhu : lvhg) + m * KP;
+          row[i] = hi;
+          row[R + i] = f32_to_bf16(v - bf16_to_f32(hi));
+        }
+    }
+    if (R < 16)  // K padding (columns 2 R .. 31 of every row)
+      for (int e = t; e < 2 * kDenseMaxTokens * (KP - 2 * R); e += kDenseThreads) {
+        const int half = e / (kDenseMaxTokens * (KP - 2 * R)), rem = e % (kDenseMaxTokens * (KP - 2 * R));
+        (half ? lvhu : lvhg)[(rem / (KP - 2 * R)) * KP + 2 * R + rem % (KP - 2 * R)] = 0;
+      }
+    __syncthreads();
+    // += [hi | lo] (rows of the tile) x [B; B] (columns c): lane operands as in the main loop
+    const uint16_t *lvh = mat ? lvhu : lvhg, *lbt = mat ? lbut : lbgt;
+    for (int j = 0; j < KP / 32; ++j) {
+      const int k0 = 32 * j + 8 * g;
+      const bf16x8 b_ = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lbt + c * R + (k0 % R)));
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(lvh + (16 * mt + l16) * KP + k0)),
+                         b_, acc[mt]);
+    }
+  }
   if (mat == 0) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -331,6 +417,25 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   const int lr = threadIdx.x >> 3, lq = threadIdx.x & 7;
   if (lr < nd)
     *reinterpret_cast<u32x4 *>(a.P + (size_t)lr * N + n0 + 8 * lq) = *reinterpret_cast<const u32x4 *>(pt + lr * 64 + 8 * lq);
+  if (LORA) {  // z partial of this column tile: p (as rounded for the down product) x A_down[tile], on MFMA
+    const int nct = (R + 15) / 16;
+    for (int tt = w; tt < MT * nct; tt += kDenseThreads / 64) {
+      const int mt = tt / nct, ct = tt % nct, i = 16 * ct + l16;
+      f32x4v z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int k0 = 32 * j + 8 * g;
+        const u32x4 bw = i < R ? *reinterpret_cast<const u32x4 *>(ladt + i * 64 + k0) : u32x4{0u, 0u, 0u, 0u};
+        z = mfma16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(pt + (16 * mt + l16) * 64 + k0)),
+                   __builtin_bit_cast(bf16x8, bw), z);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = 16 * mt + 4 * g + r;
+        if (m < nd && i < R) a.zpart[((size_t)blockIdx.x * kDenseMaxTokens + m) * R + i] = a.gbase[m] ? 0.0f : z[r];
+      }
+    }
+  }
 }
 
 // partial y over k chunk blockIdx.y for 128 output columns (blockIdx.x);
@@ -603,6 +708,13 @@ struct GlueArgs {
   uint16_t *out;          // last layer: [n][d] of the pass, rows through perm; else null
   uint16_t *hnext;        // otherwise: next layer input of the dense group, [n_dense][d]
   uint16_t *layer_in;     // optional: inspection copy of the next layer input, rows through perm
+  // LoRA (zpart null: none): y += s z B_down for sparse-path rows, z the sum
+  // over the nzb column tiles of zpart [nzb][kDenseMaxTokens][rank], in tile order
+  const float *zpart;
+  const uint16_t *Bd;     // [rank][d] of the layer
+  const uint8_t *gbase;
+  int rank, nzb;
+  float lscale;
 };
 
 // one workgroup per dense token (blockIdx.x); thread t owns columns
@@ -625,6 +737,40 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
   f32x4v y = v[0];
 #pragma unroll
   for (int q = 1; q < kDenseMaxKsplit; ++q) y += v[q];  // chunk order
+  if (a.zpart && !a.gbase[m]) {  // LoRA, sparse-path row: + s z B_down
+    __shared__ float zf[kGlueThreads];
+    __shared__ float zs[64];
+    constexpr int Q = 16;  // tile groups (16 x rank <= 1024 threads)
+    const int R = a.rank, i = tid % R, q = tid / R;
+    // thread (q, i) adds tiles q, q + Q, ...; then the Q group sums in order
+    if (q < Q)
+      zf[tid] = (q < a.nzb) ? sum_coherent(a.zpart + ((size_t)q * kDenseMaxTokens + m) * R + i,
+                                           (size_t)Q * kDenseMaxTokens * R, (a.nzb - q + Q - 1) / Q)
+                            : 0.0f;
+    __syncthreads();
+    if (tid < R) {
+      float zq[Q];
+#pragma unroll
+      for (int k = 0; k < Q; ++k) zq[k] = zf[k * R + tid];
+      float z = 0.0f;
+#pragma unroll
+      for (int k = 0; k < Q; ++k) z += zq[k];
+      zs[tid] = a.lscale * z;
+    }
+    __syncthreads();
+    if (on) {
+      f32x4v t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+      for (int k = 0; k < R; ++k) {
+        const uint2 bw = *reinterpret_cast<const uint2 *>(a.Bd + (size_t)k * a.d + c);
+        t[0] = fmaf(zs[k], bf16_to_f32(bw.x & 0xffffu), t[0]);
+        t[1] = fmaf(zs[k], bf16_to_f32(bw.x >> 16), t[1]);
+        t[2] = fmaf(zs[k], bf16_to_f32(bw.y & 0xffffu), t[2]);
+        t[3] = fmaf(zs[k], bf16_to_f32(bw.y >> 16), t[3]);
+      }
+      y += t;
+    }
+  }
   const int row = a.perm[m];
   if (a.out) {
     if (on) {
@@ -653,6 +799,112 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
     const uint2 hv = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
     *reinterpret_cast<uint2 *>(a.hnext + (size_t)m * a.d + c) = hv;
     if (a.layer_in) *reinterpret_cast<uint2 *>(a.layer_in + (size_t)row * a.d + c) = hv;
+  }
+}
+
+// ---------------------------------------------------------------- LoRA, batched
+
+// s (h A) for the group rows and both input-side adapters (A_gate, A_up) of
+// a layer, the operands of the gate/up epilogue's adapter terms.  Grid
+// (kLoraVChunks k chunks, 4 row tiles of 16, 2 adapters), 256 threads:
+// thread (row r, ranks 4 q .. 4 q + 3) sums its chunk's k in order from LDS
+// copies of the chunk; the chunk partials go to vpart, and the last chunk of
+// a (row tile, adapter) to arrive adds them in chunk order.  Base-path rows
+// get zeros (their layers see the base weights only).
+constexpr int kLoraVChunks = 8;
+constexpr int kLoraVMaxChunk = 512;  // k rows per chunk (d <= 4096)
+constexpr int kLoraVMaxRank = 64;    // ranks 8, 16, 32, 64
+struct LoraVArgs {
+  const int *ctl;          // [0] rows of the group, [1] MFMA path on
+  const uint8_t *gbase;
+  const uint16_t *H;       // [rows][K] bf16 layer input of the group
+  const uint16_t *Ag, *Au; // [K][R] of the layer
+  float *vpart;            // [2][4][kLoraVChunks][16][R]
+  float *lv;               // [2][kDenseMaxTokens][R]
+  unsigned *cnt;           // [8] arrival counts (zero between launches)
+  int K, R;
+  float s;
+};
+__global__ __launch_bounds__(256) void lora_v_kernel(LoraVArgs a) {
+  __shared__ uint16_t hs[16 * kLoraVMaxChunk];
+  __shared__ uint16_t as[kLoraVMaxChunk * kLoraVMaxRank];
+  __shared__ int flag;
+  if (!a.ctl[1]) return;
+  const int nd = min(a.ctl[0], kDenseMaxTokens);
+  const int ch = blockIdx.x, mt = blockIdx.y, ad = blockIdx.z, tid = threadIdx.x;
+  if (16 * mt >= nd) return;  // the whole (row tile, adapter) returns: no arrivals
+  const int R = a.R, kch = a.K / kLoraVChunks, k0 = ch * kch;
+  const uint16_t *A = ad ? a.Au : a.Ag;
+  // stage the chunk: 16 rows of h (rows past the group as zeros) and kch rows of A, 16 bytes per load
+  for (int e = tid; e < 16 * kch / 8; e += 256) {
+    const int r = e / (kch / 8), q = e % (kch / 8), m = 16 * mt + r;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (m < nd) v = *reinterpret_cast<const u32x4 *>(a.H + (size_t)m * a.K + k0 + 8 * q);
+    *reinterpret_cast<u32x4 *>(hs + r * kch + 8 * q) = v;
+  }
+  for (int e = tid; e < kch * R / 8; e += 256)
+    *reinterpret_cast<u32x4 *>(as + 8 * e) = *reinterpret_cast<const u32x4 *>(A + (size_t)k0 * R + 8 * e);
+  __syncthreads();
+  // thread (slice sl of NS, row r, ranks 4 q .. 4 q + 3): NS = 64 / R slices of
+  // the chunk's k, each summed in k order; the slices are then added in order
+  const int Q4 = R / 4, NS = 64 / R;
+  const int sl = tid / (16 * Q4), r = (tid / Q4) % 16, q = tid % Q4;
+  // slice bounds on multiples of 8 k (16-byte LDS reads of h); kch is a multiple of 16
+  const int kb = (sl * kch / NS) & ~7, ke = (sl == NS - 1) ? kch : ((sl + 1) * kch / NS) & ~7;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  int k = kb;
+  for (; k + 8 <= ke; k += 8) {
+    const u32x4 hv = *reinterpret_cast<const u32x4 *>(hs + r * kch + k);
+    uint2 w[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) w[e] = *reinterpret_cast<const uint2 *>(as + (k + e) * R + 4 * q);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float h = bf16_to_f32((e & 1) ? (hv[e >> 1] >> 16) : (hv[e >> 1] & 0xffffu));
+      acc[0] = fmaf(h, bf16_to_f32(w[e].x & 0xffffu), acc[0]);
+      acc[1] = fmaf(h, bf16_to_f32(w[e].x >> 16), acc[1]);
+      acc[2] = fmaf(h, bf16_to_f32(w[e].y & 0xffffu), acc[2]);
+      acc[3] = fmaf(h, bf16_to_f32(w[e].y >> 16), acc[3]);
+    }
+  }
+  for (; k < ke; ++k) {
+    const float h = bf16_to_f32(hs[r * kch + k]);
+    const uint2 w = *reinterpret_cast<const uint2 *>(as + k * R + 4 * q);
+    acc[0] = fmaf(h, bf16_to_f32(w.x & 0xffffu), acc[0]);
+    acc[1] = fmaf(h, bf16_to_f32(w.x >> 16), acc[1]);
+    acc[2] = fmaf(h, bf16_to_f32(w.y & 0xffffu), acc[2]);
+    acc[3] = fmaf(h, bf16_to_f32(w.y >> 16), acc[3]);
+  }
+  float *red = reinterpret_cast<float *>(as);  // [NS][16][R], after every thread is done with the chunk
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) red[(sl * 16 + r) * R + 4 * q + j] = acc[j];
+  __syncthreads();
+  const bool act = sl == 0;
+  if (act)
+    for (int s2 = 1; s2 < NS; ++s2)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] += red[(s2 * 16 + r) * R + 4 * q + j];
+  float *vp = a.vpart + ((size_t)(ad * 4 + mt) * kLoraVChunks) * 16 * R;  // [chunk][16][R]
+  if (act)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) store_coherent(vp + ((size_t)ch * 16 + r) * R + 4 * q + j, acc[j]);
+  if (!arrive_last(a.cnt + ad * 4 + mt, gridDim.x, &flag)) return;
+  const int m = 16 * mt + r;
+  if (act && m < nd) {
+    float v[4][kLoraVChunks];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int c2 = 0; c2 < kLoraVChunks; ++c2) v[j][c2] = load_coherent(vp + ((size_t)c2 * 16 + r) * R + 4 * q + j);
+    const bool base = a.gbase[m];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float t = 0.0f;
+#pragma unroll
+      for (int c2 = 0; c2 < kLoraVChunks; ++c2) t += v[j][c2];  // chunk order
+      a.lv[((size_t)ad * kDenseMaxTokens + m) * R + 4 * q + j] = base ? 0.0f : a.s * t;
+    }
   }
 }
 

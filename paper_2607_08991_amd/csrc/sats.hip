@@ -83,9 +83,12 @@ int dense_ksplit(int64_t d, int64_t d_ff) {
 
 // MFMA kernels specialised on the 16-row tiles that cover a pass of np tokens
 typedef void (*DenseKernel)(sats::DenseArgs);
-DenseKernel dense_gateup_fn(int np) {
+DenseKernel dense_gateup_fn(int np, bool lora = false) {
   using namespace sats;
   const int mt = (np + 15) / 16;
+  if (lora)
+    return mt <= 1 ? dense_gateup_kernel<1, true> : mt == 2 ? dense_gateup_kernel<2, true>
+                                                  : mt == 3 ? dense_gateup_kernel<3, true> : dense_gateup_kernel<4, true>;
   return mt <= 1 ? dense_gateup_kernel<1> : mt == 2 ? dense_gateup_kernel<2> : mt == 3 ? dense_gateup_kernel<3>
                                                                                         : dense_gateup_kernel<4>;
 }
@@ -171,6 +174,7 @@ struct Buffers {
   uint8_t *skip, *gbase;
   uint16_t *xd, *hnext, *pdense;  // dense group (MFMA): inputs, next inputs, p
   float *ddpart;                   // dense group down-projection partials
+  float *blv, *blvpart, *blzpart;  // batched LoRA: s (h A) per group row, its chunk partials, z per column tile
 };
 
 // Layout for passes of up to `pass` tokens (the counters live in their own
@@ -184,7 +188,7 @@ struct DecodePlan {
 };
 
 size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, int esz, int64_t L,
-              const DecodePlan &dp, Buffers *b) {
+              const DecodePlan &dp, Buffers *b, int64_t lora_rank = 0) {
   const int64_t Pp = ((pass + 3) / 4) * 4;  // tokens rounded up to whole tiles
   const int64_t tiles = Pp;                  // upper bound over tile sizes
   Carve c{base};
@@ -216,6 +220,11 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.dvpart = c.take<float>((int64_t)dp.nrc * sats::kLoraMaxRank);
   t.dzpart = c.take<float>((int64_t)dp.G * sats::kLoraMaxRank);
   t.dstate = c.take<int>(64);
+  if (lora_rank > 0) {  // batched LoRA calls only
+    t.blv = c.take<float>(2 * (int64_t)sats::kDenseMaxTokens * lora_rank);
+    t.blvpart = c.take<float>(2 * 4 * (int64_t)sats::kLoraVChunks * 16 * lora_rank);
+    t.blzpart = c.take<float>((d_ff / sats::kDenseNT) * (int64_t)sats::kDenseMaxTokens * lora_rank);
+  }
   if (b) *b = t;
   return c.off;
 }
@@ -225,6 +234,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
 // running.
 constexpr size_t kCtl = 512;
 constexpr size_t kErr = 320;
+constexpr size_t kLoraV = 448;  // [8] batched LoRA: arrivals of the s (h A) chunks
 constexpr size_t kDone = 322;  // single-token rows launch: partials written (second-stage reduction)
 
 size_t counter_count(const Plan &p, int64_t pass, const DecodePlan &dp) {
@@ -342,7 +352,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
   const bool inspect_lists = c.active_count || c.active_idx;
 
   // routing for the pass: partition, dense-group size and whether MFMA takes it
-  const bool mfma = sizeof(T) == 2 && VEC > 1 && np >= kMfmaMinTokens &&
+  const bool lora = c.Ag != nullptr;  // batched LoRA: the whole pass on MFMA (checked by the caller)
+  const bool mfma = sizeof(T) == 2 && VEC > 1 && (np >= kMfmaMinTokens || lora) &&
                     d % kDenseDownNT == 0 && d_ff % kDenseKC == 0 && d <= 4096 &&
                     (uint64_t)d * d_ff * 2 < (1ull << 31) &&
                     !getenv("SATS_NO_MFMA");
@@ -350,6 +361,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
   // the compacted sparse-path launches are left out
   const bool whole = !getenv("SATS_MFMA_BASE_GROUP_ONLY");
   const bool all_mfma = mfma && whole;
+  if (lora && !all_mfma) return fail(SATS_ERR_SHAPE, "batched LoRA pass without the MFMA path");
   {
     RouteArgs ra{};
     ra.ids = c.ids ? c.ids + base : nullptr;
@@ -367,6 +379,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     ra.gbase = b.gbase;
     ra.mfma = mfma ? 1 : 0;
     ra.whole = whole ? 1 : 0;
+    ra.min_group = lora ? 1 : kMfmaMinTokens;  // a LoRA pass has no other path for its tokens
     hipLaunchKernelGGL(route_kernel, dim3(np), dim3(kThreads), 0, c.stream, ra);
     HIP_TRY(hipGetLastError());
   }
@@ -386,9 +399,37 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       da.P = b.pdense;
       da.K = (int)d;
       da.N = (int)d_ff;
+      const size_t al = (size_t)d * c.rank;   // elements of A_gate, A_up (per layer)
+      const size_t bl = (size_t)d_ff * c.rank;  // elements of B_gate, B_up_T, A_down (per layer)
+      if (lora) {
+        LoraVArgs va{};
+        va.ctl = b.ctl;
+        va.gbase = b.gbase;
+        va.H = da.H;
+        va.Ag = static_cast<const uint16_t *>(c.Ag) + l * al;
+        va.Au = static_cast<const uint16_t *>(c.Au) + l * al;
+        va.vpart = b.blvpart;
+        va.lv = b.blv;
+        va.cnt = counters + kLoraV;
+        va.K = (int)d;
+        va.R = (int)c.rank;
+        va.s = c.lscale;
+        {
+          TimedLaunch tl(SATS_K_LORA_V, c.stream);
+          hipExtLaunchKernelGGL(lora_v_kernel, dim3(kLoraVChunks, 4, 2), dim3(256), 0, c.stream, tl.start, tl.stop,
+                                0, va);
+        }
+        HIP_TRY(hipGetLastError());
+        da.lv = b.blv;
+        da.Bg = static_cast<const uint16_t *>(c.Bg) + l * bl;
+        da.BuT = static_cast<const uint16_t *>(c.BuT) + l * bl;
+        da.Ad = static_cast<const uint16_t *>(c.Ad) + l * bl;
+        da.zpart = b.blzpart;
+        da.rank = (int)c.rank;
+      }
       {
         TimedLaunch tl(SATS_K_DENSE, c.stream);
-        hipExtLaunchKernelGGL(dense_gateup_fn(np), dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, c.stream,
+        hipExtLaunchKernelGGL(dense_gateup_fn(np, lora), dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, c.stream,
                               tl.start, tl.stop, 0, da);
       }
       HIP_TRY(hipGetLastError());
@@ -417,6 +458,14 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       ga.hnext = b.hnext;
       ga.layer_in = (c.layer_in && l + 1 < c.L) ? static_cast<uint16_t *>(c.layer_in) + ((l + 1) * c.n + base) * d
                                                  : nullptr;
+      if (lora) {
+        ga.zpart = b.blzpart;
+        ga.Bd = static_cast<const uint16_t *>(c.Bd) + l * (size_t)c.rank * d;
+        ga.gbase = b.gbase;
+        ga.rank = (int)c.rank;
+        ga.nzb = (int)(d_ff / kDenseNT);
+        ga.lscale = c.lscale;
+      }
       hipLaunchKernelGGL(dense_glue_kernel, dim3(np), dim3(kGlueThreads), 0, c.stream, ga);
       HIP_TRY(hipGetLastError());
     }
@@ -612,17 +661,30 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// LoRA calls run the single-token path, token after token (each token takes
-// its own route; the inspection outputs are written at the token's offsets).
-template <typename T>
-int run_lora(const Call &c, bool vec_ok) {
-  const int esz = (int)sizeof(T);
+int lora_check(const Call &c) {
   if (!c.Bg || !c.Au || !c.BuT || !c.Ad || !c.Bd) return fail(SATS_ERR_NULL, "all six adapter matrices are required");
   if (c.rank != 8 && c.rank != 16 && c.rank != 32 && c.rank != 64)
     return fail(SATS_ERR_SHAPE, "LoRA rank must be 8, 16, 32 or 64 (got %lld)", (long long)c.rank);
   for (const void *q : {c.Ag, c.Bg, c.Au, c.BuT, c.Ad, c.Bd})
     if (!aligned16(q)) return fail(SATS_ERR_ARG, "adapter matrices must be 16-byte aligned");
   if (!std::isfinite(c.lscale)) return fail(SATS_ERR_ARG, "LoRA scale must be finite");
+  return SATS_OK;
+}
+
+// Batches of bf16 LoRA calls run the batched passes with the whole pass on
+// MFMA (the adapters enter the gate/up epilogue and the glue); everything
+// else runs the single-token path token after token.
+bool lora_batched(const Call &c, int esz, bool vec_ok) {
+  return esz == 2 && vec_ok && c.n >= sats::kMfmaMinTokens && c.d % sats::kDenseDownNT == 0 &&
+         c.d_ff % sats::kDenseKC == 0 && c.d <= 4096 && (uint64_t)c.d * c.d_ff * 2 < (1ull << 31) &&
+         !getenv("SATS_NO_MFMA") && !getenv("SATS_MFMA_BASE_GROUP_ONLY") && !getenv("SATS_LORA_PER_TOKEN");
+}
+
+// LoRA calls on the single-token path, token after token (each token takes
+// its own route; the inspection outputs are written at the token's offsets).
+template <typename T>
+int run_lora(const Call &c, bool vec_ok) {
+  const int esz = (int)sizeof(T);
   DecodePlan dp;
   if (!vec_ok || getenv("SATS_NO_DECODE") ||
       !make_decode_plan(c.d, c.d_ff, esz, env_int("SATS_DEC_ROWS_WGS", device_cus()), &dp, (int)c.rank))
@@ -679,18 +741,23 @@ int run(const Call &c) {
                       (!c.layer_in || aligned16(c.layer_in));
   const int pass = (int)std::min<int64_t>(c.n, kMaxPass);
   const Plan p = make_plan(c.d, c.d_ff, esz, vec_ok, pass);
-  if (c.Ag) return run_lora<T>(c, vec_ok);
+  if (c.Ag) {
+    int rc = lora_check(c);
+    if (rc) return rc;
+    if (!lora_batched(c, esz, vec_ok)) return run_lora<T>(c, vec_ok);
+  }
+  const int64_t lrank = c.Ag ? c.rank : 0;
   // single-token path: one token, vector layout, h fits the LDS copy
   bool decode = c.n == 1 && vec_ok && !getenv("SATS_NO_DECODE");
   DecodePlan dp;
   if (decode) decode = make_decode_plan(c.d, c.d_ff, esz, env_int("SATS_DEC_ROWS_WGS", device_cus()), &dp);
-  const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, c.L, dp, nullptr);
+  const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, c.L, dp, nullptr, lrank);
   Workspace *ws = nullptr;
   size_t ncount = counter_count(p, pass, dp);
   int rc = ensure_workspace(c.stream, bytes, ncount, &ws);
   if (rc) return rc;
   Buffers b{};
-  layout(ws->mem, p, pass, c.d, c.d_ff, esz, c.L, dp, &b);
+  layout(ws->mem, p, pass, c.d, c.d_ff, esz, c.L, dp, &b, lrank);
   if (decode) return run_decode<T>(c, dp, b, ws->counters);
 
   for (int64_t base = 0; base < c.n; base += kMaxPass) {
@@ -1363,7 +1430,8 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, 
     for (int v = 0; v < 2; ++v)
       for (int np : {1, pass}) {
         const Plan p = make_plan(d, d_ff, elem_bytes, v == 1, np);
-        bytes = std::max(bytes, layout(nullptr, p, pass, d, d_ff, elem_bytes, n_layers, dp, nullptr));
+        bytes = std::max(bytes, layout(nullptr, p, pass, d, d_ff, elem_bytes, n_layers, dp, nullptr,
+                                       elem_bytes == 2 ? sats::kLoraMaxRank : 0));
         nc = std::max(nc, counter_count(p, pass, dp));
       }
   Workspace *ws = nullptr;
@@ -1494,6 +1562,7 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_INSPECT: return "compact_kernel";
     case SATS_K_DENSE: return "dense_mfma_kernels";
     case SATS_K_ROUTE_ACCUM: return "route_accum_kernel";
+    case SATS_K_LORA_V: return "lora_v_kernel";
     case SATS_K_DEC_GATE: return "dec_gate_kernel";
     case SATS_K_DEC_ROWS: return "dec_rows_kernel";
     case SATS_K_CAL_ERR: return "cal_err_kernel";

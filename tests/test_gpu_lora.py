@@ -202,3 +202,88 @@ def test_lora_llama_layer():
     kept = int(res["count"][0][0]) / dff
     say(f"  kept {kept:.3f}, worst rel err {worst:.3g}")
     assert 0.3 < kept < 0.7
+
+
+# ------------------------------------------------------------------ batches on the matrix cores
+
+BATCHED = [
+    # seed, layers, d, d_ff, tokens, rank: bf16 batches that take the matrix-core passes
+    (61, 2, 256, 1024, 5, 16),     # mixed routes through the table
+    (62, 1, 512, 1536, 64, 64),    # one full pass, the largest rank
+    (63, 3, 128, 512, 17, 8),      # a ragged row tile, the smallest rank
+    (64, 1, 256, 1024, 65, 32),    # two passes: 64 tokens, then 1
+    (65, 2, 4096, 1024, 3, 64),    # the widest rows (k chunks of 512)
+]
+
+
+def launches(fn):
+    """(adapter-input launches of the batched path, rows launches of the single-token path) made by fn()."""
+    import paper_2607_08991_amd as sats
+    sats.sats_timing_begin(sats.SATS_K_LORA_V, 4096)
+    sats.sats_timing_begin(sats.SATS_K_DEC_ROWS, 4096)
+    fn()
+    _, nv = sats.sats_timing_end(sats.SATS_K_LORA_V)
+    _, nr = sats.sats_timing_end(sats.SATS_K_DEC_ROWS)
+    return nv, nr
+
+
+@pytest.mark.parametrize("seed,L,d,dff,n,rank", BATCHED)
+def test_lora_batched_cases_match_oracle(seed, L, d, dff, n, rank):
+    say(f"batched lora case seed={seed} L={L} d={d} d_ff={dff} n={n} rank={rank}")
+    w_std = 1.0 / np.sqrt(d)
+    c = synth.small_case(seed, L, d, dff, "bf16", n, vocab=40, n_dense_ids=12, w_std=w_std)
+    ad = synth.stack_lora_adapters(seed, L, d, dff, rank, "bf16")
+    s = scale_for(w_std, rank)
+    ts = thresholds_for(c, "bf16", seed)
+    for lut in (None, c["route_lut"]):
+        got = {}
+        nv, nr = launches(lambda: got.update(run_lora(c, ad, rank, s, ts, lut, "bf16")))
+        assert (nv, nr) == (L * ((n + 63) // 64), 0), "the batch did not take the matrix-core passes"
+        worst = check_lora(c, ad, s, ts, lut, "bf16", got)
+        say(f"  lut={'yes' if lut is not None else 'no'} worst rel err {worst:.3g}")
+
+
+def test_lora_batched_is_deterministic_and_both_paths_match_oracle(monkeypatch):
+    """Repeated batched calls give the same bits, inspection changes nothing,
+    and the single-token path (forced by SATS_LORA_PER_TOKEN) matches the
+    oracle on the same batch.  The two paths are not compared with each
+    other: each may flip neurons inside the band, and over layers the flips
+    move the inputs, so only the oracle comparison with each path's own
+    decisions is bounded by the tolerance."""
+    L, d, dff, n, rank = 2, 256, 1024, 20, 32
+    c = synth.small_case(66, L, d, dff, "bf16", n, vocab=40, n_dense_ids=12, w_std=1 / 16)
+    ad = synth.stack_lora_adapters(66, L, d, dff, rank, "bf16")
+    ts = thresholds_for(c, "bf16", 66)
+    s = scale_for(1 / 16, rank)
+    a = run_lora(c, ad, rank, s, ts, c["route_lut"], "bf16", inspect=False)
+    b = run_lora(c, ad, rank, s, ts, c["route_lut"], "bf16", inspect=False)
+    r = run_lora(c, ad, rank, s, ts, c["route_lut"], "bf16", inspect=True)
+    np.testing.assert_array_equal(a["out"], b["out"])
+    np.testing.assert_array_equal(a["out"], r["out"])
+    say(f"batched: worst rel err {check_lora(c, ad, s, ts, c['route_lut'], 'bf16', r):.3g}")
+    monkeypatch.setenv("SATS_LORA_PER_TOKEN", "1")
+    got = {}
+    nv, nr = launches(lambda: got.update(run_lora(c, ad, rank, s, ts, c["route_lut"], "bf16")))
+    assert nv == 0 and nr == n * L
+    say(f"single-token: worst rel err {check_lora(c, ad, s, ts, c['route_lut'], 'bf16', got):.3g}")
+
+
+def test_lora_batched_llama_layer():
+    """Sixteen tokens through one Llama-3.1-8B-shaped layer (d = 4096,
+    d_ff = 14336, bf16), rank 16, scale 2, threshold at 50 % on the base
+    model, all on the sparse path."""
+    cfg = get_config(1)
+    d, dff, rank, s, n = cfg.d, cfg.d_ff, 16, 2.0, 16
+    wg, wu, wd = synth.layer_weights(cfg.seed, 0, d, dff, "bf16")
+    ad = tuple(m[None] for m in synth.lora_adapters(cfg.seed, 0, d, dff, rank, "bf16"))
+    x = synth.activations(cfg.seed, synth.S_TEST, n, d, "bf16")
+    c = dict(x=x, token_ids=np.zeros(n, np.int32), W_gate=wg[None], W_up_T=wu[None], W_down=wd[None])
+    xcal = synth.activations(cfg.seed, synth.S_CAL, 64, d, "bf16")
+    t = calibrate.calibrate_stack(xcal, c["W_gate"], c["W_up_T"], c["W_down"], [0.5], "bf16")
+    got = {}
+    nv, nr = launches(lambda: got.update(run_lora(c, ad, rank, s, t, None, "bf16")))
+    assert (nv, nr) == (1, 0)
+    worst = check_lora(c, ad, s, t, None, "bf16", got)
+    kept = got["count"][0].mean() / dff
+    say(f"batched llama layer: kept {kept:.3f}, worst rel err {worst:.3g}")
+    assert 0.3 < kept < 0.7
