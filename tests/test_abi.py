@@ -129,3 +129,17 @@ def test_route_table_arguments_rejected():
     assert call(n=-1) == _lib.SATS_ERR_SHAPE
     assert call(r_tar=1.5) == _lib.SATS_ERR_ARG
     assert call(r_tar=float("nan")) == _lib.SATS_ERR_ARG
+
+
+def test_timing_kinds_match_the_header_and_name_their_kernels():
+    text = open(HEADER).read()
+    enum = dict((k, int(v)) for k, v in re.findall(r"\b(SATS_K_[A-Z_]+)\s*=\s*(\d+)", text))
+    count = enum.pop("SATS_K_COUNT")
+    assert sorted(enum.values()) == list(range(count))
+    for name, value in enum.items():
+        assert getattr(sats, name) == value, name
+        kernel = sats.sats_kernel_name(value)
+        assert "kernel" in kernel, (name, kernel)
+    assert sats.sats_kernel_name(sats.SATS_K_LORA_V) == "lora_v_kernel"
+    with pytest.raises(sats.SatsError):
+        sats.sats_timing_begin(count, 1)
