@@ -807,10 +807,12 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
 // s (h A) for the group rows and both input-side adapters (A_gate, A_up) of
 // a layer, the operands of the gate/up epilogue's adapter terms.  Grid
 // (kLoraVChunks k chunks, 4 row tiles of 16, 2 adapters), 256 threads:
-// thread (row r, ranks 4 q .. 4 q + 3) sums its chunk's k in order from LDS
-// copies of the chunk; the chunk partials go to vpart, and the last chunk of
-// a (row tile, adapter) to arrive adds them in chunk order.  Base-path rows
-// get zeros (their layers see the base weights only).
+// thread (k slice, row r, ranks 4 q .. 4 q + 3) sums one of the 64 / R slices
+// of its chunk's k in order from LDS copies of the chunk (so every rank keeps
+// all 256 threads busy), and the slices are added in order; the chunk
+// partials go to vpart, and the last chunk of a (row tile, adapter) to
+// arrive adds them in chunk order.  Base-path rows get zeros (their layers
+// see the base weights only).
 constexpr int kLoraVChunks = 8;
 constexpr int kLoraVMaxChunk = 512;  // k rows per chunk (d <= 4096)
 constexpr int kLoraVMaxRank = 64;    // ranks 8, 16, 32, 64
