@@ -729,6 +729,15 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int c = 4 * tid;  // d <= 4096
   const bool on = c < a.d;
+  // LoRA, sparse-path row: B_down[k][c .. c + 3] of the first 16 ranks, loaded
+  // with the partials (it does not depend on z)
+  const bool lora = a.zpart && !a.gbase[m];
+  constexpr int kBdPre = 16;
+  uint2 bpre[kBdPre];
+#pragma unroll
+  for (int k = 0; k < kBdPre; ++k)
+    bpre[k] = (lora && on && k < a.rank) ? *reinterpret_cast<const uint2 *>(a.Bd + (size_t)k * a.d + c)
+                                         : make_uint2(0u, 0u);
   f32x4v v[kDenseMaxKsplit];
 #pragma unroll
   for (int q = 0; q < kDenseMaxKsplit; ++q)
@@ -737,7 +746,7 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
   f32x4v y = v[0];
 #pragma unroll
   for (int q = 1; q < kDenseMaxKsplit; ++q) y += v[q];  // chunk order
-  if (a.zpart && !a.gbase[m]) {  // LoRA, sparse-path row: + s z B_down
+  if (lora) {  // LoRA, sparse-path row: + s z B_down
     __shared__ float zf[kGlueThreads];
     __shared__ float zs[64];
     constexpr int Q = 16;  // tile groups (16 x rank <= 1024 threads)
@@ -760,8 +769,17 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
     __syncthreads();
     if (on) {
       f32x4v t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < kBdPre; ++k) {
+        if (k < R) {
+          t[0] = fmaf(zs[k], bf16_to_f32(bpre[k].x & 0xffffu), t[0]);
+          t[1] = fmaf(zs[k], bf16_to_f32(bpre[k].x >> 16), t[1]);
+          t[2] = fmaf(zs[k], bf16_to_f32(bpre[k].y & 0xffffu), t[2]);
+          t[3] = fmaf(zs[k], bf16_to_f32(bpre[k].y >> 16), t[3]);
+        }
+      }
 #pragma unroll 8
-      for (int k = 0; k < R; ++k) {
+      for (int k = kBdPre; k < R; ++k) {
         const uint2 bw = *reinterpret_cast<const uint2 *>(a.Bd + (size_t)k * a.d + c);
         t[0] = fmaf(zs[k], bf16_to_f32(bw.x & 0xffffu), t[0]);
         t[1] = fmaf(zs[k], bf16_to_f32(bw.x >> 16), t[1]);
