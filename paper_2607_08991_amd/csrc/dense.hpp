@@ -831,7 +831,7 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
 // partials go to vpart, and the last chunk of a (row tile, adapter) to
 // arrive adds them in chunk order.  Base-path rows get zeros (their layers
 // see the base weights only).
-constexpr int kLoraVChunks = 8;
+constexpr int kLoraVChunks = 16;
 constexpr int kLoraVMaxChunk = 512;  // k rows per chunk (d <= 4096)
 constexpr int kLoraVMaxRank = 64;    // ranks 8, 16, 32, 64
 struct LoraVArgs {
@@ -869,7 +869,7 @@ __global__ __launch_bounds__(256) void lora_v_kernel(LoraVArgs a) {
   // the chunk's k, each summed in k order; the slices are then added in order
   const int Q4 = R / 4, NS = 64 / R;
   const int sl = tid / (16 * Q4), r = (tid / Q4) % 16, q = tid % Q4;
-  // slice bounds on multiples of 8 k (16-byte LDS reads of h); kch is a multiple of 16
+  // slice bounds on multiples of 8 k (16-byte LDS reads of h); kch is a multiple of 8
   const int kb = (sl * kch / NS) & ~7, ke = (sl == NS - 1) ? kch : ((sl + 1) * kch / NS) & ~7;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   int k = kb;
