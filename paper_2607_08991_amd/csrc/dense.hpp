@@ -778,7 +778,7 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
           t[3] = fmaf(zs[k], bf16_to_f32(bpre[k].y >> 16), t[3]);
         }
       }
-#pragma unroll 8
+#pragma unroll 16
       for (int k = kBdPre; k < R; ++k) {
         const uint2 bw = *reinterpret_cast<const uint2 *>(a.Bd + (size_t)k * a.d + c);
         t[0] = fmaf(zs[k], bf16_to_f32(bw.x & 0xffffu), t[0]);
@@ -832,7 +832,7 @@ __global__ __launch_bounds__(kGlueThreads) void dense_glue_kernel(GlueArgs a) {
 // arrive adds them in chunk order.  Base-path rows get zeros (their layers
 // see the base weights only).
 constexpr int kLoraVChunks = 16;
-constexpr int kLoraVMaxChunk = 512;  // k rows per chunk (d <= 4096)
+constexpr int kLoraVMaxChunk = 4096 / kLoraVChunks;  // k rows per chunk (d <= 4096)
 constexpr int kLoraVMaxRank = 64;    // ranks 8, 16, 32, 64
 struct LoraVArgs {
   const int *ctl;          // [0] rows of the group, [1] MFMA path on
@@ -862,8 +862,20 @@ __global__ __launch_bounds__(256) void lora_v_kernel(LoraVArgs a) {
     if (m < nd) v = *reinterpret_cast<const u32x4 *>(a.H + (size_t)m * a.K + k0 + 8 * q);
     *reinterpret_cast<u32x4 *>(hs + r * kch + 8 * q) = v;
   }
-  for (int e = tid; e < kch * R / 8; e += 256)
-    *reinterpret_cast<u32x4 *>(as + 8 * e) = *reinterpret_cast<const u32x4 *>(A + (size_t)k0 * R + 8 * e);
+  {  // A's chunk: at most kLoraVMaxChunk * kLoraVMaxRank / 8 / 256 = 8 16-byte loads per thread, all issued first
+    constexpr int kAPer = kLoraVMaxChunk * kLoraVMaxRank / 8 / 256;
+    u32x4 av[kAPer];
+#pragma unroll
+    for (int j = 0; j < kAPer; ++j) {
+      const int e = tid + 256 * j;
+      av[j] = e < kch * R / 8 ? *reinterpret_cast<const u32x4 *>(A + (size_t)k0 * R + 8 * e) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < kAPer; ++j) {
+      const int e = tid + 256 * j;
+      if (e < kch * R / 8) *reinterpret_cast<u32x4 *>(as + 8 * e) = av[j];
+    }
+  }
   __syncthreads();
   // thread (slice sl of NS, row r, ranks 4 q .. 4 q + 3): NS = 64 / R slices of
   // the chunk's k, each summed in k order; the slices are then added in order
