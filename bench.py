@@ -204,6 +204,7 @@ def bench_stack(args, cfg):
             step(warmup + s, dense, lora)
         e1.record(stream)
         torch.cuda.synchronize()
+        sats.sats_device_status(stream)  # raises if a bounded device-side wait gave up: the timing is void
         return e0.elapsed_time(e1) / steps
 
     ms = timed()
@@ -213,9 +214,8 @@ def bench_stack(args, cfg):
         plain_ms = timed(lora=False)
         per_token_ms = None
         if batch > 1:  # the same batch token after token on the single-token path (a few steps: it is slow)
-            os.environ["SATS_LORA_PER_TOKEN"] = "1"
-            per_token_ms = timed(steps=min(args.steps, 3), warmup=1)
-            del os.environ["SATS_LORA_PER_TOKEN"]
+            with sats.options(lora_per_token=1):
+                per_token_ms = timed(steps=min(args.steps, 3), warmup=1)
         lora_res = {"rank": R, "scale": args.lora_scale, "plain_sparse_ms_per_step": round(plain_ms, 5),
                     "overhead_vs_plain_sparse": round(ms / plain_ms, 4),
                     "token_by_token_ms_per_step": None if per_token_ms is None else round(per_token_ms, 5),
@@ -490,6 +490,7 @@ def main():
             fn(args.warmup + s)
         e1.record(stream)
         torch.cuda.synchronize()
+        sats.sats_device_status(stream)  # raises if a bounded device-side wait gave up: the timing is void
         ms = e0.elapsed_time(e1) / args.steps
         kt = {}
         for k in kinds:

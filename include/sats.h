@@ -224,8 +224,8 @@ int sats_device_status(hipStream_t stream);
  * its largest candidate with Err <= b (Eq. 7), S(b) is the mean layer
  * sparsity (Eq. 9), and b* minimises |S(b) - s_tar| over every distinct
  * error value (Eq. 10; the smallest b on ties).  Then, per layer, levels
- * fine_step apart between the coarse levels around its choice are added
- * and b* is chosen again.  With guardrail != 0 (and n_layers > 1) the last
+ * fine_step apart strictly between the two coarse levels adjacent to the
+ * level of its choice (both sides of it) are added and b* is chosen again.  With guardrail != 0 (and n_layers > 1) the last
  * layer keeps its CATS threshold at level s_tar (its sparsity counts in S).
  * thresholds_out: host float [n_layers]; budget_out, realized_out: host
  * doubles (may be NULL) receiving b* and S(b*).
@@ -263,6 +263,59 @@ int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *
 int sats_route_table(const float *loss_base, const float *loss_sparse, const int32_t *token_ids, int64_t n_tokens,
                      const int32_t *heldout_ids, int64_t n_heldout, int64_t vocab, double r_tar,
                      uint8_t *route_lut, double *scores, double *tau_out, double *realized_out, hipStream_t stream);
+
+/*
+ * Execution options: which kernels the forward calls made afterwards on the
+ * calling thread run.  Every field's default, 0, is the library's own
+ * choice; sats_set_options(NULL) restores the defaults.  Meant for tests
+ * and measurement (results of every choice agree with the definition above
+ * within the stated tolerances); nothing else changes the kernels a call
+ * takes.  Errors: SATS_ERR_ARG for a value outside its range.
+ *   batch_path      SATS_BATCH_AUTO, or for batches of 2 or more bf16 tokens:
+ *                   SATS_BATCH_MFMA     every token on the matrix cores, each
+ *                                       with its own route and keep rule;
+ *                   SATS_BATCH_SPLIT    the base-path group on the matrix
+ *                                       cores, the sparse group on the
+ *                                       compacted kernels;
+ *                   SATS_BATCH_COMPACT  every token on the compacted kernels
+ *                                       (gate, then up and down over the
+ *                                       union of kept rows of each 4-token
+ *                                       tile, with a per-row token mask).
+ *   single_token    SATS_SINGLE_AUTO: one-token calls on the single-token
+ *                   kernels where the shape fits them; SATS_SINGLE_OFF: on
+ *                   the batch kernels.
+ *   dec_gate_tiles  single-token gate launch: about this many tiles (1 ..
+ *                   65536; 0 = 256).
+ *   dec_rows_wgs    single-token rows launch: workgroups, one partial of y
+ *                   each (1 .. 1024; 0 = one per compute unit).
+ *   lora_per_token  1: LoRA batches token after token on the single-token
+ *                   kernels instead of the matrix-core passes.
+ */
+enum { SATS_BATCH_AUTO = 0, SATS_BATCH_MFMA = 1, SATS_BATCH_SPLIT = 2, SATS_BATCH_COMPACT = 3 };
+enum { SATS_SINGLE_AUTO = 0, SATS_SINGLE_OFF = 1 };
+typedef struct {
+  int batch_path;
+  int single_token;
+  int dec_gate_tiles;
+  int dec_rows_wgs;
+  int lora_per_token;
+} sats_options;
+int sats_set_options(const sats_options *opt);
+
+/*
+ * The kernels a forward call (without adapters) of this shape would run
+ * under the calling thread's options, answered on the host without device
+ * work: *path receives SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA,
+ * SATS_PATH_BATCH_SPLIT or SATS_PATH_BATCH_COMPACT (for the first pass of
+ * up to 64 tokens; 0 for n_tokens == 0).  elem_bytes: 2 (bf16) or 4
+ * (float32); aligned16: whether x, out and the weights are 16-byte aligned;
+ * n_cus: compute units of the device (0: the current device's).  Errors:
+ * SATS_ERR_NULL, SATS_ERR_SHAPE and SATS_ERR_ARG as for the forward calls.
+ */
+enum { SATS_PATH_SINGLE_TOKEN = 1, SATS_PATH_BATCH_MFMA = 2, SATS_PATH_BATCH_SPLIT = 3,
+       SATS_PATH_BATCH_COMPACT = 4 };
+int sats_query_path(int64_t n_tokens, int64_t d, int64_t d_ff, int elem_bytes, int aligned16, int n_cus,
+                    int *path);
 
 /* Free every workspace of the calling process (synchronises each device). */
 int sats_release(void);

@@ -31,8 +31,10 @@ Readings where the paper is silent (listed in the design notes):
   * S(b) changes only where b crosses some Err_l(t), so the budgets tried are
     exactly those values; ties of |S(b) - s_tar| go to the smallest b.
   * Refinement: the Eq. 3 percentiles at levels spaced `fine_step` apart
-    between the coarse levels just below and just above the level of the
-    coarse choice, added to T_l; the selection is then repeated on the union.
+    strictly between the two coarse levels adjacent to the coarse level of
+    the choice (so on both sides of it; the smallest coarse level whose
+    percentile is the chosen threshold, 0 for t = 0), added to T_l; the
+    selection is then repeated on the union.
   * The guardrail layer's sparsity counts in S(b) at its fixed threshold.
 
 Arithmetic: float64 on the exact stored inputs, with the masked output
@@ -129,8 +131,17 @@ def coarse_levels(step=0.05):
     return [round(i * step, 10) for i in range(1, n)]
 
 
+def coarse_level_of(t, absg, coarse):
+    """The coarse level a chosen candidate comes from: 0 for t = 0, else the
+    smallest coarse level whose Eq. 3 percentile is t."""
+    if t == 0.0:
+        return 0.0
+    return min(q for q in coarse if percentile_threshold(absg, q) == t)
+
+
 def fine_levels(q, coarse, fine_step):
-    """Levels fine_step apart strictly between the coarse neighbours of q."""
+    """Levels fine_step apart strictly between the coarse neighbours of q
+    (q itself a coarse level: the range spans both sides of it)."""
     lo = max([c for c in coarse if c < q - 1e-12], default=0.0)
     hi = min([c for c in coarse if c > q + 1e-12], default=1.0)
     out, i = [], 1
@@ -180,14 +191,13 @@ def calibrate(x_cal, W_gate, W_up_T, W_down, s_tar, dtype, coarse_step=0.05, fin
 
     c1 = curves_for([coarse] * L)
     b1, idx1, s1 = select_budget(c1, s_tar, fixed)
-    # refinement around each layer's coarse choice (by its Eq. 3 level)
+    # refinement on both sides of each layer's coarse choice (its Eq. 3 level)
     levels2 = []
     for l in range(L):
         if l in fixed:
             levels2.append(coarse)
             continue
-        t = c1[l][0][idx1[l]]
-        q = float(np.mean(layers[l]["absg"] < t))      # the level t sits at
+        q = coarse_level_of(c1[l][0][idx1[l]], layers[l]["absg"], coarse)
         levels2.append(sorted(set(coarse) | set(fine_levels(q, coarse, fine_step))))
     c2 = curves_for(levels2)
     b2, idx2, s2 = select_budget(c2, s_tar, fixed)

@@ -19,6 +19,15 @@ SATS_ERR_DEVICE = -6
 SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DENSE = 0, 1, 2, 3, 4
 SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, SATS_K_ROUTE_ACCUM = 5, 6, 7, 8, 9
 SATS_K_LORA_V = 10
+SATS_BATCH_AUTO, SATS_BATCH_MFMA, SATS_BATCH_SPLIT, SATS_BATCH_COMPACT = 0, 1, 2, 3
+SATS_SINGLE_AUTO, SATS_SINGLE_OFF = 0, 1
+SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA, SATS_PATH_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT = 1, 2, 3, 4
+
+
+class SatsOptions(ctypes.Structure):
+    """sats_options of include/sats.h."""
+    _fields_ = [("batch_path", ctypes.c_int), ("single_token", ctypes.c_int), ("dec_gate_tiles", ctypes.c_int),
+                ("dec_rows_wgs", ctypes.c_int), ("lora_per_token", ctypes.c_int)]
 
 # exported symbols and their argument types (p = pointer, i = int64, s = stream, n = int32)
 _P, _I, _S, _N = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
@@ -42,6 +51,8 @@ SIGNATURES = {
     "sats_mlp_forward_lora": ([_P] * 11 + [_I, ctypes.c_float] + [_P] * 3 + [_I] * 4 + [_S] + [_P] * 4, _N),
     "sats_mlp_forward_lora_f32": ([_P] * 11 + [_I, ctypes.c_float] + [_P] * 3 + [_I] * 4 + [_S] + [_P] * 4, _N),
     "sats_route_table": ([_P] * 3 + [_I, _P, _I, _I, ctypes.c_double] + [_P] * 4 + [_S], _N),
+    "sats_set_options": ([ctypes.POINTER(SatsOptions)], _N),
+    "sats_query_path": ([_I, _I, _I, _N, _N, _N, ctypes.POINTER(ctypes.c_int)], _N),
     "sats_calibration_curves": ([_P] * 4 + [_I] * 3 + [_P, _I] + [_P] * 4 + [_S], _N),
     "sats_calibrate_sats": ([_P, _I] + [_P] * 3 + [_I] * 3 + [ctypes.c_double] * 3 + [_N] + [_P] * 3 + [_S], _N),
 }
@@ -155,6 +166,34 @@ def sats_device_status(stream=None):
 
 def sats_release():
     _call("sats_release")
+
+
+def sats_set_options(batch_path=0, single_token=0, dec_gate_tiles=0, dec_rows_wgs=0, lora_per_token=0):
+    """Execution options of the calling thread's later forward calls (all 0: the defaults)."""
+    o = SatsOptions(batch_path, single_token, dec_gate_tiles, dec_rows_wgs, lora_per_token)
+    _call("sats_set_options", ctypes.byref(o))
+
+
+class options:
+    """Context manager: sats_set_options(**kw) inside, the defaults after."""
+
+    def __init__(self, **kw):
+        self.kw = kw
+
+    def __enter__(self):
+        sats_set_options(**self.kw)
+        return self
+
+    def __exit__(self, *exc):
+        _call("sats_set_options", None)
+        return False
+
+
+def sats_query_path(n_tokens, d, d_ff, elem_bytes, aligned16=True, n_cus=0) -> int:
+    """The SATS_PATH_* a forward call of this shape takes under the current options (host only)."""
+    path = ctypes.c_int(-1)
+    _call("sats_query_path", n_tokens, d, d_ff, elem_bytes, int(bool(aligned16)), n_cus, ctypes.byref(path))
+    return path.value
 
 
 def sats_last_error() -> str:

@@ -105,12 +105,12 @@ int round_pow2_down(int v) {
   return p;
 }
 
-int env_int(const char *name, int dflt) {
-  const char *s = getenv(name);
-  if (!s || !*s) return dflt;
-  int v = atoi(s);
-  return v > 0 ? v : dflt;
-}
+// Execution options of the calling thread (sats_set_options).
+thread_local sats_options g_opt{};
+
+// Compacted batch kernels: target workgroup counts of the gate and down
+// launches and kept rows per wavefront of the up launch.
+constexpr int kGateTarget = 2048, kDownTarget = 512, kUpRowsPerWave = 2;
 
 struct Plan {
   int vec, CL, RG, CB;     // down lanes per row segment; gate row groups and columns per block
@@ -130,18 +130,15 @@ Plan make_plan(int64_t d, int64_t d_ff, int esz, bool vec_ok, int n_pass) {
   p.CB = gate_cl * p.vec;
   p.nblocks = (int)((d_ff + p.CB - 1) / p.CB);
   p.NT = (n_pass == 1) ? 1 : 4;
-  const int gate_target = env_int("SATS_GATE_WGS", 2048);
-  int ks = round_pow2_down(std::max(1, gate_target / p.nblocks));
+  int ks = round_pow2_down(std::max(1, kGateTarget / p.nblocks));
   ks = std::min<int64_t>(ks, std::max<int64_t>(1, d / p.RG));
   ks = std::max<int64_t>(ks, (d + 1023) / 1024);
   p.KC = (int)((d + ks - 1) / ks);
   p.KS = (int)((d + p.KC - 1) / p.KC);
   p.SW = p.CL * p.vec;
   p.n_slices = (int)((d + p.SW - 1) / p.SW);
-  const int down_target = env_int("SATS_DOWN_WGS", 512);
-  p.KCH = std::max(1, down_target / p.n_slices);
-  const int rows_per_wave = env_int("SATS_UP_ROWS_PER_WAVE", 2);
-  int64_t waves = (d_ff + rows_per_wave - 1) / rows_per_wave;
+  p.KCH = std::max(1, kDownTarget / p.n_slices);
+  int64_t waves = (d_ff + kUpRowsPerWave - 1) / kUpRowsPerWave;
   p.up_grid = (int)std::min<int64_t>(std::max<int64_t>(1, (waves + 3) / 4), 4096);
   return p;
 }
@@ -252,6 +249,19 @@ int device_cus() {
   return cus;
 }
 
+// Single-token rows workgroups: the option, else one per compute unit.
+int dec_rows_wgs(int cus = -1) { return g_opt.dec_rows_wgs > 0 ? g_opt.dec_rows_wgs : (cus >= 0 ? cus : device_cus()); }
+
+// Batch passes of np tokens: whether the matrix-core kernels run (bf16, the
+// vector layout, shapes on their tiles and matrices below 2 GB) and whether
+// they take every token (else the base-path group only).
+bool batch_mfma(int esz, bool vec_ok, int np, bool lora, int64_t d, int64_t d_ff) {
+  return esz == 2 && vec_ok && (np >= sats::kMfmaMinTokens || lora) && d % sats::kDenseDownNT == 0 &&
+         d_ff % sats::kDenseKC == 0 && d <= 4096 && (uint64_t)d * d_ff * 2 < (1ull << 31) &&
+         g_opt.batch_path != SATS_BATCH_COMPACT;
+}
+bool batch_whole() { return g_opt.batch_path != SATS_BATCH_SPLIT; }
+
 struct Workspace {
   char *mem = nullptr;
   size_t bytes = 0;
@@ -293,12 +303,12 @@ int ensure_workspace(hipStream_t stream, size_t bytes, size_t n_counters, Worksp
 // (at most kDecodeMaxG) take the rows and reduce phases, each reduce
 // workgroup owning at most one column per thread; gate tiles are one column
 // block by about d / nrc rows.  Returns false when the shape does not fit.
-bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, int lora_rank = 0) {
+bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, int lora_rank = 0, int cus = -1) {
   DecodePlan q{};
   const int64_t cb = (int64_t)(16 / esz) * 64;
   q.G = G;
   q.nblk = (int)((d_ff + cb - 1) / cb);
-  const int64_t tiles = env_int("SATS_DEC_GATE_WGS", 256);
+  const int64_t tiles = g_opt.dec_gate_tiles > 0 ? g_opt.dec_gate_tiles : 256;
   int64_t nrc = std::max<int64_t>(1, tiles / q.nblk);
   nrc = std::min<int64_t>(nrc, std::max<int64_t>(1, d / (sats::kGateThreads / 64)));  // a row per wavefront
   (void)lora_rank;
@@ -308,10 +318,13 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, i
   // slice of y each, 32 columns (128 bytes of each partial) or more; RW is
   // kept to a quarter of the CUs so that the reducers, which wait for the
   // others, never fill the device
-  q.RW = (int)std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32), std::max(1, device_cus() / 4));
+  q.RW = (int)std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32), std::max(1, (cus >= 0 ? cus : device_cus()) / 4));
   q.RW = std::min(q.RW, G);
+  // buffer descriptors address one layer's matrix with 32-bit offsets, and
+  // 0x80000000 is the offset that reads zeros: every matrix must stay below 2 GB
   const bool ok = G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
-                  (d + q.RW - 1) / q.RW <= sats::kDecodeThreads;
+                  (d + q.RW - 1) / q.RW <= sats::kDecodeThreads &&
+                  (uint64_t)d * (uint64_t)d_ff * (uint64_t)esz < (1ull << 31);
   *dp = ok ? q : DecodePlan{};
   return ok;
 }
@@ -353,13 +366,10 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
 
   // routing for the pass: partition, dense-group size and whether MFMA takes it
   const bool lora = c.Ag != nullptr;  // batched LoRA: the whole pass on MFMA (checked by the caller)
-  const bool mfma = sizeof(T) == 2 && VEC > 1 && (np >= kMfmaMinTokens || lora) &&
-                    d % kDenseDownNT == 0 && d_ff % kDenseKC == 0 && d <= 4096 &&
-                    (uint64_t)d * d_ff * 2 < (1ull << 31) &&
-                    !getenv("SATS_NO_MFMA");
+  const bool mfma = batch_mfma((int)sizeof(T), VEC > 1, np, lora, d, d_ff);
   // whole batch on MFMA (each row applies its own keep rule): known here, so
   // the compacted sparse-path launches are left out
-  const bool whole = !getenv("SATS_MFMA_BASE_GROUP_ONLY");
+  const bool whole = batch_whole();
   const bool all_mfma = mfma && whole;
   if (lora && !all_mfma) return fail(SATS_ERR_SHAPE, "batched LoRA pass without the MFMA path");
   {
@@ -675,9 +685,8 @@ int lora_check(const Call &c) {
 // MFMA (the adapters enter the gate/up epilogue and the glue); everything
 // else runs the single-token path token after token.
 bool lora_batched(const Call &c, int esz, bool vec_ok) {
-  return esz == 2 && vec_ok && c.n >= sats::kMfmaMinTokens && c.d % sats::kDenseDownNT == 0 &&
-         c.d_ff % sats::kDenseKC == 0 && c.d <= 4096 && (uint64_t)c.d * c.d_ff * 2 < (1ull << 31) &&
-         !getenv("SATS_NO_MFMA") && !getenv("SATS_MFMA_BASE_GROUP_ONLY") && !getenv("SATS_LORA_PER_TOKEN");
+  return c.n >= sats::kMfmaMinTokens && batch_mfma(esz, vec_ok, (int)std::min<int64_t>(c.n, kMaxPass), true, c.d, c.d_ff) &&
+         batch_whole() && !g_opt.lora_per_token;
 }
 
 // LoRA calls on the single-token path, token after token (each token takes
@@ -686,8 +695,8 @@ template <typename T>
 int run_lora(const Call &c, bool vec_ok) {
   const int esz = (int)sizeof(T);
   DecodePlan dp;
-  if (!vec_ok || getenv("SATS_NO_DECODE") ||
-      !make_decode_plan(c.d, c.d_ff, esz, env_int("SATS_DEC_ROWS_WGS", device_cus()), &dp, (int)c.rank))
+  if (!vec_ok || g_opt.single_token == SATS_SINGLE_OFF ||
+      !make_decode_plan(c.d, c.d_ff, esz, dec_rows_wgs(), &dp, (int)c.rank))
     return fail(SATS_ERR_SHAPE,
                 "LoRA calls need the single-token layout: d <= %d, d and d_ff multiples of %d, 16-byte aligned arrays",
                 sats::kDecodeMaxD, 16 / esz);
@@ -748,9 +757,9 @@ int run(const Call &c) {
   }
   const int64_t lrank = c.Ag ? c.rank : 0;
   // single-token path: one token, vector layout, h fits the LDS copy
-  bool decode = c.n == 1 && vec_ok && !getenv("SATS_NO_DECODE");
+  bool decode = c.n == 1 && vec_ok && g_opt.single_token != SATS_SINGLE_OFF;
   DecodePlan dp;
-  if (decode) decode = make_decode_plan(c.d, c.d_ff, esz, env_int("SATS_DEC_ROWS_WGS", device_cus()), &dp);
+  if (decode) decode = make_decode_plan(c.d, c.d_ff, esz, dec_rows_wgs(), &dp);
   const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, c.L, dp, nullptr, lrank);
   Workspace *ws = nullptr;
   size_t ncount = counter_count(p, pass, dp);
@@ -1032,7 +1041,7 @@ std::vector<double> cal_coarse(double step) {
   for (int i = 1; i < n; ++i) v.push_back(std::round(i * step * 1e10) / 1e10);
   return v;
 }
-// levels fine apart strictly between the coarse neighbours of q
+// levels fine apart strictly between the coarse neighbours of the coarse level q
 std::vector<double> cal_fine(double q, const std::vector<double> &coarse, double fine) {
   double lo = 0.0, hi = 1.0;
   for (double c : coarse) {
@@ -1104,10 +1113,13 @@ int cal_stack(const uint16_t *x, int64_t n, const uint16_t *Wg, const uint16_t *
   double b1 = 0.0, s1 = 0.0;
   std::vector<int> idx1;
   cal_select(cv, fixed, fixed_sp, s_tar, &b1, &idx1, &s1);
-  // stage 2: finer levels around each free layer's choice, added to its candidates
+  // stage 2: finer levels on both sides of each free layer's choice (between
+  // the coarse levels adjacent to the level it was chosen at: the smallest
+  // level of its threshold, since the selection keeps the first of equal
+  // thresholds), added to its candidates
   for (int64_t l = 0; l < L; ++l) {
     if (fixed[l]) continue;
-    const double q = cv[l].sp[idx1[l]];
+    const double q = cv[l].level[idx1[l]];
     const std::vector<double> fl = cal_fine(q, coarse, fine_step);
     if (fl.empty()) continue;
     if ((rc = layer_curves(l, fl, cv[l], true))) return rc;
@@ -1424,8 +1436,8 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, 
   int cus = device_cus();
   if (cus < 1) return fail(SATS_ERR_HIP, "no device");
   DecodePlan dps[2]{};  // the plain single-token plan and the one of LoRA calls at the largest rank
-  (void)make_decode_plan(d, d_ff, elem_bytes, env_int("SATS_DEC_ROWS_WGS", cus), &dps[0]);
-  (void)make_decode_plan(d, d_ff, elem_bytes, env_int("SATS_DEC_ROWS_WGS", cus), &dps[1], sats::kLoraMaxRank);
+  (void)make_decode_plan(d, d_ff, elem_bytes, dec_rows_wgs(cus), &dps[0], 0, cus);
+  (void)make_decode_plan(d, d_ff, elem_bytes, dec_rows_wgs(cus), &dps[1], sats::kLoraMaxRank, cus);
   for (const DecodePlan &dp : dps)
     for (int v = 0; v < 2; ++v)
       for (int np : {1, pass}) {
@@ -1489,6 +1501,46 @@ int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *
 }
 
 const char *sats_last_error(void) { return g_err.c_str(); }
+
+int sats_set_options(const sats_options *opt) {
+  g_err.clear();
+  if (!opt) {
+    g_opt = sats_options{};
+    return SATS_OK;
+  }
+  if (opt->batch_path < SATS_BATCH_AUTO || opt->batch_path > SATS_BATCH_COMPACT ||
+      opt->single_token < SATS_SINGLE_AUTO || opt->single_token > SATS_SINGLE_OFF || opt->dec_gate_tiles < 0 ||
+      opt->dec_gate_tiles > 65536 || opt->dec_rows_wgs < 0 || opt->dec_rows_wgs > sats::kDecodeMaxG ||
+      opt->lora_per_token < 0 || opt->lora_per_token > 1)
+    return fail(SATS_ERR_ARG, "an option is outside its range");
+  g_opt = *opt;
+  return SATS_OK;
+}
+
+int sats_query_path(int64_t n_tokens, int64_t d, int64_t d_ff, int elem_bytes, int aligned16, int n_cus,
+                    int *path) {
+  g_err.clear();
+  if (!path) return fail(SATS_ERR_NULL, "path must be non-null");
+  if (elem_bytes != 2 && elem_bytes != 4) return fail(SATS_ERR_ARG, "elem_bytes must be 2 or 4");
+  if (n_cus < 0) return fail(SATS_ERR_ARG, "n_cus must be >= 0");
+  if (d < 1 || d_ff < 1 || n_tokens < 0 || d > (1 << 24) || d_ff > (1 << 24) || n_tokens > ((int64_t)1 << 40))
+    return fail(SATS_ERR_SHAPE, "need d >= 1, d_ff >= 1, n_tokens >= 0, d and d_ff at most 2^24");
+  *path = 0;
+  if (n_tokens == 0) return SATS_OK;
+  const int vec = 16 / elem_bytes;
+  const bool vec_ok = aligned16 && d % vec == 0 && d_ff % vec == 0;
+  const int cus = n_cus > 0 ? n_cus : device_cus();
+  DecodePlan dp;
+  if (n_tokens == 1 && vec_ok && g_opt.single_token != SATS_SINGLE_OFF &&
+      make_decode_plan(d, d_ff, elem_bytes, dec_rows_wgs(cus), &dp, 0, cus)) {
+    *path = SATS_PATH_SINGLE_TOKEN;
+    return SATS_OK;
+  }
+  const int np = (int)std::min<int64_t>(n_tokens, kMaxPass);
+  if (!batch_mfma(elem_bytes, vec_ok, np, false, d, d_ff)) *path = SATS_PATH_BATCH_COMPACT;
+  else *path = batch_whole() ? SATS_PATH_BATCH_MFMA : SATS_PATH_BATCH_SPLIT;
+  return SATS_OK;
+}
 
 int sats_device_status(hipStream_t stream) {
   g_err.clear();

@@ -143,3 +143,52 @@ def test_timing_kinds_match_the_header_and_name_their_kernels():
     assert sats.sats_kernel_name(sats.SATS_K_LORA_V) == "lora_v_kernel"
     with pytest.raises(sats.SatsError):
         sats.sats_timing_begin(count, 1)
+
+
+# ------------------------------------------------------------------ options and path selection
+
+def test_options_are_validated_and_reset():
+    lib = sats.load()
+    for bad in (dict(batch_path=4), dict(batch_path=-1), dict(single_token=2), dict(dec_gate_tiles=-1),
+                dict(dec_gate_tiles=65537), dict(dec_rows_wgs=1025), dict(lora_per_token=2)):
+        o = _lib.SatsOptions(**{**dict(batch_path=0, single_token=0, dec_gate_tiles=0, dec_rows_wgs=0,
+                                       lora_per_token=0), **bad})
+        assert lib.sats_set_options(ctypes.byref(o)) == _lib.SATS_ERR_ARG, bad
+    assert lib.sats_set_options(None) == _lib.SATS_OK
+
+
+def test_query_path_follows_shapes_and_options():
+    q = sats.sats_query_path
+    L8B = (4096, 14336)
+    assert q(0, *L8B, 2, n_cus=256) == 0
+    assert q(1, *L8B, 2, n_cus=256) == sats.SATS_PATH_SINGLE_TOKEN
+    assert q(1, *L8B, 4, n_cus=256) == sats.SATS_PATH_SINGLE_TOKEN
+    assert q(4, *L8B, 2, n_cus=256) == sats.SATS_PATH_BATCH_MFMA
+    assert q(4, *L8B, 4, n_cus=256) == sats.SATS_PATH_BATCH_COMPACT       # fp32 batches: compacted kernels
+    assert q(1, *L8B, 2, aligned16=False, n_cus=256) == sats.SATS_PATH_BATCH_COMPACT
+    assert q(1, 5000, 64, 2, n_cus=256) == sats.SATS_PATH_BATCH_COMPACT    # h does not fit the LDS copy
+    with sats.options(batch_path=sats.SATS_BATCH_SPLIT, single_token=sats.SATS_SINGLE_OFF):
+        assert q(4, *L8B, 2, n_cus=256) == sats.SATS_PATH_BATCH_SPLIT
+        assert q(1, *L8B, 2, n_cus=256) == sats.SATS_PATH_BATCH_COMPACT
+    with sats.options(batch_path=sats.SATS_BATCH_COMPACT):
+        assert q(4, *L8B, 2, n_cus=256) == sats.SATS_PATH_BATCH_COMPACT
+    assert q(4, *L8B, 2, n_cus=256) == sats.SATS_PATH_BATCH_MFMA          # defaults restored
+
+
+def test_single_token_path_refuses_matrices_of_2gb():
+    """The single-token kernels address a matrix with 32-bit buffer offsets
+    (0x80000000 reads zeros), so a layer whose matrix reaches 2^31 bytes
+    takes the compacted kernels (64-bit indices) instead."""
+    q = sats.sats_query_path
+    assert q(1, 4096, 131072 - 16, 4, n_cus=256) == sats.SATS_PATH_SINGLE_TOKEN   # just below 2 GB
+    assert q(1, 4096, 131072, 4, n_cus=256) == sats.SATS_PATH_BATCH_COMPACT       # exactly 2 GB
+    assert q(1, 4096, 262144, 2, n_cus=256) == sats.SATS_PATH_BATCH_COMPACT       # bf16, 2 GB
+    assert q(1, 4096, 262144 - 8, 2, n_cus=256) == sats.SATS_PATH_SINGLE_TOKEN
+
+
+def test_query_path_rejects_bad_arguments():
+    lib = sats.load()
+    p = ctypes.c_int(0)
+    assert lib.sats_query_path(1, 8, 8, 3, 1, 256, ctypes.byref(p)) == _lib.SATS_ERR_ARG
+    assert lib.sats_query_path(1, 0, 8, 2, 1, 256, ctypes.byref(p)) == _lib.SATS_ERR_SHAPE
+    assert lib.sats_query_path(1, 8, 8, 2, 1, 256, None) == _lib.SATS_ERR_NULL

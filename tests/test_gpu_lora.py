@@ -243,9 +243,9 @@ def test_lora_batched_cases_match_oracle(seed, L, d, dff, n, rank):
         say(f"  lut={'yes' if lut is not None else 'no'} worst rel err {worst:.3g}")
 
 
-def test_lora_batched_is_deterministic_and_both_paths_match_oracle(monkeypatch):
+def test_lora_batched_is_deterministic_and_both_paths_match_oracle():
     """Repeated batched calls give the same bits, inspection changes nothing,
-    and the single-token path (forced by SATS_LORA_PER_TOKEN) matches the
+    and the single-token path (chosen by the lora_per_token option) matches the
     oracle on the same batch.  The two paths are not compared with each
     other: each may flip neurons inside the band, and over layers the flips
     move the inputs, so only the oracle comparison with each path's own
@@ -261,9 +261,10 @@ def test_lora_batched_is_deterministic_and_both_paths_match_oracle(monkeypatch):
     np.testing.assert_array_equal(a["out"], b["out"])
     np.testing.assert_array_equal(a["out"], r["out"])
     say(f"batched: worst rel err {check_lora(c, ad, s, ts, c['route_lut'], 'bf16', r):.3g}")
-    monkeypatch.setenv("SATS_LORA_PER_TOKEN", "1")
+    import paper_2607_08991_amd as sats
     got = {}
-    nv, nr = launches(lambda: got.update(run_lora(c, ad, rank, s, ts, c["route_lut"], "bf16")))
+    with sats.options(lora_per_token=1):
+        nv, nr = launches(lambda: got.update(run_lora(c, ad, rank, s, ts, c["route_lut"], "bf16")))
     assert nv == 0 and nr == n * L
     say(f"single-token: worst rel err {check_lora(c, ad, s, ts, c['route_lut'], 'bf16', got):.3g}")
 

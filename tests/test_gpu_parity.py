@@ -14,6 +14,9 @@ from oracle import calibrate, mlp, numerics
 from workloads import get_config, synth
 
 from harness import TOL, check_against_oracle, from_dev, rel_err, run_gpu, to_dev
+from paper_2607_08991_amd import (SATS_BATCH_COMPACT, SATS_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT,
+                                  SATS_PATH_BATCH_MFMA, SATS_PATH_BATCH_SPLIT, SATS_PATH_SINGLE_TOKEN)
+from paper_2607_08991_amd import options as sats_options, sats_query_path
 
 pytestmark = pytest.mark.gpu
 
@@ -75,14 +78,26 @@ def test_small_cases_match_oracle(seed, L, d, dff, dtype, n):
         assert 0.05 < kept < 0.95 or lut is not None
 
 
-def test_forward_equals_inspect_bitwise_and_is_deterministic():
-    c = synth.small_case(21, 2, 256, 1024, "bf16", 6, vocab=40, n_dense_ids=12, w_std=1 / 16)
-    ts = case_thresholds(c, "bf16")
-    a = run_gpu(c, ts, c["route_lut"], "bf16", inspect=False)
-    b = run_gpu(c, ts, c["route_lut"], "bf16", inspect=False)
-    r = run_gpu(c, ts, c["route_lut"], "bf16", inspect=True)
-    np.testing.assert_array_equal(a["out"], b["out"])
-    np.testing.assert_array_equal(a["out"], r["out"])
+@pytest.mark.parametrize("n,dtype", [(6, "bf16"), (1, "bf16"), (1, "f32")])
+def test_forward_equals_inspect_bitwise_and_is_deterministic(n, dtype):
+    """The plain forward (what callers and the benchmark run) gives the
+    inspect call's bits; one token takes the single-token kernels, checked
+    for a sparse-path and a base-path token."""
+    c = synth.small_case(21, 2, 256, 1024, dtype, n, vocab=40, n_dense_ids=12, w_std=1 / 16)
+    ts = case_thresholds(c, dtype)
+    idsets = [c["token_ids"]] if n > 1 else [np.array([int(np.argmin(c["route_lut"]))], np.int32),
+                                             np.array([int(np.argmax(c["route_lut"]))], np.int32)]
+    routes = set()
+    for ids in idsets:
+        c["token_ids"] = ids
+        a = run_gpu(c, ts, c["route_lut"], dtype, inspect=False)
+        b = run_gpu(c, ts, c["route_lut"], dtype, inspect=False)
+        r = run_gpu(c, ts, c["route_lut"], dtype, inspect=True)
+        np.testing.assert_array_equal(a["out"], b["out"])
+        np.testing.assert_array_equal(a["out"], r["out"])
+        check_against_oracle(c, ts, c["route_lut"], dtype, dict(r, out=a["out"]))
+        routes.update(r["route"].tolist())
+    assert routes == {0, 1}
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
@@ -188,17 +203,14 @@ def test_single_token_tilings_match_oracle_and_repeat_bitwise(seed, L, d, dff, d
     ts = case_thresholds(c, dtype, seed=seed)
     for ids in ([0], [int(c["route_lut"].argmax())]):  # a sparse-path and a base-path token
         c["token_ids"] = np.asarray(ids, np.int32)
-        for env in ({}, {"SATS_DEC_GATE_WGS": "1"}, {"SATS_DEC_GATE_WGS": "2000"},
-                    {"SATS_DEC_ROWS_WGS": "7"}, {"SATS_DEC_ROWS_WGS": "1000"}):
-            os.environ.update(env)
-            try:
+        for opt in ({}, {"dec_gate_tiles": 1}, {"dec_gate_tiles": 2000},
+                    {"dec_rows_wgs": 7}, {"dec_rows_wgs": 1000}):
+            with sats_options(**opt):
+                assert sats_query_path(1, d, dff, 2 if dtype == "bf16" else 4) == SATS_PATH_SINGLE_TOKEN
                 r1 = run_gpu(c, ts, c["route_lut"], dtype)
                 r2 = run_gpu(c, ts, c["route_lut"], dtype)
-            finally:
-                for k in env:
-                    del os.environ[k]
             worst = check_against_oracle(c, ts, c["route_lut"], dtype, r1)
-            say(f"  {env or 'default'} ids={ids} worst rel err {worst:.3g}")
+            say(f"  {opt or 'default'} ids={ids} worst rel err {worst:.3g}")
             for k in ("out", "layer_in", "count", "idx", "route"):
                 np.testing.assert_array_equal(r1[k], r2[k])
 
@@ -224,6 +236,47 @@ def test_config_small_fp32_layer():
     assert 0 < res["route"].sum() < n
 
 
+_LAYERS = {}
+
+
+def _llama_layer(cfg):
+    """Stored weights of the one-layer Llama-3.1-8B-shaped workload and their
+    decoded float64 values (generated once per test module)."""
+    if cfg.name not in _LAYERS:
+        say(f"generating {cfg.name} weights")
+        w = synth.layer_weights(cfg.seed, 0, cfg.d, cfg.d_ff, cfg.dtype)
+        _LAYERS.clear()
+        _LAYERS[cfg.name] = (w, [numerics.decode(m, cfg.dtype) for m in w])
+    return _LAYERS[cfg.name]
+
+
+@pytest.mark.parametrize("cfg_name", ["c2_llama8b_layer_bf16", "c2_llama8b_layer_f32"])
+def test_benchmarked_call_matches_inspect_bitwise_and_oracle(cfg_name):
+    """The call the benchmark times -- sats_mlp_forward on one token with no
+    inspection outputs -- on the full Llama-3.1-8B-shaped layer.  A
+    sparse-path token (no table, as benchmarked) and a base-path token (a
+    table routing its id to the base path, Eq. 13): the output equals the
+    inspect call's bit for bit, repeats bit for bit, and matches the oracle
+    (Eq. 1 with the Eq. 5 mask, or plain Eq. 1) within tolerance."""
+    cfg = get_config(cfg_name)
+    ts = _golden(cfg)
+    (wg, wu, wd), dec = _llama_layer(cfg)
+    lut = np.array([0, 1, 0, 0], np.uint8)
+    for ids, table in (([0], None), ([1], lut)):
+        c = dict(x=synth.decode_x(cfg, 1), token_ids=np.asarray(ids, np.int32), W_gate=wg[None],
+                 W_up_T=wu[None], W_down=wd[None])
+        fwd = run_gpu(c, ts, table, cfg.dtype, inspect=False)
+        again = run_gpu(c, ts, table, cfg.dtype, inspect=False)
+        ins = run_gpu(c, ts, table, cfg.dtype, inspect=True)
+        np.testing.assert_array_equal(fwd["out"], again["out"])
+        np.testing.assert_array_equal(fwd["out"], ins["out"])
+        worst = check_against_oracle(c, ts, table, cfg.dtype, dict(ins, out=fwd["out"]), weights=lambda l: dec)
+        kept = int(ins["count"][0][0])
+        say(f"{cfg.name} benchmarked call, route {int(ins['route'][0])}: worst rel err {worst:.3g}, kept {kept}")
+        assert ins["route"][0] == (1 if table is not None else 0)
+        assert kept == cfg.d_ff if table is not None else 0.4 * cfg.d_ff < kept < 0.6 * cfg.d_ff
+
+
 @pytest.mark.parametrize("cfg_name", ["c2_llama8b_layer_bf16", "c2_llama8b_layer_f32"])
 def test_config_llama_layer_full_size(cfg_name):
     """Llama-3.1-8B-shaped layer (4096 x 14336), bf16 and fp32 weights, all tokens
@@ -231,9 +284,7 @@ def test_config_llama_layer_full_size(cfg_name):
     batch kernels for fp32)."""
     cfg = get_config(cfg_name)
     ts = _golden(cfg)
-    say(f"generating {cfg.name} weights")
-    wg, wu, wd = synth.layer_weights(cfg.seed, 0, cfg.d, cfg.d_ff, cfg.dtype)
-    dec = [numerics.decode(w, cfg.dtype) for w in (wg, wu, wd)]
+    (wg, wu, wd), dec = _llama_layer(cfg)
     for n in (1, 4):
         c = dict(x=synth.decode_x(cfg, n), token_ids=np.zeros(n, np.int32), W_gate=wg[None],
                  W_up_T=wu[None], W_down=wd[None])
@@ -263,13 +314,12 @@ def test_mfma_dense_group_matches_oracle(seed, L, n, n_dense_ids):
         assert res["route"].sum() >= 2
     worst = check_against_oracle(c, ts, c["route_lut"], "bf16", res)
     say(f"mfma seed={seed} L={L} n={n} dense={int(res['route'].sum())} worst {worst:.3g}")
+    assert sats_query_path(n, 256, 1024, 2) == SATS_PATH_BATCH_MFMA
     # the same tokens with only the base-path group on MFMA, and with no MFMA
-    for env in ("SATS_MFMA_BASE_GROUP_ONLY", "SATS_NO_MFMA"):
-        os.environ[env] = "1"
-        try:
+    for bp, path in ((SATS_BATCH_SPLIT, SATS_PATH_BATCH_SPLIT), (SATS_BATCH_COMPACT, SATS_PATH_BATCH_COMPACT)):
+        with sats_options(batch_path=bp):
+            assert sats_query_path(n, 256, 1024, 2) == path
             ref = run_gpu(c, ts, c["route_lut"], "bf16")
-        finally:
-            del os.environ[env]
         check_against_oracle(c, ts, c["route_lut"], "bf16", ref)
         if L == 1:  # one layer: same input, so the outputs themselves must agree
             for i in range(n):
@@ -296,8 +346,8 @@ def test_mfma_dense_api_batch():
         assert rel_err(numerics.decode(res["out"][i], "bf16"), ref[i]) <= TOL["bf16"]
 
 
-@pytest.mark.parametrize("n,env", [(20, None), (5, None), (5, "SATS_NO_MFMA")])
-def test_batch_rows_are_permutation_equivariant_bitwise(n, env):
+@pytest.mark.parametrize("n,bp", [(20, 0), (5, 0), (5, SATS_BATCH_COMPACT)])
+def test_batch_rows_are_permutation_equivariant_bitwise(n, bp):
     """Permuting the tokens of a batch permutes the output rows bit for bit:
     a row's sums do not depend on its position in the batch or in the
     dense/sparse partition (MFMA path and compacted path)."""
@@ -305,14 +355,9 @@ def test_batch_rows_are_permutation_equivariant_bitwise(n, env):
     ts = case_thresholds(c, "bf16", seed=39)
     perm = np.random.default_rng(5).permutation(n)
     cp = dict(c, x=c["x"][perm], token_ids=c["token_ids"][perm])
-    if env:
-        os.environ[env] = "1"
-    try:
+    with sats_options(batch_path=bp):
         a = run_gpu(c, ts, c["route_lut"], "bf16", inspect=False)
         b = run_gpu(cp, ts, c["route_lut"], "bf16", inspect=False)
-    finally:
-        if env:
-            del os.environ[env]
     np.testing.assert_array_equal(a["out"][perm], b["out"])
 
 

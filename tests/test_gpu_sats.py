@@ -145,3 +145,13 @@ def test_calibrate_stack_matches_oracle():
     # the GPU's choice is as close to the target as the oracle's (same breakpoints)
     assert abs(S - 0.5) <= abs(s2 - 0.5) + 2e-3
     assert abs(s - S) <= 2e-3
+    # Eq. 7 at the GPU's budget b*: each free layer's threshold is the largest
+    # oracle candidate whose error is within b*, up to the float32 slack of
+    # the GPU's errors (1e-4 relative, as in the curve comparisons above)
+    slack = 1e-4 * b + 1e-7
+    assert b >= 0.0
+    for l in range(L - 1):
+        tsl, errl, spl = c2[l]
+        k = int(np.argmin(np.abs(tsl - ts[l])))
+        assert errl[k] <= b + slack, (l, errl[k], b)
+        assert not np.any(errl[k + 1:] <= b - slack), (l, errl[k + 1:], b)

@@ -242,3 +242,47 @@ def test_pins_catch_planted_mistakes(monkeypatch, mistake):
         except AssertionError:
             caught += 1
     assert caught >= 1, f"no pin caught the planted mistake {mistake}"
+
+
+# ------------------------------------------------------------------ refinement
+
+def _one_layer_refined(s_tar, seed=7, one_sided=False, monkeypatch=None):
+    c = synth.small_case(seed, 1, 16, 64, "f32", 1, w_std=0.25)
+    xcal = synth.activations(907, synth.S_CAL, 96, 16, "f32")
+    if one_sided:  # the mistake: refine only below the coarse choice
+        orig = sats.fine_levels
+        monkeypatch.setattr(sats, "fine_levels",
+                            lambda q, coarse, f: [v for v in orig(q, coarse, f) if v < q - 1e-12])
+    return sats.calibrate(xcal, c["W_gate"], c["W_up_T"], c["W_down"], s_tar, "f32", coarse_step=0.1,
+                          fine_step=0.01, guardrail=False)
+
+
+def test_refinement_spans_both_sides_of_the_coarse_choice(monkeypatch):
+    """Section 3.1 refines the search around the coarse choice.  One layer
+    whose error curve grows with t: S(b) can reach every candidate's
+    sparsity, so b* picks the candidate nearest s_tar.  At s_tar = 0.52 the
+    coarse grid (step 0.1) chooses level 0.5, and the nearest refined level
+    (0.52) lies ABOVE it: a refinement that looks only below the coarse
+    choice cannot get closer than the coarse 0.5."""
+    r = _one_layer_refined(0.52)
+    b1, idx1, s1, c1 = r["coarse"]
+    b2, idx2, s2, c2 = r["fine"]
+    ts, err, sp = c2[0]
+    assert np.all(np.diff(err) >= 0), "precondition: the error grows with the threshold"
+    N = 96 * 64
+    assert abs(s1 - 0.5) <= 2.0 / N                       # the coarse choice: level 0.5
+    assert abs(s2 - 0.52) <= 2.0 / N                      # the refined choice: level 0.52, above it
+    assert ts[idx2[0]] > c1[0][0][idx1[0]]
+    # the candidate nearest the target among all refined ones
+    assert abs(s2 - 0.52) == pytest.approx(np.min(np.abs(sp - 0.52)), abs=1e-15)
+    # and a refinement below the coarse choice only stays at 0.5: the pin catches it
+    bad = _one_layer_refined(0.52, one_sided=True, monkeypatch=monkeypatch)
+    assert abs(bad["fine"][2] - 0.52) > abs(s2 - 0.52) + 0.01
+
+
+def test_coarse_level_of_a_candidate():
+    v = np.abs(np.random.default_rng(3).standard_normal(1000))
+    coarse = [0.25, 0.5, 0.75]
+    assert sats.coarse_level_of(0.0, v, coarse) == 0.0
+    for q in coarse:
+        assert sats.coarse_level_of(float(np.quantile(v, q, method="inverted_cdf")), v, coarse) == q
