@@ -91,6 +91,31 @@ int sats_mlp_forward(const sats_bf16 *x, const int32_t *token_ids,
                      int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
                      hipStream_t stream);
 
+/*
+ * Allocation-free variant of sats_mlp_forward, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, computation and results
+ * as sats_mlp_forward (the same kernels), but the workspace is a fixed device
+ * array of the library, SATS_NOALLOC_SCRATCH_BYTES (16 MiB) on each device
+ * that runs it, held until the process ends, instead of a per-stream
+ * allocation; the call allocates and frees nothing.  That covers single-token
+ * calls at d <= 4096 and d_ff <= 16384 (any number of layers up to 64, bf16)
+ * and small batches; a call whose workspace does not fit returns
+ * SATS_ERR_WORKSPACE before any device work.  Every call on a device shares
+ * that device's array and leaves its last contents there: each call first
+ * clears the array's arrival counters with a small kernel (no memset), and
+ * calls that overlap on one device (other streams or threads) race and must
+ * not be issued.  sats_device_status also reports a bounded wait that gave up
+ * in such a call.
+ */
+#define SATS_NOALLOC_SCRATCH_BYTES (16u << 20)
+int sats_mlp_forward_noalloc(const sats_bf16 *x, const int32_t *token_ids,
+                             const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                             const sats_bf16 *W_down, const float *thresholds,
+                             const uint8_t *route_lut, sats_bf16 *out,
+                             int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
+                             hipStream_t stream);
+
 /* Base path for every token: the unmasked gated MLP of Eq. 1, same layout. */
 int sats_mlp_dense(const sats_bf16 *x, const sats_bf16 *W_gate,
                    const sats_bf16 *W_up_T, const sats_bf16 *W_down,

@@ -12,5 +12,5 @@ from ._lib import (  # noqa: F401
     sats_calibrate_sats, sats_mlp_forward_lora, sats_route_table, SATS_K_ROUTE_ACCUM, SATS_K_LORA_V,
     sats_set_options, options, sats_query_path, SATS_BATCH_AUTO, SATS_BATCH_MFMA, SATS_BATCH_SPLIT,
     SATS_BATCH_COMPACT, SATS_SINGLE_AUTO, SATS_SINGLE_OFF, SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA,
-    SATS_PATH_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT,
+    SATS_PATH_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT, sats_mlp_forward_noalloc,
 )

@@ -37,6 +37,7 @@ _INSPECT = _FWD + [_P] * 4
 SIGNATURES = {
     "sats_mlp_forward": (_FWD, _N),
     "sats_mlp_dense": (_DENSE, _N),
+    "sats_mlp_forward_noalloc": (_FWD, _N),
     "sats_mlp_forward_f32": (_FWD, _N),
     "sats_mlp_dense_f32": (_DENSE, _N),
     "sats_mlp_forward_inspect": (_INSPECT, _N),
@@ -124,6 +125,13 @@ def sats_mlp_forward(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut
                      n_tokens, d, d_ff, n_layers, stream=None):
     name = "sats_mlp_forward_f32" if _is_f32(x) else "sats_mlp_forward"
     _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+          _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers, _stream(stream))
+
+
+def sats_mlp_forward_noalloc(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out,
+                             n_tokens, d, d_ff, n_layers, stream=None):
+    """sats_mlp_forward on the library's fixed scratch array (bf16; allocates nothing)."""
+    _call("sats_mlp_forward_noalloc", _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
           _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers, _stream(stream))
 
 

@@ -329,6 +329,46 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, i
   return ok;
 }
 
+// ------------------------------------------------- allocation-free forward
+
+// Device memory of sats_mlp_forward_noalloc: a fixed array per device (each
+// GPU that runs the library holds its own copy until the process ends),
+// arrival counters in the first kScratchCounterBytes, the workspace after
+// them.  In host code `scratch` is only a stand-in for the symbol: its device
+// address is taken once per device with hipGetSymbolAddress and only that
+// address is passed to kernels and copies.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+constexpr size_t kScratchCounterBytes = (size_t)64 << 10;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+std::map<int, char *> g_scratch;  // device -> device address of its scratch
+
+// The current device's scratch address (taken on the first call on a device).
+int scratch_addr(char **out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = g_scratch.find(dev);
+  if (it == g_scratch.end()) {
+    char *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress((void **)&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(SATS_ERR_HIP, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    it = g_scratch.emplace(dev, p).first;
+  }
+  *out = it->second;
+  return SATS_OK;
+}
+
+// Zeroes counters [0, n) except the device error flag (which keeps a raised
+// error until sats_device_status reads it).  A kernel, not a memset, so that
+// the call can be captured in a HIP graph.
+__global__ void clear_counters_kernel(unsigned *c, int n, int keep) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    if (i != keep) c[i] = 0u;
+}
+
 // --------------------------------------------------------------- the call
 
 struct Call {
@@ -351,6 +391,8 @@ struct Call {
   float lscale;
   // token tok of ntot: the single-token path's offsets into the inspection arrays
   int64_t tok, ntot;
+  // allocation-free call: the workspace is the library's static scratch array
+  bool noalloc;
 };
 
 
@@ -763,8 +805,25 @@ int run(const Call &c) {
   const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, c.L, dp, nullptr, lrank);
   Workspace *ws = nullptr;
   size_t ncount = counter_count(p, pass, dp);
-  int rc = ensure_workspace(c.stream, bytes, ncount, &ws);
-  if (rc) return rc;
+  Workspace fixed{};
+  int rc = 0;
+  if (c.noalloc) {
+    if (bytes > kScratchBytes - kScratchCounterBytes || ncount * sizeof(unsigned) > kScratchCounterBytes)
+      return fail(SATS_ERR_WORKSPACE,
+                  "the call needs %zu bytes of workspace and %zu counters; the allocation-free forward has %zu and %zu",
+                  bytes, ncount, kScratchBytes - kScratchCounterBytes, kScratchCounterBytes / sizeof(unsigned));
+    char *base = nullptr;
+    if ((rc = scratch_addr(&base))) return rc;
+    fixed.counters = reinterpret_cast<unsigned *>(base);
+    fixed.n_counters = kScratchCounterBytes / sizeof(unsigned);
+    fixed.mem = base + kScratchCounterBytes;
+    fixed.bytes = kScratchBytes - kScratchCounterBytes;
+    hipLaunchKernelGGL(clear_counters_kernel, dim3(8), dim3(256), 0, c.stream, fixed.counters, (int)ncount, (int)kErr);
+    HIP_TRY(hipGetLastError());
+    ws = &fixed;
+  } else if ((rc = ensure_workspace(c.stream, bytes, ncount, &ws))) {
+    return rc;
+  }
   Buffers b{};
   layout(ws->mem, p, pass, c.d, c.d_ff, esz, c.L, dp, &b, lrank);
   if (decode) return run_decode<T>(c, dp, b, ws->counters);
@@ -1337,6 +1396,17 @@ int sats_mlp_forward(const sats_bf16 *x, const int32_t *token_ids, const sats_bf
                                  n_tokens, d, d_ff, n_layers, stream, route_mode_of(route_lut)));
 }
 
+int sats_mlp_forward_noalloc(const sats_bf16 *x, const int32_t *token_ids, const sats_bf16 *W_gate,
+                             const sats_bf16 *W_up_T, const sats_bf16 *W_down, const float *thresholds,
+                             const uint8_t *route_lut, sats_bf16 *out, int64_t n_tokens, int64_t d,
+                             int64_t d_ff, int64_t n_layers, hipStream_t stream) {
+  g_err.clear();
+  Call c = make_call(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out, n_tokens, d, d_ff,
+                     n_layers, stream, route_mode_of(route_lut));
+  c.noalloc = true;
+  return run<uint16_t>(c);
+}
+
 int sats_mlp_dense(const sats_bf16 *x, const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
                    const sats_bf16 *W_down, sats_bf16 *out, int64_t n_tokens, int64_t d,
                    int64_t d_ff, int64_t n_layers, hipStream_t stream) {
@@ -1547,16 +1617,29 @@ int sats_device_status(hipStream_t stream) {
   int dev = 0;
   HIP_TRY(hipGetDevice(&dev));
   HIP_TRY(hipStreamSynchronize(stream));
-  std::lock_guard<std::mutex> lk(g_ws_mu);
-  auto it = g_ws.find({dev, stream});
-  if (it == g_ws.end() || !it->second.counters) return SATS_OK;
-  unsigned flag = 0;
-  HIP_TRY(hipMemcpy(&flag, it->second.counters + kErr, sizeof flag, hipMemcpyDeviceToHost));
-  if (flag) {
-    const unsigned zero = 0;
-    HIP_TRY(hipMemcpy(it->second.counters + kErr, &zero, sizeof zero, hipMemcpyHostToDevice));
-    return fail(SATS_ERR_DEVICE, "a bounded device-side wait gave up (results of the affected call are invalid)");
+  // the flags of this stream's workspace and of the device's allocation-free scratch
+  std::vector<unsigned *> flags;
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    auto it = g_ws.find({dev, stream});
+    if (it != g_ws.end() && it->second.counters) flags.push_back(it->second.counters + kErr);
   }
+  {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch.find(dev);
+    if (it != g_scratch.end()) flags.push_back(reinterpret_cast<unsigned *>(it->second) + kErr);
+  }
+  bool raised = false;
+  for (unsigned *f : flags) {
+    unsigned flag = 0;
+    HIP_TRY(hipMemcpy(&flag, f, sizeof flag, hipMemcpyDeviceToHost));
+    if (flag) {
+      const unsigned zero = 0;
+      HIP_TRY(hipMemcpy(f, &zero, sizeof zero, hipMemcpyHostToDevice));
+      raised = true;
+    }
+  }
+  if (raised) return fail(SATS_ERR_DEVICE, "a bounded device-side wait gave up (results of the affected call are invalid)");
   return SATS_OK;
 }
 

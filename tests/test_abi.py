@@ -192,3 +192,11 @@ def test_query_path_rejects_bad_arguments():
     assert lib.sats_query_path(1, 8, 8, 3, 1, 256, ctypes.byref(p)) == _lib.SATS_ERR_ARG
     assert lib.sats_query_path(1, 0, 8, 2, 1, 256, ctypes.byref(p)) == _lib.SATS_ERR_SHAPE
     assert lib.sats_query_path(1, 8, 8, 2, 1, 256, None) == _lib.SATS_ERR_NULL
+
+
+def test_noalloc_rejects_a_call_past_its_scratch_before_device_work():
+    lib = sats.load()
+    rc = lib.sats_mlp_forward_noalloc(FAKE, None, FAKE, FAKE, FAKE, FAKE, None, FAKE * 4096, 64, 4096, 14336, 1,
+                                      None)
+    assert rc == _lib.SATS_ERR_WORKSPACE
+    assert "allocation-free" in sats.sats_last_error()
