@@ -500,7 +500,8 @@ def main():
         return ms, kt
 
     log(f"[bench] timing {args.steps} steps (warmup {args.warmup}), {args.copies} weight copies")
-    kinds = (sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_DEC_GATE, sats.SATS_K_DEC_ROWS)
+    kinds = (sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_DEC_GATE, sats.SATS_K_DEC_ROWS,
+             sats.SATS_K_DEC_REDUCE)
     # headline timing without per-kernel events (recording them costs a few us
     # per launch); per-kernel durations come from an identical second region
     ms, _ = timed(step_fwd)
@@ -529,7 +530,8 @@ def main():
     for name, (kms, c) in kt.items():
         b = {"gate_kernel": gate_bytes, "up_kernel": up_bytes, "down_kernel": up_bytes,
              "dec_gate_kernel": gate_bytes + gate_lora,
-             "dec_rows_kernel": 2 * up_bytes + n * d * esz + rows_lora}[name]
+             "dec_rows_kernel": 2 * up_bytes + rows_lora + (n * d * esz if R else 0),
+             "dec_reduce_kernel": n * d * esz}[name]
         kern[name] = {"avg_us": round(kms * 1e3, 3), "launches": c,
                       "algorithmic_bytes": int(b), "achieved_gbps": round(b / (kms * 1e-3) / 1e9, 1)}
     dom = max(kern, key=lambda k: kern[k]["avg_us"])

@@ -52,6 +52,7 @@ constexpr int kGateThreads = SATS_GATE_THREADS;  // gate launch
 constexpr int kGateBatch = kGateThreads >= 1024 ? 8 : 16;  // 16-byte loads in flight per lane
 constexpr int kDecodeMaxD = 4096;  // h lives in LDS
 constexpr int kDecodeMaxG = 1024;  // rows / reduce workgroups (partials of y)
+constexpr int kRedThreads = 256, kRedCols = 16;  // second reduction stage: threads and columns per workgroup
 
 // Columns of one gate column block (one 16-byte load per lane of a wavefront).
 template <typename T> constexpr int dec_block_cols() { return 64 * Elem<T>::kVec; }
@@ -825,10 +826,13 @@ __device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm, bo
   constexpr int THREADS = kDecodeThreads, NW = kDecodeWaves;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int d = a.d, G = a.G;
-  const int cpw = (d + a.RW - 1) / a.RW;  // columns of this workgroup (<= THREADS)
+  const int cpw = (d + a.RW - 1) / a.RW;  // columns of this workgroup (<= THREADS / ngr: the plan)
   const int cw0 = w * cpw;
   const int nc = max(0, min(cpw, d - cw0));
-  const int ngr = THREADS / cpw;    // partial groups
+  // partial groups: every 16th partial in workgroup order, the groups added
+  // in order -- the order of dec_reduce_kernel, so that a call with adapters
+  // at scale 0 gives the plain call's bits
+  constexpr int ngr = kRedThreads / kRedCols;
   const int c = tid % cpw, gr = tid / cpw;
   float s = 0.0f;
   if (c < nc && gr < ngr && gr < G)
@@ -914,12 +918,14 @@ __global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, in
   if (l == 0) SATS_TRACE_POINT(2);
 }
 
-// Rows: G workgroups, then the second reduction stage: the last RW of them
-// to finish each sum one slice of y over every partial (workgroup order).
-// They wait only for workgroups that are running or done, with nothing of
-// their own in flight; the wait is bounded (it raises the device error
-// flag instead of hanging).  The count goes back to zero at the start of the
-// next gate launch (which always comes before the next rows launch).
+// Rows: G workgroups, each writing its partial y.  Without adapters the
+// second reduction stage is a launch of its own (dec_reduce_kernel).  With
+// adapters it follows in this launch: the last RW workgroups to finish each
+// sum one slice of y (and add s z B_down) over every partial (workgroup
+// order).  They wait only for workgroups that are running or done, with
+// nothing of their own in flight; the wait is bounded (it raises the device
+// error flag instead of hanging).  The count goes back to zero at the start
+// of the next gate launch (which always comes before the next rows launch).
 constexpr int kSpinLimit = 1 << 20;  // polls of one wait (each a device-coherent load)
 
 template <typename T, bool LORA>
@@ -929,6 +935,7 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, 
   if (l == 0) SATS_TRACE_POINT(3);
   const int base = a.state[0];
   dec_rows<T, LORA>(a, l, base, a.G, blockIdx.x, sm, lr);
+  if constexpr (!LORA) return;  // the second stage is dec_reduce_kernel
   const int tid = threadIdx.x, G = a.G;
   __builtin_amdgcn_s_waitcnt(0);  // this thread's partial-y stores have completed
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -954,5 +961,36 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, 
   if (l == 0) SATS_TRACE_POINT(7);
 }
 
+
+// Second reduction stage of a layer without adapters, a launch of its own
+// (the kernel boundary orders it after every partial; a hand-off inside the
+// rows launch -- last arrivals counted, the reducers waiting for the count --
+// measured 2 us slower per layer, its stores and polls queued behind the
+// other workgroups' row loads).  Workgroup w owns columns [16 w, 16 w + 16):
+// 16 groups of threads each add every 16th partial in workgroup order, the
+// groups are added in order, and y (or the rounded output on the last layer)
+// and the slice's sum of squares for the next layer's input are written.
+template <typename T>
+__global__ __launch_bounds__(kRedThreads) void dec_reduce_kernel(DecodeArgs a, int l) {
+  constexpr int NG = kRedThreads / kRedCols;
+  __shared__ float red[kRedThreads];
+  const int tid = threadIdx.x, c = tid % kRedCols, g = tid / kRedCols;
+  const int d = a.d, G = a.G, col = blockIdx.x * kRedCols + c;
+  float s = 0.0f;
+  if (col < d && g < G) s = sum_coherent(a.ypart + (size_t)g * d + col, (size_t)NG * d, (G - g + NG - 1) / NG);
+  red[tid] = s;
+  __syncthreads();
+  if (tid < 64) {
+    const bool on = tid < kRedCols && blockIdx.x * kRedCols + tid < d;
+    float y = 0.0f;
+    if (on) {
+      for (int q = 0; q < NG && q < G; ++q) y += red[q * kRedCols + tid];
+      if (l == a.L - 1) static_cast<T *>(a.out)[blockIdx.x * kRedCols + tid] = Elem<T>::round(y);
+      else store_coherent(a.ybuf + blockIdx.x * kRedCols + tid, y);
+    }
+    const float sq = wave_sum(on ? y * y : 0.0f);  // the slice's sum of squares, fixed order
+    if (tid == 0 && l < a.L - 1) store_coherent(a.sspart + blockIdx.x, sq);
+  }
+}
 
 }  // namespace sats

@@ -311,19 +311,23 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, i
   const int64_t tiles = g_opt.dec_gate_tiles > 0 ? g_opt.dec_gate_tiles : 256;
   int64_t nrc = std::max<int64_t>(1, tiles / q.nblk);
   nrc = std::min<int64_t>(nrc, std::max<int64_t>(1, d / (sats::kGateThreads / 64)));  // a row per wavefront
-  (void)lora_rank;
   q.nrc = (int)nrc;
   q.gate_grid = q.nblk * q.nrc;
-  // second reduction stage: the last RW rows workgroups to finish take one
-  // slice of y each, 32 columns (128 bytes of each partial) or more; RW is
-  // kept to a quarter of the CUs so that the reducers, which wait for the
-  // others, never fill the device
-  q.RW = (int)std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32), std::max(1, (cus >= 0 ? cus : device_cus()) / 4));
-  q.RW = std::min(q.RW, G);
+  // second reduction stage: without adapters a launch of 16-column slices;
+  // with adapters the last RW rows workgroups to finish take one slice of y
+  // each, 32 columns (128 bytes of each partial) or more, RW kept to a
+  // quarter of the CUs so that the reducers, which wait for the others,
+  // never fill the device
+  // (and at most 64 columns each: 16 groups of partials per column)
+  q.RW = lora_rank > 0 ? (int)std::max<int64_t>((d + 63) / 64,
+                                                std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32),
+                                                                  std::max(1, (cus >= 0 ? cus : device_cus()) / 4)))
+                       : (int)((d + sats::kRedCols - 1) / sats::kRedCols);
+  if (lora_rank > 0) q.RW = std::min(q.RW, G);
   // buffer descriptors address one layer's matrix with 32-bit offsets, and
   // 0x80000000 is the offset that reads zeros: every matrix must stay below 2 GB
   const bool ok = G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
-                  (d + q.RW - 1) / q.RW <= sats::kDecodeThreads &&
+                  (d + q.RW - 1) / q.RW <= sats::kDecodeThreads / (sats::kRedThreads / sats::kRedCols) &&
                   (uint64_t)d * (uint64_t)d_ff * (uint64_t)esz < (1ull << 31);
   *dp = ok ? q : DecodePlan{};
   return ok;
@@ -693,6 +697,12 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
                               tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
+    if (!c.Ag) {
+      TimedLaunch tl(SATS_K_DEC_REDUCE, c.stream);
+      hipExtLaunchKernelGGL(dec_reduce_kernel<T>, dim3(dp.RW), dim3(kRedThreads), 0, c.stream, tl.start, tl.stop, 0,
+                            a, l);
+      HIP_TRY(hipGetLastError());
+    }
   }
   if (lists) {
     for (int64_t l = 0; l < c.L; ++l) {
@@ -1700,6 +1710,7 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_LORA_V: return "lora_v_kernel";
     case SATS_K_DEC_GATE: return "dec_gate_kernel";
     case SATS_K_DEC_ROWS: return "dec_rows_kernel";
+    case SATS_K_DEC_REDUCE: return "dec_reduce_kernel";
     case SATS_K_CAL_ERR: return "cal_err_kernel";
     case SATS_K_CAL_GATEUP: return "dense_gateup_kernel (calibration)";
     default: return "";
