@@ -79,7 +79,6 @@ def counter_traffic(kernel, workload_tag):
     the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_tag}_counters.txt")
-    src = os.path.join(ROOT, "paper_2607_08991_amd", "csrc", "decode.hpp")
     if not os.path.exists(path):
         return None
     fields = {}
@@ -88,6 +87,9 @@ def counter_traffic(kernel, workload_tag):
             k, sep, v = line.partition(":")
             if sep:
                 fields[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_2607_08991_amd", "csrc", fields.get("kernel_source", "decode.hpp"))
+    if not os.path.exists(src):
+        return None
     with open(src, "rb") as f:
         now = hashlib.sha256(f.read()).hexdigest()
     if fields.get("kernel_source_sha256") != now or "traffic_bytes_per_launch" not in fields:
@@ -127,6 +129,28 @@ def cpu_baseline(cfg, weights_np, ts, x_np, n_sample, adapters=None, scale=0.0):
                       f"BLAS {blas}"}
 
 
+def cpu_baseline_stack(cfg, Wnp, ts, lut, x_np, ids_np):
+    """The CPU oracle, as it is, on a sample of decode tokens through every
+    layer of a stack: route, then layer by layer (each layer's stored
+    weights decoded once for the sample), the glue between layers."""
+    from oracle import mlp, numerics  # test infrastructure: only this leg of the benchmark uses it
+    cores = len(os.sched_getaffinity(0))
+    n = len(x_np)
+    t0 = time.perf_counter()
+    r = mlp.route(ids_np, lut)
+    hs = [numerics.decode(x_np[i], cfg.dtype) for i in range(n)]
+    for l in range(cfg.n_layers):
+        wg, wu, wd = (numerics.decode(w[l], cfg.dtype) for w in Wnp)
+        for i in range(n):
+            y = mlp.layer(hs[i], wg, wu, wd, float(ts[l]), bool(r[i]))[0]
+            hs[i] = mlp.glue(y, cfg.dtype) if l < cfg.n_layers - 1 else numerics.rho(y, cfg.dtype)
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 4), "unit": "tok/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n} decode tokens of the workload ({int(r.sum())} base-routed) through all "
+                      f"{cfg.n_layers} layers of the float64 numpy oracle, each layer's weights decoded once "
+                      f"for the sample; {dt:.1f} s on a host with {cores} cores"}
+
+
 def bench_stack(args, cfg):
     """A 32/36-layer workload: one step = one call on one decode batch through every layer."""
     import torch
@@ -140,9 +164,11 @@ def bench_stack(args, cfg):
     d, d_ff, L, esz = cfg.d, cfg.d_ff, cfg.n_layers, cfg.elem_bytes
     log(f"[bench] generating {cfg.name} weights ({L} layers)")
     W = []
-    for w in synth.stack_weights(cfg.seed, L, d, d_ff, cfg.dtype):
+    Wnp = synth.stack_weights(cfg.seed, L, d, d_ff, cfg.dtype)
+    for w in Wnp:
         W.append(torch.from_numpy(w.view(np.int16)).view(torch.bfloat16).to(dev))
-        del w
+    if args.no_cpu:
+        del Wnp
     slots = max(1, args.tokens // batch)
     X = torch.from_numpy(synth.decode_x(cfg, slots * batch, idx=batch).view(np.int16)).view(
         torch.bfloat16).to(dev).view(slots, batch, d)
@@ -194,10 +220,12 @@ def bench_stack(args, cfg):
         else:
             forward(k, lora)
 
-    def timed(dense=False, lora=bool(R), steps=args.steps, warmup=args.warmup):
+    def timed(dense=False, lora=bool(R), steps=args.steps, warmup=args.warmup, kinds=()):
         for s in range(warmup):
             step(s, dense, lora)
         torch.cuda.synchronize()
+        for k in kinds:
+            sats.sats_timing_begin(k, steps * L * ((batch + 63) // 64))
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for s in range(steps):
@@ -205,9 +233,19 @@ def bench_stack(args, cfg):
         e1.record(stream)
         torch.cuda.synchronize()
         sats.sats_device_status(stream)  # raises if a bounded device-side wait gave up: the timing is void
+        if kinds:
+            kt = {}
+            for k in kinds:
+                tot, c = sats.sats_timing_end(k)
+                if c:
+                    kt[sats.sats_kernel_name(k)] = (tot / c, c / steps)
+            return e0.elapsed_time(e1) / steps, kt
         return e0.elapsed_time(e1) / steps
 
     ms = timed()
+    kinds = (sats.SATS_K_DEC_GATE, sats.SATS_K_DEC_ROWS, sats.SATS_K_DEC_REDUCE, sats.SATS_K_DENSE,
+             sats.SATS_K_DENSE_DOWN, sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_LORA_V)
+    ms_ev, kt = timed(kinds=kinds)
     dense_ms = None if args.no_dense else timed(True)
     lora_res = None
     if R:
@@ -227,6 +265,29 @@ def bench_stack(args, cfg):
             L * (2 * d * R + R * d_ff + R * d) * esz + 2 * R * esz * union[sl].sum(axis=1).mean()
     sparse_mask = routes[sl] == 0
     sp = 1.0 - (kept[sl].transpose(0, 2, 1)[sparse_mask].mean() / d_ff) if sparse_mask.any() else None
+    # each layer's realized sparsity over the sparse-routed tokens of the timed steps
+    sp_layer = ([round(float(1.0 - kept[sl].transpose(0, 2, 1)[sparse_mask][:, l].mean() / d_ff), 4)
+                 for l in range(L)] if sparse_mask.any() else None)
+    # per-kernel algorithmic bytes of one launch, averaged over the timed launches
+    rows_mean = float(kept[sl].mean())  # kept rows of a token (all d_ff for a base-routed one)
+    per_launch = {"dec_gate_kernel": d * d_ff * esz + d * esz, "dec_rows_kernel": 2 * d * esz * rows_mean,
+                  "dec_reduce_kernel": d * esz, "dense_gateup_kernel": 2 * d * d_ff * esz,
+                  "dense_down_kernel": d * d_ff * esz}
+    kern = {}
+    for name, (kms, per_step) in kt.items():
+        b = per_launch.get(name)
+        kern[name] = {"avg_us": round(kms * 1e3, 3), "launches_per_step": round(per_step, 3),
+                      "algorithmic_bytes_per_launch": None if b is None else int(b),
+                      "achieved_gbps": None if b is None else round(b / (kms * 1e-3) / 1e9, 1)}
+    dom = max((k for k in kern if kern[k]["achieved_gbps"] is not None),
+              key=lambda k: kern[k]["avg_us"] * kern[k]["launches_per_step"])
+    cpu = None
+    if not args.no_cpu:
+        ns = min(8, slots * batch)
+        log(f"[bench] timing the CPU oracle on {ns} tokens through {L} layers")
+        cpu = cpu_baseline_stack(cfg, Wnp, ts, lut, X.view(-1, d)[:ns].view(torch.int16).cpu().numpy().view(np.uint16),
+                                 ids.view(-1)[:ns].cpu().numpy())
+        del Wnp
     res = {
         "metric": METRIC, "value": round(batch * 1e3 / ms, 2), "unit": "tok/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
@@ -240,8 +301,15 @@ def bench_stack(args, cfg):
         "hbm_frac_algorithmic": round(alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "realized_sparsity_sparse_tokens": None if sp is None else round(float(sp), 4),
         "realized_base_routed_fraction": round(float(routes[sl].mean()), 4),
+        "realized_sparsity_per_layer": sp_layer,
         "dense_ms_per_step": None if dense_ms is None else round(dense_ms, 5),
         "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 4),
+        "ms_per_step_with_kernel_events": round(ms_ev, 5),
+        "kernels": kern,
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": kern[dom]["achieved_gbps"], "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(kern[dom]["achieved_gbps"] / HBM_PEAK_GBPS, 4),
+                     "traffic": counter_traffic(dom, f"{cfg.name}_b{batch}")},
+        "cpu_baseline": cpu,
     }
     if lora_res:
         res["lora"] = lora_res

@@ -357,7 +357,8 @@ const char *sats_last_error(void);
  */
 enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_DENSE = 4,
        SATS_K_DEC_GATE = 5, SATS_K_DEC_ROWS = 6, SATS_K_CAL_ERR = 7, SATS_K_CAL_GATEUP = 8,
-       SATS_K_ROUTE_ACCUM = 9, SATS_K_LORA_V = 10, SATS_K_DEC_REDUCE = 11, SATS_K_COUNT = 12 };
+       SATS_K_ROUTE_ACCUM = 9, SATS_K_LORA_V = 10, SATS_K_DEC_REDUCE = 11, SATS_K_DENSE_DOWN = 12,
+       SATS_K_COUNT = 13 };
 int sats_timing_begin(int kind, int capacity);
 int sats_timing_end(int kind, double *total_ms, int64_t *count);
 const char *sats_kernel_name(int kind);

@@ -20,6 +20,7 @@ SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DENSE = 0, 1, 2, 3, 
 SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, SATS_K_ROUTE_ACCUM = 5, 6, 7, 8, 9
 SATS_K_LORA_V = 10
 SATS_K_DEC_REDUCE = 11
+SATS_K_DENSE_DOWN = 12
 SATS_BATCH_AUTO, SATS_BATCH_MFMA, SATS_BATCH_SPLIT, SATS_BATCH_COMPACT = 0, 1, 2, 3
 SATS_SINGLE_AUTO, SATS_SINGLE_OFF = 0, 1
 SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA, SATS_PATH_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT = 1, 2, 3, 4

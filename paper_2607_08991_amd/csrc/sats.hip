@@ -499,7 +499,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       const int ks = dense_ksplit(d, d_ff);
       dd.kchunk = (int)(((d_ff + ks - 1) / ks + kDenseKC - 1) / kDenseKC * kDenseKC);
       {
-        TimedLaunch tl(SATS_K_DENSE, c.stream);
+        TimedLaunch tl(SATS_K_DENSE_DOWN, c.stream);
         hipExtLaunchKernelGGL(dense_down_fn(np), dim3(d / kDenseDownNT, ks), dim3(kDenseThreads), 0, c.stream,
                               tl.start, tl.stop, 0, dd);
       }
@@ -1705,7 +1705,8 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_UP: return "up_kernel";
     case SATS_K_DOWN: return "down_kernel";
     case SATS_K_INSPECT: return "compact_kernel";
-    case SATS_K_DENSE: return "dense_mfma_kernels";
+    case SATS_K_DENSE: return "dense_gateup_kernel";
+    case SATS_K_DENSE_DOWN: return "dense_down_kernel";
     case SATS_K_ROUTE_ACCUM: return "route_accum_kernel";
     case SATS_K_LORA_V: return "lora_v_kernel";
     case SATS_K_DEC_GATE: return "dec_gate_kernel";
