@@ -55,6 +55,8 @@ def parse():
     p.add_argument("--lora-rank", type=int, default=0,
                    help="single-layer workloads: run the LoRA-aware sparse path with adapters of this rank")
     p.add_argument("--lora-scale", type=float, default=2.0)
+    p.add_argument("--batch-path", default="auto", choices=["auto", "mfma", "split", "compact"],
+                   help="kernels of batched calls (sats_set_options batch_path)")
     p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of this many MiB (counter calibration)")
     return p.parse_args()
@@ -213,8 +215,10 @@ def bench_stack(args, cfg):
     routes = np.array(routes)
     kept = np.array(kept, dtype=np.float64)  # [slots][L][batch]
 
+    sel = None  # timed slots (default: all of them, in turn)
+
     def step(s, dense=False, lora=bool(R)):
-        k = s % slots
+        k = s % slots if sel is None else sel[s % len(sel)]
         if dense:
             sats.sats_mlp_dense(X[k], *W, out[k], batch, d, d_ff, L, stream)
         else:
@@ -243,6 +247,17 @@ def bench_stack(args, cfg):
         return e0.elapsed_time(e1) / steps
 
     ms = timed()
+    # batches whose every token takes the sparse path: timed on their own, against the dense path
+    all_sparse = None
+    if batch > 1 and not args.no_dense:
+        sparse_slots = [k for k in range(slots) if not routes[k].any()]
+        if sparse_slots:
+            sel = sparse_slots
+            a_ms, a_dense = timed(), timed(True)
+            sel = None
+            all_sparse = {"slots": len(sparse_slots), "of_slots": slots, "ms_per_step": round(a_ms, 5),
+                          "dense_ms_per_step": round(a_dense, 5), "speedup_vs_dense": round(a_dense / a_ms, 4),
+                          "union_fraction_per_layer_mean": round(float(union[sparse_slots].mean() / d_ff), 4)}
     kinds = (sats.SATS_K_DEC_GATE, sats.SATS_K_DEC_ROWS, sats.SATS_K_DEC_REDUCE, sats.SATS_K_DENSE,
              sats.SATS_K_DENSE_DOWN, sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_LORA_V)
     ms_ev, kt = timed(kinds=kinds)
@@ -294,7 +309,7 @@ def bench_stack(args, cfg):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype,
         "data": "synthetic",
         "config": {"workload": cfg.name + (f", LoRA rank {R} on the sparse path" if R else ""),
-                   "d": d, "d_ff": d_ff, "n_layers": L, "decode_batch": batch,
+                   "d": d, "d_ff": d_ff, "n_layers": L, "decode_batch": batch, "batch_path": args.batch_path,
                    "route": "route_lut", "base_routed_ids": cfg.n_dense_ids, "vocab": cfg.vocab},
         "algorithmic_bytes_per_step": int(alg),
         "hbm_gbps_algorithmic": round(alg / (ms * 1e-3) / 1e9, 1),
@@ -302,6 +317,7 @@ def bench_stack(args, cfg):
         "realized_sparsity_sparse_tokens": None if sp is None else round(float(sp), 4),
         "realized_base_routed_fraction": round(float(routes[sl].mean()), 4),
         "realized_sparsity_per_layer": sp_layer,
+        "all_sparse_steps": all_sparse,
         "dense_ms_per_step": None if dense_ms is None else round(dense_ms, 5),
         "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms, 4),
         "ms_per_step_with_kernel_events": round(ms_ev, 5),
@@ -472,6 +488,8 @@ def main():
     from workloads import get_config, synth
 
     sats.load()
+    sats.sats_set_options(batch_path={"auto": sats.SATS_BATCH_AUTO, "mfma": sats.SATS_BATCH_MFMA,
+                                      "split": sats.SATS_BATCH_SPLIT, "compact": sats.SATS_BATCH_COMPACT}[args.batch_path])
     if args.workload == "sats-calib":
         return bench_calib(args)
     if args.workload == "route-lut":

@@ -118,6 +118,9 @@ struct DenseArgs {
   const uint16_t *Wb;     // W_gate [K][N] or W_down [K][N] (output dim contiguous)
   const uint16_t *Wt;     // W_up_T [N][K] (gate/up only)
   uint16_t *P;            // gate/up output p, [n_dense][N] bf16
+  uint8_t *uflag;         // gate/up: [N] 1 where some row keeps the column (the union of the
+                          // keep sets; every column once a base-path row is in the group);
+                          // down: the same flags of its K rows, rows without one are not read
   float *part;            // down output partials, [KSPLIT][n_dense][N]
   int K, N, kchunk;       // reduction length, output columns, k per split (down)
   float *cal_g;           // calibration (gate/up): g = SiLU(a) in float32, [rows][N] (P unused) ...
@@ -400,6 +403,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   }
   if (mat == 1) {
     const float thr = a.thr ? *a.thr : 0.0f;
+    bool any = false;  // some row of the group keeps column c
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -409,9 +413,15 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
           const float gv = xs[m * kDenseXP + c];
           const bool keep = a.gbase[m] || fabsf(gv) >= thr;  // Eq. 4-5; every column on the base path
           pt[m * 64 + c] = keep ? f32_to_bf16(gv * acc[mt][r]) : (uint16_t)0;
+          any = any || keep;
           if (a.keep_out) a.keep_out[(size_t)a.perm[m] * N + n0 + c] = (uint8_t)keep;
         }
       }
+    // the four lanes of column c (g = 0..3) hold its rows; lane g = 0 publishes the union flag
+    int u = any ? 1 : 0;
+    u |= __shfl_xor(u, 16, 64);
+    u |= __shfl_xor(u, 32, 64);
+    if (a.uflag && g == 0) a.uflag[n0 + c] = (uint8_t)u;
   }
   __syncthreads();
   const int lr = threadIdx.x >> 3, lq = threadIdx.x & 7;
@@ -441,10 +451,21 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
 // partial y over k chunk blockIdx.y for 128 output columns (blockIdx.x);
 // wavefront w takes columns 16 w .. 16 w + 15.  A stage holds 64 W_down
 // rows of 256 bytes (16 KB) and the matching 64 entries of p rows (8 KB).
+//
+// Rows of W_down that no row of the group keeps (their p column is zero for
+// every row: the union of the keep sets excludes them) are not read: their
+// loads take the offset past the buffer, which writes zeros to LDS without a
+// memory access.  Each lane holds the union flags of its two rows in every
+// stage of the chunk as a bit mask (up to kDownFlagStages stages; longer
+// chunks read every row).  With a base-path row in the group every flag is
+// set and every row is read.
+constexpr int kDownFlagStages = 32;
+
 template <int MT>
 __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
       rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t sflag[kDownFlagStages * kDenseKC];
   if (!a.ctl[1]) return;
   const int nd = min(a.ctl[0], 16 * MT);
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -464,6 +485,19 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   const uint32_t oh = (uint32_t)(((size_t)hr * K + kb + 8 * row_pos(hr, hp)) * 2);
   const bool hv = hr < nd;
   const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;
+  // bit 2 s (2 s + 1): row wr (wr + 4) of stage s is in the union of the keep
+  // sets (the chunk's flags go through LDS: one 4-byte load per thread)
+  uint64_t fl = ~0ull;
+  if (a.uflag && S <= kDownFlagStages) {
+    const int t = threadIdx.x;
+    if (4 * t < S * kDenseKC) *reinterpret_cast<uint32_t *>(sflag + 4 * t) = *reinterpret_cast<const uint32_t *>(a.uflag + kb + 4 * t);
+    __syncthreads();
+    fl = 0ull;
+    for (int s = 0; s < S; ++s) {
+      fl |= (uint64_t)(sflag[kDenseKC * s + wr] != 0) << (2 * s);
+      fl |= (uint64_t)(sflag[kDenseKC * s + wr + 4] != 0) << (2 * s + 1);
+    }
+  }
   f32x4v acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4v{0.f, 0.f, 0.f, 0.f};
@@ -471,8 +505,10 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   {                                                                                          \
     const bool v_ = (SN) < S;                                                                \
     const uint32_t ss_ = (uint32_t)(SN);                                                     \
-    dma16<2>(rsw, (BUF) + w * 2048, dense_off(v_, ow0 + ss_ * sw, 0));                       \
-    dma16<2>(rsw, (BUF) + w * 2048 + 1024, dense_off(v_, ow1 + ss_ * sw, 1));                \
+    const bool f0_ = v_ && ((fl >> (2 * ((SN) & 31))) & 1ull);                              \
+    const bool f1_ = v_ && ((fl >> (2 * ((SN) & 31) + 1)) & 1ull);                          \
+    dma16<2>(rsw, (BUF) + w * 2048, dense_off(f0_, ow0 + ss_ * sw, 0));                      \
+    dma16<2>(rsw, (BUF) + w * 2048 + 1024, dense_off(f1_, ow1 + ss_ * sw, 1));               \
     dma16<0>(rsh, (BUF) + 16384 + w * 1024, dense_off(v_ && hv, oh + ss_ * sk, 2));          \
   }
 #define SATS_DN_COMPUTE(BUF)                                                                 \

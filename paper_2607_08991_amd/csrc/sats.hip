@@ -170,6 +170,7 @@ struct Buffers {
   int *perm, *ctl;        // batched path: token partition and dense-group control words
   uint8_t *skip, *gbase;
   uint16_t *xd, *hnext, *pdense;  // dense group (MFMA): inputs, next inputs, p
+  uint8_t *uflag;                  // dense group: union of the keep sets per column
   float *ddpart;                   // dense group down-projection partials
   float *blv, *blvpart, *blzpart;  // batched LoRA: s (h A) per group row, its chunk partials, z per column tile
 };
@@ -212,6 +213,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.xd = c.take<uint16_t>(Pp * d);
   t.hnext = c.take<uint16_t>(Pp * d);
   t.pdense = c.take<uint16_t>(Pp * d_ff);
+  t.uflag = c.take<uint8_t>(d_ff);
   t.ddpart = c.take<float>((int64_t)sats::kDenseMaxKsplit * Pp * d);
   t.dgpart = c.take<float>((int64_t)sats::dec_nrcp(dp.nrc) * d_ff);
   t.dvpart = c.take<float>((int64_t)dp.nrc * sats::kLoraMaxRank);
@@ -449,6 +451,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       da.perm = b.perm;
       da.thr = c.thr ? c.thr + l : nullptr;
       da.keep_out = inspect_lists ? b.keep : nullptr;
+      da.uflag = b.uflag;
       da.H = (l == 0) ? b.xd : b.hnext;
       da.Wb = static_cast<const uint16_t *>(c.Wg) + l * wl;
       da.Wt = static_cast<const uint16_t *>(c.Wu) + l * wl;
@@ -494,6 +497,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       dd.H = b.pdense;
       dd.Wb = static_cast<const uint16_t *>(c.Wd) + l * wl;
       dd.part = b.ddpart;
+      dd.uflag = b.uflag;
       dd.K = (int)d_ff;
       dd.N = (int)d;
       const int ks = dense_ksplit(d, d_ff);
