@@ -74,6 +74,7 @@ struct DecodeArgs {
   float *ybuf;            // [d]
   float *sspart;          // [RW]           per-reduce-workgroup sums of y^2
   int G, RW;              // rows workgroups (partials of y), reduce workgroups
+  int nss;                // slice sums of squares of y per layer: one per 16 columns
   int *state;             // [1] the token's route (1: base path), set by the layer-0 gate launch
   unsigned *done;         // [1] rows workgroups whose partial y is written (cleared by the gate launch)
   unsigned *err;          // device error flag (a bounded wait gave up)
@@ -203,7 +204,7 @@ struct InputRegs {
 
 template <typename T, int THREADS>
 __device__ __forceinline__ void dec_input_issue(const DecodeArgs &a, int l, InputRegs<THREADS> &r) {
-  const int G = a.RW;  // slice sums of squares of the previous layer's reduce
+  const int G = a.nss;  // slice sums of squares of the previous layer's reduce
   constexpr int VEC = Elem<T>::kVec;
   const int tid = threadIdx.x, d = a.d;
   // every field gets a value on both branches: finish() passes all of them
@@ -888,15 +889,15 @@ __device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm, bo
     if (l == a.L - 1) static_cast<T *>(a.out)[cw0 + tid] = Elem<T>::round(y);
     else store_coherent(a.ybuf + cw0 + tid, y);
   }
-  float sq = (tid < nc) ? y * y : 0.0f;  // slice sum of squares, fixed order
-  sq = wave_sum(sq);
-  if (lane == 0) sm.scal[wv] = sq;
-  __syncthreads();
-  if (tid == 0 && l < a.L - 1) {
-    float tot = 0.0f;
-    for (int i = 0; i < NW; ++i) tot += sm.scal[i];
-    store_coherent(a.sspart + w, tot);
+  // sums of squares per 16 columns (the slices of dec_reduce_kernel, added in
+  // its order: the cpw <= 64 columns sit in wavefront 0, 16 lanes a slice)
+  if (wv == 0 && l < a.L - 1) {
+    float sq = (tid < nc) ? y * y : 0.0f;
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) sq += __shfl_xor(sq, m, 64);
+    if ((lane & 15) == 0 && lane < nc) store_coherent(a.sspart + (cw0 + lane) / kRedCols, sq);
   }
+  (void)NW;
 }
 
 // ------------------------------------------------------------------ kernels

@@ -205,7 +205,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.blk_mask = c.take<uint32_t>(tiles * d_ff);
   t.keep = c.take<uint8_t>(std::max(Pp, L) * d_ff);
   t.ypart = c.take<float>((int64_t)dp.G * d);
-  t.sspart = c.take<float>(std::max(dp.G, dp.RW));
+  t.sspart = c.take<float>(std::max<int64_t>(std::max(dp.G, dp.RW), (d + sats::kRedCols - 1) / sats::kRedCols));
   t.perm = c.take<int>(Pp);
   t.ctl = c.take<int>(64);
   t.skip = c.take<uint8_t>(Pp);
@@ -320,12 +320,17 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, i
   // each, 32 columns (128 bytes of each partial) or more, RW kept to a
   // quarter of the CUs so that the reducers, which wait for the others,
   // never fill the device
-  // (and at most 64 columns each: 16 groups of partials per column)
-  q.RW = lora_rank > 0 ? (int)std::max<int64_t>((d + 63) / 64,
-                                                std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32),
-                                                                  std::max(1, (cus >= 0 ? cus : device_cus()) / 4)))
-                       : (int)((d + sats::kRedCols - 1) / sats::kRedCols);
-  if (lora_rank > 0) q.RW = std::min(q.RW, G);
+  // (and at most 64 columns each, a whole number of 16-column slices:
+  // 16 groups of partials per column, sums of squares per 16 columns)
+  if (lora_rank > 0) {
+    const int64_t rw0 = std::min<int64_t>(G, std::max<int64_t>((d + 63) / 64,
+                                                               std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32),
+                                                                                 std::max(1, (cus >= 0 ? cus : device_cus()) / 4))));
+    const int64_t cpw = (((d + rw0 - 1) / rw0 + sats::kRedCols - 1) / sats::kRedCols) * sats::kRedCols;
+    q.RW = (int)((d + cpw - 1) / cpw);
+  } else {
+    q.RW = (int)((d + sats::kRedCols - 1) / sats::kRedCols);
+  }
   // buffer descriptors address one layer's matrix with 32-bit offsets, and
   // 0x80000000 is the offset that reads zeros: every matrix must stay below 2 GB
   const bool ok = G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
@@ -660,6 +665,7 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   a.RW = dp.RW;
   a.ypart = b.ypart;
   a.done = counters + kDone;
+  a.nss = (int)((c.d + kRedCols - 1) / kRedCols);
   a.err = counters + kErr;
   a.ybuf = b.ybuf;
   a.sspart = b.sspart;
