@@ -169,6 +169,7 @@ def bench_stack(args, cfg):
     Wnp = synth.stack_weights(cfg.seed, L, d, d_ff, cfg.dtype)
     for w in Wnp:
         W.append(torch.from_numpy(w.view(np.int16)).view(torch.bfloat16).to(dev))
+    W[0] = W[0].transpose(-1, -2).contiguous()  # the library takes W_gate one row per neuron
     if args.no_cpu:
         del Wnp
     slots = max(1, args.tokens // batch)
@@ -258,8 +259,9 @@ def bench_stack(args, cfg):
             all_sparse = {"slots": len(sparse_slots), "of_slots": slots, "ms_per_step": round(a_ms, 5),
                           "dense_ms_per_step": round(a_dense, 5), "speedup_vs_dense": round(a_dense / a_ms, 4),
                           "union_fraction_per_layer_mean": round(float(union[sparse_slots].mean() / d_ff), 4)}
-    kinds = (sats.SATS_K_DEC_GATE, sats.SATS_K_DEC_ROWS, sats.SATS_K_DEC_REDUCE, sats.SATS_K_DENSE,
-             sats.SATS_K_DENSE_DOWN, sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_LORA_V)
+    kinds = (sats.SATS_K_DEC_LAYER, sats.SATS_K_DEC_REDUCE, sats.SATS_K_DEC_LORA_V, sats.SATS_K_DEC_REDUCE_LORA,
+             sats.SATS_K_DENSE, sats.SATS_K_DENSE_DOWN, sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN,
+             sats.SATS_K_LORA_V)
     ms_ev, kt = timed(kinds=kinds)
     dense_ms = None if args.no_dense else timed(True)
     lora_res = None
@@ -285,7 +287,7 @@ def bench_stack(args, cfg):
                  for l in range(L)] if sparse_mask.any() else None)
     # per-kernel algorithmic bytes of one launch, averaged over the timed launches
     rows_mean = float(kept[sl].mean())  # kept rows of a token (all d_ff for a base-routed one)
-    per_launch = {"dec_gate_kernel": d * d_ff * esz + d * esz, "dec_rows_kernel": 2 * d * esz * rows_mean,
+    per_launch = {"dec_layer_kernel": d * d_ff * esz + d * esz + 2 * d * esz * rows_mean,
                   "dec_reduce_kernel": d * esz, "dense_gateup_kernel": 2 * d * d_ff * esz,
                   "dense_down_kernel": d * d_ff * esz}
     kern = {}
@@ -351,6 +353,7 @@ def bench_calib(args):
     log(f"[bench] generating {cfg.name} weights and {n} calibration rows")
     wnp = synth.layer_weights(cfg.seed, 0, d, d_ff, cfg.dtype)
     W = [torch.from_numpy(w.view(np.int16)).view(torch.bfloat16).to(dev) for w in wnp]
+    W[0] = W[0].t().contiguous()  # the library takes W_gate one row per neuron
     xnp = synth.activations(cfg.seed, synth.S_CAL, n, d, cfg.dtype)
     X = torch.from_numpy(xnp.view(np.int16)).view(torch.bfloat16).to(dev)
     levels = [0.0] + [round(0.05 * i, 4) for i in range(1, 20)]
@@ -513,6 +516,7 @@ def main():
         return t.view(tdt).to(dev) if a.dtype == np.uint16 else t.to(dev)
 
     base = [up(w) for w in wnp]
+    base[0] = base[0].t().contiguous()  # the library takes W_gate one row per neuron
     R = args.lora_rank
     if R:  # the adapters travel with each weight copy
         base += [up(m) for m in synth.lora_adapters(cfg.seed, 0, d, d_ff, R, cfg.dtype)]
@@ -586,8 +590,8 @@ def main():
         return ms, kt
 
     log(f"[bench] timing {args.steps} steps (warmup {args.warmup}), {args.copies} weight copies")
-    kinds = (sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_DEC_GATE, sats.SATS_K_DEC_ROWS,
-             sats.SATS_K_DEC_REDUCE)
+    kinds = (sats.SATS_K_GATE, sats.SATS_K_UP, sats.SATS_K_DOWN, sats.SATS_K_DEC_LAYER, sats.SATS_K_DEC_LORA_V,
+             sats.SATS_K_DEC_REDUCE, sats.SATS_K_DEC_REDUCE_LORA)
     # headline timing without per-kernel events (recording them costs a few us
     # per launch); per-kernel durations come from an identical second region
     ms, _ = timed(step_fwd)
@@ -611,13 +615,15 @@ def main():
 
     up_bytes = updown_row * a_mean / L
     kern = {}
-    gate_lora = (2 * d * R + R * d_ff) * esz if R else 0
-    rows_lora = (2 * R * esz * a_mean / L + R * d * esz) if R else 0
+    # LoRA: B_gate at every column and B_up_T, A_down at the kept rows in the
+    # layer launch; A_gate and A_up in the input launch; B_down in the reduction
+    layer_lora = (R * d_ff * esz + 2 * R * esz * a_mean / L) if R else 0
     for name, (kms, c) in kt.items():
         b = {"gate_kernel": gate_bytes, "up_kernel": up_bytes, "down_kernel": up_bytes,
-             "dec_gate_kernel": gate_bytes + gate_lora,
-             "dec_rows_kernel": 2 * up_bytes + rows_lora + (n * d * esz if R else 0),
-             "dec_reduce_kernel": n * d * esz}[name]
+             "dec_layer_kernel": gate_bytes + 2 * up_bytes + layer_lora,
+             "dec_lora_v_kernel": 2 * d * R * esz + n * d * esz,
+             "dec_reduce_kernel": n * d * esz,
+             "dec_reduce_lora_kernel": n * d * esz + R * d * esz}[name]
         kern[name] = {"avg_us": round(kms * 1e3, 3), "launches": c,
                       "algorithmic_bytes": int(b), "achieved_gbps": round(b / (kms * 1e-3) / 1e9, 1)}
     dom = max(kern, key=lambda k: kern[k]["avg_us"])

@@ -9,7 +9,7 @@
  *            precomputed per vocabulary id; a score below tau selects the
  *            sparse path, any other the base path)
  *   for each layer l = 0 .. n_layers-1, with h the layer input:
- *     a    = h . W_gate[l]                               gated MLP, Eq. 1
+ *     a_j  = W_gate_T[l][j] . h  (a = h W_gate)        gated MLP, Eq. 1
  *     g    = SiLU(a) = a / (1 + exp(-a))                 Eq. 2
  *     keep = all columns                   if r == 1     (base MLP, Eq. 1)
  *            { j : |g_j| >= thresholds[l] } if r == 0    (CATS mask, Eq. 4-5)
@@ -27,9 +27,12 @@
  * Layouts (row-major, dense, no padding):
  *   x, out        [n_tokens][d]
  *   token_ids     [n_tokens]
- *   W_gate        [n_layers][d][d_ff]      orientation of x . W_gate
+ *   W_gate_T      [n_layers][d_ff][d]      W_gate transposed: row j = column j of W_gate
  *   W_up_T        [n_layers][d_ff][d]      W_up transposed: row j = column j of W_up
- *   W_down        [n_layers][d_ff][d]
+ *   W_down        [n_layers][d_ff][d]      row j = the output weights of neuron j
+ * (every weight matrix holds one row of d weights per neuron: a linear
+ * layer's weight as it is stored for W_gate and W_up, and its transpose for
+ * W_down)
  *   thresholds    [n_layers]               float32, >= 0 or +inf
  *   route_lut     [vocab]                  uint8
  *
@@ -85,7 +88,7 @@ enum {
  * exactly (in-place); any other overlap is rejected.
  */
 int sats_mlp_forward(const sats_bf16 *x, const int32_t *token_ids,
-                     const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                     const sats_bf16 *W_gate_T, const sats_bf16 *W_up_T,
                      const sats_bf16 *W_down, const float *thresholds,
                      const uint8_t *route_lut, sats_bf16 *out,
                      int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
@@ -110,26 +113,26 @@ int sats_mlp_forward(const sats_bf16 *x, const int32_t *token_ids,
  */
 #define SATS_NOALLOC_SCRATCH_BYTES (16u << 20)
 int sats_mlp_forward_noalloc(const sats_bf16 *x, const int32_t *token_ids,
-                             const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                             const sats_bf16 *W_gate_T, const sats_bf16 *W_up_T,
                              const sats_bf16 *W_down, const float *thresholds,
                              const uint8_t *route_lut, sats_bf16 *out,
                              int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
                              hipStream_t stream);
 
 /* Base path for every token: the unmasked gated MLP of Eq. 1, same layout. */
-int sats_mlp_dense(const sats_bf16 *x, const sats_bf16 *W_gate,
+int sats_mlp_dense(const sats_bf16 *x, const sats_bf16 *W_gate_T,
                    const sats_bf16 *W_up_T, const sats_bf16 *W_down,
                    sats_bf16 *out, int64_t n_tokens, int64_t d, int64_t d_ff,
                    int64_t n_layers, hipStream_t stream);
 
 /* float32 twins: x, weights and out are float32; rho rounds to float32. */
 int sats_mlp_forward_f32(const float *x, const int32_t *token_ids,
-                         const float *W_gate, const float *W_up_T,
+                         const float *W_gate_T, const float *W_up_T,
                          const float *W_down, const float *thresholds,
                          const uint8_t *route_lut, float *out,
                          int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
                          hipStream_t stream);
-int sats_mlp_dense_f32(const float *x, const float *W_gate, const float *W_up_T,
+int sats_mlp_dense_f32(const float *x, const float *W_gate_T, const float *W_up_T,
                        const float *W_down, float *out, int64_t n_tokens, int64_t d,
                        int64_t d_ff, int64_t n_layers, hipStream_t stream);
 
@@ -143,7 +146,7 @@ int sats_mlp_dense_f32(const float *x, const float *W_gate, const float *W_up_T,
  *   layer_in      [n_layers][n_tokens][d]    input h of each layer
  */
 int sats_mlp_forward_inspect(const sats_bf16 *x, const int32_t *token_ids,
-                             const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+                             const sats_bf16 *W_gate_T, const sats_bf16 *W_up_T,
                              const sats_bf16 *W_down, const float *thresholds,
                              const uint8_t *route_lut, sats_bf16 *out,
                              int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
@@ -151,7 +154,7 @@ int sats_mlp_forward_inspect(const sats_bf16 *x, const int32_t *token_ids,
                              int32_t *active_count, int32_t *active_idx,
                              sats_bf16 *layer_in);
 int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids,
-                                 const float *W_gate, const float *W_up_T,
+                                 const float *W_gate_T, const float *W_up_T,
                                  const float *W_down, const float *thresholds,
                                  const uint8_t *route_lut, float *out,
                                  int64_t n_tokens, int64_t d, int64_t d_ff, int64_t n_layers,
@@ -187,14 +190,14 @@ int sats_mlp_forward_inspect_f32(const float *x, const int32_t *token_ids,
  * (a required array), SATS_ERR_SHAPE (rank or shape), SATS_ERR_ARG
  * (alignment, non-finite scale), and those of sats_mlp_forward.
  */
-int sats_mlp_forward_lora(const sats_bf16 *x, const int32_t *token_ids, const sats_bf16 *W_gate,
+int sats_mlp_forward_lora(const sats_bf16 *x, const int32_t *token_ids, const sats_bf16 *W_gate_T,
                           const sats_bf16 *W_up_T, const sats_bf16 *W_down, const sats_bf16 *A_gate,
                           const sats_bf16 *B_gate, const sats_bf16 *A_up, const sats_bf16 *B_up_T,
                           const sats_bf16 *A_down, const sats_bf16 *B_down, int64_t rank, float scale,
                           const float *thresholds, const uint8_t *route_lut, sats_bf16 *out, int64_t n_tokens,
                           int64_t d, int64_t d_ff, int64_t n_layers, hipStream_t stream, uint8_t *route_out,
                           int32_t *active_count, int32_t *active_idx, sats_bf16 *layer_in);
-int sats_mlp_forward_lora_f32(const float *x, const int32_t *token_ids, const float *W_gate, const float *W_up_T,
+int sats_mlp_forward_lora_f32(const float *x, const int32_t *token_ids, const float *W_gate_T, const float *W_up_T,
                               const float *W_down, const float *A_gate, const float *B_gate, const float *A_up,
                               const float *B_up_T, const float *A_down, const float *B_down, int64_t rank,
                               float scale, const float *thresholds, const uint8_t *route_lut, float *out,
@@ -227,7 +230,7 @@ int sats_device_status(hipStream_t stream);
  *
  * sats_calibration_curves -- one layer.  h [n][d] holds the layer's inputs
  * for n calibration rows (device, bf16; the base-path inputs in a stack),
- * W_gate [d][d_ff], W_up_T [d_ff][d], W_down [d_ff][d] (device, bf16).  For
+ * W_gate_T, W_up_T, W_down [d_ff][d] each (device, bf16).  For
  * each level q_k of levels[n_levels] (host, ascending in [0, 1]) the
  * candidate threshold t_k is the Eq. 3 order statistic v_(ceil(q_k N)) of the
  * N = n d_ff post-gate magnitudes |SiLU(h W_gate)| (q_k = 0 gives t_k = 0;
@@ -255,11 +258,11 @@ int sats_device_status(hipStream_t stream);
  * thresholds_out: host float [n_layers]; budget_out, realized_out: host
  * doubles (may be NULL) receiving b* and S(b*).
  */
-int sats_calibration_curves(const sats_bf16 *h, const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
+int sats_calibration_curves(const sats_bf16 *h, const sats_bf16 *W_gate_T, const sats_bf16 *W_up_T,
                             const sats_bf16 *W_down, int64_t n, int64_t d, int64_t d_ff,
                             const double *levels, int64_t n_levels, float *t_out, double *err_out,
                             double *sp_out, float *err_rows, hipStream_t stream);
-int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *W_gate,
+int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *W_gate_T,
                         const sats_bf16 *W_up_T, const sats_bf16 *W_down, int64_t d, int64_t d_ff,
                         int64_t n_layers, double s_tar, double coarse_step, double fine_step,
                         int guardrail, float *thresholds_out, double *budget_out,
@@ -309,10 +312,9 @@ int sats_route_table(const float *loss_base, const float *loss_sparse, const int
  *   single_token    SATS_SINGLE_AUTO: one-token calls on the single-token
  *                   kernels where the shape fits them; SATS_SINGLE_OFF: on
  *                   the batch kernels.
- *   dec_gate_tiles  single-token gate launch: about this many tiles (1 ..
- *                   65536; 0 = 256).
- *   dec_rows_wgs    single-token rows launch: workgroups, one partial of y
- *                   each (1 .. 1024; 0 = one per compute unit).
+ *   dec_block_cols  single-token layer launch: gate columns per workgroup,
+ *                   one partial of y each (1 .. 64; 0 = d_ff over the
+ *                   compute units, at least 8).
  *   lora_per_token  1: LoRA batches token after token on the single-token
  *                   kernels instead of the matrix-core passes.
  */
@@ -321,8 +323,7 @@ enum { SATS_SINGLE_AUTO = 0, SATS_SINGLE_OFF = 1 };
 typedef struct {
   int batch_path;
   int single_token;
-  int dec_gate_tiles;
-  int dec_rows_wgs;
+  int dec_block_cols;
   int lora_per_token;
 } sats_options;
 int sats_set_options(const sats_options *opt);
@@ -356,9 +357,9 @@ const char *sats_last_error(void);
  * returns the summed duration and the number of launches timed, and disarms.
  */
 enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_DENSE = 4,
-       SATS_K_DEC_GATE = 5, SATS_K_DEC_ROWS = 6, SATS_K_CAL_ERR = 7, SATS_K_CAL_GATEUP = 8,
+       SATS_K_DEC_LAYER = 5, SATS_K_DEC_LORA_V = 6, SATS_K_CAL_ERR = 7, SATS_K_CAL_GATEUP = 8,
        SATS_K_ROUTE_ACCUM = 9, SATS_K_LORA_V = 10, SATS_K_DEC_REDUCE = 11, SATS_K_DENSE_DOWN = 12,
-       SATS_K_COUNT = 13 };
+       SATS_K_DEC_REDUCE_LORA = 13, SATS_K_COUNT = 14 };
 int sats_timing_begin(int kind, int capacity);
 int sats_timing_end(int kind, double *total_ms, int64_t *count);
 const char *sats_kernel_name(int kind);

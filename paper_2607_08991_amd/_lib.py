@@ -17,10 +17,11 @@ LIB_PATH = os.path.join(_PKG, "libsats.so")
 SATS_OK, SATS_ERR_NULL, SATS_ERR_SHAPE, SATS_ERR_HIP, SATS_ERR_WORKSPACE, SATS_ERR_ARG = 0, -1, -2, -3, -4, -5
 SATS_ERR_DEVICE = -6
 SATS_K_GATE, SATS_K_UP, SATS_K_DOWN, SATS_K_INSPECT, SATS_K_DENSE = 0, 1, 2, 3, 4
-SATS_K_DEC_GATE, SATS_K_DEC_ROWS, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, SATS_K_ROUTE_ACCUM = 5, 6, 7, 8, 9
+SATS_K_DEC_LAYER, SATS_K_DEC_LORA_V, SATS_K_CAL_ERR, SATS_K_CAL_GATEUP, SATS_K_ROUTE_ACCUM = 5, 6, 7, 8, 9
 SATS_K_LORA_V = 10
 SATS_K_DEC_REDUCE = 11
 SATS_K_DENSE_DOWN = 12
+SATS_K_DEC_REDUCE_LORA = 13
 SATS_BATCH_AUTO, SATS_BATCH_MFMA, SATS_BATCH_SPLIT, SATS_BATCH_COMPACT = 0, 1, 2, 3
 SATS_SINGLE_AUTO, SATS_SINGLE_OFF = 0, 1
 SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA, SATS_PATH_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT = 1, 2, 3, 4
@@ -28,8 +29,8 @@ SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA, SATS_PATH_BATCH_SPLIT, SATS_PATH_B
 
 class SatsOptions(ctypes.Structure):
     """sats_options of include/sats.h."""
-    _fields_ = [("batch_path", ctypes.c_int), ("single_token", ctypes.c_int), ("dec_gate_tiles", ctypes.c_int),
-                ("dec_rows_wgs", ctypes.c_int), ("lora_per_token", ctypes.c_int)]
+    _fields_ = [("batch_path", ctypes.c_int), ("single_token", ctypes.c_int), ("dec_block_cols", ctypes.c_int),
+                ("lora_per_token", ctypes.c_int)]
 
 # exported symbols and their argument types (p = pointer, i = int64, s = stream, n = int32)
 _P, _I, _S, _N = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
@@ -123,43 +124,43 @@ def _call(name, *args):
     _check(getattr(load(), name)(*args))
 
 
-def sats_mlp_forward(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out,
+def sats_mlp_forward(x, token_ids, W_gate_T, W_up_T, W_down, thresholds, route_lut, out,
                      n_tokens, d, d_ff, n_layers, stream=None):
     name = "sats_mlp_forward_f32" if _is_f32(x) else "sats_mlp_forward"
-    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate_T), _ptr(W_up_T), _ptr(W_down),
           _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers, _stream(stream))
 
 
-def sats_mlp_forward_noalloc(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out,
+def sats_mlp_forward_noalloc(x, token_ids, W_gate_T, W_up_T, W_down, thresholds, route_lut, out,
                              n_tokens, d, d_ff, n_layers, stream=None):
     """sats_mlp_forward on the library's fixed scratch array (bf16; allocates nothing)."""
-    _call("sats_mlp_forward_noalloc", _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+    _call("sats_mlp_forward_noalloc", _ptr(x), _ptr(token_ids), _ptr(W_gate_T), _ptr(W_up_T), _ptr(W_down),
           _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers, _stream(stream))
 
 
-def sats_mlp_dense(x, W_gate, W_up_T, W_down, out, n_tokens, d, d_ff, n_layers, stream=None):
+def sats_mlp_dense(x, W_gate_T, W_up_T, W_down, out, n_tokens, d, d_ff, n_layers, stream=None):
     name = "sats_mlp_dense_f32" if _is_f32(x) else "sats_mlp_dense"
-    _call(name, _ptr(x), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down), _ptr(out), n_tokens, d, d_ff,
+    _call(name, _ptr(x), _ptr(W_gate_T), _ptr(W_up_T), _ptr(W_down), _ptr(out), n_tokens, d, d_ff,
           n_layers, _stream(stream))
 
 
-def sats_mlp_forward_inspect(x, token_ids, W_gate, W_up_T, W_down, thresholds, route_lut, out,
+def sats_mlp_forward_inspect(x, token_ids, W_gate_T, W_up_T, W_down, thresholds, route_lut, out,
                              n_tokens, d, d_ff, n_layers, stream=None, route_out=None,
                              active_count=None, active_idx=None, layer_in=None):
     name = "sats_mlp_forward_inspect_f32" if _is_f32(x) else "sats_mlp_forward_inspect"
-    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate_T), _ptr(W_up_T), _ptr(W_down),
           _ptr(thresholds), _ptr(route_lut), _ptr(out), n_tokens, d, d_ff, n_layers,
           _stream(stream), _ptr(route_out), _ptr(active_count), _ptr(active_idx), _ptr(layer_in))
 
 
-def sats_mlp_forward_lora(x, token_ids, W_gate, W_up_T, W_down, adapters, rank, scale, thresholds, route_lut,
+def sats_mlp_forward_lora(x, token_ids, W_gate_T, W_up_T, W_down, adapters, rank, scale, thresholds, route_lut,
                           out, n_tokens, d, d_ff, n_layers, stream=None, route_out=None, active_count=None,
                           active_idx=None, layer_in=None):
     """LoRA-aware routed sparse forward; adapters = (A_gate, B_gate, A_up, B_up_T, A_down, B_down)."""
     name = "sats_mlp_forward_lora_f32" if _is_f32(x) else "sats_mlp_forward_lora"
     if len(adapters) != 6:
         raise ValueError("adapters = (A_gate, B_gate, A_up, B_up_T, A_down, B_down)")
-    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down),
+    _call(name, _ptr(x), _ptr(token_ids), _ptr(W_gate_T), _ptr(W_up_T), _ptr(W_down),
           *(_ptr(m) for m in adapters), int(rank), float(scale), _ptr(thresholds), _ptr(route_lut), _ptr(out),
           n_tokens, d, d_ff, n_layers, _stream(stream), _ptr(route_out), _ptr(active_count), _ptr(active_idx),
           _ptr(layer_in))
@@ -178,9 +179,9 @@ def sats_release():
     _call("sats_release")
 
 
-def sats_set_options(batch_path=0, single_token=0, dec_gate_tiles=0, dec_rows_wgs=0, lora_per_token=0):
+def sats_set_options(batch_path=0, single_token=0, dec_block_cols=0, lora_per_token=0):
     """Execution options of the calling thread's later forward calls (all 0: the defaults)."""
-    o = SatsOptions(batch_path, single_token, dec_gate_tiles, dec_rows_wgs, lora_per_token)
+    o = SatsOptions(batch_path, single_token, dec_block_cols, lora_per_token)
     _call("sats_set_options", ctypes.byref(o))
 
 
@@ -242,7 +243,7 @@ def _host(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
 
 
-def sats_calibration_curves(h, W_gate, W_up_T, W_down, n, d, d_ff, levels, err_rows=None, stream=None):
+def sats_calibration_curves(h, W_gate_T, W_up_T, W_down, n, d, d_ff, levels, err_rows=None, stream=None):
     """SATS curves of one layer (Eq. 3 candidates at `levels`, Eq. 6 errors, sparsities).
 
     h and the weights are device tensors (bf16); levels is a host sequence.
@@ -253,13 +254,13 @@ def sats_calibration_curves(h, W_gate, W_up_T, W_down, n, d, d_ff, levels, err_r
     t = np.zeros(len(lv), np.float32)
     err = np.zeros(len(lv), np.float64)
     sp = np.zeros(len(lv), np.float64)
-    _call("sats_calibration_curves", _ptr(h), _ptr(W_gate), _ptr(W_up_T), _ptr(W_down), n, d, d_ff,
+    _call("sats_calibration_curves", _ptr(h), _ptr(W_gate_T), _ptr(W_up_T), _ptr(W_down), n, d, d_ff,
           lv.ctypes.data, len(lv), t.ctypes.data, err.ctypes.data, sp.ctypes.data, _ptr(err_rows),
           _stream(stream))
     return t, err, sp
 
 
-def sats_calibrate_sats(x_cal, n_cal, W_gate, W_up_T, W_down, d, d_ff, n_layers, s_tar,
+def sats_calibrate_sats(x_cal, n_cal, W_gate_T, W_up_T, W_down, d, d_ff, n_layers, s_tar,
                         coarse_step=0.05, fine_step=0.005, guardrail=True, stream=None):
     """SATS thresholds of a stack (Eq. 7-10, coarse to fine, final-layer guardrail).
 
@@ -269,7 +270,7 @@ def sats_calibrate_sats(x_cal, n_cal, W_gate, W_up_T, W_down, d, d_ff, n_layers,
     ts = np.zeros(n_layers, np.float32)
     b = ctypes.c_double(0.0)
     s = ctypes.c_double(0.0)
-    _call("sats_calibrate_sats", _ptr(x_cal), n_cal, _ptr(W_gate), _ptr(W_up_T), _ptr(W_down), d, d_ff,
+    _call("sats_calibrate_sats", _ptr(x_cal), n_cal, _ptr(W_gate_T), _ptr(W_up_T), _ptr(W_down), d, d_ff,
           n_layers, float(s_tar), float(coarse_step), float(fine_step), int(bool(guardrail)),
           ts.ctypes.data, ctypes.addressof(b), ctypes.addressof(s), _stream(stream))
     return ts, b.value, s.value

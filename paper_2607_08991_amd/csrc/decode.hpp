@@ -1,28 +1,29 @@
-// Single-token (decode batch 1) path: three plain launches per layer.
+// Single-token (decode batch 1) path: one layer is one launch plus the
+// second reduction stage.
 //
-//   gate    W_gate is cut into tiles one 16-byte load per lane wide (64 lanes:
-//           512 bf16 or 256 fp32 columns, 1 KB of each row) by a chunk of
-//           rows.  A workgroup forms h . tile for its tile, sums its
-//           wavefronts' partials in LDS and writes one partial a per column
-//           and row chunk.
-//   rows    Work units are (column block, share): every workgroup of a
-//           column block adds the block's row-chunk partials in chunk order,
-//           applies SiLU (Eq. 2) and the keep rule (Eq. 4-5, or every column
-//           on the base path, Eq. 13) and compacts the kept columns in LDS;
-//           all of them get the same list, and each takes an even share of
-//           it: u_j = W_up_T[j] . h, p_j = g_j u_j (Eq. 1) and
-//           p_j W_down[j] accumulated into the workgroup's partial y, the
-//           rows of both projections read in the same batches.
+//   layer   Workgroup w owns the gate columns [cw w, cw w + cw) (cw <= 64).
+//           Its wavefronts read whole rows of W_gate^T, one column's d
+//           weights contiguous, and form a_j = h . W_gate[:, j] in a fixed
+//           order; then SiLU (Eq. 2) and the keep rule (Eq. 4-5, or every
+//           column on the base path, Eq. 13) give the workgroup's own kept
+//           list in LDS, and its two halves stream the listed rows of W_up_T
+//           and W_down: u_j = W_up_T[j] . h, p_j = g_j u_j (Eq. 1) and
+//           p_j W_down[j] summed into the workgroup's partial y.  No value
+//           crosses workgroups inside the launch: there is no hand-off to
+//           wait for, and the row reads of one workgroup overlap the gate
+//           reads of the others.
 //   reduce  Workgroup w adds every partial for its own slice of columns in
 //           workgroup order: y, or the rounded output on the last layer, and
 //           the slice's sum of squares for the next layer's input
 //           rho(y / sqrt(mean(y^2) + 1e-6)).
 //
-// Workgroups have 1024 threads (16 wavefronts per CU keep more row reads in
-// flight than 8).  Partials cross workgroups through device-coherent stores
-// and loads; kernel boundaries order the phases.  The assignment of work
-// depends only on the data, never on timing, so every sum has a fixed order
-// and results are reproducible bit for bit.
+// With LoRA adapters (Section 5) a small launch first forms h A_gate and
+// h A_up, and the reduction adds the down adapter.
+//
+// Workgroups have 1024 threads (16 wavefronts per CU keep enough reads in
+// flight).  The assignment of work depends only on the data, never on
+// timing, so every sum has a fixed order and results are reproducible bit
+// for bit.
 #pragma once
 
 #include "kernels.hpp"
@@ -43,41 +44,30 @@ __device__ unsigned long long sats_trace_buf[4096 * 16];
   } while (0)
 #endif
 
-constexpr int kDecodeThreads = 1024;  // rows and reduce launches
+constexpr int kDecodeThreads = 1024;  // layer, LoRA input and LoRA reduce launches
 constexpr int kDecodeWaves = kDecodeThreads / 64;
-#ifndef SATS_GATE_THREADS
-#define SATS_GATE_THREADS 1024
-#endif
-constexpr int kGateThreads = SATS_GATE_THREADS;  // gate launch
-constexpr int kGateBatch = kGateThreads >= 1024 ? 8 : 16;  // 16-byte loads in flight per lane
-constexpr int kDecodeMaxD = 4096;  // h lives in LDS
-constexpr int kDecodeMaxG = 1024;  // rows / reduce workgroups (partials of y)
+constexpr int kDecodeMaxD = 4096;     // h lives in LDS
+constexpr int kDecodeMaxCols = 64;    // gate columns of a workgroup (one wavefront ballot)
+constexpr int kDecodeMaxG = 4096;     // layer workgroups (partials of y)
 constexpr int kRedThreads = 256, kRedCols = 16;  // second reduction stage: threads and columns per workgroup
-
-// Columns of one gate column block (one 16-byte load per lane of a wavefront).
-template <typename T> constexpr int dec_block_cols() { return 64 * Elem<T>::kVec; }
-// Gate partials of one column are stored contiguously, padded to whole 16 bytes.
-__host__ __device__ constexpr int dec_nrcp(int nrc) { return (nrc + 3) & ~3; }
+constexpr int kGateQ = 4;             // 16-byte loads per lane in one gate piece
+constexpr int kVRows = 256;           // input rows per workgroup of the LoRA input launch
 
 struct DecodeArgs {
   const void *x;          // [d] call input (storage type)
   void *out;              // [d]
-  const void *Wg, *Wu, *Wd;  // stacked weights
+  const void *Wg, *Wu, *Wd;  // stacked weights, each [L][d_ff][d]: W_gate^T, W_up_T, W_down
   const float *thr;       // [L] (unused on the base path)
   const int32_t *ids;
   const uint8_t *lut;
   int route_mode;
   int L, d, d_ff;
-  int nblk, nrc;          // gate tiles: column blocks x row chunks
-  float *gpart;           // [d_ff][nrcp]   partial a of each row chunk (nrcp = nrc rounded up to 4)
+  int cw;                 // gate columns per layer workgroup
   float *ypart;           // [G][d]         per-workgroup partial y
   float *ybuf;            // [d]
-  float *sspart;          // [RW]           per-reduce-workgroup sums of y^2
-  int G, RW;              // rows workgroups (partials of y), reduce workgroups
+  float *sspart;          // [nss]          sums of y^2 per 16 columns
+  int G, RW;              // layer workgroups (partials of y), reduce workgroups
   int nss;                // slice sums of squares of y per layer: one per 16 columns
-  int *state;             // [1] the token's route (1: base path), set by the layer-0 gate launch
-  unsigned *done;         // [1] rows workgroups whose partial y is written (cleared by the gate launch)
-  unsigned *err;          // device error flag (a bounded wait gave up)
   uint8_t *route_out;     // optional [1]
   uint8_t *keep_out;      // optional [L][d_ff]
   void *layer_in;         // optional [L][...]: layer l's input at layer_in + l * in_stride
@@ -88,30 +78,32 @@ struct DecodeArgs {
   const void *Ag, *Bg, *Au, *BuT, *Ad, *Bd;
   int rank;
   float lscale;
-  float *vpart;           // [nrc][rank] per gate row chunk: partial h . A_up
-  float *zpart;           // [G][rank]   per rows workgroup: sum of p_j A_down[j] over its kept rows
+  float *vpart;           // [nvc][2][rank] per input row chunk: partial h . A_gate, h . A_up
+  int nvc;                // row chunks of the LoRA input launch
+  float *zpart;           // [G][rank]      per layer workgroup: sum of p_j A_down[j] over its kept rows
 };
 
 constexpr int kLoraMaxRank = 64;  // ranks 8, 16, 32, 64
 
 struct DecodeSmem {
-  float hs[kDecodeMaxD];                // layer input
-  float red[2 * kDecodeMaxD];           // gate: wavefront partials; rows: parts of u, half sums
-  int mj[kDecodeThreads / 2];           // kept columns of the current column block ...
-  float mg[kDecodeThreads / 2];         // ... and their g values
+  float hs[kDecodeMaxD];                // layer input (zero past d)
+  u32x4 hq[kDecodeMaxD * 4 / 16];       // the same, packed in the storage type (gate reads, 16 bytes a load)
+  float red[2 * kDecodeMaxD];           // column sums; rows: parts of u, half sums; reduce: partial groups
+  int mj[kDecodeMaxCols];               // kept columns of the workgroup ...
+  float mg[kDecodeMaxCols];             // ... and their g values
   int wcnt[kDecodeWaves];
   float scal[kDecodeWaves];
-  int flag;
-  float lv[2][kDecodeWaves][kLoraMaxRank];  // LoRA: wavefront partials of h . A (gate, up)
-  float lz[kLoraMaxRank];                    // LoRA: h . A_up (rows) or z (reduce)
+  float lv[2][kDecodeWaves][kLoraMaxRank];  // LoRA: wavefront partials (input launch), gate adapter terms
+  float lvg[kLoraMaxRank];                   // LoRA: h . A_gate
+  float lz[kLoraMaxRank];                    // LoRA: h . A_up (layer) or z (reduce)
 };
 
-// LoRA operands of a rows workgroup's kept rows (list position i): the up
+// LoRA operands of the workgroup's kept rows (list position i): the up
 // adapter's contribution w_i = s (h A_up) . B_up_T[j] and A_down[j].
 template <typename T>
 struct LoraRows {
-  float lw[kDecodeThreads / 2];
-  T lad[64 * Elem<T>::kVec * kLoraMaxRank];  // [list position][rank]: one column block's list at most
+  float lw[kDecodeMaxCols];
+  T lad[kDecodeMaxCols * kLoraMaxRank];  // [list position][rank]
 };
 
 // Four consecutive floats at byte offset voff of buffer r, written through to
@@ -141,28 +133,6 @@ __device__ __forceinline__ u32x4 load_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t vo
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 2);
 }
 
-// Sum of the nrc gate partials of column `col`, in row-chunk order: 16 bytes
-// per load, written through by the gate launch and read from the
-// device-coherent level.
-__device__ __forceinline__ float gate_sum(__amdgpu_buffer_rsrc_t gp, int col, int nrc) {
-  const int nq = dec_nrcp(nrc) / 4;
-  const uint32_t base = (uint32_t)col * (uint32_t)(nq * 16);
-  float s = 0.0f;
-  for (int q0 = 0; q0 < nq; q0 += 4) {
-    f32x4 v[4];  // up to 16 partials in flight
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t off = (q0 + i < nq) ? base + (uint32_t)((q0 + i) * 16) : kOffNone;
-      v[i] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(gp, (int)off, 0, 16 /* coherent */));
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if ((q0 + i) * 4 + j < nrc) s += v[i][j];
-  }
-  return s;
-}
 
 // Sums of R values over the 64 lanes of a wavefront (R a power of two),
 // by halving exchanges: at the step with lane mask m each lane keeps half of
@@ -195,11 +165,14 @@ __device__ __forceinline__ float rows_sum(float (&v)[R], int lane) {
 // and the G slice sums of squares; finish() forms
 // h = rho(y / sqrt(mean(y^2) + 1e-6)) into LDS (and the inspection copy when
 // `record`).
+// slice sums of squares (one per 16 columns of y) per thread
+template <int THREADS> constexpr int kSlicesPer() { return (kDecodeMaxD / kRedCols + THREADS - 1) / THREADS; }
+
 template <int THREADS>
 struct InputRegs {
   u32x4 xv[kDecodeMaxD / (4 * THREADS)];  // layer 0: x, 16 bytes at a time (d <= 4096)
   float yv[kDecodeMaxD / THREADS];
-  float ss[kDecodeMaxG / THREADS];
+  float ss[kSlicesPer<THREADS>()];
 };
 
 template <typename T, int THREADS>
@@ -214,7 +187,7 @@ __device__ __forceinline__ void dec_input_issue(const DecodeArgs &a, int l, Inpu
 #pragma unroll
   for (int i = 0; i < kDecodeMaxD / THREADS; ++i) r.yv[i] = 0.0f;
 #pragma unroll
-  for (int i = 0; i < kDecodeMaxG / THREADS; ++i) r.ss[i] = 0.0f;
+  for (int i = 0; i < kSlicesPer<THREADS>(); ++i) r.ss[i] = 0.0f;
   if (l == 0) {
 #pragma unroll
     for (int i = 0; i < kDecodeMaxD / (4 * THREADS); ++i) {
@@ -226,7 +199,7 @@ __device__ __forceinline__ void dec_input_issue(const DecodeArgs &a, int l, Inpu
 #pragma unroll
     for (int i = 0; i < kDecodeMaxD / THREADS; ++i) r.yv[i] = load_coherent(a.ybuf + min(i * THREADS + tid, d - 1));
 #pragma unroll
-    for (int i = 0; i < kDecodeMaxG / THREADS; ++i)
+    for (int i = 0; i < kSlicesPer<THREADS>(); ++i)
       r.ss[i] = (tid + i * THREADS < G) ? load_coherent(a.sspart + tid + i * THREADS) : 0.0f;
   }
 }
@@ -243,7 +216,7 @@ __device__ __forceinline__ void dec_input_finish(const DecodeArgs &a, int l, Inp
 #pragma unroll
   for (int i = 0; i < kDecodeMaxD / THREADS; ++i) asm volatile("" : "+v"(r.yv[i])::"memory");
 #pragma unroll
-  for (int i = 0; i < kDecodeMaxG / THREADS; ++i) asm volatile("" : "+v"(r.ss[i])::"memory");
+  for (int i = 0; i < kSlicesPer<THREADS>(); ++i) asm volatile("" : "+v"(r.ss[i])::"memory");
 #pragma unroll
   for (int i = 0; i < kDecodeMaxD / (4 * THREADS); ++i) asm volatile("" : "+v"(r.xv[i])::"memory");
   if (l == 0) {
@@ -259,7 +232,7 @@ __device__ __forceinline__ void dec_input_finish(const DecodeArgs &a, int l, Inp
   } else {
     float s = 0.0f;  // total sum of squares of y, in a fixed order
 #pragma unroll
-    for (int i = 0; i < kDecodeMaxG / THREADS; ++i) s += r.ss[i];
+    for (int i = 0; i < kSlicesPer<THREADS>(); ++i) s += r.ss[i];
     s = wave_sum(s);
     if (lane == 0) sm.scal[wv] = s;
     __syncthreads();
@@ -279,243 +252,154 @@ __device__ __forceinline__ void dec_input_finish(const DecodeArgs &a, int l, Inp
   __syncthreads();
 }
 
-// ------------------------------------------------------------------ LoRA adapters
-//
+
+// ------------------------------------------------------------------ LoRA input
+
 // The sparse path of a fine-tuned routed model adds s A B to each projection
-// (Section 5).  Every product splits over the gate's row chunks: a gate tile
-// over rows k0 .. k0 + kn adds s (h[k0..] A_gate[k0..]) B_gate to its partial
-// of a, so the row-chunk sums give h (W_gate + s A_gate B_gate) with no step
-// of its own; the tiles of column block 0 also write h[k0..] A_up[k0..], whose
-// sum the rows launch uses for the up adapter of its kept rows.  The down
-// adapter's first factor is summed over the kept rows (z = sum p_j A_down[j])
-// next to each rows workgroup's partial y, and the second reduction stage
-// adds s z B_down.
-
-constexpr int kLoraPieces = 2;  // 16-byte pieces of an A matrix per thread and pass
-
+// (Section 5).  h A_gate and h A_up (rank values each) are formed once per
+// layer by a launch of their own: workgroup c takes input rows
+// [kVRows c, kVRows c + kVRows) of both A matrices and writes its partial
+// sums; the layer launch adds the chunks in order.  The gate adapter term
+// s (h A_gate) . B_gate[:, j] is added to a_j, the up adapter term
+// s (h A_up) . B_up_T[j] to u_j of each kept row, and the down adapter's
+// first factor z = sum p_j A_down[j] is summed next to each partial y; the
+// second reduction stage adds s z B_down.
 template <typename T>
-struct LoraGateRegs {
-  u32x4 ag[kLoraPieces], au[kLoraPieces];  // A_gate / A_up pieces of one pass over the tile's rows
-};
-
-// B_gate rows at the tile's columns, staged in LDS by loads that write LDS
-// (no registers held across the tile): row r at lb[r], 16 bytes per lane.
-struct LoraGateSmem {
-  uint8_t lb[kLoraMaxRank][1024];
-};
-
-// One pass of A loads: pieces p0 + tid, p0 + tid + THREADS (16 bytes each) of
-// rows k0 .. k0 + kn of A_gate (and of A_up when `up`).
-template <typename T>
-__device__ __forceinline__ void lora_a_issue(const DecodeArgs &a, int l, int k0, int kn, bool up, int p0,
-                                             LoraGateRegs<T> &lr) {
+__global__ __launch_bounds__(kDecodeThreads) void dec_lora_v_kernel(DecodeArgs a, int l) {
+  __shared__ DecodeSmem sm;
   constexpr int VEC = Elem<T>::kVec;
-  const int R = a.rank, tid = threadIdx.x;
-  const uint32_t abytes = (uint32_t)((size_t)a.d * R * sizeof(T));
-  const __amdgpu_buffer_rsrc_t rg = weight_rsrc(static_cast<const T *>(a.Ag) + (size_t)l * a.d * R, abytes);
-  const __amdgpu_buffer_rsrc_t ru = weight_rsrc(static_cast<const T *>(a.Au) + (size_t)l * a.d * R, abytes);
-  const int np = kn * R / VEC;
-  const uint32_t abase = (uint32_t)((size_t)k0 * R * sizeof(T));
+  constexpr int M = kVRows * kLoraMaxRank / (VEC * kDecodeThreads);  // passes at the largest rank
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int R = a.rank, RQ = R / VEC;  // 16-byte pieces per row of an A matrix
+  const int k0 = blockIdx.x * kVRows, kn = max(0, min(a.d, k0 + kVRows) - k0);
+  const size_t al = (size_t)a.d * R;
+  const __amdgpu_buffer_rsrc_t rg = weight_rsrc(static_cast<const T *>(a.Ag) + (size_t)l * al, (uint32_t)(al * sizeof(T)));
+  const __amdgpu_buffer_rsrc_t ru = weight_rsrc(static_cast<const T *>(a.Au) + (size_t)l * al, (uint32_t)(al * sizeof(T)));
+  // piece p = tid + kDecodeThreads m: row k0 + p / RQ, ranks VEC (p % RQ) ..
+  // (p % RQ = lane % RQ: RQ divides 64)
+  u32x4 qg[M], qu[M];
 #pragma unroll
-  for (int m = 0; m < kLoraPieces; ++m) {
-    const int pc = p0 + tid + m * kGateThreads;
-    const uint32_t off = pc < np ? abase + (uint32_t)pc * 16u : kOffNone;
-    lr.ag[m] = __builtin_amdgcn_raw_buffer_load_b128(rg, (int)off, 0, 0);
-    lr.au[m] = up ? __builtin_amdgcn_raw_buffer_load_b128(ru, (int)off, 0, 0) : u32x4{0u, 0u, 0u, 0u};
+  for (int m = 0; m < M; ++m) {
+    const int p = tid + m * kDecodeThreads;
+    const uint32_t off = p < kn * RQ ? (uint32_t)(((size_t)k0 * R + (size_t)p * VEC) * sizeof(T)) : kOffNone;
+    qg[m] = load_rsrc(rg, off, 0);
+    qu[m] = load_rsrc(ru, off, 0);
   }
-}
-
-// This wavefront's rows of B_gate (wv, wv + NW, ...) at the lane's columns,
-// straight into LDS.
-template <typename T>
-__device__ __forceinline__ void lora_b_issue(const DecodeArgs &a, int l, int col, LoraGateSmem &ls) {
-  constexpr int NW = kGateThreads / 64;
-  const int R = a.rank, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const __amdgpu_buffer_rsrc_t rb = weight_rsrc(static_cast<const T *>(a.Bg) + (size_t)l * R * a.d_ff,
-                                                (uint32_t)((size_t)R * a.d_ff * sizeof(T)));
-  // every row slot is loaded, past the rank from past the buffer (zeros): a
-  // branch around these loads would cost the compiler its record of which
-  // LDS bytes they write, and with it waits on every load before LDS reads
+  InputRegs<kDecodeThreads> ir;
+  dec_input_issue<T, kDecodeThreads>(a, l, ir);
+  dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, false);
+  float sg[VEC], su[VEC];
 #pragma unroll
-  for (int m = 0; m < kLoraMaxRank / NW; ++m) {
-    const int row = wv + m * NW;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (__attribute__((address_space(3))) void *)ls.lb[row], 16,
-                                             row < R ? (int)(col * sizeof(T)) : (int)kOffNone,
-                                             row < R ? (int)((size_t)row * a.d_ff * sizeof(T)) : 0, 0, 0);
-  }
-}
-
-// h . A over the tile's rows: each lane adds its pieces of one pass to sv
-// (every piece of a thread covers the same rank indices: THREADS pieces
-// span whole rows); lora_v_reduce then adds the lanes of equal index by
-// halving exchanges, and lanes 0 .. R / VEC - 1 write the wavefront's sums.
-template <typename T>
-__device__ __forceinline__ void lora_a_acc(const DecodeArgs &a, int k0, int kn, int p0, const u32x4 (&pc)[kLoraPieces],
-                                           float (&sv)[Elem<T>::kVec], const DecodeSmem &sm) {
-  constexpr int VEC = Elem<T>::kVec;
-  const int R = a.rank, np = kn * R / VEC;
+  for (int v = 0; v < VEC; ++v) sg[v] = su[v] = 0.0f;
 #pragma unroll
-  for (int m = 0; m < kLoraPieces; ++m) {
-    const int p = p0 + threadIdx.x + m * kGateThreads;
-    if (p < np) {
-      const float hv = sm.hs[k0 + p * VEC / R];
+  for (int m = 0; m < M; ++m) {
+    const int p = tid + m * kDecodeThreads;
+    if (p < kn * RQ) {
+      const float hv = sm.hs[k0 + p / RQ];
 #pragma unroll
-      for (int v = 0; v < VEC; ++v) sv[v] = fmaf(hv, unpack<T>(pc[m], v), sv[v]);
+      for (int v = 0; v < VEC; ++v) {
+        sg[v] = fmaf(hv, unpack<T>(qg[m], v), sg[v]);
+        su[v] = fmaf(hv, unpack<T>(qu[m], v), su[v]);
+      }
     }
   }
-}
-
-template <typename T>
-__device__ __forceinline__ void lora_v_reduce(const DecodeArgs &a, float (&sv)[Elem<T>::kVec],
-                                              float (&out)[kLoraMaxRank]) {
-  constexpr int VEC = Elem<T>::kVec;
-  const int RQ = a.rank / VEC, lane = threadIdx.x & 63;
+  // lanes of equal lane % RQ hold the same ranks: halving exchanges add them
   for (int msk = 32; msk >= max(RQ, 1); msk >>= 1)
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) sv[v] += __shfl_xor(sv[v], msk, 64);
+    for (int v = 0; v < VEC; ++v) {
+      sg[v] += __shfl_xor(sg[v], msk, 64);
+      su[v] += __shfl_xor(su[v], msk, 64);
+    }
   if (lane < RQ) {
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) out[lane * VEC + v] = sv[v];
+    for (int v = 0; v < VEC; ++v) {
+      sm.lv[0][wv][lane * VEC + v] = sg[v];
+      sm.lv[1][wv][lane * VEC + v] = su[v];
+    }
+  }
+  __syncthreads();
+  if (tid < 2 * R) {  // the wavefronts' sums in order
+    const int ad = tid / R, i = tid % R;
+    float s = 0.0f;
+    for (int q = 0; q < kDecodeWaves; ++q) s += sm.lv[ad][q][i];
+    store_coherent(a.vpart + ((size_t)blockIdx.x * 2 + ad) * R + i, s);
   }
 }
 
 // ------------------------------------------------------------------ gate
 
-// One batch of a gate tile: rows k0w + NW (r0 + u), u < GB, of this
-// wavefront (past its nr rows the last row is read again and given weight 0).
-template <typename T, int GB, int NW>
-__device__ __forceinline__ void gate_issue(__amdgpu_buffer_rsrc_t wr, uint32_t row0_bytes, uint32_t stride_bytes,
-                                           int r0, int nr, uint32_t lo, u32x4 (&q)[GB]) {
-#pragma unroll
-  for (int u = 0; u < GB; ++u) q[u] = load_rsrc(wr, lo, row0_bytes + (uint32_t)min(r0 + u, nr - 1) * stride_bytes);
-}
+// The gate columns of a workgroup: wavefront wv takes columns wv, wv + 16,
+// ... of the block, each a row of W_gate^T read in pieces of kGateQ 16-byte
+// loads per lane (npc pieces per row); P pieces in all for this wavefront.
+struct GatePieces {
+  int c0, nc, npc, P, wv;
+};
 
-template <typename T, int GB, int NW>
-__device__ __forceinline__ void gate_consume(const DecodeSmem &sm, int k0w, int r0, int nr, const u32x4 (&q)[GB],
-                                             float (&acc)[Elem<T>::kVec]) {
+template <typename T>
+__device__ __forceinline__ void gate_piece_issue(__amdgpu_buffer_rsrc_t wr, const GatePieces &gp, int d, int p,
+                                                 u32x4 (&q)[kGateQ]) {
+  const int lane = threadIdx.x & 63;
+  const int cl = min(gp.wv + 16 * (p / gp.npc), gp.nc - 1), qi = p % gp.npc;  // wavefront-uniform
+  const uint32_t row_bytes = (uint32_t)d * (uint32_t)sizeof(T);
+  const uint32_t soff = (uint32_t)(gp.c0 + cl) * row_bytes;
 #pragma unroll
-  for (int u = 0; u < GB; ++u) {
-    const float hv = sm.hs[k0w + min(r0 + u, nr - 1) * NW];
-    const float hu = (r0 + u < nr) ? hv : 0.0f;
-#pragma unroll
-    for (int v = 0; v < Elem<T>::kVec; ++v) acc[v] = fmaf(hu, unpack<T>(q[u], v), acc[v]);
+  for (int u = 0; u < kGateQ; ++u) {
+    const uint32_t byte = (uint32_t)((qi * kGateQ + u) * 64 + lane) * 16u;
+    q[u] = load_rsrc(wr, (p < gp.P && byte < row_bytes) ? byte : kOffNone, soff);
   }
 }
 
-// Gate tiles blockIdx.x, blockIdx.x + gridDim.x, ... (tile t: column block
-// t % nblk, row chunk t / nblk); forms h in LDS before the first tile's
-// products (its loads follow the tile's first weight loads).
-template <typename T, bool LORA>
-__device__ void dec_gate(const DecodeArgs &a, int l, DecodeSmem &sm, LoraGateSmem &ls, bool record) {
-  constexpr int THREADS = kGateThreads, VEC = Elem<T>::kVec, NW = THREADS / 64;
-  constexpr int CB = dec_block_cols<T>();
-  constexpr int GB = kGateBatch;
-  static_assert(NW * CB <= 2 * kDecodeMaxD, "gate partials fit the LDS buffer");
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int d = a.d, d_ff = a.d_ff;
-  const int rows = (d + a.nrc - 1) / a.nrc;
-  const __amdgpu_buffer_rsrc_t wr =
-      weight_rsrc(static_cast<const T *>(a.Wg) + (size_t)l * d * d_ff, (uint32_t)((size_t)d * d_ff * sizeof(T)));
-  const uint32_t stride = (uint32_t)((size_t)NW * d_ff * sizeof(T));  // between a wavefront's rows
-  InputRegs<THREADS> ir;
-  bool have_input = false;
-  // LoRA: the token's route (base-path tokens use the base weights only)
-  constexpr bool lora = LORA;
-  const float lsc = !lora ? 0.0f
-                          : ((l == 0 ? token_is_base(a.route_mode, a.ids, a.lut, 0) : a.state[0]) ? 0.0f : a.lscale);
-  for (int t = blockIdx.x; t < a.nblk * a.nrc; t += gridDim.x) {
-    const int cb = t % a.nblk, rc = t / a.nblk;
-    const int k0 = rc * rows, kn = max(0, min(d, k0 + rows) - k0);
-    const int col = cb * CB + lane * VEC;
-    const int nr = (kn - wv + NW - 1) / NW;  // this wavefront's rows: k0 + wv + NW r, r < nr
-    // Lanes past d_ff read in-bounds data of the next row (or zeros past the
-    // matrix) and their sums are never stored, so only nr guards the loads.
-    const bool live = nr > 0;
-    const uint32_t row0 = (uint32_t)((size_t)(k0 + wv) * d_ff * sizeof(T));  // wavefront-uniform
-    const uint32_t lo = (uint32_t)(col * sizeof(T));
-    float acc[VEC];
+// Adds a piece's products to acc (even and odd elements apart); after a
+// column's last piece the wavefront sum (lanes in a fixed order) goes to
+// colsum[column] and acc restarts.  Each weight load meets the 16 bytes of
+// packed h at the same elements (zero past d; the weights past the row are
+// read as zeros).
+template <typename T>
+__device__ __forceinline__ void gate_piece_use(const DecodeSmem &sm, const GatePieces &gp, int p,
+                                               const u32x4 (&q)[kGateQ], float (&acc)[2], float *colsum) {
+  constexpr int VEC = Elem<T>::kVec;
+  const int lane = threadIdx.x & 63, qi = p % gp.npc;
+  u32x4 hv[kGateQ];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) acc[v] = 0.0f;
-    u32x4 q[GB];
-    // LoRA: B_gate rows go to LDS now; the A pieces are loaded with the
-    // wavefront's last weight batch and used after it (a wait for them
-    // earlier would also wait for the weight loads issued before them)
-    LoraGateRegs<T> lr;
-    const bool a_early = !live || nr <= GB;
-    if constexpr (LORA) {
-      lora_b_issue<T>(a, l, col, ls);
-      if (a_early) lora_a_issue<T>(a, l, k0, kn, cb == 0, 0, lr);
-    }
-    if (live) gate_issue<T, GB, NW>(wr, row0, stride, 0, nr, lo, q);
-    if (!have_input) {  // h is needed from the first batch on; its loads follow the weights'
-      dec_input_issue<T, THREADS>(a, l, ir);
-      dec_input_finish<T, THREADS>(a, l, ir, sm, record);
-      have_input = true;
-      if (l == 0) SATS_TRACE_POINT(1);
-    }
-    if (live) {
-      gate_consume<T, GB, NW>(sm, k0 + wv, 0, nr, q, acc);
-      for (int r0 = GB; r0 < nr; r0 += GB) {
-        if (LORA && r0 + GB >= nr) lora_a_issue<T>(a, l, k0, kn, cb == 0, 0, lr);
-        gate_issue<T, GB, NW>(wr, row0, stride, r0, nr, lo, q);
-        gate_consume<T, GB, NW>(sm, k0 + wv, r0, nr, q, acc);
+  for (int u = 0; u < kGateQ; ++u) hv[u] = sm.hq[(qi * kGateQ + u) * 64 + lane];  // at most 16 KB of a row
+#pragma unroll
+  for (int u = 0; u < kGateQ; ++u)
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v & 1] = fmaf(unpack<T>(hv[u], v), unpack<T>(q[u], v), acc[v & 1]);
+  if (qi == gp.npc - 1) {
+    const float s = wave_sum(acc[0] + acc[1]);
+    if (lane == 0) colsum[gp.wv + 16 * (p / gp.npc)] = s;
+    acc[0] = acc[1] = 0.0f;
+  }
+}
+
+// h (in LDS as float, zero past d) packed in the storage type: exact, h is
+// rounded to it.
+template <typename T>
+__device__ __forceinline__ void pack_input(DecodeSmem &sm) {
+  constexpr int VEC = Elem<T>::kVec, NP = kDecodeMaxD * (int)sizeof(T) / 16;
+  for (int i = threadIdx.x; i < NP; i += kDecodeThreads) {
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(sm.hs + i * VEC);
+    u32x4 q;
+    if constexpr (sizeof(T) == 2) {
+      const f32x4 lo = src[0], hi = src[1];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        q[j] = (uint32_t)f32_to_bf16(lo[2 * j]) | ((uint32_t)f32_to_bf16(lo[2 * j + 1]) << 16);
+        q[j + 2] = (uint32_t)f32_to_bf16(hi[2 * j]) | ((uint32_t)f32_to_bf16(hi[2 * j + 1]) << 16);
       }
+    } else {
+      q = __builtin_bit_cast(u32x4, src[0]);
     }
-    if constexpr (LORA) {  // this tile's h . A_gate (and h . A_up on column block 0)
-      float sg[VEC], su[VEC];
-#pragma unroll
-      for (int v = 0; v < VEC; ++v) sg[v] = su[v] = 0.0f;
-      const int np = kn * a.rank / VEC, pp = kLoraPieces * kGateThreads;
-      for (int p0 = 0; p0 < np; p0 += pp) {
-        if (p0 > 0) lora_a_issue<T>(a, l, k0, kn, cb == 0, p0, lr);
-        lora_a_acc<T>(a, k0, kn, p0, lr.ag, sg, sm);
-        if (cb == 0) lora_a_acc<T>(a, k0, kn, p0, lr.au, su, sm);
-      }
-      lora_v_reduce<T>(a, sg, sm.lv[0][wv]);
-      if (cb == 0) lora_v_reduce<T>(a, su, sm.lv[1][wv]);
-      __syncthreads();
-      if (l == 0) SATS_TRACE_POINT(13);
-      if (cb == 0 && tid < a.rank) {
-        float v = 0.0f;
-#pragma unroll
-        for (int q2 = 0; q2 < NW; ++q2) v += sm.lv[1][q2][tid];
-        store_coherent(a.vpart + (size_t)rc * a.rank + tid, v);
-      }
-    }
-    if (LORA && lsc != 0.0f) {  // s (h[k0..] A_gate[k0..]) B_gate: this wavefront's rows of B_gate
-#pragma unroll
-      for (int m = 0; m < kLoraMaxRank / NW; ++m) {
-        const int row = wv + m * NW;
-        if (row < a.rank) {
-          float vg = 0.0f;
-#pragma unroll
-          for (int q2 = 0; q2 < NW; ++q2) vg += sm.lv[0][q2][row];
-          vg *= lsc;
-          const u32x4 bq = *reinterpret_cast<const u32x4 *>(&ls.lb[row][lane * 16]);
-#pragma unroll
-          for (int v = 0; v < VEC; ++v) acc[v] = fmaf(vg, unpack<T>(bq, v), acc[v]);
-        }
-      }
-    }
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) sm.red[wv * CB + lane * VEC + v] = acc[v];
-    __syncthreads();
-    if (tid < CB && cb * CB + tid < d_ff) {
-      float s = 0.0f;
-#pragma unroll
-      for (int q2 = 0; q2 < NW; ++q2) s += sm.red[q2 * CB + tid];
-      store_coherent(a.gpart + (size_t)(cb * CB + tid) * dec_nrcp(a.nrc) + rc, s);
-    }
-    __syncthreads();  // LDS reuse by the next tile
+    sm.hq[i] = q;
   }
 }
 
 // ------------------------------------------------------------------ rows
 
 // The workgroup's wavefronts form two halves of 8; half hf takes its own
-// rows of the unit, and wavefront v of a half owns column chunks v, v + 8,
-// ... of d (64 lanes x 16 bytes each) for both projections.
+// part of the kept list, and wavefront v of a half owns column chunks v,
+// v + 8, ... of d (64 lanes x 16 bytes each) for both projections.
 
 // One batch: loads of this wavefront's chunks of the kept rows
 // list[r0 + r], r < R (rows at or past `end` are not read).
@@ -587,45 +471,11 @@ __device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)
   }
 }
 
-// LoRA: h . A_up from the gate launch's row-chunk partials, in a fixed
-// order: thread (q, i) adds chunks q, q + 8, ... (its first loads are issued
-// at the start of the rows launch, ahead of every streaming load of its
-// wavefront, since loads complete in issue order), then thread i adds the 8
-// groups, into sm.lz.
-constexpr int kLoraVG = 8, kLoraVQ = 4;
-__device__ __forceinline__ void lora_vu_issue(const DecodeArgs &a, float (&vq)[kLoraVQ]) {
-  const int R = a.rank, tid = threadIdx.x, i = tid % R, q = tid / R;
-#pragma unroll
-  for (int k = 0; k < kLoraVQ; ++k) {
-    const int rc = q + kLoraVG * k;
-    vq[k] = (q < kLoraVG && rc < a.nrc) ? load_coherent(a.vpart + (size_t)rc * R + i) : 0.0f;
-  }
-}
-__device__ __forceinline__ void lora_vu_finish(const DecodeArgs &a, const float (&vq)[kLoraVQ], DecodeSmem &sm) {
-  const int R = a.rank, tid = threadIdx.x, i = tid % R, q = tid / R;
-  float *flat = &sm.lv[0][0][0];
-  float v = 0.0f;
-#pragma unroll
-  for (int k = 0; k < kLoraVQ; ++k) v += vq[k];
-  const int rest = a.nrc - q - kLoraVG * kLoraVQ;  // chunks past the first loads
-  if (q < kLoraVG && rest > 0)
-    v += sum_coherent(a.vpart + (size_t)(q + kLoraVG * kLoraVQ) * R + i, (size_t)kLoraVG * R,
-                      (rest + kLoraVG - 1) / kLoraVG);
-  flat[tid] = v;
-  __syncthreads();
-  if (tid < R) {
-    float u = 0.0f;
-#pragma unroll
-    for (int g = 0; g < kLoraVG; ++g) u += flat[g * R + tid];
-    sm.lz[tid] = u;
-  }
-}
-
-// LoRA: for the kept rows list[i0 .. i0 + mn) of a unit, w_i = s (h A_up) .
+// LoRA: for the kept rows list[i0 .. i0 + mn), w_i = s (h A_up) .
 // B_up_T[j] into lr.lw and A_down[j] into lr.lad (R / VEC adjacent threads
-// per row, 16 bytes each).  The loads of the first pass are issued before
-// the unit's first row batches (loads complete in issue order) and used
-// after them; further passes (more than THREADS / (R / VEC) rows) follow.
+// per row, 16 bytes each).  The loads are issued before the first row
+// batches (loads complete in issue order) and used after them; one pass
+// covers a workgroup's list (at most 64 rows of R / VEC <= 16 pieces).
 template <typename T>
 struct LoraPrepRegs {
   u32x4 bu, ad;
@@ -664,128 +514,164 @@ __device__ __forceinline__ void lora_prep_use(const DecodeArgs &a, const DecodeS
   }
 }
 
-// Rows phase of workgroup w (of G): units w, w + G, ... of nblk x S units
-// (S = max(1, G / nblk) shares per column block); writes the workgroup's
-// partial y.  h is formed first (its loads overlap the first block's partial
-// sums).
+
+// ------------------------------------------------------------------ layer
+
+// One layer of one token (see the top of this file); workgroup w writes its
+// partial y to ypart[w] (and z to zpart[w] with adapters).
 template <typename T, bool LORA>
-__device__ void dec_rows(const DecodeArgs &a, int l, int base, int G, int w, DecodeSmem &sm, LoraRows<T> &lr) {
-  constexpr int VEC = Elem<T>::kVec, NW = kDecodeWaves;
-  constexpr int CB = dec_block_cols<T>();
+__global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a, int l) {
+  __shared__ DecodeSmem sm;
+  __shared__ LoraRows<T> lr;
+  constexpr int VEC = Elem<T>::kVec;
   constexpr int CH = 64 * VEC;              // elements per chunk (one 16-byte load per lane)
   constexpr int DMAX = kDecodeMaxD / CH;    // chunks per row
   constexpr int NCH = (DMAX + 7) / 8;       // chunks per wavefront of a half
   constexpr int R = 8 / NCH;                // rows of two batches (2 x 8 loads in flight per lane)
   constexpr int RB = R > 2 ? R / 4 : 1;     // rows per batch
-  static_assert(CB <= kDecodeThreads / 2 && 4 * R * 8 <= 2 * kDecodeMaxD, "single-token tiling");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), hw = wv & 7, hf = wv >> 3;
-  const int d = a.d, d_ff = a.d_ff, nblk = a.nblk;
+  const int w = blockIdx.x;
+  const int d = a.d, d_ff = a.d_ff;
   const size_t wl = (size_t)d * d_ff;
-  const int S = max(1, G / nblk), units = nblk * S;
+  const int base = token_is_base(a.route_mode, a.ids, a.lut, 0);
+  if (l == 0 && w == 0 && tid == 0 && a.route_out) a.route_out[0] = (uint8_t)base;
+  if (l == 0) SATS_TRACE_POINT(0);
+  const bool lora = LORA && !base;
   const float thr = base ? 0.0f : a.thr[l];
-  const __amdgpu_buffer_rsrc_t Wu = weight_rsrc(static_cast<const T *>(a.Wu) + (size_t)l * wl, (uint32_t)(wl * sizeof(T)));
-  const __amdgpu_buffer_rsrc_t Wd = weight_rsrc(static_cast<const T *>(a.Wd) + (size_t)l * wl, (uint32_t)(wl * sizeof(T)));
-  const __amdgpu_buffer_rsrc_t gp =
-      weight_rsrc(a.gpart, (uint32_t)((size_t)d_ff * dec_nrcp(a.nrc) * sizeof(float)));
+  const uint32_t wbytes = (uint32_t)(wl * sizeof(T));
+  const __amdgpu_buffer_rsrc_t Wg = weight_rsrc(static_cast<const T *>(a.Wg) + (size_t)l * wl, wbytes);
+  const __amdgpu_buffer_rsrc_t Wu = weight_rsrc(static_cast<const T *>(a.Wu) + (size_t)l * wl, wbytes);
+  const __amdgpu_buffer_rsrc_t Wd = weight_rsrc(static_cast<const T *>(a.Wd) + (size_t)l * wl, wbytes);
 
+  // ---- gate: the first two pieces of every wavefront go out first
+  GatePieces gp;
+  gp.c0 = w * a.cw;
+  gp.nc = max(1, min(a.cw, d_ff - gp.c0));
+  gp.npc = ((d * (int)sizeof(T) + 1023) / 1024 + kGateQ - 1) / kGateQ;
+  gp.wv = wv;
+  gp.P = (wv < gp.nc ? (gp.nc - wv + 15) / 16 : 0) * gp.npc;
+  u32x4 qa[kGateQ], qb[kGateQ];
+  gate_piece_issue<T>(Wg, gp, d, 0, qa);
+  gate_piece_issue<T>(Wg, gp, d, 1, qb);
+  // LoRA: B_gate at the block's columns (thread (c, i): ranks i, i + 16, ...)
+  // and the chunk partials of h A_gate, h A_up; used once h is formed
+  constexpr int BQ = kLoraMaxRank / kDecodeWaves;
+  float bgv[BQ];
+  float vq[2];
+  const int lc = tid & 63, li = tid >> 6;
+  if (lora) {
+    const T *bg = static_cast<const T *>(a.Bg) + (size_t)l * a.rank * d_ff + gp.c0 + min(lc, gp.nc - 1);
+#pragma unroll
+    for (int m = 0; m < BQ; ++m) {
+      const int i = li + m * kDecodeWaves;
+      bgv[m] = (i < a.rank) ? Elem<T>::get(bg + (size_t)i * d_ff) : 0.0f;
+    }
+    // thread t < 2 rank: adapter t / rank, rank index t % rank, chunks c = 0, 1 (more below)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      vq[c] = (tid < 2 * a.rank && c < a.nvc)
+                  ? load_coherent(a.vpart + ((size_t)c * 2 + tid / a.rank) * a.rank + tid % a.rank)
+                  : 0.0f;
+  }
   InputRegs<kDecodeThreads> ir;
+  dec_input_issue<T, kDecodeThreads>(a, l, ir);
+  for (int k = d + tid; k < kDecodeMaxD; k += kDecodeThreads) sm.hs[k] = 0.0f;  // past d: no products
+  dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, a.layer_in != nullptr && w == 0);
+  pack_input<T>(sm);
+  __syncthreads();
+  if (l == 0) SATS_TRACE_POINT(1);
+  if (lora) {  // h A_gate into lvg, h A_up into lz; then the gate adapter terms
+    if (tid < 2 * a.rank) {
+      float v = vq[0] + vq[1];
+      for (int c = 2; c < a.nvc; ++c) v += load_coherent(a.vpart + ((size_t)c * 2 + tid / a.rank) * a.rank + tid % a.rank);
+      if (tid < a.rank) sm.lvg[tid] = v;
+      else sm.lz[tid - a.rank] = v;
+    }
+    __syncthreads();
+    float t = 0.0f;
+#pragma unroll
+    for (int m = 0; m < BQ; ++m) {
+      const int i = li + m * kDecodeWaves;
+      if (i < a.rank) t = fmaf(sm.lvg[i], bgv[m], t);
+    }
+    sm.lv[0][li][lc] = t;
+  }
+  float acc[2] = {0.0f, 0.0f};
+  for (int p = 0; p < gp.P; p += 2) {
+    gate_piece_use<T>(sm, gp, p, qa, acc, sm.red);
+    if (p + 2 < gp.P) gate_piece_issue<T>(Wg, gp, d, p + 2, qa);
+    if (p + 1 < gp.P) {
+      gate_piece_use<T>(sm, gp, p + 1, qb, acc, sm.red);
+      if (p + 3 < gp.P) gate_piece_issue<T>(Wg, gp, d, p + 3, qb);
+    }
+  }
+  __syncthreads();
+  if (l == 0) SATS_TRACE_POINT(2);
+  // ---- keep list: one lane per column
+  if (wv == 0) {
+    const bool on = lane < gp.nc && gp.c0 + lane < d_ff;
+    float av = on ? sm.red[lane] : 0.0f;
+    if (lora && a.lscale != 0.0f) {
+      float t = 0.0f;
+      for (int q = 0; q < kDecodeWaves; ++q) t += sm.lv[0][q][lane];
+      av += a.lscale * t;
+    }
+    const float g = silu(av);
+    const bool keep = on && (base || fabsf(g) >= thr);
+    if (a.keep_out && on) a.keep_out[(size_t)l * d_ff + gp.c0 + lane] = (uint8_t)keep;
+    const uint64_t bal = __ballot(keep);
+    const int rk = __popcll(bal & ((1ull << lane) - 1ull));
+    if (keep) {
+      sm.mj[rk] = gp.c0 + lane;
+      sm.mg[rk] = g;
+    }
+    if (lane == 0) sm.wcnt[0] = __popcll(bal);
+  }
+  __syncthreads();
+  const int tot = sm.wcnt[0];
+  if (l == 0) SATS_TRACE_POINT(4);
+
+  // ---- rows: half hf takes list[b, e)
+  const int hn = (tot + 1) / 2;
+  const int b = hf * hn, e = min(tot, (hf + 1) * hn);
+  const int nbt = (hn + RB - 1) / RB;  // batches (both halves run the same number)
   float hreg[NCH][VEC];  // h at this lane's columns
   float yacc[NCH][VEC];
+  u32x4 au[RB][NCH], ad[RB][NCH], cu[RB][NCH], cd[RB][NCH];
+  LoraPrepRegs<T> lp;
+  if (lora) lora_prep_load<T>(a, l, sm, 0, tot, 0, lp);
+  if (nbt > 0) rows_issue<T, RB, NCH>(Wu, Wd, sm, b, e, d, au, ad);
+  if (nbt > 1) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + RB, e, d, cu, cd);
 #pragma unroll
   for (int c = 0; c < NCH; ++c)
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) hreg[c][v] = yacc[c][v] = 0.0f;
-  int par = 0;  // LDS slot parity for the parts of u
-  const bool lora = LORA && !base;
+    for (int v = 0; v < VEC; ++v) {
+      const int k = (hw + c * 8) * CH + lane * VEC + v;
+      hreg[c][v] = (k < d) ? sm.hs[k] : 0.0f;
+      yacc[c][v] = 0.0f;
+    }
   float zh = 0.0f;  // LoRA, lane i < rank of wavefront 0 of each half: z_i over the half's kept rows
-  float vq[kLoraVQ];
-  if (lora) {
-    lora_vu_issue(a, vq);
-    asm volatile("" ::: "memory");  // keeps these loads ahead of the partial sums' and the rows'
+  if (lora) {  // the up adapter's terms and A_down of the kept rows
+    lora_prep_use<T>(a, sm, lr, 0, tot, 0, lp);
+    __syncthreads();
   }
-
-  for (int un = w; un < units; un += G) {
-    const int cb = un % nblk, sub = un / nblk;
-    // the block's keep list (every workgroup of the block forms the same one)
-    const int gcol = cb * CB + tid;
-    bool keep = false;
-    float g = 0.0f;
-    if (tid < CB && gcol < d_ff) {
-      g = silu(gate_sum(gp, gcol, a.nrc));
-      keep = base || (fabsf(g) >= thr);
-      if (sub == 0 && a.keep_out) a.keep_out[(size_t)l * d_ff + gcol] = (uint8_t)keep;
-    }
-    // h's loads follow the partials' (the keep list is on the critical path)
-    // and are waited for only after the first rows are issued
-    if (un == w) dec_input_issue<T, kDecodeThreads>(a, l, ir);
-    const uint64_t bal = __ballot(keep);
-    const int rank = __popcll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) sm.wcnt[wv] = __popcll(bal);
-    __syncthreads();
-    int off = 0, tot = 0;
-    for (int i = 0; i < NW; ++i) {
-      off += (i < wv) ? sm.wcnt[i] : 0;
-      tot += sm.wcnt[i];
-    }
-    if (keep) {
-      sm.mj[off + rank] = gcol;
-      sm.mg[off + rank] = g;
-    }
-    __syncthreads();
-    // this unit's rows: list[i0, i0 + mn); half hf takes [b, e)
-    const int i0 = (int)(((int64_t)sub * tot) / S);
-    const int mn = (int)(((int64_t)(sub + 1) * tot) / S) - i0;
-    const int hn = (mn + 1) / 2;
-    const int b = i0 + hf * hn, e = i0 + min(mn, (hf + 1) * hn);
-    if (l == 0 && un == w) SATS_TRACE_POINT(4);
-    if (lora && un == w) lora_vu_finish(a, vq, sm);
-    // batches of RB rows in two register sets: the next batch is always in
-    // flight while one is used (both halves run the same number of batches)
-    const int nbt = (hn + RB - 1) / RB;
-    u32x4 au[RB][NCH], ad[RB][NCH], cu[RB][NCH], cd[RB][NCH];
-    LoraPrepRegs<T> lp;
-    if (lora) lora_prep_load<T>(a, l, sm, i0, mn, 0, lp);
-    if (nbt > 0) rows_issue<T, RB, NCH>(Wu, Wd, sm, b, e, d, au, ad);
-    if (nbt > 1) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + RB, e, d, cu, cd);
-    if (un == w) {
-      dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, false);
-#pragma unroll
-      for (int c = 0; c < NCH; ++c)
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-          const int k = (hw + c * 8) * CH + lane * VEC + v;
-          hreg[c][v] = (k < d) ? sm.hs[k] : 0.0f;
-        }
-    }
-    if (lora) {  // the up adapter's terms and A_down of this unit's rows
-      if (l == 0 && un == w) SATS_TRACE_POINT(8);
-      const int rq = a.rank / VEC;
-      lora_prep_use<T>(a, sm, lr, i0, mn, 0, lp);
-      for (int b0 = kDecodeThreads; b0 < mn * rq; b0 += kDecodeThreads) {
-        lora_prep_load<T>(a, l, sm, i0, mn, b0, lp);
-        lora_prep_use<T>(a, sm, lr, i0, mn, b0, lp);
-      }
-      __syncthreads();
-      if (l == 0 && un == w) SATS_TRACE_POINT(9);
-    }
-    for (int i = 0; i < nbt; i += 2) {
-      rows_consume<T, RB, NCH>(sm, hreg, yacc, b + i * RB, e, par, au, ad, lora, lr, a.rank, zh);
+  int par = 0;  // LDS slot parity for the parts of u
+  for (int i = 0; i < nbt; i += 2) {
+    rows_consume<T, RB, NCH>(sm, hreg, yacc, b + i * RB, e, par, au, ad, lora, lr, a.rank, zh);
+    par ^= 1;
+    if (i + 2 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
+    if (i + 1 < nbt) {
+      rows_consume<T, RB, NCH>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
       par ^= 1;
-      if (i + 2 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
-      if (i + 1 < nbt) {
-        rows_consume<T, RB, NCH>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
-        par ^= 1;
-        if (i + 3 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
-      }
+      if (i + 3 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
     }
-    __syncthreads();  // the next unit rewrites the list
   }
+  __syncthreads();
   if (lora) {  // z = half 0's sum + half 1's
     if (wv == 8 && lane < a.rank) lr.lw[lane] = zh;
     __syncthreads();
     if (wv == 0 && lane < a.rank) store_coherent(a.zpart + (size_t)w * a.rank + lane, zh + lr.lw[lane]);
-    if (l == 0) SATS_TRACE_POINT(10);
   }
   if (l == 0) SATS_TRACE_POINT(5);
   // the two halves' sums, added in half order, are this workgroup's partial y
@@ -900,74 +786,20 @@ __device__ void dec_reduce(const DecodeArgs &a, int l, int w, DecodeSmem &sm, bo
   (void)NW;
 }
 
+
 // ------------------------------------------------------------------ kernels
 
-// Gate tiles (any grid); LORA: with the adapters of the sparse path.
-template <typename T, bool LORA>
-__global__ __launch_bounds__(kGateThreads) void dec_gate_kernel(DecodeArgs a, int l) {
+// Second reduction stage with adapters: workgroup w (of RW) takes one slice
+// of y and adds s z B_down (z summed over the partials in workgroup order).
+template <typename T>
+__global__ __launch_bounds__(kDecodeThreads) void dec_reduce_lora_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
-  __shared__ LoraGateSmem ls;
-  if (blockIdx.x == 0 && threadIdx.x == 0)  // the previous rows launch has finished
-    __hip_atomic_store(a.done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (l == 0 && blockIdx.x == 0 && threadIdx.x == 0) {
-    const int base = token_is_base(a.route_mode, a.ids, a.lut, 0);
-    a.state[0] = base;
-    if (a.route_out) a.route_out[0] = (uint8_t)base;
-  }
-  if (l == 0) SATS_TRACE_POINT(0);
-  dec_gate<T, LORA>(a, l, sm, ls, a.layer_in != nullptr && blockIdx.x == 0);
-  if (l == 0) SATS_TRACE_POINT(2);
+  dec_reduce<T, true>(a, l, blockIdx.x, sm, token_is_base(a.route_mode, a.ids, a.lut, 0));
 }
-
-// Rows: G workgroups, each writing its partial y.  Without adapters the
-// second reduction stage is a launch of its own (dec_reduce_kernel).  With
-// adapters it follows in this launch: the last RW workgroups to finish each
-// sum one slice of y (and add s z B_down) over every partial (workgroup
-// order).  They wait only for workgroups that are running or done, with
-// nothing of their own in flight; the wait is bounded (it raises the device
-// error flag instead of hanging).  The count goes back to zero at the start
-// of the next gate launch (which always comes before the next rows launch).
-constexpr int kSpinLimit = 1 << 20;  // polls of one wait (each a device-coherent load)
-
-template <typename T, bool LORA>
-__global__ __launch_bounds__(kDecodeThreads) void dec_rows_kernel(DecodeArgs a, int l) {
-  __shared__ DecodeSmem sm;
-  __shared__ LoraRows<T> lr;
-  if (l == 0) SATS_TRACE_POINT(3);
-  const int base = a.state[0];
-  dec_rows<T, LORA>(a, l, base, a.G, blockIdx.x, sm, lr);
-  if constexpr (!LORA) return;  // the second stage is dec_reduce_kernel
-  const int tid = threadIdx.x, G = a.G;
-  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial-y stores have completed
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __syncthreads();
-  if (tid == 0) sm.flag = (int)__hip_atomic_fetch_add(a.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  const int ticket = sm.flag;
-  if (ticket < G - a.RW) return;
-  if (tid == 0) {
-    int polls = 0;
-    while (__hip_atomic_load(a.done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (unsigned)G) {
-      if (++polls >= kSpinLimit) {
-        __hip_atomic_store(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  __syncthreads();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  if (l == 0) SATS_TRACE_POINT(6);
-  dec_reduce<T, LORA>(a, l, ticket - (G - a.RW), sm, base);
-  if (l == 0) SATS_TRACE_POINT(7);
-}
-
 
 // Second reduction stage of a layer without adapters, a launch of its own
-// (the kernel boundary orders it after every partial; a hand-off inside the
-// rows launch -- last arrivals counted, the reducers waiting for the count --
-// measured 2 us slower per layer, its stores and polls queued behind the
-// other workgroups' row loads).  Workgroup w owns columns [16 w, 16 w + 16):
+// (the kernel boundary orders it after every partial).  Workgroup w owns
+// columns [16 w, 16 w + 16):
 // 16 groups of threads each add every 16th partial in workgroup order, the
 // groups are added in order, and y (or the rounded output on the last layer)
 // and the slice's sum of squares for the next layer's input are written.

@@ -23,9 +23,10 @@
 //
 // MFMA operand layout of v_mfma_f32_16x16x32_bf16 (wavefront of 64 lanes):
 // lane l supplies A[l % 16][8 (l / 16) + e] and B[8 (l / 16) + e][l % 16],
-// e = 0..7, and receives C[4 (l / 16) + r][l % 16], r = 0..3.  W_gate and
-// W_down are stored with the output dimension contiguous, so their operands
-// are read from LDS transposed; W_up_T and H rows are already k-major.
+// e = 0..7, and receives C[4 (l / 16) + r][l % 16], r = 0..3.  W_gate_T,
+// W_up_T and H rows are k-major (one row per output column or input row);
+// W_down is stored with the output dimension contiguous, so its operand is
+// read from LDS transposed.
 #pragma once
 
 #include "kernels.hpp"
@@ -115,8 +116,9 @@ struct DenseArgs {
   const float *thr;       // threshold of this layer (gate/up)
   uint8_t *keep_out;      // optional inspection: [n][N] keep flags, rows through perm
   const uint16_t *H;      // [n_dense][K] bf16 layer input (gate/up) or p (down)
-  const uint16_t *Wb;     // W_gate [K][N] or W_down [K][N] (output dim contiguous)
-  const uint16_t *Wt;     // W_up_T [N][K] (gate/up only)
+  const uint16_t *Wb;     // down: W_down [K][N] (output dim contiguous)
+  const uint16_t *Wg;     // gate/up: W_gate_T [N][K]
+  const uint16_t *Wt;     // gate/up: W_up_T [N][K]
   uint16_t *P;            // gate/up output p, [n_dense][N] bf16
   uint8_t *uflag;         // gate/up: [N] 1 where some row keeps the column (the union of the
                           // keep sets; every column once a base-path row is in the group);
@@ -151,12 +153,12 @@ struct DenseArgs {
 // A buffer load into LDS writes 16 bytes per lane at consecutive addresses,
 // so the tile layout is chosen through the global address each lane reads.
 // LDS tiles:
-//   k-row tile  W_gate rows (128 bytes each) or W_down rows (256 bytes each)
-//               of the stage; chunk q (16 bytes) of row r sits at position
-//               q ^ (2 ((r >> 3) & 3)), so that the transposed operand reads
-//               of a wavefront touch distinct banks
-//   row tile    W_up_T rows n0..n0+63 or H rows, 128 bytes (64 k) each;
-//               chunk q of row r sits at q ^ ((r >> 1) & 7)
+//   k-row tile  W_down rows (256 bytes each) of the stage; chunk q (16
+//               bytes) of row r sits at position q ^ (2 ((r >> 3) & 3)), so
+//               that the transposed operand reads of a wavefront touch
+//               distinct banks
+//   row tile    W_gate_T or W_up_T rows n0..n0+63, or H rows, 128 bytes
+//               (64 k) each; chunk q of row r sits at q ^ ((r >> 1) & 7)
 
 constexpr int kDenseThreads = 512;             // 8 wavefronts
 constexpr int kDenseKC = 64;                   // k rows per stage
@@ -260,16 +262,15 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   const int n0 = blockIdx.x * kDenseNT;
   const int K = a.K, N = a.N;
   const int S = K / kDenseKC;
-  const __amdgpu_buffer_rsrc_t rsg = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
+  const __amdgpu_buffer_rsrc_t rsg = dense_rsrc(a.Wg, (uint32_t)((size_t)K * N * 2));
   const __amdgpu_buffer_rsrc_t rsu = dense_rsrc(a.Wt, (uint32_t)((size_t)K * N * 2));
   const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
   // wavefront w loads rows 8 w .. 8 w + 7 of each tile (1 KB); lane: row dr, slot dp
   const int dr = 8 * w + (lane >> 3), dp = lane & 7;
-  const uint32_t og = (uint32_t)(((size_t)dr * N + n0 + 8 * krow_pos(dr, dp)) * 2);
-  const uint32_t ou = (uint32_t)(((size_t)(n0 + dr) * K + 8 * row_pos(dr, dp)) * 2);
+  const uint32_t ou = (uint32_t)(((size_t)(n0 + dr) * K + 8 * row_pos(dr, dp)) * 2);  // W_gate_T and W_up_T
   const uint32_t oh = (uint32_t)(((size_t)dr * K + 8 * row_pos(dr, dp)) * 2);
   const bool hv = dr < nd;
-  const uint32_t sg = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;  // per stage
+  const uint32_t sk = kDenseKC * 2;  // per stage
   f32x4v acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4v{0.f, 0.f, 0.f, 0.f};
@@ -277,14 +278,14 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   {                                                                                          \
     const bool v_ = (SN) < S;                                                                \
     const uint32_t ss_ = (uint32_t)(SN);                                                     \
-    dma16<2>(rsg, (BUF) + w * 1024, dense_off(v_, og + ss_ * sg, 0));                        \
+    dma16<2>(rsg, (BUF) + w * 1024, dense_off(v_, ou + ss_ * sk, 0));                        \
     dma16<2>(rsu, (BUF) + 8192 + w * 1024, dense_off(v_, ou + ss_ * sk, 1));                 \
     dma16<0>(rsh, (BUF) + 16384 + w * 1024, dense_off(v_ && hv, oh + ss_ * sk, 2));          \
   }
 #define SATS_GU_COMPUTE(BUF)                                                                 \
   {                                                                                          \
     _Pragma("unroll") for (int j = 0; j < 2; ++j) {                                          \
-      const bf16x8 b_ = mat == 0 ? krow_operand((BUF), 128, c, j, g) : row_operand((BUF) + 8192, c, j, g); \
+      const bf16x8 b_ = row_operand((BUF) + 8192 * mat, c, j, g);                            \
       _Pragma("unroll") for (int mt = 0; mt < MT; ++mt)                                      \
         acc[mt] = mfma16(row_operand((BUF) + 16384, 16 * mt + l16, j, g), b_, acc[mt]);      \
     }                                                                                        \

@@ -3,7 +3,7 @@
 // One layer runs as three kernels over a tile of at most NT tokens
 // (blockIdx.z selects the tile):
 //
-//   gate_kernel   a = h . W_gate (split over rows of W_gate), then the last
+//   gate_kernel   a_j = W_gate_T[j] . h (split over chunks of d), then the last
 //                 workgroup to finish a column block sums the row-split
 //                 partials in a fixed order and applies SiLU (Eq. 2), the
 //                 keep rule |g| >= t (Eq. 4-5; every column for base-path
@@ -31,10 +31,7 @@
 namespace sats {
 
 constexpr int kThreads = 256;
-#ifndef SATS_GATE_LANES
-#define SATS_GATE_LANES 16
-#endif
-constexpr int kGateLanes = SATS_GATE_LANES;  // lanes across a gate row segment (x 16 bytes)
+constexpr int kGateCols = 64;  // gate columns per column block of the batch kernels
 constexpr float kGlueEps = 1e-6f;
 
 // ------------------------------------------------------------------ elements
@@ -189,7 +186,7 @@ __device__ __forceinline__ int token_is_base(int mode, const int32_t *ids, const
 // ------------------------------------------------------------------ gate
 
 struct GateArgs {
-  const void *W;         // W_gate of this layer, [d][d_ff]
+  const void *W;         // W_gate_T of this layer, [d_ff][d]
   const void *x;         // layer 0: call input [n][d]; otherwise null
   const float *ybuf;     // layer > 0: previous layer's y, [P][d]
   const float *ss;       // layer > 0: per-slice sums of y^2, [tiles][n_slices][NT]
@@ -215,16 +212,14 @@ struct GateArgs {
 
 template <typename T, int VEC, int NT>
 __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
-  constexpr int CL = (VEC == 1) ? 64 : kGateLanes;  // lanes across one row segment
-  constexpr int RG = kThreads / CL;                 // row groups
-  constexpr int CB = CL * VEC;                      // columns per block
+  constexpr int CB = kGateCols;  // columns per block
+  constexpr int STEP = 64 * VEC;  // k covered by one wavefront load
   extern __shared__ float smem[];
   __shared__ int flag;
   __shared__ int wcnt[kThreads / 64];
   __shared__ float tscale[NT];
   __shared__ int tbase[NT];
   __shared__ int tskip[NT];
-
   const int tid = threadIdx.x;
   const int blk = blockIdx.x, ks = blockIdx.y, tile = blockIdx.z;
   if (a.ctl[0] == a.n && a.skip[0]) return;  // every token is on the dense MFMA path
@@ -276,59 +271,45 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
   }
   __syncthreads();
 
-  // ---- partial gate projection over this row chunk
-  const int cl = tid % CL, rg = tid / CL;
-  const int c0 = blk * CB + cl * VEC;
-  float acc[NT][VEC];
+  // ---- partial gate projection over rows [k0, k0 + kc): wavefront wv takes
+  // columns wv, wv + 4, ... of the block, each lane VEC consecutive weights of
+  // a row of W_gate_T per load; the lanes are added in a fixed order
+  const int lane = tid & 63, wv = tid >> 6;
+  for (int cc = wv; cc < CB; cc += kThreads / 64) {
+    const int col = blk * CB + cc;
+    float u[NT];
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+    for (int t = 0; t < NT; ++t) u[t] = 0.0f;
+    if (col < a.d_ff) {
+      const T *__restrict__ wp = W + (size_t)col * a.d + k0;
+      int k = lane * VEC;
+      if constexpr (VEC > 1) {
+        for (; k + STEP < kc; k += 2 * STEP) {  // two loads in flight
+          const u32x4 w0 = load_raw<T>(wp + k), w1 = load_raw<T>(wp + k + STEP);
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) acc[t][v] = 0.0f;
-  if (c0 < a.d_ff) {
-    const T *__restrict__ wp = W + (size_t)k0 * a.d_ff + c0;
-    int k = rg;
-    if constexpr (VEC > 1) {
-      // whole batches of 8 rows: 8 loads in flight before the first use
-      for (; k + 7 * RG < kc; k += 8 * RG) {
-        u32x4 wq[8];
+          for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) wq[u] = load_raw<T>(wp + (size_t)(k + u * RG) * a.d_ff);
+            for (int v = 0; v < VEC; ++v) {
+              u[t] = fmaf(hs[t * a.KC + k + v], unpack<T>(w0, v), u[t]);
+              u[t] = fmaf(hs[t * a.KC + k + STEP + v], unpack<T>(w1, v), u[t]);
+            }
+        }
+      }
+      for (; k < kc; k += STEP) {
+        float w[VEC];
+        load_vec<T, VEC>(wp + k, w);
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int t = 0; t < NT; ++t)
 #pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            const float hv = hs[t * a.KC + k + u * RG];
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(hv, unpack<T>(wq[u], v), acc[t][v]);
-          }
+          for (int v = 0; v < VEC; ++v) u[t] = fmaf(hs[t * a.KC + k + v], w[v], u[t]);
       }
     }
-    for (; k < kc; k += RG) {
-      float w[VEC];
-      load_vec<T, VEC>(wp + (size_t)k * a.d_ff, w);
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const float hv = hs[t * a.KC + k];
+    for (int t = 0; t < NT; ++t) u[t] = wave_sum(u[t]);
+    if (lane == 0 && col < a.d_ff) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(hv, w[v], acc[t][v]);
-      }
-    }
-  }
-  __syncthreads();
-  float *red = smem;  // [RG][NT][CB]
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) red[(rg * NT + t) * CB + cl * VEC + v] = acc[t][v];
-  __syncthreads();
-  for (int o = tid; o < NT * CB; o += kThreads) {
-    const int t = o / CB, c = o - t * CB;
-    const int col = blk * CB + c;
-    if (t < nt && col < a.d_ff) {
-      float s = 0.0f;
-#pragma unroll
-      for (int r = 0; r < RG; ++r) s += red[(r * NT + t) * CB + c];
-      store_coherent(a.gpart + (((size_t)tile * a.KS + ks) * NT + t) * a.d_ff + col, s);
+      for (int t = 0; t < NT; ++t)
+        if (t < nt) store_coherent(a.gpart + (((size_t)tile * a.KS + ks) * NT + t) * a.d_ff + col, u[t]);
     }
   }
 
@@ -351,7 +332,6 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(GateArgs a) {
   }
   const bool act = mask != 0;
   const uint64_t bal = __ballot(act);
-  const int lane = tid & 63, wv = tid >> 6;
   const int rank = __popcll(bal & ((1ull << lane) - 1ull));
   if (lane == 0) wcnt[wv] = __popcll(bal);
   __syncthreads();

@@ -113,7 +113,7 @@ thread_local sats_options g_opt{};
 constexpr int kGateTarget = 2048, kDownTarget = 512, kUpRowsPerWave = 2;
 
 struct Plan {
-  int vec, CL, RG, CB;     // down lanes per row segment; gate row groups and columns per block
+  int vec, CL, CB;         // down lanes per row segment; gate columns per block
   int nblocks;             // gate column blocks
   int KS, KC;              // gate row split
   int SW, n_slices, KCH;   // down column slices and list chunks
@@ -125,15 +125,16 @@ Plan make_plan(int64_t d, int64_t d_ff, int esz, bool vec_ok, int n_pass) {
   Plan p{};
   p.vec = vec_ok ? 16 / esz : 1;
   p.CL = (p.vec == 1) ? 64 : 16;  // down-projection lanes per row segment
-  const int gate_cl = (p.vec == 1) ? 64 : sats::kGateLanes;
-  p.RG = sats::kThreads / gate_cl;
-  p.CB = gate_cl * p.vec;
+  p.CB = sats::kGateCols;
   p.nblocks = (int)((d_ff + p.CB - 1) / p.CB);
   p.NT = (n_pass == 1) ? 1 : 4;
-  int ks = round_pow2_down(std::max(1, kGateTarget / p.nblocks));
-  ks = std::min<int64_t>(ks, std::max<int64_t>(1, d / p.RG));
+  // gate: d in chunks of whole wavefront loads (64 x vec elements), about
+  // kGateTarget workgroups, at most 1024 rows of h per chunk in LDS
+  const int64_t step = 64 * (int64_t)p.vec;
+  int64_t ks = round_pow2_down(std::max(1, kGateTarget / p.nblocks));
+  ks = std::min<int64_t>(ks, std::max<int64_t>(1, d / step));
   ks = std::max<int64_t>(ks, (d + 1023) / 1024);
-  p.KC = (int)((d + ks - 1) / ks);
+  p.KC = (int)((((d + ks - 1) / ks) + step - 1) / step * step);
   p.KS = (int)((d + p.KC - 1) / p.KC);
   p.SW = p.CL * p.vec;
   p.n_slices = (int)((d + p.SW - 1) / p.SW);
@@ -164,9 +165,7 @@ struct Buffers {
   uint32_t *blk_mask;
   uint8_t *keep;
   float *ypart, *sspart;  // single-token path: per-workgroup partial y and sums of squares
-  float *dgpart;          // single-token path: partial gate sums per row chunk
-  float *dvpart, *dzpart; // single-token path, LoRA: partial h . A_up per row chunk, z per rows workgroup
-  int *dstate;            // single-token path: the token's route
+  float *dvpart, *dzpart; // single-token path, LoRA: partial h . A per input row chunk, z per layer workgroup
   int *perm, *ctl;        // batched path: token partition and dense-group control words
   uint8_t *skip, *gbase;
   uint16_t *xd, *hnext, *pdense;  // dense group (MFMA): inputs, next inputs, p
@@ -178,11 +177,10 @@ struct Buffers {
 // Layout for passes of up to `pass` tokens (the counters live in their own
 // zero-initialised allocation).
 struct DecodePlan {
-  int G = 0;           // rows workgroups, one partial y each (0: path not used)
-  int RW = 0;          // reduce workgroups (128-byte column slices where d allows)
-  int nblk = 0;        // gate column blocks
-  int nrc = 0;         // gate row chunks
-  int gate_grid = 0;   // workgroups of the gate launch
+  int G = 0;           // layer workgroups, one partial y each (0: path not used)
+  int cw = 0;          // gate columns per layer workgroup
+  int RW = 0;          // reduce workgroups
+  int nvc = 0;         // LoRA input launch: row chunks of the adapters' A matrices
 };
 
 size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, int esz, int64_t L,
@@ -215,10 +213,8 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.pdense = c.take<uint16_t>(Pp * d_ff);
   t.uflag = c.take<uint8_t>(d_ff);
   t.ddpart = c.take<float>((int64_t)sats::kDenseMaxKsplit * Pp * d);
-  t.dgpart = c.take<float>((int64_t)sats::dec_nrcp(dp.nrc) * d_ff);
-  t.dvpart = c.take<float>((int64_t)dp.nrc * sats::kLoraMaxRank);
+  t.dvpart = c.take<float>((int64_t)dp.nvc * 2 * sats::kLoraMaxRank);
   t.dzpart = c.take<float>((int64_t)dp.G * sats::kLoraMaxRank);
-  t.dstate = c.take<int>(64);
   if (lora_rank > 0) {  // batched LoRA calls only
     t.blv = c.take<float>(2 * (int64_t)sats::kDenseMaxTokens * lora_rank);
     t.blvpart = c.take<float>(2 * 4 * (int64_t)sats::kLoraVChunks * 16 * lora_rank);
@@ -234,7 +230,6 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
 constexpr size_t kCtl = 512;
 constexpr size_t kErr = 320;
 constexpr size_t kLoraV = 448;  // [8] batched LoRA: arrivals of the s (h A) chunks
-constexpr size_t kDone = 322;  // single-token rows launch: partials written (second-stage reduction)
 
 size_t counter_count(const Plan &p, int64_t pass, const DecodePlan &dp) {
   const int64_t tiles = ((pass + 3) / 4) * 4;
@@ -251,8 +246,6 @@ int device_cus() {
   return cus;
 }
 
-// Single-token rows workgroups: the option, else one per compute unit.
-int dec_rows_wgs(int cus = -1) { return g_opt.dec_rows_wgs > 0 ? g_opt.dec_rows_wgs : (cus >= 0 ? cus : device_cus()); }
 
 // Batch passes of np tokens: whether the matrix-core kernels run (bf16, the
 // vector layout, shapes on their tiles and matrices below 2 GB) and whether
@@ -301,31 +294,25 @@ int ensure_workspace(hipStream_t stream, size_t bytes, size_t n_counters, Worksp
   return SATS_OK;
 }
 
-// Single-token plan.  h is held in LDS (d <= kDecodeMaxD); `G` workgroups
-// (at most kDecodeMaxG) take the rows and reduce phases, each reduce
-// workgroup owning at most one column per thread; gate tiles are one column
-// block by about d / nrc rows.  Returns false when the shape does not fit.
-bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, int lora_rank = 0, int cus = -1) {
+// Single-token plan.  h is held in LDS (d <= kDecodeMaxD).  Layer workgroup
+// w owns gate columns [cw w, cw w + cw): cw is the option, else d_ff spread
+// over the compute units (one workgroup each), at least 8 and at most 64
+// columns.  The second reduction stage: without adapters a launch of
+// 16-column slices; with adapters about 64 columns per workgroup (each one
+// also sums every partial z), a whole number of 16-column slices.
+// Returns false when the shape does not fit.
+bool make_decode_plan(int64_t d, int64_t d_ff, int esz, DecodePlan *dp, int lora_rank = 0, int cus = -1) {
   DecodePlan q{};
-  const int64_t cb = (int64_t)(16 / esz) * 64;
-  q.G = G;
-  q.nblk = (int)((d_ff + cb - 1) / cb);
-  const int64_t tiles = g_opt.dec_gate_tiles > 0 ? g_opt.dec_gate_tiles : 256;
-  int64_t nrc = std::max<int64_t>(1, tiles / q.nblk);
-  nrc = std::min<int64_t>(nrc, std::max<int64_t>(1, d / (sats::kGateThreads / 64)));  // a row per wavefront
-  q.nrc = (int)nrc;
-  q.gate_grid = q.nblk * q.nrc;
-  // second reduction stage: without adapters a launch of 16-column slices;
-  // with adapters the last RW rows workgroups to finish take one slice of y
-  // each, 32 columns (128 bytes of each partial) or more, RW kept to a
-  // quarter of the CUs so that the reducers, which wait for the others,
-  // never fill the device
-  // (and at most 64 columns each, a whole number of 16-column slices:
-  // 16 groups of partials per column, sums of squares per 16 columns)
+  if (cus < 0) cus = device_cus();
+  int64_t cw = g_opt.dec_block_cols > 0 ? g_opt.dec_block_cols
+                                        : std::max<int64_t>(8, (d_ff + std::max(cus, 1) - 1) / std::max(cus, 1));
+  cw = std::min<int64_t>(cw, sats::kDecodeMaxCols);
+  q.cw = (int)cw;
+  const int64_t G = (d_ff + cw - 1) / cw;
+  q.G = (int)std::min<int64_t>(G, sats::kDecodeMaxG + 1);
+  q.nvc = (int)((d + sats::kVRows - 1) / sats::kVRows);
   if (lora_rank > 0) {
-    const int64_t rw0 = std::min<int64_t>(G, std::max<int64_t>((d + 63) / 64,
-                                                               std::min<int64_t>(std::max<int64_t>(1, (d + 31) / 32),
-                                                                                 std::max(1, (cus >= 0 ? cus : device_cus()) / 4))));
+    const int64_t rw0 = (d + 63) / 64;
     const int64_t cpw = (((d + rw0 - 1) / rw0 + sats::kRedCols - 1) / sats::kRedCols) * sats::kRedCols;
     q.RW = (int)((d + cpw - 1) / cpw);
   } else {
@@ -333,7 +320,7 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, int G, DecodePlan *dp, i
   }
   // buffer descriptors address one layer's matrix with 32-bit offsets, and
   // 0x80000000 is the offset that reads zeros: every matrix must stay below 2 GB
-  const bool ok = G >= 1 && G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
+  const bool ok = G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
                   (d + q.RW - 1) / q.RW <= sats::kDecodeThreads / (sats::kRedThreads / sats::kRedCols) &&
                   (uint64_t)d * (uint64_t)d_ff * (uint64_t)esz < (1ull << 31);
   *dp = ok ? q : DecodePlan{};
@@ -458,7 +445,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       da.keep_out = inspect_lists ? b.keep : nullptr;
       da.uflag = b.uflag;
       da.H = (l == 0) ? b.xd : b.hnext;
-      da.Wb = static_cast<const uint16_t *>(c.Wg) + l * wl;
+      da.Wg = static_cast<const uint16_t *>(c.Wg) + l * wl;
       da.Wt = static_cast<const uint16_t *>(c.Wu) + l * wl;
       da.P = b.pdense;
       da.K = (int)d;
@@ -579,7 +566,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     g.KS = p.KS;
     g.KC = p.KC;
     g.nblocks = p.nblocks;
-    const size_t gate_lds = sizeof(float) * std::max<size_t>((size_t)NT * p.KC, (size_t)p.RG * NT * p.CB);
+    const size_t gate_lds = sizeof(float) * (size_t)NT * p.KC;
     {
       TimedLaunch tl(SATS_K_GATE, c.stream);
       hipExtLaunchKernelGGL((gate_kernel<T, VEC, NT>), dim3(p.nblocks, p.KS, tiles), dim3(kThreads), gate_lds,
@@ -644,6 +631,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
 template <typename T>
 int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *counters) {
   using namespace sats;
+  (void)counters;
   DecodeArgs a{};
   a.x = c.x;
   a.out = c.out;
@@ -657,16 +645,11 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   a.L = (int)c.L;
   a.d = (int)c.d;
   a.d_ff = (int)c.d_ff;
-  a.nblk = dp.nblk;
-  a.nrc = dp.nrc;
-  a.gpart = b.dgpart;
-  a.state = b.dstate;
+  a.cw = dp.cw;
   a.G = dp.G;
   a.RW = dp.RW;
   a.ypart = b.ypart;
-  a.done = counters + kDone;
   a.nss = (int)((c.d + kRedCols - 1) / kRedCols);
-  a.err = counters + kErr;
   a.ybuf = b.ybuf;
   a.sspart = b.sspart;
   a.route_out = c.route_out;
@@ -683,36 +666,37 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   a.rank = (int)c.rank;
   a.lscale = c.lscale;
   a.vpart = b.dvpart;
+  a.nvc = dp.nvc;
   a.zpart = b.dzpart;
-  // two plain launches per layer (the rows launch ends with the second
-  // reduction stage); kernel boundaries order the phases
+  // per layer: [LoRA input] -> layer -> second reduction stage; kernel
+  // boundaries order the phases
   for (int l = 0; l < (int)c.L; ++l) {
+    if (c.Ag) {
+      TimedLaunch tl(SATS_K_DEC_LORA_V, c.stream);
+      hipExtLaunchKernelGGL(dec_lora_v_kernel<T>, dim3(dp.nvc), dim3(kDecodeThreads), 0, c.stream, tl.start,
+                            tl.stop, 0, a, l);
+      HIP_TRY(hipGetLastError());
+    }
     {
-      TimedLaunch tl(SATS_K_DEC_GATE, c.stream);
+      TimedLaunch tl(SATS_K_DEC_LAYER, c.stream);
       if (c.Ag)
-        hipExtLaunchKernelGGL((dec_gate_kernel<T, true>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream,
+        hipExtLaunchKernelGGL((dec_layer_kernel<T, true>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
                               tl.start, tl.stop, 0, a, l);
       else
-        hipExtLaunchKernelGGL((dec_gate_kernel<T, false>), dim3(dp.gate_grid), dim3(kGateThreads), 0, c.stream,
+        hipExtLaunchKernelGGL((dec_layer_kernel<T, false>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
                               tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
-    {
-      TimedLaunch tl(SATS_K_DEC_ROWS, c.stream);
-      if (c.Ag)
-        hipExtLaunchKernelGGL((dec_rows_kernel<T, true>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
-                              tl.start, tl.stop, 0, a, l);
-      else
-        hipExtLaunchKernelGGL((dec_rows_kernel<T, false>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
-                              tl.start, tl.stop, 0, a, l);
-    }
-    HIP_TRY(hipGetLastError());
-    if (!c.Ag) {
+    if (c.Ag) {
+      TimedLaunch tl(SATS_K_DEC_REDUCE_LORA, c.stream);
+      hipExtLaunchKernelGGL(dec_reduce_lora_kernel<T>, dim3(dp.RW), dim3(kDecodeThreads), 0, c.stream, tl.start,
+                            tl.stop, 0, a, l);
+    } else {
       TimedLaunch tl(SATS_K_DEC_REDUCE, c.stream);
       hipExtLaunchKernelGGL(dec_reduce_kernel<T>, dim3(dp.RW), dim3(kRedThreads), 0, c.stream, tl.start, tl.stop, 0,
                             a, l);
-      HIP_TRY(hipGetLastError());
     }
+    HIP_TRY(hipGetLastError());
   }
   if (lists) {
     for (int64_t l = 0; l < c.L; ++l) {
@@ -758,7 +742,7 @@ int run_lora(const Call &c, bool vec_ok) {
   const int esz = (int)sizeof(T);
   DecodePlan dp;
   if (!vec_ok || g_opt.single_token == SATS_SINGLE_OFF ||
-      !make_decode_plan(c.d, c.d_ff, esz, dec_rows_wgs(), &dp, (int)c.rank))
+      !make_decode_plan(c.d, c.d_ff, esz, &dp, (int)c.rank))
     return fail(SATS_ERR_SHAPE,
                 "LoRA calls need the single-token layout: d <= %d, d and d_ff multiples of %d, 16-byte aligned arrays",
                 sats::kDecodeMaxD, 16 / esz);
@@ -821,7 +805,7 @@ int run(const Call &c) {
   // single-token path: one token, vector layout, h fits the LDS copy
   bool decode = c.n == 1 && vec_ok && g_opt.single_token != SATS_SINGLE_OFF;
   DecodePlan dp;
-  if (decode) decode = make_decode_plan(c.d, c.d_ff, esz, dec_rows_wgs(), &dp);
+  if (decode) decode = make_decode_plan(c.d, c.d_ff, esz, &dp);
   const size_t bytes = layout(nullptr, p, pass, c.d, c.d_ff, esz, c.L, dp, nullptr, lrank);
   Workspace *ws = nullptr;
   size_t ncount = counter_count(p, pass, dp);
@@ -941,7 +925,7 @@ int cal_gate_up(const uint16_t *h, const uint16_t *Wg, const uint16_t *Wu, int64
     DenseArgs da{};
     da.ctl = cb.ctl + 2 * i;
     da.H = h + i * kDenseMaxTokens * d;
-    da.Wb = Wg;
+    da.Wg = Wg;
     da.Wt = Wu;
     da.K = (int)d;
     da.N = (int)d_ff;
@@ -1526,8 +1510,8 @@ int sats_reserve(int64_t max_tokens, int64_t d, int64_t d_ff, int64_t n_layers, 
   int cus = device_cus();
   if (cus < 1) return fail(SATS_ERR_HIP, "no device");
   DecodePlan dps[2]{};  // the plain single-token plan and the one of LoRA calls at the largest rank
-  (void)make_decode_plan(d, d_ff, elem_bytes, dec_rows_wgs(cus), &dps[0], 0, cus);
-  (void)make_decode_plan(d, d_ff, elem_bytes, dec_rows_wgs(cus), &dps[1], sats::kLoraMaxRank, cus);
+  (void)make_decode_plan(d, d_ff, elem_bytes, &dps[0], 0, cus);
+  (void)make_decode_plan(d, d_ff, elem_bytes, &dps[1], sats::kLoraMaxRank, cus);
   for (const DecodePlan &dp : dps)
     for (int v = 0; v < 2; ++v)
       for (int np : {1, pass}) {
@@ -1599,9 +1583,8 @@ int sats_set_options(const sats_options *opt) {
     return SATS_OK;
   }
   if (opt->batch_path < SATS_BATCH_AUTO || opt->batch_path > SATS_BATCH_COMPACT ||
-      opt->single_token < SATS_SINGLE_AUTO || opt->single_token > SATS_SINGLE_OFF || opt->dec_gate_tiles < 0 ||
-      opt->dec_gate_tiles > 65536 || opt->dec_rows_wgs < 0 || opt->dec_rows_wgs > sats::kDecodeMaxG ||
-      opt->lora_per_token < 0 || opt->lora_per_token > 1)
+      opt->single_token < SATS_SINGLE_AUTO || opt->single_token > SATS_SINGLE_OFF || opt->dec_block_cols < 0 ||
+      opt->dec_block_cols > sats::kDecodeMaxCols || opt->lora_per_token < 0 || opt->lora_per_token > 1)
     return fail(SATS_ERR_ARG, "an option is outside its range");
   g_opt = *opt;
   return SATS_OK;
@@ -1622,7 +1605,7 @@ int sats_query_path(int64_t n_tokens, int64_t d, int64_t d_ff, int elem_bytes, i
   const int cus = n_cus > 0 ? n_cus : device_cus();
   DecodePlan dp;
   if (n_tokens == 1 && vec_ok && g_opt.single_token != SATS_SINGLE_OFF &&
-      make_decode_plan(d, d_ff, elem_bytes, dec_rows_wgs(cus), &dp, 0, cus)) {
+      make_decode_plan(d, d_ff, elem_bytes, &dp, 0, cus)) {
     *path = SATS_PATH_SINGLE_TOKEN;
     return SATS_OK;
   }
@@ -1719,9 +1702,10 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_DENSE_DOWN: return "dense_down_kernel";
     case SATS_K_ROUTE_ACCUM: return "route_accum_kernel";
     case SATS_K_LORA_V: return "lora_v_kernel";
-    case SATS_K_DEC_GATE: return "dec_gate_kernel";
-    case SATS_K_DEC_ROWS: return "dec_rows_kernel";
+    case SATS_K_DEC_LAYER: return "dec_layer_kernel";
+    case SATS_K_DEC_LORA_V: return "dec_lora_v_kernel";
     case SATS_K_DEC_REDUCE: return "dec_reduce_kernel";
+    case SATS_K_DEC_REDUCE_LORA: return "dec_reduce_lora_kernel";
     case SATS_K_CAL_ERR: return "cal_err_kernel";
     case SATS_K_CAL_GATEUP: return "dense_gateup_kernel (calibration)";
     default: return "";

@@ -40,6 +40,17 @@ def to_dev(a, dtype: str):
     return torch.from_numpy(a).cuda()
 
 
+def gate_dev(w_gate, dtype: str):
+    """W_gate ([.., d, d_ff], the orientation of x W_gate) on the device in the
+    library's layout: one row of d weights per neuron, [.., d_ff, d]."""
+    return to_dev(np.ascontiguousarray(np.swapaxes(np.asarray(w_gate), -1, -2)), dtype)
+
+
+def weights_dev(case, dtype: str):
+    """The three weight stacks of `case` on the device, as the library takes them."""
+    return gate_dev(case["W_gate"], dtype), to_dev(case["W_up_T"], dtype), to_dev(case["W_down"], dtype)
+
+
 def from_dev(t):
     torch = torch_mod()
     if t.dtype == torch.bfloat16:
@@ -60,7 +71,7 @@ def run_gpu(case, thresholds, lut, dtype, inspect=True, dense=False, out_is_x=Fa
     n, d = x.shape
     L, _, d_ff = case["W_gate"].shape
     dx = to_dev(x, dtype)
-    wg, wu, wd = (to_dev(case[k], dtype) for k in ("W_gate", "W_up_T", "W_down"))
+    wg, wu, wd = weights_dev(case, dtype)
     ids = to_dev(np.asarray(case["token_ids"], np.int32), dtype)
     thr = torch.tensor(np.asarray(thresholds, np.float32)).cuda()
     dl = to_dev(lut, dtype) if lut is not None else None

@@ -149,10 +149,9 @@ def test_timing_kinds_match_the_header_and_name_their_kernels():
 
 def test_options_are_validated_and_reset():
     lib = sats.load()
-    for bad in (dict(batch_path=4), dict(batch_path=-1), dict(single_token=2), dict(dec_gate_tiles=-1),
-                dict(dec_gate_tiles=65537), dict(dec_rows_wgs=1025), dict(lora_per_token=2)):
-        o = _lib.SatsOptions(**{**dict(batch_path=0, single_token=0, dec_gate_tiles=0, dec_rows_wgs=0,
-                                       lora_per_token=0), **bad})
+    for bad in (dict(batch_path=4), dict(batch_path=-1), dict(single_token=2), dict(dec_block_cols=-1),
+                dict(dec_block_cols=65), dict(lora_per_token=2)):
+        o = _lib.SatsOptions(**{**dict(batch_path=0, single_token=0, dec_block_cols=0, lora_per_token=0), **bad})
         assert lib.sats_set_options(ctypes.byref(o)) == _lib.SATS_ERR_ARG, bad
     assert lib.sats_set_options(None) == _lib.SATS_OK
 

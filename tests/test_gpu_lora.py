@@ -16,7 +16,7 @@ import pytest
 from oracle import calibrate, lora, mlp, numerics
 from workloads import get_config, synth
 
-from harness import BAND, TOL, act_torch_dtype, band_mask, from_dev, rel_err, to_dev
+from harness import BAND, TOL, act_torch_dtype, band_mask, from_dev, rel_err, to_dev, weights_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -47,7 +47,7 @@ def run_lora(case, adapters, rank, scale, thresholds, lut, dtype, inspect=True):
     n, d = x.shape
     L, _, d_ff = case["W_gate"].shape
     dx = to_dev(x, dtype)
-    wg, wu, wd = (to_dev(case[k], dtype) for k in ("W_gate", "W_up_T", "W_down"))
+    wg, wu, wd = weights_dev(case, dtype)
     ad = tuple(to_dev(m, dtype) for m in adapters)
     ids = to_dev(np.asarray(case["token_ids"], np.int32), dtype)
     thr = torch.tensor(np.asarray(thresholds, np.float32)).cuda()
@@ -217,13 +217,13 @@ BATCHED = [
 
 
 def launches(fn):
-    """(adapter-input launches of the batched path, rows launches of the single-token path) made by fn()."""
+    """(adapter-input launches of the batched path, layer launches of the single-token path) made by fn()."""
     import paper_2607_08991_amd as sats
     sats.sats_timing_begin(sats.SATS_K_LORA_V, 4096)
-    sats.sats_timing_begin(sats.SATS_K_DEC_ROWS, 4096)
+    sats.sats_timing_begin(sats.SATS_K_DEC_LAYER, 4096)
     fn()
     _, nv = sats.sats_timing_end(sats.SATS_K_LORA_V)
-    _, nr = sats.sats_timing_end(sats.SATS_K_DEC_ROWS)
+    _, nr = sats.sats_timing_end(sats.SATS_K_DEC_LAYER)
     return nv, nr
 
 

@@ -194,17 +194,18 @@ def test_batch_rows_match_single_token_calls():
 @pytest.mark.parametrize("seed,L,d,dff,dtype", [(41, 3, 256, 1000, "bf16"), (42, 2, 4096, 1024, "bf16"),
                                                 (43, 2, 512, 1536, "f32"), (44, 2, 24, 40, "bf16")])
 def test_single_token_tilings_match_oracle_and_repeat_bitwise(seed, L, d, dff, dtype):
-    """The single-token kernels under several gate tilings (row chunks per
-    column block) and rows grids (partials of y): each matches the oracle on
-    a sparse-path and a base-path token, and a repeated call gives the same
+    """The single-token kernels under several column blocks per workgroup
+    (1, 7, 16 and 64 gate columns: from one column per workgroup to a full
+    ballot, and the automatic choice): each matches the oracle on a
+    sparse-path and a base-path token, and a repeated call gives the same
     bits (every sum has a fixed order)."""
     c = synth.small_case(seed, L, d, dff, dtype, 1, vocab=40, n_dense_ids=12,
                          w_std=1.0 / np.sqrt(d))
     ts = case_thresholds(c, dtype, seed=seed)
     for ids in ([0], [int(c["route_lut"].argmax())]):  # a sparse-path and a base-path token
         c["token_ids"] = np.asarray(ids, np.int32)
-        for opt in ({}, {"dec_gate_tiles": 1}, {"dec_gate_tiles": 2000},
-                    {"dec_rows_wgs": 7}, {"dec_rows_wgs": 1000}):
+        for opt in ({}, {"dec_block_cols": 1}, {"dec_block_cols": 7}, {"dec_block_cols": 16},
+                    {"dec_block_cols": 64}):
             with sats_options(**opt):
                 assert sats_query_path(1, d, dff, 2 if dtype == "bf16" else 4) == SATS_PATH_SINGLE_TOKEN
                 r1 = run_gpu(c, ts, c["route_lut"], dtype)

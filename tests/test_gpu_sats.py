@@ -17,7 +17,7 @@ two bf16 terms; the oracle is float64 on the same stored values):
 import numpy as np
 import pytest
 
-from harness import from_dev, to_dev
+from harness import from_dev, gate_dev, to_dev, weights_dev
 from oracle import calibrate, numerics, sats as osats
 from workloads import synth
 
@@ -62,7 +62,7 @@ def _gpu_curves(x, wg, wu, wd, levels, rows=True):
     n, d = x.shape
     dff = wg.shape[1]
     er = torch.zeros((n, len(levels)), dtype=torch.float32, device="cuda") if rows else None
-    t, err, sp = sats.sats_calibration_curves(to_dev(x, "bf16"), to_dev(wg, "bf16"), to_dev(wu, "bf16"),
+    t, err, sp = sats.sats_calibration_curves(to_dev(x, "bf16"), gate_dev(wg, "bf16"), to_dev(wu, "bf16"),
                                               to_dev(wd, "bf16"), n, d, dff, levels, err_rows=er)
     return t, err, sp, (er.cpu().numpy() if rows else None)
 
@@ -117,7 +117,7 @@ def test_calibrate_stack_matches_oracle():
     L, d, dff, n = 3, 256, 1024, 96
     c = synth.small_case(71, L, d, dff, "bf16", n, w_std=1.0 / np.sqrt(d))
     x = c["x"]
-    dw = [to_dev(c[k], "bf16") for k in ("W_gate", "W_up_T", "W_down")]
+    dw = list(weights_dev(c, "bf16"))
     ts, b, s = sats.sats_calibrate_sats(to_dev(x, "bf16"), n, *dw, d, dff, L, 0.5,
                                         coarse_step=0.1, fine_step=0.02, guardrail=True)
     # the GPU's own layer inputs on the base path

@@ -126,7 +126,7 @@ def test_qwen_batch4_reads_the_union_of_kept_rows(mode):
         np.array([sparse_ids[5], base_ids[3], sparse_ids[99], sparse_ids[1000]])
     c = dict(x=synth.decode_x(cfg, 4, idx=77), token_ids=ids.astype(np.int32), W_gate=wg, W_up_T=wu, W_down=wd)
     assert sats.sats_query_path(4, cfg.d, cfg.d_ff, 2) == sats.SATS_PATH_BATCH_MFMA
-    kinds = (sats.SATS_K_DENSE, sats.SATS_K_DENSE_DOWN, sats.SATS_K_DEC_ROWS)
+    kinds = (sats.SATS_K_DENSE, sats.SATS_K_DENSE_DOWN, sats.SATS_K_DEC_LAYER)
     for k in kinds:
         sats.sats_timing_begin(k, 256)
     res = run_gpu(c, ts, lut, cfg.dtype)

@@ -8,7 +8,7 @@ import sys
 import numpy as np
 import pytest
 
-from harness import to_dev, from_dev
+from harness import to_dev, from_dev, weights_dev
 from workloads import get_config, synth
 
 pytestmark = pytest.mark.gpu
@@ -35,7 +35,7 @@ def _both(c, ts, lut):
     x = to_dev(c["x"], "bf16")
     n, d = c["x"].shape
     L, _, dff = c["W_gate"].shape
-    w = [to_dev(c[k], "bf16") for k in ("W_gate", "W_up_T", "W_down")]
+    w = list(weights_dev(c, "bf16"))
     ids = to_dev(np.asarray(c["token_ids"], np.int32), "bf16") if lut is not None else None
     dl = to_dev(lut, "bf16") if lut is not None else None
     thr = torch.tensor(np.asarray(ts, np.float32)).cuda()
