@@ -544,13 +544,17 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   const __amdgpu_buffer_rsrc_t Wu = weight_rsrc(static_cast<const T *>(a.Wu) + (size_t)l * wl, wbytes);
   const __amdgpu_buffer_rsrc_t Wd = weight_rsrc(static_cast<const T *>(a.Wd) + (size_t)l * wl, wbytes);
 
-  // ---- gate: the first two pieces of every wavefront go out first
+  // ---- gate: wavefront wv reads columns wv, wv + 16, ... of the block
   GatePieces gp;
   gp.c0 = w * a.cw;
   gp.nc = max(1, min(a.cw, d_ff - gp.c0));
   gp.npc = ((d * (int)sizeof(T) + 1023) / 1024 + kGateQ - 1) / kGateQ;
   gp.wv = wv;
   gp.P = (wv < gp.nc ? (gp.nc - wv + 15) / 16 : 0) * gp.npc;
+  // the layer input's loads go first: h is formed while the first gate
+  // pieces are in flight, not after them (loads complete in issue order)
+  InputRegs<kDecodeThreads> ir;
+  dec_input_issue<T, kDecodeThreads>(a, l, ir);
   u32x4 qa[kGateQ], qb[kGateQ];
   gate_piece_issue<T>(Wg, gp, d, 0, qa);
   gate_piece_issue<T>(Wg, gp, d, 1, qb);
@@ -574,8 +578,6 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
                   ? load_coherent(a.vpart + ((size_t)c * 2 + tid / a.rank) * a.rank + tid % a.rank)
                   : 0.0f;
   }
-  InputRegs<kDecodeThreads> ir;
-  dec_input_issue<T, kDecodeThreads>(a, l, ir);
   for (int k = d + tid; k < kDecodeMaxD; k += kDecodeThreads) sm.hs[k] = 0.0f;  // past d: no products
   dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, a.layer_in != nullptr && w == 0);
   pack_input<T>(sm);
