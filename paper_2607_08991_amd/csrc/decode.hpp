@@ -68,6 +68,8 @@ struct DecodeArgs {
   float *sspart;          // [nss]          sums of y^2 per 16 columns
   int G, RW;              // layer workgroups (partials of y), reduce workgroups
   int nss;                // slice sums of squares of y per layer: one per 16 columns
+  int fused_reduce;       // 1: the last layer workgroup to finish does the second stage (small layers)
+  unsigned *done;         // [1] layer workgroups finished (fused_reduce; the last one resets it)
   uint8_t *route_out;     // optional [1]
   uint8_t *keep_out;      // optional [L][d_ff]
   void *layer_in;         // optional [L][...]: layer l's input at layer_in + l * in_stride
@@ -93,6 +95,7 @@ struct DecodeSmem {
   float mg[kDecodeMaxCols];             // ... and their g values
   int wcnt[kDecodeWaves];
   float scal[kDecodeWaves];
+  int flag;
   float lv[2][kDecodeWaves][kLoraMaxRank];  // LoRA: wavefront partials (input launch), gate adapter terms
   float lvg[kLoraMaxRank];                   // LoRA: h . A_gate
   float lz[kLoraMaxRank];                    // LoRA: h . A_up (layer) or z (reduce)
@@ -397,17 +400,19 @@ __device__ __forceinline__ void pack_input(DecodeSmem &sm) {
 
 // ------------------------------------------------------------------ rows
 
-// The workgroup's wavefronts form two halves of 8; half hf takes its own
-// part of the kept list, and wavefront v of a half owns column chunks v,
-// v + 8, ... of d (64 lanes x 16 bytes each) for both projections.
+// The workgroup's wavefronts form 16 / HW row groups of HW wavefronts
+// (HW = 8 for rows of more than 4 chunks, 4 or 2 for shorter ones, so that
+// no wavefront idles on a short row); group gr takes its own part of the
+// kept list, and wavefront v of a group owns column chunks v, v + HW, ... of
+// d (64 lanes x 16 bytes each) for both projections.
 
 // One batch: loads of this wavefront's chunks of the kept rows
 // list[r0 + r], r < R (rows at or past `end` are not read).
-template <typename T, int R, int NCH>
+template <typename T, int R, int NCH, int HW>
 __device__ __forceinline__ void rows_issue(__amdgpu_buffer_rsrc_t Wu, __amdgpu_buffer_rsrc_t Wd, const DecodeSmem &sm,
                                            int r0, int end, int d, u32x4 (&bu)[R][NCH], u32x4 (&bd)[R][NCH]) {
   constexpr int VEC = Elem<T>::kVec, CH = 64 * VEC;
-  const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 7);
+  const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) % HW);
   uint32_t soff[R];
 #pragma unroll
   for (int r = 0; r < R; ++r)
@@ -417,31 +422,31 @@ __device__ __forceinline__ void rows_issue(__amdgpu_buffer_rsrc_t Wu, __amdgpu_b
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int k = (hw + c * 8) * CH + lane * VEC;
+      const int k = (hw + c * HW) * CH + lane * VEC;
       bu[r][c] = (k < d && r0 + r < end) ? load_rsrc(Wu, (uint32_t)(k * sizeof(T)), soff[r]) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int k = (hw + c * 8) * CH + lane * VEC;
+      const int k = (hw + c * HW) * CH + lane * VEC;
       bd[r][c] = (k < d && r0 + r < end) ? load_rsrc(Wd, (uint32_t)(k * sizeof(T)), soff[r]) : u32x4{0u, 0u, 0u, 0u};
     }
 }
 
 // Uses one batch: this wavefront's parts of u_j = W_up_T[j] . h go to its
-// half's LDS slot `par`; after the barrier every wavefront of the half adds
-// the half's parts in wavefront order, p_j = g_j u_j, and accumulates p_j
-// times its chunks of W_down[j].
-template <typename T, int R, int NCH>
+// group's LDS slot `par`; after the barrier every wavefront of the group
+// adds the group's parts in wavefront order, p_j = g_j u_j, and accumulates
+// p_j times its chunks of W_down[j].
+template <typename T, int R, int NCH, int HW>
 __device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)[NCH][Elem<T>::kVec],
                                              float (&yacc)[NCH][Elem<T>::kVec], int r0, int end, int par,
                                              const u32x4 (&bu)[R][NCH], const u32x4 (&bd)[R][NCH], bool lora,
                                              const LoraRows<T> &lr, int rank, float &zh) {
   constexpr int VEC = Elem<T>::kVec;
-  const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) & 7);
-  const int hf = __builtin_amdgcn_readfirstlane(threadIdx.x >> 9);
-  float *part = sm.red + (hf * 2 + par) * (R * 8);  // [R][8] parts of u of this half
+  const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) % HW);
+  const int gr = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) / HW);
+  float *part = sm.red + (gr * 2 + par) * (R * HW);  // [R][HW] parts of u of this group
   float u[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -452,17 +457,17 @@ __device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)
       for (int v = 0; v < VEC; ++v) u[r] = fmaf(hreg[c][v], unpack<T>(bu[r][c], v), u[r]);
   }
   const float us = rows_sum<R>(u, lane);
-  if ((lane & (64 / R - 1)) == 0) part[(lane / (64 / R)) * 8 + hw] = us;
+  if ((lane & (64 / R - 1)) == 0) part[(lane / (64 / R)) * HW + hw] = us;
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     float ut = 0.0f;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) ut += part[r * 8 + q];
+    for (int q = 0; q < HW; ++q) ut += part[r * HW + q];
     const int li = max(0, min(r0 + r, end - 1));
     if (lora) ut += lr.lw[li];  // the up adapter's term of this kept row
     const float pr = (r0 + r < end) ? sm.mg[li] * ut : 0.0f;
-    if (lora && hw == 0 && lane < rank && r0 + r < end)  // z_lane += p_j A_down[j][lane], this half's rows in order
+    if (lora && hw == 0 && lane < rank && r0 + r < end)  // z_lane += p_j A_down[j][lane], this group's rows in order
       zh = fmaf(pr, Elem<T>::value(lr.lad[(size_t)li * rank + lane]), zh);
 #pragma unroll
     for (int c = 0; c < NCH; ++c)
@@ -517,20 +522,73 @@ __device__ __forceinline__ void lora_prep_use(const DecodeArgs &a, const DecodeS
 
 // ------------------------------------------------------------------ layer
 
+// Second reduction stage inside the layer launch (small layers: d <=
+// kFusedMaxD, G <= kFusedMaxG): the last workgroup to finish adds the G
+// partials in the order of dec_reduce_kernel (16 groups, each every 16th
+// partial in workgroup order, the groups in order; slice sums of squares by
+// the same exchanges), so either form gives the same bits.  Thread t takes
+// groups t / 128 and t / 128 + 8 at columns 4 (t % 128) .. + 3, every
+// 16-byte partial load issued before any is used.
+constexpr int kFusedMaxD = 512, kFusedMaxG = 96;
+
+template <typename T>
+__device__ void dec_reduce_all(const DecodeArgs &a, int l, DecodeSmem &sm) {
+  constexpr int NG = kRedThreads / kRedCols, FQ = kFusedMaxG / NG, NQ = kFusedMaxD / 4;
+  static_assert(NG * kFusedMaxD <= 2 * kDecodeMaxD && 2 * kDecodeThreads == NG * NQ, "fused second stage tiling");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int d = a.d, G = a.G;
+  const __amdgpu_buffer_rsrc_t yp = weight_rsrc(a.ypart, (uint32_t)((size_t)G * d * sizeof(float)));
+  f32x4 v[2][FQ];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int q = 0; q < FQ; ++q) {
+      const int it = tid + h * kDecodeThreads, g = it / NQ, c4 = 4 * (it % NQ), k = g + NG * q;
+      const uint32_t off = (c4 < d && k < G) ? (uint32_t)(((size_t)k * d + c4) * sizeof(float)) : kOffNone;
+      v[h][q] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(yp, (int)off, 0, 16 /* coherent */));
+    }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int it = tid + h * kDecodeThreads, g = it / NQ, c4 = 4 * (it % NQ);
+    f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int q = 0; q < FQ; ++q)
+      if (g + NG * q < G) s += v[h][q];
+    if (c4 < d) *reinterpret_cast<f32x4 *>(&sm.red[g * kFusedMaxD + c4]) = s;
+  }
+  __syncthreads();
+  if (tid < kFusedMaxD) {
+    const int col = tid;
+    const bool on = col < d;
+    float y = 0.0f;
+    if (on) {
+      for (int q = 0; q < NG && q < G; ++q) y += sm.red[q * kFusedMaxD + col];
+      if (l == a.L - 1) static_cast<T *>(a.out)[col] = Elem<T>::round(y);
+      else store_coherent(a.ybuf + col, y);
+    }
+    float sq = on ? y * y : 0.0f;
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) sq += __shfl_xor(sq, m, 64);
+    if ((lane & 15) == 0 && on && l < a.L - 1) store_coherent(a.sspart + col / kRedCols, sq);
+  }
+}
+
 // One layer of one token (see the top of this file); workgroup w writes its
 // partial y to ypart[w] (and z to zpart[w] with adapters).
-template <typename T, bool LORA>
+template <typename T, bool LORA, int HW>
 __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a, int l) {
   __shared__ DecodeSmem sm;
   __shared__ LoraRows<T> lr;
   constexpr int VEC = Elem<T>::kVec;
   constexpr int CH = 64 * VEC;              // elements per chunk (one 16-byte load per lane)
-  constexpr int DMAX = kDecodeMaxD / CH;    // chunks per row
-  constexpr int NCH = (DMAX + 7) / 8;       // chunks per wavefront of a half
+  constexpr int DMAX = HW == 8 ? kDecodeMaxD / CH : HW;  // chunks per row (at most)
+  constexpr int NCH = (DMAX + HW - 1) / HW;  // chunks per wavefront of a row group
+  constexpr int NGR = kDecodeWaves / HW;    // row groups
   constexpr int R = 8 / NCH;                // rows of two batches (2 x 8 loads in flight per lane)
   constexpr int RB = R > 2 ? R / 4 : 1;     // rows per batch
+  static_assert(HW == 2 || HW == 4 || HW == 8, "row group width");
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), hw = wv & 7, hf = wv >> 3;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6), hw = wv % HW, gr = wv / HW;
   const int w = blockIdx.x;
   const int d = a.d, d_ff = a.d_ff;
   const size_t wl = (size_t)d * d_ff;
@@ -634,75 +692,85 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   const int tot = sm.wcnt[0];
   if (l == 0) SATS_TRACE_POINT(4);
 
-  // ---- rows: half hf takes list[b, e)
-  const int hn = (tot + 1) / 2;
-  const int b = hf * hn, e = min(tot, (hf + 1) * hn);
-  const int nbt = (hn + RB - 1) / RB;  // batches (both halves run the same number)
+  // ---- rows: group gr takes list[b, e)
+  const int hn = (tot + NGR - 1) / NGR;
+  const int b = gr * hn, e = min(tot, (gr + 1) * hn);
+  const int nbt = (hn + RB - 1) / RB;  // batches (every group runs the same number)
   float hreg[NCH][VEC];  // h at this lane's columns
   float yacc[NCH][VEC];
   u32x4 au[RB][NCH], ad[RB][NCH], cu[RB][NCH], cd[RB][NCH];
   LoraPrepRegs<T> lp;
   if (lora) lora_prep_load<T>(a, l, sm, 0, tot, 0, lp);
-  if (nbt > 0) rows_issue<T, RB, NCH>(Wu, Wd, sm, b, e, d, au, ad);
-  if (nbt > 1) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + RB, e, d, cu, cd);
+  if (nbt > 0) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b, e, d, au, ad);
+  if (nbt > 1) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + RB, e, d, cu, cd);
 #pragma unroll
   for (int c = 0; c < NCH; ++c)
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
-      const int k = (hw + c * 8) * CH + lane * VEC + v;
+      const int k = (hw + c * HW) * CH + lane * VEC + v;
       hreg[c][v] = (k < d) ? sm.hs[k] : 0.0f;
       yacc[c][v] = 0.0f;
     }
-  float zh = 0.0f;  // LoRA, lane i < rank of wavefront 0 of each half: z_i over the half's kept rows
+  float zh = 0.0f;  // LoRA, lane i < rank of wavefront 0 of each group: z_i over the group's kept rows
   if (lora) {  // the up adapter's terms and A_down of the kept rows
     lora_prep_use<T>(a, sm, lr, 0, tot, 0, lp);
     __syncthreads();
   }
   int par = 0;  // LDS slot parity for the parts of u
   for (int i = 0; i < nbt; i += 2) {
-    rows_consume<T, RB, NCH>(sm, hreg, yacc, b + i * RB, e, par, au, ad, lora, lr, a.rank, zh);
+    rows_consume<T, RB, NCH, HW>(sm, hreg, yacc, b + i * RB, e, par, au, ad, lora, lr, a.rank, zh);
     par ^= 1;
-    if (i + 2 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
+    if (i + 2 < nbt) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
     if (i + 1 < nbt) {
-      rows_consume<T, RB, NCH>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
+      rows_consume<T, RB, NCH, HW>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
       par ^= 1;
-      if (i + 3 < nbt) rows_issue<T, RB, NCH>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
+      if (i + 3 < nbt) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
     }
   }
   __syncthreads();
-  if (lora) {  // z = half 0's sum + half 1's
-    if (wv == 8 && lane < a.rank) lr.lw[lane] = zh;
+  if (lora) {  // z = the groups' sums, added in group order
+    if (hw == 0 && gr > 0 && lane < a.rank) sm.lv[1][gr][lane] = zh;
     __syncthreads();
-    if (wv == 0 && lane < a.rank) store_coherent(a.zpart + (size_t)w * a.rank + lane, zh + lr.lw[lane]);
+    if (wv == 0 && lane < a.rank) {
+      float z = zh;
+      for (int q = 1; q < NGR; ++q) z += sm.lv[1][q][lane];
+      store_coherent(a.zpart + (size_t)w * a.rank + lane, z);
+    }
   }
   if (l == 0) SATS_TRACE_POINT(5);
-  // the two halves' sums, added in half order, are this workgroup's partial y
-  float *hsum = sm.red;  // [d]
-  if (hf == 1) {
+  // the groups' sums, added in group order, are this workgroup's partial y
+  // (groups 1 .. NGR - 1 pass theirs through LDS: NGR - 1 rows of d)
+  static_assert((NGR - 1) * DMAX * CH <= 2 * kDecodeMaxD, "group sums fit the LDS buffer");
+  if (gr > 0) {
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int k = (hw + c * 8) * CH + lane * VEC;
+      const int k = (hw + c * HW) * CH + lane * VEC;
       if (k < d) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) hsum[k + v] = yacc[c][v];
+        for (int v = 0; v < VEC; ++v) sm.red[(gr - 1) * d + k + v] = yacc[c][v];
       }
     }
   }
   __syncthreads();
-  if (hf == 0) {
+  if (gr == 0) {
     const __amdgpu_buffer_rsrc_t yr = weight_rsrc(a.ypart + (size_t)w * d, (uint32_t)(d * sizeof(float)));
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-      const int k = (hw + c * 8) * CH + lane * VEC;
+      const int k = (hw + c * HW) * CH + lane * VEC;
       if (k < d) {
+        float y[VEC];
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+          y[v] = yacc[c][v];
+          for (int q = 1; q < NGR; ++q) y[v] += sm.red[(q - 1) * d + k + v];
+        }
 #pragma unroll
         for (int v = 0; v < VEC; v += 4)
-          store_coherent4(yr, (uint32_t)((k + v) * sizeof(float)), yacc[c][v] + hsum[k + v],
-                          yacc[c][v + 1] + hsum[k + v + 1], yacc[c][v + 2] + hsum[k + v + 2],
-                          yacc[c][v + 3] + hsum[k + v + 3]);
+          store_coherent4(yr, (uint32_t)((k + v) * sizeof(float)), y[v], y[v + 1], y[v + 2], y[v + 3]);
       }
     }
   }
+  if (!LORA && a.fused_reduce && arrive_last(a.done, (unsigned)a.G, &sm.flag)) dec_reduce_all<T>(a, l, sm);
 }
 
 // ------------------------------------------------------------------ reduce

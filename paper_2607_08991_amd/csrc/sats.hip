@@ -181,6 +181,7 @@ struct DecodePlan {
   int cw = 0;          // gate columns per layer workgroup
   int RW = 0;          // reduce workgroups
   int nvc = 0;         // LoRA input launch: row chunks of the adapters' A matrices
+  bool fused = false;  // second stage inside the layer launch (no adapters, few partials)
 };
 
 size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, int esz, int64_t L,
@@ -230,6 +231,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
 constexpr size_t kCtl = 512;
 constexpr size_t kErr = 320;
 constexpr size_t kLoraV = 448;  // [8] batched LoRA: arrivals of the s (h A) chunks
+constexpr size_t kDecDone = 324;  // single-token layer launch: workgroups finished (small layers)
 
 size_t counter_count(const Plan &p, int64_t pass, const DecodePlan &dp) {
   const int64_t tiles = ((pass + 3) / 4) * 4;
@@ -295,17 +297,21 @@ int ensure_workspace(hipStream_t stream, size_t bytes, size_t n_counters, Worksp
 }
 
 // Single-token plan.  h is held in LDS (d <= kDecodeMaxD).  Layer workgroup
-// w owns gate columns [cw w, cw w + cw): cw is the option, else d_ff spread
-// over the compute units (one workgroup each), at least 8 and at most 64
-// columns.  The second reduction stage: without adapters a launch of
-// 16-column slices; with adapters about 64 columns per workgroup (each one
-// also sums every partial z), a whole number of 16-column slices.
-// Returns false when the shape does not fit.
+// w owns gate columns [cw w, cw w + cw): cw is the option, else the layer's
+// weights (W_gate and about half of the other two) spread over workgroups of
+// about kDecWgBytes each, at most one per compute unit, at most 64 columns.
+// The second reduction stage: without adapters a launch of 16-column slices,
+// or, for small layers (d <= kFusedMaxD, G <= kFusedMaxG), the last layer
+// workgroup to finish; with adapters about 64 columns per workgroup (each one also
+// sums every partial z), a whole number of 16-column slices.  Returns false
+// when the shape does not fit.
+constexpr int64_t kDecWgBytes = 64 << 10;
+
 bool make_decode_plan(int64_t d, int64_t d_ff, int esz, DecodePlan *dp, int lora_rank = 0, int cus = -1) {
   DecodePlan q{};
   if (cus < 0) cus = device_cus();
-  int64_t cw = g_opt.dec_block_cols > 0 ? g_opt.dec_block_cols
-                                        : std::max<int64_t>(8, (d_ff + std::max(cus, 1) - 1) / std::max(cus, 1));
+  const int64_t wgs = std::min<int64_t>(std::max(cus, 1), std::max<int64_t>(1, (2 * d * d_ff * esz + kDecWgBytes - 1) / kDecWgBytes));
+  int64_t cw = g_opt.dec_block_cols > 0 ? g_opt.dec_block_cols : (d_ff + wgs - 1) / wgs;
   cw = std::min<int64_t>(cw, sats::kDecodeMaxCols);
   q.cw = (int)cw;
   const int64_t G = (d_ff + cw - 1) / cw;
@@ -320,6 +326,7 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, DecodePlan *dp, int lora
   }
   // buffer descriptors address one layer's matrix with 32-bit offsets, and
   // 0x80000000 is the offset that reads zeros: every matrix must stay below 2 GB
+  q.fused = lora_rank == 0 && d <= sats::kFusedMaxD && G <= sats::kFusedMaxG;
   const bool ok = G <= sats::kDecodeMaxG && d <= sats::kDecodeMaxD &&
                   (d + q.RW - 1) / q.RW <= sats::kDecodeThreads / (sats::kRedThreads / sats::kRedCols) &&
                   (uint64_t)d * (uint64_t)d_ff * (uint64_t)esz < (1ull << 31);
@@ -628,10 +635,20 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
   return SATS_OK;
 }
 
+// The layer kernel for this call: with or without adapters, and rows split
+// over groups of 2, 4 or 8 wavefronts by the number of 16-byte chunks per row.
+template <typename T>
+void (*dec_layer_fn(bool lora, int64_t d))(sats::DecodeArgs, int) {
+  using namespace sats;
+  const int64_t chunks = (d * (int64_t)sizeof(T) + 1023) / 1024;
+  if (chunks <= 2) return lora ? dec_layer_kernel<T, true, 2> : dec_layer_kernel<T, false, 2>;
+  if (chunks <= 4) return lora ? dec_layer_kernel<T, true, 4> : dec_layer_kernel<T, false, 4>;
+  return lora ? dec_layer_kernel<T, true, 8> : dec_layer_kernel<T, false, 8>;
+}
+
 template <typename T>
 int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *counters) {
   using namespace sats;
-  (void)counters;
   DecodeArgs a{};
   a.x = c.x;
   a.out = c.out;
@@ -650,6 +667,8 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
   a.RW = dp.RW;
   a.ypart = b.ypart;
   a.nss = (int)((c.d + kRedCols - 1) / kRedCols);
+  a.fused_reduce = (dp.fused && !c.Ag) ? 1 : 0;
+  a.done = counters + kDecDone;
   a.ybuf = b.ybuf;
   a.sspart = b.sspart;
   a.route_out = c.route_out;
@@ -679,14 +698,11 @@ int run_decode(const Call &c, const DecodePlan &dp, const Buffers &b, unsigned *
     }
     {
       TimedLaunch tl(SATS_K_DEC_LAYER, c.stream);
-      if (c.Ag)
-        hipExtLaunchKernelGGL((dec_layer_kernel<T, true>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
-                              tl.start, tl.stop, 0, a, l);
-      else
-        hipExtLaunchKernelGGL((dec_layer_kernel<T, false>), dim3(dp.G), dim3(kDecodeThreads), 0, c.stream,
-                              tl.start, tl.stop, 0, a, l);
+      auto kern = dec_layer_fn<T>(c.Ag != nullptr, c.d);
+      hipExtLaunchKernelGGL(kern, dim3(dp.G), dim3(kDecodeThreads), 0, c.stream, tl.start, tl.stop, 0, a, l);
     }
     HIP_TRY(hipGetLastError());
+    if (a.fused_reduce) continue;
     if (c.Ag) {
       TimedLaunch tl(SATS_K_DEC_REDUCE_LORA, c.stream);
       hipExtLaunchKernelGGL(dec_reduce_lora_kernel<T>, dim3(dp.RW), dim3(kDecodeThreads), 0, c.stream, tl.start,
