@@ -613,14 +613,12 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   // pieces are in flight, not after them (loads complete in issue order)
   InputRegs<kDecodeThreads> ir;
   dec_input_issue<T, kDecodeThreads>(a, l, ir);
-  u32x4 qa[kGateQ], qb[kGateQ];
-  gate_piece_issue<T>(Wg, gp, d, 0, qa);
-  gate_piece_issue<T>(Wg, gp, d, 1, qb);
   // LoRA: B_gate at the block's columns (thread (c, i): ranks i, i + 16, ...)
-  // and the chunk partials of h A_gate, h A_up; used once h is formed
-  constexpr int BQ = kLoraMaxRank / kDecodeWaves;
+  // and every chunk partial of h A_gate, h A_up (all loads issued at once,
+  // ahead of the weights); used once h is formed
+  constexpr int BQ = kLoraMaxRank / kDecodeWaves, VC = kDecodeMaxD / kVRows;
   float bgv[BQ];
-  float vq[2];
+  float vq[VC];
   const int lc = tid & 63, li = tid >> 6;
   if (lora) {
     const T *bg = static_cast<const T *>(a.Bg) + (size_t)l * a.rank * d_ff + gp.c0 + min(lc, gp.nc - 1);
@@ -629,22 +627,27 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
       const int i = li + m * kDecodeWaves;
       bgv[m] = (i < a.rank) ? Elem<T>::get(bg + (size_t)i * d_ff) : 0.0f;
     }
-    // thread t < 2 rank: adapter t / rank, rank index t % rank, chunks c = 0, 1 (more below)
+    // thread t < 2 rank: adapter t / rank, rank index t % rank, chunk c
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < VC; ++c)
       vq[c] = (tid < 2 * a.rank && c < a.nvc)
                   ? load_coherent(a.vpart + ((size_t)c * 2 + tid / a.rank) * a.rank + tid % a.rank)
                   : 0.0f;
   }
+  u32x4 qa[kGateQ], qb[kGateQ];
+  gate_piece_issue<T>(Wg, gp, d, 0, qa);
+  gate_piece_issue<T>(Wg, gp, d, 1, qb);
   for (int k = d + tid; k < kDecodeMaxD; k += kDecodeThreads) sm.hs[k] = 0.0f;  // past d: no products
   dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, a.layer_in != nullptr && w == 0);
   pack_input<T>(sm);
   __syncthreads();
   if (l == 0) SATS_TRACE_POINT(1);
   if (lora) {  // h A_gate into lvg, h A_up into lz; then the gate adapter terms
-    if (tid < 2 * a.rank) {
-      float v = vq[0] + vq[1];
-      for (int c = 2; c < a.nvc; ++c) v += load_coherent(a.vpart + ((size_t)c * 2 + tid / a.rank) * a.rank + tid % a.rank);
+    if (tid < 2 * a.rank) {  // the chunks in order
+      float v = 0.0f;
+#pragma unroll
+      for (int c = 0; c < VC; ++c)
+        if (c < a.nvc) v += vq[c];
       if (tid < a.rank) sm.lvg[tid] = v;
       else sm.lz[tid - a.rank] = v;
     }
