@@ -449,7 +449,10 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   }
 }
 
-// partial y over k chunk blockIdx.y for 128 output columns (blockIdx.x);
+// partial y over one k chunk for 128 output columns; workgroup b takes
+// column tile b / ks and k chunk b % ks, so that consecutive workgroups (which
+// the dispatcher spreads over the 8 XCDs in turn) take different k chunks and
+// each XCD's L2 fetches only its chunks of p, not all of it;
 // wavefront w takes columns 16 w .. 16 w + 15.  A stage holds 64 W_down
 // rows of 256 bytes (16 KB) and the matching 64 entries of p rows (8 KB).
 //
@@ -471,9 +474,10 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   const int nd = min(a.ctl[0], 16 * MT);
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, l16 = lane & 15, c = 16 * w + l16;
-  const int n0 = blockIdx.x * kDenseDownNT;
+  const int ks = gridDim.x / (a.N / kDenseDownNT), kc = blockIdx.x % ks;
+  const int n0 = (blockIdx.x / ks) * kDenseDownNT;
   const int K = a.K, N = a.N;
-  const int kb = blockIdx.y * a.kchunk, ke = min(K, kb + a.kchunk);
+  const int kb = kc * a.kchunk, ke = min(K, kb + a.kchunk);
   const int S = ke > kb ? (ke - kb) / kDenseKC : 0;
   const __amdgpu_buffer_rsrc_t rsw = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
   const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
@@ -536,7 +540,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   for (int i = 0; i < MT; ++i) {
     const int e = threadIdx.x + i * kDenseThreads, m = e >> 5, q = e & 31;
     if (m < nd)
-      *reinterpret_cast<f32x4v *>(a.part + ((size_t)blockIdx.y * nd + m) * N + n0 + 4 * q) =
+      *reinterpret_cast<f32x4v *>(a.part + ((size_t)kc * nd + m) * N + n0 + 4 * q) =
           *reinterpret_cast<const f32x4v *>((m < 32 ? x0 : x1) + (m & 31) * XP + 4 * q);
   }
 }

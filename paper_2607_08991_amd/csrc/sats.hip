@@ -503,7 +503,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       dd.kchunk = (int)(((d_ff + ks - 1) / ks + kDenseKC - 1) / kDenseKC * kDenseKC);
       {
         TimedLaunch tl(SATS_K_DENSE_DOWN, c.stream);
-        hipExtLaunchKernelGGL(dense_down_fn(np), dim3(d / kDenseDownNT, ks), dim3(kDenseThreads), 0, c.stream,
+        hipExtLaunchKernelGGL(dense_down_fn(np), dim3(d / kDenseDownNT * ks), dim3(kDenseThreads), 0, c.stream,
                               tl.start, tl.stop, 0, dd);
       }
       HIP_TRY(hipGetLastError());
