@@ -248,13 +248,56 @@ __device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const
     if (s_ < (S)) COMPUTE(CUR);                                                              \
   }
 
+// The ring of groups of at most 16 rows: eight 18 KB stages (W_gate_T and
+// W_up_T 8 KB each, H 2 KB), seven in flight.  Wavefronts 0-1 also load the
+// 16 H rows (three loads per stage, the others two), so their wait allows
+// 18 outstanding loads and the others' 12.
+#define SATS_DENSE_RING8(S, ISSUE, COMPUTE)                                                  \
+  {                                                                                          \
+    ISSUE(rg0, 0);                                                                           \
+    ISSUE(rg1, 1);                                                                           \
+    ISSUE(rg2, 2);                                                                           \
+    ISSUE(rg3, 3);                                                                           \
+    ISSUE(rg4, 4);                                                                           \
+    ISSUE(rg5, 5);                                                                           \
+    ISSUE(rg6, 6);                                                                           \
+    for (int s0 = 0; s0 < (S); s0 += 8) {                                                    \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg0, rg7, 0)                                       \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg1, rg0, 1)                                       \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg2, rg1, 2)                                       \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg3, rg2, 3)                                       \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg4, rg3, 4)                                       \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg5, rg4, 5)                                       \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg6, rg5, 6)                                       \
+      SATS_DENSE_STEP8(S, ISSUE, COMPUTE, rg7, rg6, 7)                                       \
+    }                                                                                        \
+    __builtin_amdgcn_s_waitcnt(0);                                                           \
+  }
+#define SATS_DENSE_STEP8(S, ISSUE, COMPUTE, CUR, NXT, P)                                     \
+  {                                                                                          \
+    const int s_ = s0 + (P);                                                                 \
+    if (w < 2)                                                                               \
+      dense_stage_barrier<18>();                                                             \
+    else                                                                                     \
+      dense_stage_barrier<12>();                                                             \
+    ISSUE(NXT, s_ + 7);                                                                      \
+    if (s_ < (S)) COMPUTE(CUR);                                                              \
+  }
+
 // p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every row of
 // the group (MT 16-row tiles; rows past the group are read as zeros).
-// Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
+// Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.  Groups of
+// one row tile use the eight-stage ring of 18 KB stages, larger ones six
+// stages of 24 KB.
 template <int MT, bool LORA = false>
 __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
-      rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
+  constexpr int NB = MT == 1 ? 8 : 6, SB = MT == 1 ? 18 * 1024 : kDenseStageBytes;  // ring stages and their bytes
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[NB * SB];
+  uint8_t *const rg0 = ring, *const rg1 = ring + SB, *const rg2 = ring + 2 * SB, *const rg3 = ring + 3 * SB,
+                 *const rg4 = ring + 4 * SB, *const rg5 = ring + 5 * SB;
+  uint8_t *const rg6 = ring + (NB > 6 ? 6 : 0) * SB, *const rg7 = ring + (NB > 7 ? 7 : 0) * SB;
+  (void)rg6;
+  (void)rg7;
   if (!a.ctl[1]) return;
   const int nd = min(a.ctl[0], 16 * MT);
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -280,7 +323,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
     const uint32_t ss_ = (uint32_t)(SN);                                                     \
     dma16<2>(rsg, (BUF) + w * 1024, dense_off(v_, ou + ss_ * sk, 0));                        \
     dma16<2>(rsu, (BUF) + 8192 + w * 1024, dense_off(v_, ou + ss_ * sk, 1));                 \
-    dma16<0>(rsh, (BUF) + 16384 + w * 1024, dense_off(v_ && hv, oh + ss_ * sk, 2));          \
+    if (MT > 1 || w < 2) dma16<0>(rsh, (BUF) + 16384 + w * 1024, dense_off(v_ && hv, oh + ss_ * sk, 2)); \
   }
 #define SATS_GU_COMPUTE(BUF)                                                                 \
   {                                                                                          \
@@ -308,7 +351,11 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
       plv[j] = (e < 32 * R) ? *reinterpret_cast<const u32x4 *>(a.lv + 4 * e) : u32x4{0u, 0u, 0u, 0u};
     }
   }
-  SATS_DENSE_RING(S, SATS_GU_ISSUE, SATS_GU_COMPUTE)
+  if constexpr (MT == 1) {
+    SATS_DENSE_RING8(S, SATS_GU_ISSUE, SATS_GU_COMPUTE)
+  } else {
+    SATS_DENSE_RING(S, SATS_GU_ISSUE, SATS_GU_COMPUTE)
+  }
 #undef SATS_GU_ISSUE
 #undef SATS_GU_COMPUTE
   // epilogue: SiLU(a) through LDS to the W_up wavefronts, p through LDS to
