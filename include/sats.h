@@ -283,8 +283,11 @@ int sats_calibrate_sats(const sats_bf16 *x_cal, int64_t n_cal, const sats_bf16 *
  * tau.  route_lut [vocab] (device) receives 0 (sparse path) where
  * s(x) < tau*, else 1 (base path) -- the table the forward calls take.
  * scores [vocab] (device double, or NULL) receives s; tau_out and
- * realized_out (host, or NULL) receive tau* and R(tau*).  Synchronises the
- * stream; allocates its own buffers.  Errors: SATS_ERR_NULL, SATS_ERR_SHAPE,
+ * realized_out (host, or NULL) receive tau* and R(tau*); the selection of
+ * tau* runs on the device.  Synchronises the stream; its device buffers are
+ * kept per device from call to call (calls are serialised; sats_release
+ * frees them).  On an error route_lut is left as it was.  Errors:
+ * SATS_ERR_NULL, SATS_ERR_SHAPE,
  * SATS_ERR_ARG (r_tar outside [0, 1], an id outside [0, vocab), a loss
  * difference NaN or >= 2^31).  The per-id sums of d must stay below 2^32.
  */
@@ -343,7 +346,8 @@ enum { SATS_PATH_SINGLE_TOKEN = 1, SATS_PATH_BATCH_MFMA = 2, SATS_PATH_BATCH_SPL
 int sats_query_path(int64_t n_tokens, int64_t d, int64_t d_ff, int elem_bytes, int aligned16, int n_cus,
                     int *path);
 
-/* Free every workspace of the calling process (synchronises each device). */
+/* Free every workspace of the calling process, and the routing-table
+ * construction's kept buffers (synchronises each device). */
 int sats_release(void);
 
 /* Thread-local text of the last error returned on this thread ("" if none). */
@@ -355,11 +359,14 @@ const char *sats_last_error(void);
  * (SATS_K_*), recorded on the stream the kernel is launched on.
  * sats_timing_end(kind, &total_ms, &count) waits for the recorded events,
  * returns the summed duration and the number of launches timed, and disarms.
+ * SATS_K_ROUTE_ACCUM times the per-chunk pass over the routing split
+ * (route_part_kernel; for vocabularies past 2^22 ids the atomic form,
+ * route_accum_kernel), SATS_K_ROUTE_MERGE the merge of its entries.
  */
 enum { SATS_K_GATE = 0, SATS_K_UP = 1, SATS_K_DOWN = 2, SATS_K_INSPECT = 3, SATS_K_DENSE = 4,
        SATS_K_DEC_LAYER = 5, SATS_K_DEC_LORA_V = 6, SATS_K_CAL_ERR = 7, SATS_K_CAL_GATEUP = 8,
        SATS_K_ROUTE_ACCUM = 9, SATS_K_LORA_V = 10, SATS_K_DEC_REDUCE = 11, SATS_K_DENSE_DOWN = 12,
-       SATS_K_DEC_REDUCE_LORA = 13, SATS_K_COUNT = 14 };
+       SATS_K_DEC_REDUCE_LORA = 13, SATS_K_ROUTE_MERGE = 14, SATS_K_COUNT = 15 };
 int sats_timing_begin(int kind, int capacity);
 int sats_timing_end(int kind, double *total_ms, int64_t *count);
 const char *sats_kernel_name(int kind);

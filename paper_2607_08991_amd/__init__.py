@@ -13,5 +13,5 @@ from ._lib import (  # noqa: F401
     sats_set_options, options, sats_query_path, SATS_BATCH_AUTO, SATS_BATCH_MFMA, SATS_BATCH_SPLIT,
     SATS_BATCH_COMPACT, SATS_SINGLE_AUTO, SATS_SINGLE_OFF, SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA,
     SATS_PATH_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT, sats_mlp_forward_noalloc,
-    SATS_K_DEC_REDUCE, SATS_K_DENSE_DOWN, SATS_K_DEC_REDUCE_LORA,
+    SATS_K_DEC_REDUCE, SATS_K_DENSE_DOWN, SATS_K_DEC_REDUCE_LORA, SATS_K_ROUTE_MERGE,
 )

@@ -22,6 +22,7 @@ SATS_K_LORA_V = 10
 SATS_K_DEC_REDUCE = 11
 SATS_K_DENSE_DOWN = 12
 SATS_K_DEC_REDUCE_LORA = 13
+SATS_K_ROUTE_MERGE = 14
 SATS_BATCH_AUTO, SATS_BATCH_MFMA, SATS_BATCH_SPLIT, SATS_BATCH_COMPACT = 0, 1, 2, 3
 SATS_SINGLE_AUTO, SATS_SINGLE_OFF = 0, 1
 SATS_PATH_SINGLE_TOKEN, SATS_PATH_BATCH_MFMA, SATS_PATH_BATCH_SPLIT, SATS_PATH_BATCH_COMPACT = 1, 2, 3, 4

@@ -1,24 +1,40 @@
 // Routing-table construction (Section 3.2, Eq. 11-14): per-id scores from a
 // routing corpus and the table of the calibrated threshold.
 //
-//   route_accum_kernel<DAMAGE>
+// Per-id sums of a corpus split, in two launches without global atomics:
+//   route_part_kernel<DAMAGE>
 //       a chunk of kRouteChunk occurrences per workgroup: the excess damage
 //       d = max(0, l_sparse - l_base) (Eq. 11) of each, in float32, as an
 //       integer number of 2^-32 units (rounded half to even); the chunk's
 //       occurrences are gathered per id in an LDS hash table (open
 //       addressing, twice as many slots as occurrences, so every probe
-//       sequence ends) with LDS integer atomics, and each id of the chunk
-//       then adds its sum and count to the id's totals with one global
-//       integer atomic each (a frequent id costs one atomic per chunk, not
-//       per occurrence; integer sums are exact in any order).  The totals
-//       are held in kRouteCopies copies, workgroup w adding into copy
-//       w % kRouteCopies: a frequent id's atomics, which serialise per
-//       address, are spread over the copies.  DAMAGE false: counts only
-//       (the held-out split).
+//       sequence ends) and written out as one (id, count, sum) entry per
+//       distinct id, grouped by id range (2^rbits ids a range, at most
+//       kRouteRanges ranges), with the start of each range's entries.
+//       DAMAGE false: counts only (the held-out split).
+//   route_merge_kernel<DAMAGE>
+//       workgroup (r, p) adds the entries of range r of the chunks of group p
+//       into an LDS table of the range's ids and writes it to totals part p
+//       (every id of the range, zeros included).  Integer sums are exact in
+//       any order, so neither the order of a chunk's entries nor the split
+//       into groups changes a total.
+//   route_accum_kernel<DAMAGE>
+//       vocabularies past kRoutePartMaxVocab: the chunk's LDS table adds
+//       each id's sum and count into totals copy w % kRouteCopies with one
+//       global integer atomic each.
 //   route_score_kernel
-//       the copies added (integers), s(x) = 2^-32 (double(S_x) / double(C_x))
+//       the parts added (integers), s(x) = 2^-32 (double(S_x) / double(C_x))
 //       (the empirical mean of Eq. 12), +inf for ids without occurrences;
-//       the held-out counts' copies added likewise.
+//       the held-out counts' parts likewise; and F, the held-out
+//       occurrences whose id has a finite score.
+//   route_select_pass_kernel, route_select_final_kernel, route_decide_kernel
+//       Eq. 14 on the device: T, the least count c <= F with c / n_heldout
+//       >= r_tar; the T-th smallest held-out occurrence score o by a radix
+//       select on the bits of the scores (eight passes of 8 bits, each a
+//       histogram weighted by the held-out counts, every workgroup replaying
+//       the earlier passes' choices from their histograms); then the
+//       smallest score above o and the counts at or below and below o; of o
+//       and that next score the one whose R is nearer r_tar, o on ties.
 //   route_table_kernel
 //       table[x] = 0 (sparse path) if s(x) < tau, else 1 (Eq. 13).
 #pragma once
@@ -30,7 +46,11 @@ namespace sats {
 constexpr int kRouteThreads = 1024;
 constexpr int kRouteChunk = 4096;  // occurrences per workgroup (4 per thread)
 constexpr uint32_t kRouteNoId = 0xffffffffu;
-constexpr int kRouteCopies = 32;  // copies of the per-id totals
+constexpr int kRouteCopies = 32;  // copies of the per-id totals (atomic form)
+constexpr int kRouteRanges = kRouteThreads;  // id ranges of the partitioned form (one per thread in a scan)
+constexpr int kRouteMaxRangeBits = 12;       // ids per range at most 4096 (the merge's LDS table)
+constexpr int64_t kRoutePartMaxVocab = (int64_t)kRouteRanges << kRouteMaxRangeBits;
+constexpr int kRouteParts = 8;               // chunk groups of the merge: parts of the totals
 
 struct RouteAccumArgs {
   const int32_t *ids;
@@ -46,13 +66,14 @@ struct RouteAccumArgs {
 constexpr int kRouteSlots = 2 * kRouteChunk;
 static_assert(kRouteSlots == 1 << 13, "the slot hash takes the top 13 bits");
 
+// The chunk's occurrences [base, base + kRouteChunk) gathered per id into
+// the LDS table skey / scnt / ssum (every slot initialised here); ends with
+// a barrier.
 template <bool DAMAGE>
-__global__ __launch_bounds__(kRouteThreads) void route_accum_kernel(RouteAccumArgs a) {
-  __shared__ uint32_t skey[kRouteSlots];
-  __shared__ uint32_t scnt[kRouteSlots];
-  __shared__ unsigned long long ssum[DAMAGE ? kRouteSlots : 1];
+__device__ __forceinline__ void route_chunk_table(const int32_t *ids, const float *lb, const float *ls, int64_t n,
+                                                  int vocab, unsigned *err, int64_t base, uint32_t *skey,
+                                                  uint32_t *scnt, unsigned long long *ssum) {
   const int tid = threadIdx.x;
-  const int64_t base = (int64_t)blockIdx.x * kRouteChunk;
   constexpr int PER = kRouteChunk / kRouteThreads, SPER = kRouteSlots / kRouteThreads;
   uint32_t k[PER];
   unsigned long long q[PER];
@@ -62,23 +83,23 @@ __global__ __launch_bounds__(kRouteThreads) void route_accum_kernel(RouteAccumAr
     const int64_t i = base + tid + m * kRouteThreads;
     k[m] = kRouteNoId;
     q[m] = 0ull;
-    if (i < a.n) {
-      const int32_t x = a.ids[i];
-      if (x >= 0 && x < a.vocab) {
+    if (i < n) {
+      const int32_t x = ids[i];
+      if (x >= 0 && x < vocab) {
         k[m] = (uint32_t)x;
         if constexpr (DAMAGE) {
-          const float diff = a.ls[i] - a.lb[i];  // float32, as in Eq. 11
-          if (diff < 2147483648.0f) {             // also false for NaN
+          const float diff = ls[i] - lb[i];  // float32, as in Eq. 11
+          if (diff < 2147483648.0f) {         // also false for NaN
             // d 2^32 is exact in float32 and rintf rounds half to even: an
             // integer-valued float below 2^63, converted exactly
             q[m] = (unsigned long long)rintf(fmaxf(diff, 0.0f) * 4294967296.0f);
           } else {
             k[m] = kRouteNoId;
-            __hip_atomic_store(a.err, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(err, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           }
         }
       } else {
-        __hip_atomic_store(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
   }
@@ -106,9 +127,20 @@ __global__ __launch_bounds__(kRouteThreads) void route_accum_kernel(RouteAccumAr
       }
       h = (h + 1) & (kRouteSlots - 1);
     }
-    if (probe == kRouteSlots) __hip_atomic_store(a.err, 3u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (probe == kRouteSlots) __hip_atomic_store(err, 3u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
+}
+
+template <bool DAMAGE>
+__global__ __launch_bounds__(kRouteThreads) void route_accum_kernel(RouteAccumArgs a) {
+  __shared__ uint32_t skey[kRouteSlots];
+  __shared__ uint32_t scnt[kRouteSlots];
+  __shared__ unsigned long long ssum[DAMAGE ? kRouteSlots : 1];
+  constexpr int SPER = kRouteSlots / kRouteThreads;
+  const int tid = threadIdx.x;
+  route_chunk_table<DAMAGE>(a.ids, a.lb, a.ls, a.n, a.vocab, a.err, (int64_t)blockIdx.x * kRouteChunk, skey, scnt,
+                            ssum);
   const size_t cp = (size_t)(blockIdx.x % kRouteCopies) * (size_t)a.vocab;
 #pragma unroll
   for (int m = 0; m < SPER; ++m) {
@@ -120,27 +152,292 @@ __global__ __launch_bounds__(kRouteThreads) void route_accum_kernel(RouteAccumAr
   }
 }
 
-__global__ __launch_bounds__(256) void route_score_kernel(const unsigned long long *sum, const unsigned *count,
-                                                          const unsigned *hcount, int vocab, double *score,
-                                                          unsigned *hcount_total) {
-  const int x = blockIdx.x * 256 + threadIdx.x;
-  if (x >= vocab) return;
-  unsigned long long sx = 0ull;
-  unsigned c = 0u, h = 0u;
+struct RoutePartArgs {
+  const int32_t *ids;
+  const float *lb, *ls;  // DAMAGE: per-occurrence losses of the base and sparse paths
+  int64_t n;
+  int vocab;
+  int rbits, nr;         // 2^rbits ids a range, nr ranges (<= kRouteRanges)
+  int nchunks;
+  u32x4 *ent;            // [nchunks][kRouteChunk] (id, count, sum lo, sum hi), grouped by range
+  uint32_t *off;         // [nr + 1][nchunks] start of range r in chunk c's entries (row nr: their number)
+  unsigned *err;
+};
+
+template <bool DAMAGE>
+__global__ __launch_bounds__(kRouteThreads) void route_part_kernel(RoutePartArgs a) {
+  __shared__ uint32_t skey[kRouteSlots];
+  __shared__ uint32_t scnt[kRouteSlots];
+  __shared__ unsigned long long ssum[DAMAGE ? kRouteSlots : 1];
+  __shared__ uint32_t hist[kRouteRanges];
+  __shared__ uint32_t wtot[kRouteThreads / 64];
+  static_assert(kRouteRanges == kRouteThreads, "one range per thread in the scan");
+  constexpr int SPER = kRouteSlots / kRouteThreads;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int c = blockIdx.x;
+  hist[tid] = 0u;
+  route_chunk_table<DAMAGE>(a.ids, a.lb, a.ls, a.n, a.vocab, a.err, (int64_t)c * kRouteChunk, skey, scnt, ssum);
 #pragma unroll
-  for (int k = 0; k < kRouteCopies; ++k) {
-    sx += sum[(size_t)k * vocab + x];
-    c += count[(size_t)k * vocab + x];
-    h += hcount[(size_t)k * vocab + x];
+  for (int m = 0; m < SPER; ++m) {
+    const uint32_t key = skey[tid + m * kRouteThreads];
+    if (key != kRouteNoId) atomicAdd(&hist[key >> a.rbits], 1u);
   }
-  score[x] = c ? ldexp((double)sx / (double)c, -32) : __builtin_huge_val();
-  hcount_total[x] = h;
+  __syncthreads();
+  // exclusive scan of the ranges' entry counts: within the wavefront, then
+  // the wavefronts' totals
+  const uint32_t hv = hist[tid];
+  uint32_t incl = hv;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += t;
+  }
+  if (lane == 63) wtot[wv] = incl;
+  __syncthreads();
+  uint32_t excl = incl - hv;
+  for (int q = 0; q < wv; ++q) excl += wtot[q];
+  if (tid < a.nr) a.off[(size_t)tid * a.nchunks + c] = excl;
+  if (tid == kRouteThreads - 1) a.off[(size_t)a.nr * a.nchunks + c] = excl + hv;  // ranges past nr are empty
+  hist[tid] = excl;  // the range's next free entry (every thread read its count above)
+  __syncthreads();
+  u32x4 *ce = a.ent + (size_t)c * kRouteChunk;
+#pragma unroll
+  for (int m = 0; m < SPER; ++m) {
+    const int sl = tid + m * kRouteThreads;
+    const uint32_t key = skey[sl];
+    if (key == kRouteNoId) continue;
+    const uint32_t pos = atomicAdd(&hist[key >> a.rbits], 1u);
+    const unsigned long long sm = DAMAGE ? ssum[sl] : 0ull;
+    ce[pos] = u32x4{key, scnt[sl], (uint32_t)sm, (uint32_t)(sm >> 32)};
+  }
 }
 
-__global__ __launch_bounds__(256) void route_table_kernel(const double *score, int vocab, double tau,
-                                                          uint8_t *table) {
+struct RouteMergeArgs {
+  const u32x4 *ent;
+  const uint32_t *off;
+  int nchunks, rbits, nr, vocab, parts;
+  unsigned *count;           // [parts][vocab]
+  unsigned long long *sum;   // [parts][vocab] (DAMAGE)
+};
+
+template <bool DAMAGE>
+__global__ __launch_bounds__(kRouteThreads) void route_merge_kernel(RouteMergeArgs a) {
+  constexpr int WMAX = 1 << kRouteMaxRangeBits, U = 4;
+  __shared__ uint32_t lc[WMAX];
+  __shared__ unsigned long long lsum[DAMAGE ? WMAX : 1];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int r = blockIdx.x, p = blockIdx.y, W = 1 << a.rbits;
+  for (int i = tid; i < W; i += kRouteThreads) {
+    lc[i] = 0u;
+    if constexpr (DAMAGE) lsum[i] = 0ull;
+  }
+  __syncthreads();
+  const int c0 = (int)((int64_t)p * a.nchunks / a.parts), c1 = (int)((int64_t)(p + 1) * a.nchunks / a.parts);
+  for (int c = c0 + wv; c < c1; c += kRouteThreads / 64) {
+    const uint32_t b = a.off[(size_t)r * a.nchunks + c], e = a.off[(size_t)(r + 1) * a.nchunks + c];
+    const u32x4 *ce = a.ent + (size_t)c * kRouteChunk;
+    for (uint32_t j = b + lane; j < e; j += 64 * U) {
+      u32x4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) v[u] = (j + 64 * u < e) ? ce[j + 64 * u] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (j + 64 * u >= e) continue;
+        const uint32_t k = v[u][0] & (uint32_t)(W - 1);
+        atomicAdd(&lc[k], v[u][1]);
+        if constexpr (DAMAGE) atomicAdd(&lsum[k], (unsigned long long)v[u][2] | ((unsigned long long)v[u][3] << 32));
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < W; i += kRouteThreads) {
+    const int64_t id = (int64_t)r * W + i;
+    if (id < a.vocab) {
+      a.count[(size_t)p * a.vocab + id] = lc[i];
+      if constexpr (DAMAGE) a.sum[(size_t)p * a.vocab + id] = lsum[i];
+    }
+  }
+}
+
+// Device-side words of the Eq. 14 selection (zeroed before the score launch).
+enum : int {
+  kSelF = 0,                         // held-out occurrences with a finite score
+  kSelHist = 8,                      // [8][256] weighted byte histograms of the radix passes
+  kSelNext = kSelHist + 8 * 256,     // ~bits of the smallest score above o (atomic max; 0: none)
+  kSelAtOrBelow = kSelNext + 1,      // held-out occurrences scoring <= o
+  kSelBelow = kSelNext + 2,          // ... < o
+  kSelWords = kSelNext + 3
+};
+
+__global__ __launch_bounds__(256) void route_score_kernel(const unsigned long long *sum, const unsigned *count,
+                                                          const unsigned *hcount, int parts, int vocab,
+                                                          double *score, unsigned *hcount_total,
+                                                          unsigned long long *sel) {
+  __shared__ unsigned long long wsum[4];
   const int x = blockIdx.x * 256 + threadIdx.x;
-  if (x < vocab) table[x] = score[x] < tau ? 0 : 1;
+  unsigned long long f = 0ull;
+  if (x < vocab) {
+    unsigned long long sx = 0ull;
+    unsigned c = 0u, h = 0u;
+    for (int k = 0; k < parts; ++k) {
+      sx += sum[(size_t)k * vocab + x];
+      c += count[(size_t)k * vocab + x];
+      h += hcount[(size_t)k * vocab + x];
+    }
+    score[x] = c ? ldexp((double)sx / (double)c, -32) : __builtin_huge_val();
+    hcount_total[x] = h;
+    if (c) f = h;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) f += __shfl_xor(f, o, 64);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = f;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned long long t = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    if (t) atomicAdd(sel + kSelF, t);
+  }
+}
+
+// R(c) = c / n_heldout, and T = the least c in [0, F] with R(c) >= r_tar
+// (F + 1 when there is none).
+__device__ __forceinline__ double route_r(unsigned long long c, long long nh) {
+  return nh ? (double)c / (double)nh : 0.0;
+}
+__device__ __forceinline__ unsigned long long route_target(unsigned long long F, long long nh, double r_tar) {
+  unsigned long long lo = 0ull, hi = F + 1ull;
+  while (lo < hi) {
+    const unsigned long long mid = lo + (hi - lo) / 2ull;
+    if (route_r(mid, nh) >= r_tar) hi = mid;
+    else lo = mid + 1ull;
+  }
+  return lo;
+}
+
+// The bits chosen by the first `passes` radix passes (high byte first) and
+// the rank left within them, from the passes' histograms.
+__device__ __forceinline__ unsigned long long route_replay(const unsigned long long *sel, int passes,
+                                                           unsigned long long T) {
+  unsigned long long prefix = 0ull, rank = T;
+  for (int k = 0; k < passes; ++k) {
+    const unsigned long long *h = sel + kSelHist + 256 * k;
+    int b = 0;
+    for (; b < 255 && h[b] < rank; ++b) rank -= h[b];
+    prefix |= (unsigned long long)b << (56 - 8 * k);
+  }
+  return prefix;
+}
+
+struct RouteSelArgs {
+  const double *score;
+  const unsigned *h;       // held-out occurrences per id
+  int vocab;
+  long long nh;
+  double r_tar;
+  unsigned long long *sel; // kSelWords
+  double *out;             // [2] tau*, R(tau*)
+  const unsigned *err;
+};
+
+// Radix pass k: the held-out occurrences (weights h) of candidate ids (h > 0,
+// finite score) whose score bits match the bytes chosen so far, by their
+// byte k (from the top).  Scores are >= 0, so their bit patterns order like
+// the doubles.
+__global__ __launch_bounds__(1024) void route_select_pass_kernel(RouteSelArgs a, int k) {
+  __shared__ unsigned long long lh[256];
+  __shared__ unsigned long long sp[2];
+  const int tid = threadIdx.x;
+  if (tid < 256) lh[tid] = 0ull;
+  if (tid == 0) {
+    const unsigned long long F = a.sel[kSelF], T = route_target(F, a.nh, a.r_tar);
+    sp[0] = route_replay(a.sel, k, T);
+    sp[1] = (T > 0ull && T <= F) ? 1ull : 0ull;
+  }
+  __syncthreads();
+  if (!sp[1]) return;  // no radix select (uniform)
+  const int x = blockIdx.x * 1024 + tid;
+  if (x < a.vocab) {
+    const unsigned w = a.h[x];
+    const double s = a.score[x];
+    if (w && s != __builtin_huge_val()) {
+      const unsigned long long bits = __builtin_bit_cast(unsigned long long, s);
+      if (k == 0 || (bits >> (64 - 8 * k)) == (sp[0] >> (64 - 8 * k)))
+        atomicAdd(&lh[(bits >> (56 - 8 * k)) & 255ull], (unsigned long long)w);
+    }
+  }
+  __syncthreads();
+  if (tid < 256 && lh[tid]) atomicAdd(a.sel + kSelHist + 256 * k + tid, lh[tid]);
+}
+
+// After the eight passes, o = the T-th smallest occurrence score: the
+// smallest candidate score above o (every candidate when T = 0) and the
+// weights at or below and below o.
+__global__ __launch_bounds__(1024) void route_select_final_kernel(RouteSelArgs a) {
+  __shared__ unsigned long long lw[3];
+  __shared__ unsigned long long sp[2];
+  const int tid = threadIdx.x;
+  if (tid < 3) lw[tid] = 0ull;
+  if (tid == 0) {
+    const unsigned long long F = a.sel[kSelF], T = route_target(F, a.nh, a.r_tar);
+    sp[0] = route_replay(a.sel, T > 0ull && T <= F ? 8 : 0, T);
+    sp[1] = T > F ? 0ull : (T == 0ull ? 1ull : 2ull);  // 0: +inf; 1: the smallest candidate; 2: around o
+  }
+  __syncthreads();
+  if (!sp[1]) return;
+  const int x = blockIdx.x * 1024 + tid;
+  if (x < a.vocab) {
+    const unsigned w = a.h[x];
+    const double s = a.score[x];
+    if (w && s != __builtin_huge_val()) {
+      const unsigned long long bits = __builtin_bit_cast(unsigned long long, s);
+      if (sp[1] == 1ull || bits > sp[0]) atomicMax(&lw[0], ~bits);
+      if (sp[1] == 2ull && bits <= sp[0]) atomicAdd(&lw[1], (unsigned long long)w);
+      if (sp[1] == 2ull && bits < sp[0]) atomicAdd(&lw[2], (unsigned long long)w);
+    }
+  }
+  __syncthreads();
+  if (tid == 0 && lw[0]) atomicMax(a.sel + kSelNext, lw[0]);
+  if (tid == 1 && lw[1]) atomicAdd(a.sel + kSelAtOrBelow, lw[1]);
+  if (tid == 2 && lw[2]) atomicAdd(a.sel + kSelBelow, lw[2]);
+}
+
+// tau* and R(tau*) from the words above (one thread).
+__global__ void route_decide_kernel(RouteSelArgs a) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const unsigned long long F = a.sel[kSelF], T = route_target(F, a.nh, a.r_tar);
+  const double inf = __builtin_huge_val();
+  if (T > F) {  // every candidate falls short of r_tar: the largest, +inf
+    a.out[0] = inf;
+    a.out[1] = route_r(F, a.nh);
+    return;
+  }
+  const unsigned long long nx = a.sel[kSelNext];
+  const double vstar = nx ? __builtin_bit_cast(double, ~nx) : inf;
+  if (T == 0ull) {  // no occurrence below: the smallest candidate
+    a.out[0] = vstar;
+    a.out[1] = route_r(0ull, a.nh);
+    return;
+  }
+  const double o = __builtin_bit_cast(double, route_replay(a.sel, 8, T));
+  const unsigned long long wstar = nx ? a.sel[kSelAtOrBelow] : F, wpred = a.sel[kSelBelow];
+  if (fabs(route_r(wpred, a.nh) - a.r_tar) <= fabs(route_r(wstar, a.nh) - a.r_tar)) {
+    a.out[0] = o;
+    a.out[1] = route_r(wpred, a.nh);
+  } else {
+    a.out[0] = vstar;
+    a.out[1] = route_r(wstar, a.nh);
+  }
+}
+
+__global__ __launch_bounds__(256) void route_table_kernel(const double *score, int vocab, const double *tau,
+                                                          const unsigned *err, uint8_t *table) {
+  const int x = blockIdx.x * 256 + threadIdx.x;
+  if (x < vocab && !*err) table[x] = score[x] < *tau ? 0 : 1;
+}
+
+// Zeroes n words (a kernel, not a memset, so that it can sit in a captured graph).
+__global__ __launch_bounds__(256) void route_clear_kernel(unsigned long long *w, int n, unsigned *err) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) w[i] = 0ull;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *err = 0u;
 }
 
 }  // namespace sats

@@ -58,7 +58,8 @@ Timer g_timer[SATS_K_COUNT];
 // kernel's execution and not a separate marker's.
 struct TimedLaunch {
   hipEvent_t start = nullptr, stop = nullptr;
-  TimedLaunch(int kind, hipStream_t) {
+  TimedLaunch(int kind, hipStream_t) {  // kind < 0: an untimed launch
+    if (kind < 0 || kind >= SATS_K_COUNT) return;
     Timer &tm = g_timer[kind];
     if (tm.armed && tm.used < tm.cap) {
       const int slot = tm.used++;
@@ -1238,87 +1239,47 @@ int forward_lora(const T *x, const int32_t *token_ids, const T *W_gate, const T 
 }
 // --------------------------------------------------------------- routing table
 
-// tau* of Eq. 14 over the candidates (distinct values of cs, weights cw =
-// held-out occurrences, and +inf).  R(tau) = W(tau) / n_heldout with W(tau)
-// the weight of the scores below tau grows strictly from candidate to
-// candidate, so |R - r_tar| falls and then rises: the best candidate is the
-// first one with R >= r_tar or the one before it (the earlier on ties).  The
-// first one is found through the weighted order statistic o of rank T' (the
-// least weight with R >= r_tar): it is the least score above o (+inf if
-// none), and o is the candidate before it.  The order statistic is a radix
-// select on the bit patterns of the scores (non-negative doubles order like
-// their patterns), 8 bits per pass.
-void route_select(const std::vector<double> &cs, const std::vector<unsigned> &cw, int64_t nh, double r_tar,
-                  double *tau, double *r) {
-  const size_t n = cs.size();
-  uint64_t F = 0;
-  for (unsigned w : cw) F += w;
-  auto R = [&](uint64_t c) { return nh ? (double)c / (double)nh : 0.0; };
-  // T': the least c in [0, F] with R(c) >= r_tar (F + 1 if none)
-  uint64_t lo = 0, hi = F + 1;
-  while (lo < hi) {
-    const uint64_t mid = lo + (hi - lo) / 2;
-    if (R(mid) >= r_tar) hi = mid;
-    else lo = mid + 1;
-  }
-  const uint64_t T = lo;
-  if (T > F) {  // every candidate falls short of r_tar: the largest, +inf
-    *tau = INFINITY;
-    *r = R(F);
-    return;
-  }
-  double vstar = INFINITY, pred = 0.0;
-  bool has_pred = false;
-  uint64_t wstar = F, wpred = 0;
-  if (T == 0) {
-    for (double v : cs) vstar = std::min(vstar, v);
-    wstar = 0;
-  } else {
-    // o = the T-th smallest occurrence score (weighted radix select)
-    std::vector<uint32_t> idx(n);
-    for (size_t i = 0; i < n; ++i) idx[i] = (uint32_t)i;
-    uint64_t prefix = 0, rank = T;
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      uint64_t hist[256] = {0};
-      for (uint32_t i : idx) {
-        uint64_t bits;
-        std::memcpy(&bits, &cs[i], 8);
-        hist[(bits >> shift) & 255u] += cw[i];
-      }
-      unsigned b = 0;
-      for (; b < 255 && hist[b] < rank; ++b) rank -= hist[b];
-      prefix |= (uint64_t)b << shift;
-      std::vector<uint32_t> keep;
-      for (uint32_t i : idx) {
-        uint64_t bits;
-        std::memcpy(&bits, &cs[i], 8);
-        if (((bits >> shift) & 255u) == b) keep.push_back(i);
-      }
-      idx.swap(keep);
-    }
-    double o;
-    std::memcpy(&o, &prefix, 8);
-    has_pred = true;
-    pred = o;
-    wstar = 0;
-    for (size_t i = 0; i < n; ++i) {
-      if (cs[i] > o) vstar = std::min(vstar, cs[i]);
-      else wstar += cw[i];                   // scores <= o lie below vstar
-      if (cs[i] < o) wpred += cw[i];
-    }
-    if (vstar == INFINITY) wstar = F;
-  }
-  if (has_pred && std::fabs(R(wpred) - r_tar) <= std::fabs(R(wstar) - r_tar)) {
-    *tau = pred;
-    *r = R(wpred);
-  } else {
-    *tau = vstar;
-    *r = R(wstar);
-  }
+// Device buffers of the routing-table construction, kept from call to call
+// per device (grown when a call needs more; freed by sats_release).  Calls
+// hold g_route_mu throughout (each call synchronises its stream before it
+// returns), so two calls never share them at once.
+struct RouteBuffers {
+  size_t ent = 0, off = 0, parts = 0, vocab = 0;  // capacities: entries, offsets, part words, ids
+  sats::u32x4 *pent = nullptr;
+  uint32_t *poff = nullptr;
+  unsigned *cnt = nullptr, *hcnt = nullptr, *htot = nullptr, *err = nullptr;
+  unsigned long long *sum = nullptr, *sel = nullptr;
+  double *score = nullptr, *out = nullptr;
+};
+std::mutex g_route_mu;
+std::map<int, RouteBuffers> g_route;
+
+template <typename P> int route_grow(P **p, size_t *cap, size_t need) {
+  if (*p && *cap >= need) return SATS_OK;
+  if (*p) HIP_TRY(hipFree(*p));
+  *p = nullptr;
+  *cap = 0;
+  if (hipMalloc((void **)p, std::max<size_t>(need, 1) * sizeof(P)) != hipSuccess)
+    return fail(SATS_ERR_WORKSPACE, "routing-table buffer of %zu bytes failed", need * sizeof(P));
+  *cap = need;
+  return SATS_OK;
 }
 
-// The routing-table construction of Eq. 11-14 (synchronous; buffers of its
-// own, like calibration).
+int route_release_all() {
+  std::lock_guard<std::mutex> lk(g_route_mu);
+  for (auto &kv : g_route) {
+    HIP_TRY(hipSetDevice(kv.first));
+    HIP_TRY(hipDeviceSynchronize());
+    RouteBuffers &b = kv.second;
+    for (void *q : {(void *)b.pent, (void *)b.poff, (void *)b.cnt, (void *)b.hcnt, (void *)b.htot, (void *)b.err,
+                    (void *)b.sum, (void *)b.sel, (void *)b.score, (void *)b.out})
+      if (q) HIP_TRY(hipFree(q));
+  }
+  g_route.clear();
+  return SATS_OK;
+}
+
+// The routing-table construction of Eq. 11-14 (synchronous).
 int route_build(const float *lb, const float *ls, const int32_t *ids, int64_t n, const int32_t *hids, int64_t nh,
                 int64_t vocab, double r_tar, uint8_t *table, double *score_out, double *tau_out,
                 double *realized_out, hipStream_t s) {
@@ -1329,76 +1290,91 @@ int route_build(const float *lb, const float *ls, const int32_t *ids, int64_t n,
     return fail(SATS_ERR_SHAPE, "need n_tokens, n_heldout >= 0 and 1 <= vocab < 2^31");
   if (!(r_tar >= 0.0 && r_tar <= 1.0)) return fail(SATS_ERR_ARG, "r_tar must be in [0, 1]");
   const size_t V = (size_t)vocab;
-  unsigned long long *sum = nullptr;
-  unsigned *cnt = nullptr, *hcnt = nullptr, *htot = nullptr, *err = nullptr;
-  double *score = score_out;
-  struct Free {
-    void *p[6] = {};
-    ~Free() {
-      for (void *q : p)
-        if (q) (void)hipFree(q);
-    }
-  } fr;
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(g_route_mu);
+  RouteBuffers &b = g_route[dev];
+  // partitioned sums (ranges of 2^rbits ids, at most kRouteRanges of them),
+  // or per-chunk atomics into kRouteCopies copies past kRoutePartMaxVocab
+  const bool part = vocab <= kRoutePartMaxVocab;
+  int rbits = 10;
+  while (((vocab + (1ll << rbits) - 1) >> rbits) > kRouteRanges) ++rbits;
+  const int nr = (int)((vocab + (1ll << rbits) - 1) >> rbits);
+  const int64_t nc = (n + kRouteChunk - 1) / kRouteChunk, nhc = (nh + kRouteChunk - 1) / kRouteChunk;
+  if (nc > INT32_MAX || nhc > INT32_MAX) return fail(SATS_ERR_SHAPE, "too many occurrences");
+  const int P = part ? kRouteParts : kRouteCopies;
+  const int64_t mc = std::max<int64_t>(nc, nhc);
   int rc = 0;
-  const size_t VC = V * kRouteCopies;
-  if ((rc = cal_alloc(&sum, VC)) || (rc = cal_alloc(&cnt, VC)) || (rc = cal_alloc(&hcnt, VC)) ||
-      (rc = cal_alloc(&htot, V)) || (rc = cal_alloc(&err, 1)))
+  size_t cap_sum = b.parts, cap_h = b.parts, cap_v = b.vocab, cap_v2 = b.vocab, cap_sel = kSelWords, cap_o = 2,
+         cap_e = 1;
+  if ((part && ((rc = route_grow(&b.pent, &b.ent, (size_t)mc * kRouteChunk)) ||
+                (rc = route_grow(&b.poff, &b.off, (size_t)(nr + 1) * mc)))) ||
+      (rc = route_grow(&b.cnt, &b.parts, (size_t)P * V)) || (rc = route_grow(&b.sum, &cap_sum, (size_t)P * V)) ||
+      (rc = route_grow(&b.hcnt, &cap_h, (size_t)P * V)) || (rc = route_grow(&b.htot, &b.vocab, V)) ||
+      (rc = route_grow(&b.score, &cap_v, V)))
     return rc;
-  fr.p[0] = sum;
-  fr.p[1] = cnt;
-  fr.p[2] = hcnt;
-  fr.p[3] = err;
-  fr.p[5] = htot;
-  if (!score) {
-    if ((rc = cal_alloc(&score, V))) return rc;
-    fr.p[4] = score;
+  (void)cap_v2;
+  if (!b.sel && ((rc = route_grow(&b.sel, &cap_sel, (size_t)kSelWords)) || (rc = route_grow(&b.out, &cap_o, 2)) ||
+                 (rc = route_grow(&b.err, &cap_e, 1))))
+    return rc;
+  double *score = score_out ? score_out : b.score;
+  hipLaunchKernelGGL(route_clear_kernel, dim3(8), dim3(256), 0, s, b.sel, (int)kSelWords, b.err);
+  if (part) {
+    // each split: entries per chunk, then the merge of every range (the
+    // merge also runs for an empty split: zero totals)
+    for (int split = 0; split < 2; ++split) {
+      const bool dmg = split == 0;
+      const int64_t nn = dmg ? n : nh, ch = dmg ? nc : nhc;
+      if (nn > 0) {
+        RoutePartArgs pa{dmg ? ids : hids, lb, ls, nn, (int)vocab, rbits, nr, (int)ch, b.pent, b.poff, b.err};
+        TimedLaunch tl(dmg ? SATS_K_ROUTE_ACCUM : -1, s);
+        hipExtLaunchKernelGGL(dmg ? route_part_kernel<true> : route_part_kernel<false>, dim3((unsigned)ch),
+                              dim3(kRouteThreads), 0, s, tl.start, tl.stop, 0, pa);
+        HIP_TRY(hipGetLastError());
+      }
+      RouteMergeArgs ma{b.pent, b.poff, (int)ch, rbits, nr, (int)vocab, P, dmg ? b.cnt : b.hcnt, b.sum};
+      TimedLaunch tl(dmg ? SATS_K_ROUTE_MERGE : -1, s);
+      hipExtLaunchKernelGGL(dmg ? route_merge_kernel<true> : route_merge_kernel<false>, dim3(nr, P),
+                            dim3(kRouteThreads), 0, s, tl.start, tl.stop, 0, ma);
+      HIP_TRY(hipGetLastError());
+    }
+  } else {
+    HIP_TRY(hipMemsetAsync(b.sum, 0, (size_t)P * V * sizeof(unsigned long long), s));
+    HIP_TRY(hipMemsetAsync(b.cnt, 0, (size_t)P * V * sizeof(unsigned), s));
+    HIP_TRY(hipMemsetAsync(b.hcnt, 0, (size_t)P * V * sizeof(unsigned), s));
+    if (n > 0) {
+      RouteAccumArgs ra{ids, lb, ls, n, (int)vocab, b.sum, b.cnt, b.err};
+      TimedLaunch tl(SATS_K_ROUTE_ACCUM, s);
+      hipExtLaunchKernelGGL(route_accum_kernel<true>, dim3((unsigned)nc), dim3(kRouteThreads), 0, s, tl.start,
+                            tl.stop, 0, ra);
+    }
+    if (nh > 0) {
+      RouteAccumArgs ra{hids, nullptr, nullptr, nh, (int)vocab, nullptr, b.hcnt, b.err};
+      hipLaunchKernelGGL(route_accum_kernel<false>, dim3((unsigned)nhc), dim3(kRouteThreads), 0, s, ra);
+    }
+    HIP_TRY(hipGetLastError());
   }
-  HIP_TRY(hipMemsetAsync(sum, 0, VC * sizeof(unsigned long long), s));
-  HIP_TRY(hipMemsetAsync(cnt, 0, VC * sizeof(unsigned), s));
-  HIP_TRY(hipMemsetAsync(hcnt, 0, VC * sizeof(unsigned), s));
-  HIP_TRY(hipMemsetAsync(err, 0, sizeof(unsigned), s));
-  if (n > 0) {
-    RouteAccumArgs ra{ids, lb, ls, n, (int)vocab, sum, cnt, err};
-    TimedLaunch tl(SATS_K_ROUTE_ACCUM, s);
-    hipExtLaunchKernelGGL(route_accum_kernel<true>, dim3((unsigned)((n + kRouteChunk - 1) / kRouteChunk)),
-                          dim3(kRouteThreads), 0, s, tl.start, tl.stop, 0, ra);
-  }
-  if (nh > 0) {
-    RouteAccumArgs ra{hids, nullptr, nullptr, nh, (int)vocab, nullptr, hcnt, err};
-    hipLaunchKernelGGL(route_accum_kernel<false>, dim3((unsigned)((nh + kRouteChunk - 1) / kRouteChunk)),
-                       dim3(kRouteThreads), 0, s, ra);
-  }
-  hipLaunchKernelGGL(route_score_kernel, dim3((unsigned)((V + 255) / 256)), dim3(256), 0, s, sum, cnt, hcnt,
-                     (int)vocab, score, htot);
+  const unsigned vb = (unsigned)((V + 255) / 256), vk = (unsigned)((V + 1023) / 1024);
+  hipLaunchKernelGGL(route_score_kernel, dim3(vb), dim3(256), 0, s, b.sum, b.cnt, b.hcnt, P, (int)vocab, score,
+                     b.htot, b.sel);
+  // Eq. 14 on the device
+  RouteSelArgs sa{score, b.htot, (int)vocab, (long long)nh, r_tar, b.sel, b.out, b.err};
+  for (int k = 0; k < 8; ++k)
+    hipLaunchKernelGGL(route_select_pass_kernel, dim3(vk), dim3(1024), 0, s, sa, k);
+  hipLaunchKernelGGL(route_select_final_kernel, dim3(vk), dim3(1024), 0, s, sa);
+  hipLaunchKernelGGL(route_decide_kernel, dim3(1), dim3(64), 0, s, sa);
+  hipLaunchKernelGGL(route_table_kernel, dim3(vb), dim3(256), 0, s, score, (int)vocab, b.out, b.err, table);
   HIP_TRY(hipGetLastError());
-  std::vector<double> hs(V);
-  std::vector<unsigned> hh(V);
+  double res[2] = {0.0, 0.0};
   unsigned herr = 0;
-  HIP_TRY(hipMemcpyAsync(hs.data(), score, V * sizeof(double), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipMemcpyAsync(hh.data(), htot, V * sizeof(unsigned), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipMemcpyAsync(&herr, err, sizeof(unsigned), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(res, b.out, sizeof res, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipMemcpyAsync(&herr, b.err, sizeof herr, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
   if (herr == 1) return fail(SATS_ERR_ARG, "a token id is outside [0, vocab)");
   if (herr == 2) return fail(SATS_ERR_ARG, "a loss difference is NaN or at least 2^31");
   if (herr) return fail(SATS_ERR_DEVICE, "routing table: a chunk's id table overflowed");
-  // Eq. 14: candidates are the distinct finite scores of the held-out ids and
-  // +inf; R(tau) = (held-out occurrences with s < tau) / n_heldout; the
-  // nearest to r_tar wins, the smallest tau on ties.
-  std::vector<double> cs;
-  std::vector<unsigned> cw;
-  for (size_t x = 0; x < V; ++x)
-    if (hh[x] && std::isfinite(hs[x])) {
-      cs.push_back(hs[x]);
-      cw.push_back(hh[x]);
-    }
-  double best_tau = 0.0, best_r = 0.0;
-  route_select(cs, cw, nh, r_tar, &best_tau, &best_r);
-  hipLaunchKernelGGL(route_table_kernel, dim3((unsigned)((V + 255) / 256)), dim3(256), 0, s, score, (int)vocab,
-                     best_tau, table);
-  HIP_TRY(hipGetLastError());
-  HIP_TRY(hipStreamSynchronize(s));
-  if (tau_out) *tau_out = best_tau;
-  if (realized_out) *realized_out = best_r;
+  if (tau_out) *tau_out = res[0];
+  if (realized_out) *realized_out = res[1];
   return SATS_OK;
 }
 }  // namespace
@@ -1553,7 +1529,9 @@ int sats_release(void) {
   }
   g_ws.clear();
   HIP_TRY(hipSetDevice(cur));
-  return SATS_OK;
+  int rc = route_release_all();
+  HIP_TRY(hipSetDevice(cur));
+  return rc;
 }
 
 int sats_calibration_curves(const sats_bf16 *h, const sats_bf16 *W_gate, const sats_bf16 *W_up_T,
@@ -1716,7 +1694,8 @@ const char *sats_kernel_name(int kind) {
     case SATS_K_INSPECT: return "compact_kernel";
     case SATS_K_DENSE: return "dense_gateup_kernel";
     case SATS_K_DENSE_DOWN: return "dense_down_kernel";
-    case SATS_K_ROUTE_ACCUM: return "route_accum_kernel";
+    case SATS_K_ROUTE_ACCUM: return "route_part_kernel";
+    case SATS_K_ROUTE_MERGE: return "route_merge_kernel";
     case SATS_K_LORA_V: return "lora_v_kernel";
     case SATS_K_DEC_LAYER: return "dec_layer_kernel";
     case SATS_K_DEC_LORA_V: return "dec_lora_v_kernel";
