@@ -27,14 +27,16 @@
 //       (the empirical mean of Eq. 12), +inf for ids without occurrences;
 //       the held-out counts' parts likewise; and F, the held-out
 //       occurrences whose id has a finite score.
-//   route_select_pass_kernel, route_select_final_kernel, route_decide_kernel
+//   route_select_pass_kernel, route_select_final_kernel
 //       Eq. 14 on the device: T, the least count c <= F with c / n_heldout
 //       >= r_tar; the T-th smallest held-out occurrence score o by a radix
 //       select on the bits of the scores (eight passes of 8 bits, each a
-//       histogram weighted by the held-out counts, every workgroup replaying
-//       the earlier passes' choices from their histograms); then the
-//       smallest score above o and the counts at or below and below o; of o
-//       and that next score the one whose R is nearer r_tar, o on ties.
+//       histogram weighted by the held-out counts; the first is made by the
+//       score launch, and each launch takes the bits chosen so far from the
+//       previous one and the previous histogram); then the smallest score
+//       above o and the counts at or below and below o, and the last
+//       workgroup picks of o and that next score the one whose R is nearer
+//       r_tar, o on ties.
 //   route_table_kernel
 //       table[x] = 0 (sparse path) if s(x) < tau, else 1 (Eq. 13).
 #pragma once
@@ -262,19 +264,38 @@ __global__ __launch_bounds__(kRouteThreads) void route_merge_kernel(RouteMergeAr
 // Device-side words of the Eq. 14 selection (zeroed before the score launch).
 enum : int {
   kSelF = 0,                         // held-out occurrences with a finite score
+  kSelDone = 1,                      // workgroups of the final pass finished (the last one decides)
   kSelHist = 8,                      // [8][256] weighted byte histograms of the radix passes
   kSelNext = kSelHist + 8 * 256,     // ~bits of the smallest score above o (atomic max; 0: none)
   kSelAtOrBelow = kSelNext + 1,      // held-out occurrences scoring <= o
   kSelBelow = kSelNext + 2,          // ... < o
-  kSelWords = kSelNext + 3
+  kSelState = kSelNext + 3,          // [9][2] bits chosen and rank left after k radix passes
+  kSelWords = kSelState + 18
 };
 
+// Candidate ids of Eq. 14: held out (weight h > 0) with a finite score.
+// Scores are >= 0, so their bit patterns order like the doubles.
+__device__ __forceinline__ bool route_candidate(unsigned w, double s) { return w && s != __builtin_huge_val(); }
+
+// Radix pass k's histogram: the weights of the candidates whose score bits
+// match `prefix` above byte k (from the top), by their byte k.
+__device__ __forceinline__ void route_hist_add(unsigned long long *lh, unsigned long long bits, unsigned w, int k,
+                                               unsigned long long prefix) {
+  if (k == 0 || (bits >> (64 - 8 * k)) == (prefix >> (64 - 8 * k)))
+    atomicAdd(&lh[(bits >> (56 - 8 * k)) & 255ull], (unsigned long long)w);
+}
+
+// Totals of the parts, the scores (Eq. 12), the held-out totals, F, and the
+// first radix pass's histogram (which does not depend on the rank).
 __global__ __launch_bounds__(256) void route_score_kernel(const unsigned long long *sum, const unsigned *count,
                                                           const unsigned *hcount, int parts, int vocab,
                                                           double *score, unsigned *hcount_total,
                                                           unsigned long long *sel) {
   __shared__ unsigned long long wsum[4];
+  __shared__ unsigned long long lh[256];
   const int x = blockIdx.x * 256 + threadIdx.x;
+  lh[threadIdx.x] = 0ull;
+  __syncthreads();
   unsigned long long f = 0ull;
   if (x < vocab) {
     unsigned long long sx = 0ull;
@@ -284,9 +305,13 @@ __global__ __launch_bounds__(256) void route_score_kernel(const unsigned long lo
       c += count[(size_t)k * vocab + x];
       h += hcount[(size_t)k * vocab + x];
     }
-    score[x] = c ? ldexp((double)sx / (double)c, -32) : __builtin_huge_val();
+    const double sc = c ? ldexp((double)sx / (double)c, -32) : __builtin_huge_val();
+    score[x] = sc;
     hcount_total[x] = h;
-    if (c) f = h;
+    if (route_candidate(h, sc)) {
+      f = h;
+      route_hist_add(lh, __builtin_bit_cast(unsigned long long, sc), h, 0, 0ull);
+    }
   }
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) f += __shfl_xor(f, o, 64);
@@ -296,6 +321,7 @@ __global__ __launch_bounds__(256) void route_score_kernel(const unsigned long lo
     const unsigned long long t = wsum[0] + wsum[1] + wsum[2] + wsum[3];
     if (t) atomicAdd(sel + kSelF, t);
   }
+  if (lh[threadIdx.x]) atomicAdd(sel + kSelHist + threadIdx.x, lh[threadIdx.x]);
 }
 
 // R(c) = c / n_heldout, and T = the least c in [0, F] with R(c) >= r_tar
@@ -313,20 +339,6 @@ __device__ __forceinline__ unsigned long long route_target(unsigned long long F,
   return lo;
 }
 
-// The bits chosen by the first `passes` radix passes (high byte first) and
-// the rank left within them, from the passes' histograms.
-__device__ __forceinline__ unsigned long long route_replay(const unsigned long long *sel, int passes,
-                                                           unsigned long long T) {
-  unsigned long long prefix = 0ull, rank = T;
-  for (int k = 0; k < passes; ++k) {
-    const unsigned long long *h = sel + kSelHist + 256 * k;
-    int b = 0;
-    for (; b < 255 && h[b] < rank; ++b) rank -= h[b];
-    prefix |= (unsigned long long)b << (56 - 8 * k);
-  }
-  return prefix;
-}
-
 struct RouteSelArgs {
   const double *score;
   const unsigned *h;       // held-out occurrences per id
@@ -338,89 +350,112 @@ struct RouteSelArgs {
   const unsigned *err;
 };
 
-// Radix pass k: the held-out occurrences (weights h) of candidate ids (h > 0,
-// finite score) whose score bits match the bytes chosen so far, by their
-// byte k (from the top).  Scores are >= 0, so their bit patterns order like
-// the doubles.
-__global__ __launch_bounds__(1024) void route_select_pass_kernel(RouteSelArgs a, int k) {
-  __shared__ unsigned long long lh[256];
-  __shared__ unsigned long long sp[2];
+// The state after k radix passes (k >= 1) in st[0] (bits chosen) and st[1]
+// (rank left), from the state after k - 1 (state 0: nothing chosen, rank T)
+// and pass k - 1's histogram; workgroup 0 records it for the next launch.
+// Also st[2]: whether a radix select runs at all (0 < T <= F), st[3]: T,
+// st[4]: F.  Every workgroup computes the same values.
+__device__ __forceinline__ void route_state(const RouteSelArgs &a, int k, unsigned long long *hb,
+                                            unsigned long long *st) {
   const int tid = threadIdx.x;
-  if (tid < 256) lh[tid] = 0ull;
+  if (tid < 256) hb[tid] = a.sel[kSelHist + 256 * (k - 1) + tid];
   if (tid == 0) {
     const unsigned long long F = a.sel[kSelF], T = route_target(F, a.nh, a.r_tar);
-    sp[0] = route_replay(a.sel, k, T);
-    sp[1] = (T > 0ull && T <= F) ? 1ull : 0ull;
+    st[2] = (T > 0ull && T <= F) ? 1ull : 0ull;
+    st[3] = T;
+    st[4] = F;
+    st[0] = k == 1 ? 0ull : a.sel[kSelState + 2 * (k - 1)];
+    st[1] = k == 1 ? T : a.sel[kSelState + 2 * (k - 1) + 1];
   }
   __syncthreads();
-  if (!sp[1]) return;  // no radix select (uniform)
+  if (tid == 0 && st[2]) {
+    unsigned long long rank = st[1];
+    int b = 0;
+    for (; b < 255 && hb[b] < rank; ++b) rank -= hb[b];
+    st[0] |= (unsigned long long)b << (56 - 8 * (k - 1));
+    st[1] = rank;
+    if (blockIdx.x == 0) {
+      a.sel[kSelState + 2 * k] = st[0];
+      a.sel[kSelState + 2 * k + 1] = rank;
+    }
+  }
+  __syncthreads();
+}
+
+// Radix pass k (1..7): the histogram of byte k of the candidates matching
+// the bytes chosen so far.
+__global__ __launch_bounds__(1024) void route_select_pass_kernel(RouteSelArgs a, int k) {
+  __shared__ unsigned long long lh[256], hb[256], st[5];
+  const int tid = threadIdx.x;
+  if (tid < 256) lh[tid] = 0ull;
+  route_state(a, k, hb, st);
+  if (!st[2]) return;  // no radix select (uniform)
   const int x = blockIdx.x * 1024 + tid;
   if (x < a.vocab) {
     const unsigned w = a.h[x];
     const double s = a.score[x];
-    if (w && s != __builtin_huge_val()) {
-      const unsigned long long bits = __builtin_bit_cast(unsigned long long, s);
-      if (k == 0 || (bits >> (64 - 8 * k)) == (sp[0] >> (64 - 8 * k)))
-        atomicAdd(&lh[(bits >> (56 - 8 * k)) & 255ull], (unsigned long long)w);
-    }
+    if (route_candidate(w, s)) route_hist_add(lh, __builtin_bit_cast(unsigned long long, s), w, k, st[0]);
   }
   __syncthreads();
   if (tid < 256 && lh[tid]) atomicAdd(a.sel + kSelHist + 256 * k + tid, lh[tid]);
 }
 
-// After the eight passes, o = the T-th smallest occurrence score: the
-// smallest candidate score above o (every candidate when T = 0) and the
-// weights at or below and below o.
+// After the eight passes, o = the T-th smallest held-out occurrence score:
+// the smallest candidate score above o (every candidate when T = 0) and the
+// weights at or below and below o; the last workgroup to finish then picks
+// tau* and R(tau*): of o and the next score the one whose R is nearer
+// r_tar (o on ties); +inf when even every candidate falls short of r_tar.
 __global__ __launch_bounds__(1024) void route_select_final_kernel(RouteSelArgs a) {
-  __shared__ unsigned long long lw[3];
-  __shared__ unsigned long long sp[2];
+  __shared__ unsigned long long lw[3], hb[256], st[5];
+  __shared__ int last;
   const int tid = threadIdx.x;
   if (tid < 3) lw[tid] = 0ull;
-  if (tid == 0) {
-    const unsigned long long F = a.sel[kSelF], T = route_target(F, a.nh, a.r_tar);
-    sp[0] = route_replay(a.sel, T > 0ull && T <= F ? 8 : 0, T);
-    sp[1] = T > F ? 0ull : (T == 0ull ? 1ull : 2ull);  // 0: +inf; 1: the smallest candidate; 2: around o
-  }
-  __syncthreads();
-  if (!sp[1]) return;
+  route_state(a, 8, hb, st);
+  const unsigned long long F = st[4], T = st[3], o = st[0];
+  const int mode = T > F ? 0 : (T == 0ull ? 1 : 2);  // 0: +inf; 1: the smallest candidate; 2: around o
   const int x = blockIdx.x * 1024 + tid;
-  if (x < a.vocab) {
+  if (mode && x < a.vocab) {
     const unsigned w = a.h[x];
     const double s = a.score[x];
-    if (w && s != __builtin_huge_val()) {
+    if (route_candidate(w, s)) {
       const unsigned long long bits = __builtin_bit_cast(unsigned long long, s);
-      if (sp[1] == 1ull || bits > sp[0]) atomicMax(&lw[0], ~bits);
-      if (sp[1] == 2ull && bits <= sp[0]) atomicAdd(&lw[1], (unsigned long long)w);
-      if (sp[1] == 2ull && bits < sp[0]) atomicAdd(&lw[2], (unsigned long long)w);
+      if (mode == 1 || bits > o) atomicMax(&lw[0], ~bits);
+      if (mode == 2 && bits <= o) atomicAdd(&lw[1], (unsigned long long)w);
+      if (mode == 2 && bits < o) atomicAdd(&lw[2], (unsigned long long)w);
     }
   }
   __syncthreads();
-  if (tid == 0 && lw[0]) atomicMax(a.sel + kSelNext, lw[0]);
-  if (tid == 1 && lw[1]) atomicAdd(a.sel + kSelAtOrBelow, lw[1]);
-  if (tid == 2 && lw[2]) atomicAdd(a.sel + kSelBelow, lw[2]);
-}
-
-// tau* and R(tau*) from the words above (one thread).
-__global__ void route_decide_kernel(RouteSelArgs a) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const unsigned long long F = a.sel[kSelF], T = route_target(F, a.nh, a.r_tar);
+  if (tid == 0 && lw[0]) __hip_atomic_fetch_max(a.sel + kSelNext, lw[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 1 && lw[1]) __hip_atomic_fetch_add(a.sel + kSelAtOrBelow, lw[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 2 && lw[2]) __hip_atomic_fetch_add(a.sel + kSelBelow, lw[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // the last workgroup to arrive sees every other one's totals
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned long long prev = __hip_atomic_fetch_add(a.sel + kSelDone, 1ull, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT);
+    last = prev == gridDim.x - 1ull;
+  }
+  __syncthreads();
+  if (!last || tid != 0) return;
   const double inf = __builtin_huge_val();
-  if (T > F) {  // every candidate falls short of r_tar: the largest, +inf
+  if (mode == 0) {  // every candidate falls short of r_tar: the largest, +inf
     a.out[0] = inf;
     a.out[1] = route_r(F, a.nh);
     return;
   }
-  const unsigned long long nx = a.sel[kSelNext];
+  const unsigned long long nx = __hip_atomic_load(a.sel + kSelNext, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const double vstar = nx ? __builtin_bit_cast(double, ~nx) : inf;
-  if (T == 0ull) {  // no occurrence below: the smallest candidate
+  if (mode == 1) {  // no occurrence below: the smallest candidate
     a.out[0] = vstar;
     a.out[1] = route_r(0ull, a.nh);
     return;
   }
-  const double o = __builtin_bit_cast(double, route_replay(a.sel, 8, T));
-  const unsigned long long wstar = nx ? a.sel[kSelAtOrBelow] : F, wpred = a.sel[kSelBelow];
+  const unsigned long long wle = __hip_atomic_load(a.sel + kSelAtOrBelow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const unsigned long long wpred = __hip_atomic_load(a.sel + kSelBelow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const unsigned long long wstar = nx ? wle : F;
   if (fabs(route_r(wpred, a.nh) - a.r_tar) <= fabs(route_r(wstar, a.nh) - a.r_tar)) {
-    a.out[0] = o;
+    a.out[0] = __builtin_bit_cast(double, o);
     a.out[1] = route_r(wpred, a.nh);
   } else {
     a.out[0] = vstar;

@@ -1247,7 +1247,8 @@ struct RouteBuffers {
   size_t ent = 0, off = 0, parts = 0, vocab = 0;  // capacities: entries, offsets, part words, ids
   sats::u32x4 *pent = nullptr;
   uint32_t *poff = nullptr;
-  unsigned *cnt = nullptr, *hcnt = nullptr, *htot = nullptr, *err = nullptr;
+  unsigned *cnt = nullptr, *hcnt = nullptr, *htot = nullptr;
+  unsigned *err = nullptr;  // inside out (its third word)
   unsigned long long *sum = nullptr, *sel = nullptr;
   double *score = nullptr, *out = nullptr;
 };
@@ -1271,8 +1272,8 @@ int route_release_all() {
     HIP_TRY(hipSetDevice(kv.first));
     HIP_TRY(hipDeviceSynchronize());
     RouteBuffers &b = kv.second;
-    for (void *q : {(void *)b.pent, (void *)b.poff, (void *)b.cnt, (void *)b.hcnt, (void *)b.htot, (void *)b.err,
-                    (void *)b.sum, (void *)b.sel, (void *)b.score, (void *)b.out})
+    for (void *q : {(void *)b.pent, (void *)b.poff, (void *)b.cnt, (void *)b.hcnt, (void *)b.htot, (void *)b.sum,
+                    (void *)b.sel, (void *)b.score, (void *)b.out})
       if (q) HIP_TRY(hipFree(q));
   }
   g_route.clear();
@@ -1314,9 +1315,11 @@ int route_build(const float *lb, const float *ls, const int32_t *ids, int64_t n,
       (rc = route_grow(&b.score, &cap_v, V)))
     return rc;
   (void)cap_v2;
-  if (!b.sel && ((rc = route_grow(&b.sel, &cap_sel, (size_t)kSelWords)) || (rc = route_grow(&b.out, &cap_o, 2)) ||
-                 (rc = route_grow(&b.err, &cap_e, 1))))
+  // out: tau*, R(tau*) and the error flag (one copy back)
+  if (!b.sel && ((rc = route_grow(&b.sel, &cap_sel, (size_t)kSelWords)) || (rc = route_grow(&b.out, &cap_o, 3))))
     return rc;
+  b.err = reinterpret_cast<unsigned *>(b.out + 2);
+  (void)cap_e;
   double *score = score_out ? score_out : b.score;
   hipLaunchKernelGGL(route_clear_kernel, dim3(8), dim3(256), 0, s, b.sel, (int)kSelWords, b.err);
   if (part) {
@@ -1359,17 +1362,16 @@ int route_build(const float *lb, const float *ls, const int32_t *ids, int64_t n,
                      b.htot, b.sel);
   // Eq. 14 on the device
   RouteSelArgs sa{score, b.htot, (int)vocab, (long long)nh, r_tar, b.sel, b.out, b.err};
-  for (int k = 0; k < 8; ++k)
+  for (int k = 1; k < 8; ++k)
     hipLaunchKernelGGL(route_select_pass_kernel, dim3(vk), dim3(1024), 0, s, sa, k);
   hipLaunchKernelGGL(route_select_final_kernel, dim3(vk), dim3(1024), 0, s, sa);
-  hipLaunchKernelGGL(route_decide_kernel, dim3(1), dim3(64), 0, s, sa);
   hipLaunchKernelGGL(route_table_kernel, dim3(vb), dim3(256), 0, s, score, (int)vocab, b.out, b.err, table);
   HIP_TRY(hipGetLastError());
-  double res[2] = {0.0, 0.0};
-  unsigned herr = 0;
+  double res[3] = {0.0, 0.0, 0.0};  // tau*, R(tau*), the error flag in the low word of the third
   HIP_TRY(hipMemcpyAsync(res, b.out, sizeof res, hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipMemcpyAsync(&herr, b.err, sizeof herr, hipMemcpyDeviceToHost, s));
   HIP_TRY(hipStreamSynchronize(s));
+  unsigned herr = 0;
+  std::memcpy(&herr, &res[2], sizeof herr);
   if (herr == 1) return fail(SATS_ERR_ARG, "a token id is outside [0, vocab)");
   if (herr == 2) return fail(SATS_ERR_ARG, "a loss difference is NaN or at least 2^31");
   if (herr) return fail(SATS_ERR_DEVICE, "routing table: a chunk's id table overflowed");
