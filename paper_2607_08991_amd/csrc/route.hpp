@@ -270,7 +270,8 @@ enum : int {
   kSelAtOrBelow = kSelNext + 1,      // held-out occurrences scoring <= o
   kSelBelow = kSelNext + 2,          // ... < o
   kSelState = kSelNext + 3,          // [9][2] bits chosen and rank left after k radix passes
-  kSelWords = kSelState + 18
+  kSelT = kSelState + 18,            // T (written by the first radix launch)
+  kSelWords = kSelT + 1
 };
 
 // Candidate ids of Eq. 14: held out (weight h > 0) with a finite score.
@@ -352,15 +353,19 @@ struct RouteSelArgs {
 
 // The state after k radix passes (k >= 1) in st[0] (bits chosen) and st[1]
 // (rank left), from the state after k - 1 (state 0: nothing chosen, rank T)
-// and pass k - 1's histogram; workgroup 0 records it for the next launch.
-// Also st[2]: whether a radix select runs at all (0 < T <= F), st[3]: T,
-// st[4]: F.  Every workgroup computes the same values.
+// and pass k - 1's histogram hb: byte b is the first bin whose running total
+// reaches the rank (bin 255 at the latest), the rank less the bins before
+// it.  Workgroup 0 records the state for the next launch.  Also st[2]:
+// whether a radix select runs at all (0 < T <= F), st[3]: T, st[4]: F.
+// Every workgroup computes the same values.
 __device__ __forceinline__ void route_state(const RouteSelArgs &a, int k, unsigned long long *hb,
                                             unsigned long long *st) {
-  const int tid = threadIdx.x;
+  __shared__ unsigned long long wt[4];
+  const int tid = threadIdx.x, lane = tid & 63;
   if (tid < 256) hb[tid] = a.sel[kSelHist + 256 * (k - 1) + tid];
   if (tid == 0) {
-    const unsigned long long F = a.sel[kSelF], T = route_target(F, a.nh, a.r_tar);
+    const unsigned long long F = a.sel[kSelF], T = k == 1 ? route_target(F, a.nh, a.r_tar) : a.sel[kSelT];
+    if (k == 1 && blockIdx.x == 0) a.sel[kSelT] = T;
     st[2] = (T > 0ull && T <= F) ? 1ull : 0ull;
     st[3] = T;
     st[4] = F;
@@ -368,15 +373,33 @@ __device__ __forceinline__ void route_state(const RouteSelArgs &a, int k, unsign
     st[1] = k == 1 ? T : a.sel[kSelState + 2 * (k - 1) + 1];
   }
   __syncthreads();
-  if (tid == 0 && st[2]) {
-    unsigned long long rank = st[1];
-    int b = 0;
-    for (; b < 255 && hb[b] < rank; ++b) rank -= hb[b];
-    st[0] |= (unsigned long long)b << (56 - 8 * (k - 1));
-    st[1] = rank;
-    if (blockIdx.x == 0) {
-      a.sel[kSelState + 2 * k] = st[0];
-      a.sel[kSelState + 2 * k + 1] = rank;
+  // every thread takes the state before the one thread that picks the bin
+  // rewrites it (after the next barrier)
+  const unsigned long long pfx = st[0], rank = st[1];
+  const bool on = st[2] != 0ull;
+  // running totals of the 256 bins: within each wavefront, then the
+  // wavefronts before
+  unsigned long long cum = 0ull;
+  if (tid < 256) {
+    cum = hb[tid];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const unsigned long long t = __shfl_up(cum, o, 64);
+      if (lane >= o) cum += t;
+    }
+    if (lane == 63) wt[tid >> 6] = cum;
+  }
+  __syncthreads();
+  if (tid < 256 && on) {
+    for (int q = 0; q < (tid >> 6); ++q) cum += wt[q];
+    const unsigned long long excl = cum - hb[tid];
+    if (excl < rank && (cum >= rank || tid == 255)) {  // exactly one bin
+      st[0] = pfx | ((unsigned long long)tid << (56 - 8 * (k - 1)));
+      st[1] = rank - excl;
+      if (blockIdx.x == 0) {
+        a.sel[kSelState + 2 * k] = pfx | ((unsigned long long)tid << (56 - 8 * (k - 1)));
+        a.sel[kSelState + 2 * k + 1] = rank - excl;
+      }
     }
   }
   __syncthreads();
@@ -387,15 +410,14 @@ __device__ __forceinline__ void route_state(const RouteSelArgs &a, int k, unsign
 __global__ __launch_bounds__(1024) void route_select_pass_kernel(RouteSelArgs a, int k) {
   __shared__ unsigned long long lh[256], hb[256], st[5];
   const int tid = threadIdx.x;
+  const int x = blockIdx.x * 1024 + tid;
+  // this thread's id first: its loads overlap those of the state
+  const unsigned w = x < a.vocab ? a.h[x] : 0u;
+  const double s = x < a.vocab ? a.score[x] : 0.0;
   if (tid < 256) lh[tid] = 0ull;
   route_state(a, k, hb, st);
   if (!st[2]) return;  // no radix select (uniform)
-  const int x = blockIdx.x * 1024 + tid;
-  if (x < a.vocab) {
-    const unsigned w = a.h[x];
-    const double s = a.score[x];
-    if (route_candidate(w, s)) route_hist_add(lh, __builtin_bit_cast(unsigned long long, s), w, k, st[0]);
-  }
+  if (route_candidate(w, s)) route_hist_add(lh, __builtin_bit_cast(unsigned long long, s), w, k, st[0]);
   __syncthreads();
   if (tid < 256 && lh[tid]) atomicAdd(a.sel + kSelHist + 256 * k + tid, lh[tid]);
 }
@@ -409,14 +431,14 @@ __global__ __launch_bounds__(1024) void route_select_final_kernel(RouteSelArgs a
   __shared__ unsigned long long lw[3], hb[256], st[5];
   __shared__ int last;
   const int tid = threadIdx.x;
+  const int x = blockIdx.x * 1024 + tid;
+  const unsigned w = x < a.vocab ? a.h[x] : 0u;
+  const double s = x < a.vocab ? a.score[x] : 0.0;
   if (tid < 3) lw[tid] = 0ull;
   route_state(a, 8, hb, st);
   const unsigned long long F = st[4], T = st[3], o = st[0];
   const int mode = T > F ? 0 : (T == 0ull ? 1 : 2);  // 0: +inf; 1: the smallest candidate; 2: around o
-  const int x = blockIdx.x * 1024 + tid;
-  if (mode && x < a.vocab) {
-    const unsigned w = a.h[x];
-    const double s = a.score[x];
+  if (mode) {
     if (route_candidate(w, s)) {
       const unsigned long long bits = __builtin_bit_cast(unsigned long long, s);
       if (mode == 1 || bits > o) atomicMax(&lw[0], ~bits);
