@@ -100,3 +100,26 @@ def test_route_table_full_vocabulary():
         assert r == route.routed_fraction(s_ref, held, tau)
         np.testing.assert_array_equal(table, route.route_table(s_ref, tau))
         say(f"  r_tar {r_tar}: tau {tau:.6g}, R {r:.4f}, sparse ids {int((table == 0).sum())}")
+
+
+@pytest.mark.parametrize("vocab", [1_500_000, 1 << 22, (1 << 22) + 4099])
+def test_route_table_wide_vocabularies(vocab):
+    """Id ranges of 2048 and 4096 ids (the widest the partitioned sums take),
+    and a vocabulary past 2^22 ids, whose chunk tables are added with global
+    atomics instead.  A third of the ids are drawn uniformly over the whole
+    vocabulary so that every range is hit; these calls also reuse the kept
+    device buffers at other sizes."""
+    n, nh = 20000, 3000
+    ids, lb, ls = synth.routing_corpus(8, n, vocab)
+    held = synth.routing_corpus(8, nh, vocab, split=1)[0]
+    ids, held = ids.copy(), held.copy()
+    ids[::3] = synth.uniform_ids(n, vocab, (8, synth.S_ROUTE, 7))[::3]
+    held[::3] = synth.uniform_ids(nh, vocab, (8, synth.S_ROUTE, 8))[::3]
+    say(f"route wide vocabulary {vocab}")
+    s_ref, _, _ = route.scores(ids, lb, ls, vocab)
+    for r_tar in (0.3, 0.6):
+        table, tau, r, s = run(ids, lb, ls, held, vocab, r_tar)
+        np.testing.assert_array_equal(s, s_ref)
+        t_ref, r_ref = route.select_tau(s_ref, held, r_tar)
+        assert (tau, r) == (t_ref, r_ref), (r_tar, tau, t_ref)
+        np.testing.assert_array_equal(table, route.route_table(s_ref, t_ref))
