@@ -125,11 +125,12 @@ struct DenseArgs {
                           // down: the same flags of its K rows, rows without one are not read
   float *part;            // down output partials, [KSPLIT][n_dense][N]
   int K, N, kchunk;       // reduction length, output columns, k per split (down)
+  int nt;                 // gate/up: output columns per workgroup (a multiple of 8, at most 64)
   float *cal_g;           // calibration (gate/up): g = SiLU(a) in float32, [rows][N] (P unused) ...
   uint16_t *cal_ph, *cal_pl;  // ... and p = g u as two bf16 terms, hi = rne(p), lo = rne(p - hi)
   // LoRA adapters of the sparse path (gate/up with LORA): lv [2][kDenseMaxTokens][rank]
   // = s (h A_gate), s (h A_up) per group row; B_gate [rank][N], B_up_T [N][rank] and
-  // A_down [N][rank] of the layer; zpart [N / 64][kDenseMaxTokens][rank]: per column
+  // A_down [N][rank] of the layer; zpart [tiles][kDenseMaxTokens][rank]: per column
   // tile, sum of p_j A_down[j] over its columns (zero for base-path rows)
   const float *lv;
   const uint16_t *Bg, *BuT, *Ad;
@@ -284,11 +285,14 @@ __device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const
     if (s_ < (S)) COMPUTE(CUR);                                                              \
   }
 
-// p = SiLU(h W_gate) * (h W_up) for 64 columns (blockIdx.x) and every row of
-// the group (MT 16-row tiles; rows past the group are read as zeros).
-// Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.  Groups of
-// one row tile use the eight-stage ring of 18 KB stages, larger ones six
-// stages of 24 KB.
+// p = SiLU(h W_gate) * (h W_up) for the nt columns [nt b, nt b + nt) of
+// workgroup b and every row of the group (MT 16-row tiles; rows past the group
+// are read as zeros).  The MFMA tiles always span 64 columns: rows of W_gate_T
+// and W_up_T past the workgroup's columns are read as zeros without a memory
+// access (nt = d_ff / 256 fills every compute unit at the Llama and Qwen3
+// shapes).  Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
+// Groups of one row tile use the eight-stage ring of 18 KB stages, larger ones
+// six stages of 24 KB.
 template <int MT, bool LORA = false>
 __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a) {
   constexpr int NB = MT == 1 ? 8 : 6, SB = MT == 1 ? 18 * 1024 : kDenseStageBytes;  // ring stages and their bytes
@@ -302,15 +306,17 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   const int nd = min(a.ctl[0], 16 * MT);
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int mat = w >> 2, g = lane >> 4, l16 = lane & 15, c = 16 * (w & 3) + l16;
-  const int n0 = blockIdx.x * kDenseNT;
+  const int n0 = blockIdx.x * a.nt;
   const int K = a.K, N = a.N;
+  const int ncol = min(a.nt, N - n0);  // this workgroup's columns (a multiple of 8)
   const int S = K / kDenseKC;
   const __amdgpu_buffer_rsrc_t rsg = dense_rsrc(a.Wg, (uint32_t)((size_t)K * N * 2));
   const __amdgpu_buffer_rsrc_t rsu = dense_rsrc(a.Wt, (uint32_t)((size_t)K * N * 2));
   const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
   // wavefront w loads rows 8 w .. 8 w + 7 of each tile (1 KB); lane: row dr, slot dp
   const int dr = 8 * w + (lane >> 3), dp = lane & 7;
-  const uint32_t ou = (uint32_t)(((size_t)(n0 + dr) * K + 8 * row_pos(dr, dp)) * 2);  // W_gate_T and W_up_T
+  const bool wv_ = dr < ncol;  // a weight row of this workgroup (else zeros, no memory access)
+  const uint32_t ou = (uint32_t)(((size_t)(n0 + min(dr, ncol - 1)) * K + 8 * row_pos(dr, dp)) * 2);
   const uint32_t oh = (uint32_t)(((size_t)dr * K + 8 * row_pos(dr, dp)) * 2);
   const bool hv = dr < nd;
   const uint32_t sk = kDenseKC * 2;  // per stage
@@ -321,8 +327,8 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   {                                                                                          \
     const bool v_ = (SN) < S;                                                                \
     const uint32_t ss_ = (uint32_t)(SN);                                                     \
-    dma16<2>(rsg, (BUF) + w * 1024, dense_off(v_, ou + ss_ * sk, 0));                        \
-    dma16<2>(rsu, (BUF) + 8192 + w * 1024, dense_off(v_, ou + ss_ * sk, 1));                 \
+    dma16<2>(rsg, (BUF) + w * 1024, dense_off(v_ && wv_, ou + ss_ * sk, 0));                 \
+    dma16<2>(rsu, (BUF) + 8192 + w * 1024, dense_off(v_ && wv_, ou + ss_ * sk, 1));          \
     if (MT > 1 || w < 2) dma16<0>(rsh, (BUF) + 16384 + w * 1024, dense_off(v_ && hv, oh + ss_ * sk, 2)); \
   }
 #define SATS_GU_COMPUTE(BUF)                                                                 \
@@ -340,10 +346,12 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   u32x4 pbg = {0u, 0u, 0u, 0u}, pbu = {0u, 0u, 0u, 0u}, pad = {0u, 0u, 0u, 0u}, plv[4];
   if (LORA) {
     const int t = threadIdx.x;
-    if (t < 8 * R) {
-      pbg = *reinterpret_cast<const u32x4 *>(a.Bg + (size_t)(t >> 3) * N + n0 + 8 * (t & 7));
-      pbu = *reinterpret_cast<const u32x4 *>(a.BuT + (size_t)n0 * R + 8 * t);  // rows n0 .. n0 + 63: contiguous
-      pad = *reinterpret_cast<const u32x4 *>(a.Ad + (size_t)n0 * R + 8 * t);
+    if (t < 8 * R) {  // columns of the tile only (zeros past them)
+      if (8 * (t & 7) < ncol) pbg = *reinterpret_cast<const u32x4 *>(a.Bg + (size_t)(t >> 3) * N + n0 + 8 * (t & 7));
+      if (8 * t < ncol * R) {  // rows n0 .. n0 + ncol - 1: contiguous
+        pbu = *reinterpret_cast<const u32x4 *>(a.BuT + (size_t)n0 * R + 8 * t);
+        pad = *reinterpret_cast<const u32x4 *>(a.Ad + (size_t)n0 * R + 8 * t);
+      }
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -436,7 +444,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = 16 * mt + 4 * g + r;
-          if (m < nd) {
+          if (m < nd && c < ncol) {
             const float gv = xs[m * kDenseXP + c];
             const float pv = gv * acc[mt][r];
             const uint16_t hi = f32_to_bf16(pv);
@@ -462,18 +470,18 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
           const bool keep = a.gbase[m] || fabsf(gv) >= thr;  // Eq. 4-5; every column on the base path
           pt[m * 64 + c] = keep ? f32_to_bf16(gv * acc[mt][r]) : (uint16_t)0;
           any = any || keep;
-          if (a.keep_out) a.keep_out[(size_t)a.perm[m] * N + n0 + c] = (uint8_t)keep;
+          if (a.keep_out && c < ncol) a.keep_out[(size_t)a.perm[m] * N + n0 + c] = (uint8_t)keep;
         }
       }
     // the four lanes of column c (g = 0..3) hold its rows; lane g = 0 publishes the union flag
     int u = any ? 1 : 0;
     u |= __shfl_xor(u, 16, 64);
     u |= __shfl_xor(u, 32, 64);
-    if (a.uflag && g == 0) a.uflag[n0 + c] = (uint8_t)u;
+    if (a.uflag && g == 0 && c < ncol) a.uflag[n0 + c] = (uint8_t)u;
   }
   __syncthreads();
   const int lr = threadIdx.x >> 3, lq = threadIdx.x & 7;
-  if (lr < nd)
+  if (lr < nd && 8 * lq < ncol)
     *reinterpret_cast<u32x4 *>(a.P + (size_t)lr * N + n0 + 8 * lq) = *reinterpret_cast<const u32x4 *>(pt + lr * 64 + 8 * lq);
   if (LORA) {  // z partial of this column tile: p (as rounded for the down product) x A_down[tile], on MFMA
     const int nct = (R + 15) / 16;

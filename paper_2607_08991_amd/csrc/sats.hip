@@ -220,7 +220,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   if (lora_rank > 0) {  // batched LoRA calls only
     t.blv = c.take<float>(2 * (int64_t)sats::kDenseMaxTokens * lora_rank);
     t.blvpart = c.take<float>(2 * 4 * (int64_t)sats::kLoraVChunks * 16 * lora_rank);
-    t.blzpart = c.take<float>((d_ff / sats::kDenseNT) * (int64_t)sats::kDenseMaxTokens * lora_rank);
+    t.blzpart = c.take<float>((d_ff / 32) * (int64_t)sats::kDenseMaxTokens * lora_rank);  // tiles of >= 32 columns
   }
   if (b) *b = t;
   return c.off;
@@ -241,6 +241,18 @@ size_t counter_count(const Plan &p, int64_t pass, const DecodePlan &dp) {
 }
 
 // ------------------------------------------------------- single-token plan
+
+int device_cus();
+
+// Columns per gate/up workgroup: 64, or d_ff spread evenly over the compute
+// units (a multiple of 8, at least 32) when tiles of 64 would leave some of
+// them idle (Llama shape: 256 tiles of 56; Qwen3: 256 of 48).
+int dense_tile_cols(int64_t d_ff) {
+  const int cus = std::max(1, device_cus());
+  if (d_ff / sats::kDenseNT >= cus) return sats::kDenseNT;
+  const int64_t nt = ((d_ff + cus - 1) / cus + 7) / 8 * 8;
+  return (int)std::clamp<int64_t>(nt, 32, sats::kDenseNT);
+}
 
 int device_cus() {
   int dev = 0, cus = 0;
@@ -442,6 +454,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
     HIP_TRY(hipGetLastError());
   }
 
+  const int nt_gu = mfma ? dense_tile_cols(d_ff) : sats::kDenseNT;  // gate/up columns per workgroup
   for (int64_t l = 0; l < c.L; ++l) {
     if (mfma) {
       // base-path group on MFMA (kernels return at once when the group is small)
@@ -458,6 +471,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       da.P = b.pdense;
       da.K = (int)d;
       da.N = (int)d_ff;
+      da.nt = nt_gu;
       const size_t al = (size_t)d * c.rank;   // elements of A_gate, A_up (per layer)
       const size_t bl = (size_t)d_ff * c.rank;  // elements of B_gate, B_up_T, A_down (per layer)
       if (lora) {
@@ -488,8 +502,8 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       }
       {
         TimedLaunch tl(SATS_K_DENSE, c.stream);
-        hipExtLaunchKernelGGL(dense_gateup_fn(np, lora), dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, c.stream,
-                              tl.start, tl.stop, 0, da);
+        hipExtLaunchKernelGGL(dense_gateup_fn(np, lora), dim3((unsigned)((d_ff + da.nt - 1) / da.nt)),
+                              dim3(kDenseThreads), 0, c.stream, tl.start, tl.stop, 0, da);
       }
       HIP_TRY(hipGetLastError());
       DenseArgs dd{};
@@ -523,7 +537,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
         ga.Bd = static_cast<const uint16_t *>(c.Bd) + l * (size_t)c.rank * d;
         ga.gbase = b.gbase;
         ga.rank = (int)c.rank;
-        ga.nzb = (int)(d_ff / kDenseNT);
+        ga.nzb = (int)((d_ff + nt_gu - 1) / nt_gu);
         ga.lscale = c.lscale;
       }
       hipLaunchKernelGGL(dense_glue_kernel, dim3(np), dim3(kGlueThreads), 0, c.stream, ga);
@@ -946,13 +960,14 @@ int cal_gate_up(const uint16_t *h, const uint16_t *Wg, const uint16_t *Wu, int64
     da.Wt = Wu;
     da.K = (int)d;
     da.N = (int)d_ff;
+    da.nt = dense_tile_cols(d_ff);
     const size_t o = (size_t)i * kDenseMaxTokens * d_ff;
     da.cal_g = cb.G + o;
     da.cal_ph = cb.ph + o;
     da.cal_pl = cb.pl + o;
     TimedLaunch tl(SATS_K_CAL_GATEUP, s);
-    hipExtLaunchKernelGGL(dense_gateup_kernel<4>, dim3(d_ff / kDenseNT), dim3(kDenseThreads), 0, s, tl.start,
-                          tl.stop, 0, da);
+    hipExtLaunchKernelGGL(dense_gateup_kernel<4>, dim3((unsigned)((d_ff + da.nt - 1) / da.nt)), dim3(kDenseThreads),
+                          0, s, tl.start, tl.stop, 0, da);
     HIP_TRY(hipGetLastError());
   }
   return SATS_OK;
