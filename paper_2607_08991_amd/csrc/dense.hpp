@@ -219,12 +219,15 @@ __device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const
 // The stage loop shared by both products: stage s lives in ring buffer
 // s % 6; `issue(buf, s)` starts three buffer loads per lane for stage s
 // (loads past the k range read zeros) and `compute(buf)` consumes a stage.
-#define SATS_DENSE_RING(S, ISSUE, COMPUTE)                                                   \
+// SATS_DENSE_RING_H runs HOOK after the first two stages are issued.
+#define SATS_DENSE_RING(S, ISSUE, COMPUTE) SATS_DENSE_RING_H(S, ISSUE, COMPUTE, (void)0)
+#define SATS_DENSE_RING_H(S, ISSUE, COMPUTE, HOOK)                                           \
   {                                                                                          \
     uint8_t *const rb_[6] = {rg0, rg1, rg2, rg3, rg4, rg5};                                  \
     (void)rb_;                                                                               \
     ISSUE(rg0, 0);                                                                           \
     ISSUE(rg1, 1);                                                                           \
+    HOOK;                                                                                    \
     ISSUE(rg2, 2);                                                                           \
     ISSUE(rg3, 3);                                                                           \
     ISSUE(rg4, 4);                                                                           \
@@ -516,7 +519,8 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
 // loads take the offset past the buffer, which writes zeros to LDS without a
 // memory access.  Each lane holds the union flags of its two rows in every
 // stage of the chunk as a bit mask (up to kDownFlagStages stages; longer
-// chunks read every row).  With a base-path row in the group every flag is
+// chunks read every row), formed while the first two stages, which read
+// every row, are in flight.  With a base-path row in the group every flag is
 // set and every row is read.
 constexpr int kDownFlagStages = 32;
 
@@ -524,7 +528,6 @@ template <int MT>
 __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
       rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
-  __shared__ __attribute__((aligned(16))) uint8_t sflag[kDownFlagStages * kDenseKC];
   if (!a.ctl[1]) return;
   const int nd = min(a.ctl[0], 16 * MT);
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -546,18 +549,39 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   const bool hv = hr < nd;
   const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;
   // bit 2 s (2 s + 1): row wr (wr + 4) of stage s is in the union of the keep
-  // sets (the chunk's flags go through LDS: one 4-byte load per thread)
+  // sets.  Lane t < S loads the flags of this wavefront's rows 8 w .. 8 w + 7
+  // in stage t (8 bytes); one ballot per row gathers that row's flags over
+  // the stages, and each lane interleaves the two rows it loads.  The flags'
+  // load goes out first and the first two stages read every row, so the mask
+  // is formed while they are in flight.
+  const bool use_fl = a.uflag && S <= kDownFlagStages;
+  const uint64_t f8 =
+      (use_fl && lane < S) ? *reinterpret_cast<const uint64_t *>(a.uflag + kb + kDenseKC * lane + 8 * w) : 0ull;
   uint64_t fl = ~0ull;
-  if (a.uflag && S <= kDownFlagStages) {
-    const int t = threadIdx.x;
-    if (4 * t < S * kDenseKC) *reinterpret_cast<uint32_t *>(sflag + 4 * t) = *reinterpret_cast<const uint32_t *>(a.uflag + kb + 4 * t);
-    __syncthreads();
-    fl = 0ull;
-    for (int s = 0; s < S; ++s) {
-      fl |= (uint64_t)(sflag[kDenseKC * s + wr] != 0) << (2 * s);
-      fl |= (uint64_t)(sflag[kDenseKC * s + wr + 4] != 0) << (2 * s + 1);
+  auto row_flags = [&]() -> uint64_t {
+    if (!use_fl) return ~0ull;
+    const int r0 = lane >> 4;  // wr = 8 w + r0
+    uint64_t b0 = 0ull, b4 = 0ull;
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const uint64_t x0 = __ballot(((f8 >> (8 * rr)) & 0xffull) != 0ull);
+      const uint64_t x4 = __ballot(((f8 >> (8 * (rr + 4))) & 0xffull) != 0ull);
+      if (rr == r0) {
+        b0 = x0;
+        b4 = x4;
+      }
     }
-  }
+    auto spread = [](uint64_t v) {  // bit i to bit 2 i (i < 32)
+      v &= 0xffffffffull;
+      v = (v | (v << 16)) & 0x0000ffff0000ffffull;
+      v = (v | (v << 8)) & 0x00ff00ff00ff00ffull;
+      v = (v | (v << 4)) & 0x0f0f0f0f0f0f0f0full;
+      v = (v | (v << 2)) & 0x3333333333333333ull;
+      v = (v | (v << 1)) & 0x5555555555555555ull;
+      return v;
+    };
+    return spread(b0) | (spread(b4) << 1);
+  };
   f32x4v acc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4v{0.f, 0.f, 0.f, 0.f};
@@ -579,7 +603,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
         acc[mt] = mfma16(row_operand((BUF) + 16384, 16 * mt + l16, j, g), b_, acc[mt]);      \
     }                                                                                        \
   }
-  SATS_DENSE_RING(S, SATS_DN_ISSUE, SATS_DN_COMPUTE)
+  SATS_DENSE_RING_H(S, SATS_DN_ISSUE, SATS_DN_COMPUTE, fl = row_flags())
 #undef SATS_DN_ISSUE
 #undef SATS_DN_COMPUTE
   // through LDS to 16-byte row stores: rows 0-31 in one stage buffer, 32-63 in the next
@@ -794,6 +818,7 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
 }
 
 #undef SATS_DENSE_RING
+#undef SATS_DENSE_RING_H
 #undef SATS_DENSE_STEP
 
 struct GlueArgs {

@@ -76,6 +76,9 @@ constexpr int kMaxPass = 64;  // tokens per pass through the layers
 // d_ff chunks of the dense group's down-projection: about 256 workgroups,
 // each chunk a whole number of 64-row stages
 int dense_ksplit(int64_t d, int64_t d_ff) {
+#ifdef SATS_KS
+  return SATS_KS;
+#endif
   const int64_t tiles = d / sats::kDenseDownNT;
   int64_t ks = std::max<int64_t>(1, (256 + tiles - 1) / tiles);
   ks = std::min<int64_t>(ks, std::min<int64_t>(sats::kDenseMaxKsplit, std::max<int64_t>(1, d_ff / sats::kDenseKC)));
