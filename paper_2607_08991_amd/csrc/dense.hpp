@@ -126,6 +126,7 @@ struct DenseArgs {
   float *part;            // down output partials, [KSPLIT][n_dense][N]
   int K, N, kchunk;       // reduction length, output columns, k per split (down)
   int nt;                 // gate/up: output columns per workgroup (a multiple of 8, at most 64)
+  int hcap;               // rows of H allocated (the first stages read them all, before the group's size is known)
   float *cal_g;           // calibration (gate/up): g = SiLU(a) in float32, [rows][N] (P unused) ...
   uint16_t *cal_ph, *cal_pl;  // ... and p = g u as two bf16 terms, hi = rne(p), lo = rne(p - hi)
   // LoRA adapters of the sparse path (gate/up with LORA): lv [2][kDenseMaxTokens][rank]
@@ -256,10 +257,12 @@ __device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const
 // W_up_T 8 KB each, H 2 KB), seven in flight.  Wavefronts 0-1 also load the
 // 16 H rows (three loads per stage, the others two), so their wait allows
 // 18 outstanding loads and the others' 12.
-#define SATS_DENSE_RING8(S, ISSUE, COMPUTE)                                                  \
+#define SATS_DENSE_RING8(S, ISSUE, COMPUTE) SATS_DENSE_RING8_H(S, ISSUE, COMPUTE, (void)0)
+#define SATS_DENSE_RING8_H(S, ISSUE, COMPUTE, HOOK)                                          \
   {                                                                                          \
     ISSUE(rg0, 0);                                                                           \
     ISSUE(rg1, 1);                                                                           \
+    HOOK;                                                                                    \
     ISSUE(rg2, 2);                                                                           \
     ISSUE(rg3, 3);                                                                           \
     ISSUE(rg4, 4);                                                                           \
@@ -305,8 +308,12 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   uint8_t *const rg6 = ring + (NB > 6 ? 6 : 0) * SB, *const rg7 = ring + (NB > 7 ? 7 : 0) * SB;
   (void)rg6;
   (void)rg7;
-  if (!a.ctl[1]) return;
-  const int nd = min(a.ctl[0], 16 * MT);
+  // the group's control words are read while the first two stages load
+  // (every allocated row of H: rows past the group feed only results that
+  // are not stored); a workgroup of an empty group then waits for its loads
+  // and returns
+  const int ctl_on = a.ctl[1], ctl_n = a.ctl[0];
+  int nd = 16 * MT;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int mat = w >> 2, g = lane >> 4, l16 = lane & 15, c = 16 * (w & 3) + l16;
   const int n0 = blockIdx.x * a.nt;
@@ -315,13 +322,13 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   const int S = K / kDenseKC;
   const __amdgpu_buffer_rsrc_t rsg = dense_rsrc(a.Wg, (uint32_t)((size_t)K * N * 2));
   const __amdgpu_buffer_rsrc_t rsu = dense_rsrc(a.Wt, (uint32_t)((size_t)K * N * 2));
-  const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
+  const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)min(a.hcap, 16 * MT) * K * 2));
   // wavefront w loads rows 8 w .. 8 w + 7 of each tile (1 KB); lane: row dr, slot dp
   const int dr = 8 * w + (lane >> 3), dp = lane & 7;
   const bool wv_ = dr < ncol;  // a weight row of this workgroup (else zeros, no memory access)
   const uint32_t ou = (uint32_t)(((size_t)(n0 + min(dr, ncol - 1)) * K + 8 * row_pos(dr, dp)) * 2);
   const uint32_t oh = (uint32_t)(((size_t)dr * K + 8 * row_pos(dr, dp)) * 2);
-  const bool hv = dr < nd;
+  bool hv = true;  // rows of the group (all rows until the group's size is known)
   const uint32_t sk = kDenseKC * 2;  // per stage
   f32x4v acc[MT];
 #pragma unroll
@@ -362,11 +369,19 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
       plv[j] = (e < 32 * R) ? *reinterpret_cast<const u32x4 *>(a.lv + 4 * e) : u32x4{0u, 0u, 0u, 0u};
     }
   }
+#define SATS_GU_GROUP                                                                        \
+  if (!ctl_on) {                                                                             \
+    __builtin_amdgcn_s_waitcnt(0);                                                           \
+    return;                                                                                  \
+  }                                                                                          \
+  nd = min(ctl_n, 16 * MT);                                                                  \
+  hv = dr < nd
   if constexpr (MT == 1) {
-    SATS_DENSE_RING8(S, SATS_GU_ISSUE, SATS_GU_COMPUTE)
+    SATS_DENSE_RING8_H(S, SATS_GU_ISSUE, SATS_GU_COMPUTE, SATS_GU_GROUP)
   } else {
-    SATS_DENSE_RING(S, SATS_GU_ISSUE, SATS_GU_COMPUTE)
+    SATS_DENSE_RING_H(S, SATS_GU_ISSUE, SATS_GU_COMPUTE, SATS_GU_GROUP)
   }
+#undef SATS_GU_GROUP
 #undef SATS_GU_ISSUE
 #undef SATS_GU_COMPUTE
   // epilogue: SiLU(a) through LDS to the W_up wavefronts, p through LDS to
@@ -528,8 +543,10 @@ template <int MT>
 __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
       rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
-  if (!a.ctl[1]) return;
-  const int nd = min(a.ctl[0], 16 * MT);
+  // the group's control words are read while the first two stages load (as
+  // in the gate/up kernel)
+  const int ctl_on = a.ctl[1], ctl_n = a.ctl[0];
+  int nd = 16 * MT;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = lane >> 4, l16 = lane & 15, c = 16 * w + l16;
   const int ks = gridDim.x / (a.N / kDenseDownNT), kc = blockIdx.x % ks;
@@ -538,7 +555,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   const int kb = kc * a.kchunk, ke = min(K, kb + a.kchunk);
   const int S = ke > kb ? (ke - kb) / kDenseKC : 0;
   const __amdgpu_buffer_rsrc_t rsw = dense_rsrc(a.Wb, (uint32_t)((size_t)K * N * 2));
-  const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)nd * K * 2));
+  const __amdgpu_buffer_rsrc_t rsh = dense_rsrc(a.H, (uint32_t)((size_t)min(a.hcap, 16 * MT) * K * 2));
   // wavefront w loads W_down rows 8 w .. 8 w + 7 (two loads of 4 rows) and
   // p rows 8 w .. 8 w + 7
   const int wr = 8 * w + (lane >> 4), wp = lane & 15;
@@ -546,7 +563,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
   const uint32_t ow1 = (uint32_t)(((size_t)(kb + wr + 4) * N + n0 + 8 * krow_pos(wr + 4, wp)) * 2);
   const int hr = 8 * w + (lane >> 3), hp = lane & 7;
   const uint32_t oh = (uint32_t)(((size_t)hr * K + kb + 8 * row_pos(hr, hp)) * 2);
-  const bool hv = hr < nd;
+  bool hv = true;  // rows of the group (all rows until the group's size is known)
   const uint32_t sw = (uint32_t)kDenseKC * N * 2, sk = kDenseKC * 2;
   // bit 2 s (2 s + 1): row wr (wr + 4) of stage s is in the union of the keep
   // sets.  Lane t < S loads the flags of this wavefront's rows 8 w .. 8 w + 7
@@ -603,7 +620,16 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
         acc[mt] = mfma16(row_operand((BUF) + 16384, 16 * mt + l16, j, g), b_, acc[mt]);      \
     }                                                                                        \
   }
-  SATS_DENSE_RING_H(S, SATS_DN_ISSUE, SATS_DN_COMPUTE, fl = row_flags())
+#define SATS_DN_GROUP                                                                        \
+  if (!ctl_on) {                                                                             \
+    __builtin_amdgcn_s_waitcnt(0);                                                           \
+    return;                                                                                  \
+  }                                                                                          \
+  nd = min(ctl_n, 16 * MT);                                                                  \
+  hv = hr < nd;                                                                              \
+  fl = row_flags()
+  SATS_DENSE_RING_H(S, SATS_DN_ISSUE, SATS_DN_COMPUTE, SATS_DN_GROUP)
+#undef SATS_DN_GROUP
 #undef SATS_DN_ISSUE
 #undef SATS_DN_COMPUTE
   // through LDS to 16-byte row stores: rows 0-31 in one stage buffer, 32-63 in the next
@@ -819,6 +845,9 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
 
 #undef SATS_DENSE_RING
 #undef SATS_DENSE_RING_H
+#undef SATS_DENSE_RING8_H
+#undef SATS_DENSE_RING8
+#undef SATS_DENSE_STEP8
 #undef SATS_DENSE_STEP
 
 struct GlueArgs {

@@ -173,6 +173,7 @@ struct Buffers {
   int *perm, *ctl;        // batched path: token partition and dense-group control words
   uint8_t *skip, *gbase;
   uint16_t *xd, *hnext, *pdense;  // dense group (MFMA): inputs, next inputs, p
+  int prows;                       // ... rows of each of those three
   uint8_t *uflag;                  // dense group: union of the keep sets per column
   float *ddpart;                   // dense group down-projection partials
   float *blv, *blvpart, *blzpart;  // batched LoRA: s (h A) per group row, its chunk partials, z per column tile
@@ -213,6 +214,7 @@ size_t layout(char *base, const Plan &p, int64_t pass, int64_t d, int64_t d_ff, 
   t.ctl = c.take<int>(64);
   t.skip = c.take<uint8_t>(Pp);
   t.gbase = c.take<uint8_t>(Pp);
+  t.prows = (int)Pp;
   t.xd = c.take<uint16_t>(Pp * d);
   t.hnext = c.take<uint16_t>(Pp * d);
   t.pdense = c.take<uint16_t>(Pp * d_ff);
@@ -475,6 +477,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       da.K = (int)d;
       da.N = (int)d_ff;
       da.nt = nt_gu;
+      da.hcap = b.prows;
       const size_t al = (size_t)d * c.rank;   // elements of A_gate, A_up (per layer)
       const size_t bl = (size_t)d_ff * c.rank;  // elements of B_gate, B_up_T, A_down (per layer)
       if (lora) {
@@ -512,6 +515,7 @@ int run_pass(const Call &c, const Plan &p, const Buffers &b, unsigned *counters,
       DenseArgs dd{};
       dd.ctl = b.ctl;
       dd.H = b.pdense;
+      dd.hcap = b.prows;
       dd.Wb = static_cast<const uint16_t *>(c.Wd) + l * wl;
       dd.part = b.ddpart;
       dd.uflag = b.uflag;
@@ -964,6 +968,7 @@ int cal_gate_up(const uint16_t *h, const uint16_t *Wg, const uint16_t *Wu, int64
     da.K = (int)d;
     da.N = (int)d_ff;
     da.nt = dense_tile_cols(d_ff);
+    da.hcap = (int)(n - i * kDenseMaxTokens);  // calibration rows from this pass's first on
     const size_t o = (size_t)i * kDenseMaxTokens * d_ff;
     da.cal_g = cb.G + o;
     da.cal_ph = cb.ph + o;
