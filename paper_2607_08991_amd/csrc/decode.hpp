@@ -130,6 +130,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t weight_rsrc(const void *base, 
 // Byte offset that is out of range of every buffer here (all are smaller
 // than 2 GB): a buffer load at it returns zeros without a memory access.
 constexpr uint32_t kOffNone = 0x80000000u;
+// s_waitcnt operand for vmcnt(0) alone (expcnt and lgkmcnt at their maxima)
+constexpr int kWaitVm0 = 0x0F70;
 
 // 16 bytes at base + soff + voff, not kept in the caches (streamed once).
 __device__ __forceinline__ u32x4 load_rsrc(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
@@ -407,30 +409,32 @@ __device__ __forceinline__ void pack_input(DecodeSmem &sm) {
 // d (64 lanes x 16 bytes each) for both projections.
 
 // One batch: loads of this wavefront's chunks of the kept rows
-// list[r0 + r], r < R (rows at or past `end` are not read).
+// list[r0 + r], r < R.  Every load is issued: rows at or past `end` (and
+// chunks past d) read at kOffNone, zeros without a memory access, so no
+// branch or zero fill sits between the loads and nothing waits on them here.
 template <typename T, int R, int NCH, int HW>
 __device__ __forceinline__ void rows_issue(__amdgpu_buffer_rsrc_t Wu, __amdgpu_buffer_rsrc_t Wd, const DecodeSmem &sm,
                                            int r0, int end, int d, u32x4 (&bu)[R][NCH], u32x4 (&bd)[R][NCH]) {
   constexpr int VEC = Elem<T>::kVec, CH = 64 * VEC;
   const int lane = threadIdx.x & 63, hw = __builtin_amdgcn_readfirstlane((threadIdx.x >> 6) % HW);
-  uint32_t soff[R];
+  uint32_t soff[R];  // zero for rows past the end (kOffNone is then out of range whatever the row)
 #pragma unroll
   for (int r = 0; r < R; ++r)
-    soff[r] = (uint32_t)((size_t)__builtin_amdgcn_readfirstlane(sm.mj[max(0, min(r0 + r, end - 1))]) * d * sizeof(T));
+    soff[r] = r0 + r < end ? (uint32_t)((size_t)__builtin_amdgcn_readfirstlane(sm.mj[r0 + r]) * d * sizeof(T)) : 0u;
   // all rows of W_up_T first: the up products can start while W_down arrives
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int k = (hw + c * HW) * CH + lane * VEC;
-      bu[r][c] = (k < d && r0 + r < end) ? load_rsrc(Wu, (uint32_t)(k * sizeof(T)), soff[r]) : u32x4{0u, 0u, 0u, 0u};
+      bu[r][c] = load_rsrc(Wu, (k < d && r0 + r < end) ? (uint32_t)(k * sizeof(T)) : kOffNone, soff[r]);
     }
 #pragma unroll
   for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
       const int k = (hw + c * HW) * CH + lane * VEC;
-      bd[r][c] = (k < d && r0 + r < end) ? load_rsrc(Wd, (uint32_t)(k * sizeof(T)), soff[r]) : u32x4{0u, 0u, 0u, 0u};
+      bd[r][c] = load_rsrc(Wd, (k < d && r0 + r < end) ? (uint32_t)(k * sizeof(T)) : kOffNone, soff[r]);
     }
 }
 
@@ -474,6 +478,12 @@ __device__ __forceinline__ void rows_consume(DecodeSmem &sm, const float (&hreg)
 #pragma unroll
       for (int v = 0; v < VEC; ++v) yacc[c][v] = fmaf(pr, unpack<T>(bd[r][c], v), yacc[c][v]);
   }
+  // the sums are taken here, not sunk to the end of the caller's pass: the
+  // batch's registers are then free for the loads that refill them
+#pragma unroll
+  for (int c = 0; c < NCH; ++c)
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) asm volatile("" : "+v"(yacc[c][v]));
 }
 
 // LoRA: for the kept rows list[i0 .. i0 + mn), w_i = s (h A_up) .
@@ -592,11 +602,15 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   const int w = blockIdx.x;
   const int d = a.d, d_ff = a.d_ff;
   const size_t wl = (size_t)d * d_ff;
-  const int base = token_is_base(a.route_mode, a.ids, a.lut, 0);
-  if (l == 0 && w == 0 && tid == 0 && a.route_out) a.route_out[0] = (uint8_t)base;
+  // the route sets only the keep rule and, with adapters, whether their terms
+  // load.  Without adapters the table lookup (the id, then its entry) is two
+  // buffer loads that return zero when there is no table: no branch and no
+  // wait on them comes before the first weight loads, and the entry is read
+  // at the keep list
+  const bool lut = !LORA && a.route_mode == ROUTE_LUT;
+  const int base0 = LORA ? token_is_base(a.route_mode, a.ids, a.lut, 0) : a.route_mode == ROUTE_BASE;
   if (l == 0) SATS_TRACE_POINT(0);
-  const bool lora = LORA && !base;
-  const float thr = base ? 0.0f : a.thr[l];
+  const bool lora = LORA && !base0;
   const uint32_t wbytes = (uint32_t)(wl * sizeof(T));
   const __amdgpu_buffer_rsrc_t Wg = weight_rsrc(static_cast<const T *>(a.Wg) + (size_t)l * wl, wbytes);
   const __amdgpu_buffer_rsrc_t Wu = weight_rsrc(static_cast<const T *>(a.Wu) + (size_t)l * wl, wbytes);
@@ -613,6 +627,7 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   // pieces are in flight, not after them (loads complete in issue order)
   InputRegs<kDecodeThreads> ir;
   dec_input_issue<T, kDecodeThreads>(a, l, ir);
+  int rid = __builtin_amdgcn_raw_buffer_load_b32(weight_rsrc(a.ids, lut ? 4u : 0u), 0, 0, 0);
   // LoRA: B_gate at the block's columns (thread (c, i): ranks i, i + 16, ...)
   // and every chunk partial of h A_gate, h A_up (all loads issued at once,
   // ahead of the weights); used once h is formed
@@ -639,6 +654,14 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   gate_piece_issue<T>(Wg, gp, d, 1, qb);
   for (int k = d + tid; k < kDecodeMaxD; k += kDecodeThreads) sm.hs[k] = 0.0f;  // past d: no products
   dec_input_finish<T, kDecodeThreads>(a, l, ir, sm, a.layer_in != nullptr && w == 0);
+  // (rid passed through as a lane value: the entry then stays in a vector
+  // register until the keep list instead of being waited for here)
+  asm volatile("" : "+v"(rid));
+  const int lent = __builtin_amdgcn_raw_buffer_load_b8(weight_rsrc(a.lut, lut ? 0x7fffffffu : 0u), rid, 0, 0);
+  // the layer's threshold the same way, read at the keep list (zero on the base path)
+  const float thr = __builtin_bit_cast(
+      float, __builtin_amdgcn_raw_buffer_load_b32(weight_rsrc(a.thr, base0 ? 0u : (uint32_t)(l + 1) * 4u),
+                                                  (int)(l * 4), 0, 0));
   pack_input<T>(sm);
   __syncthreads();
   if (l == 0) SATS_TRACE_POINT(1);
@@ -660,15 +683,27 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
     }
     sm.lv[0][li][lc] = t;
   }
+  // the loop issues the next pieces on every pass (past the last piece they
+  // read zeros without a memory access) and the last pass is taken out of
+  // it: with no branch around a load, both buffers stay in flight, where a
+  // conditional issue makes the compiler assume the first buffer may be the
+  // newer one and wait for both
   float acc[2] = {0.0f, 0.0f};
-  for (int p = 0; p < gp.P; p += 2) {
+  int p = 0;
+  for (; p + 2 < gp.P; p += 2) {
     gate_piece_use<T>(sm, gp, p, qa, acc, sm.red);
-    if (p + 2 < gp.P) gate_piece_issue<T>(Wg, gp, d, p + 2, qa);
-    if (p + 1 < gp.P) {
-      gate_piece_use<T>(sm, gp, p + 1, qb, acc, sm.red);
-      if (p + 3 < gp.P) gate_piece_issue<T>(Wg, gp, d, p + 3, qb);
-    }
+    gate_piece_issue<T>(Wg, gp, d, p + 2, qa);
+    gate_piece_use<T>(sm, gp, p + 1, qb, acc, sm.red);
+    gate_piece_issue<T>(Wg, gp, d, p + 3, qb);
   }
+  if (p < gp.P) gate_piece_use<T>(sm, gp, p, qa, acc, sm.red);
+  if (p + 1 < gp.P) gate_piece_use<T>(sm, gp, p + 1, qb, acc, sm.red);
+  // every load of the wavefront has landed here (the last pieces were used and
+  // the route entry and threshold came before them); the explicit wait says
+  // so to the compiler, which otherwise keeps loads of the loop (and, on the
+  // wavefronts that skip the keep list, those two) pending and waits for the
+  // first row batches before the second is issued
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
   __syncthreads();
   if (l == 0) SATS_TRACE_POINT(2);
   // ---- keep list: one lane per column
@@ -681,6 +716,7 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
       av += a.lscale * t;
     }
     const float g = silu(av);
+    const int base = base0 | (lent != 0);
     const bool keep = on && (base || fabsf(g) >= thr);
     if (a.keep_out && on) a.keep_out[(size_t)l * d_ff + gp.c0 + lane] = (uint8_t)keep;
     const uint64_t bal = __ballot(keep);
@@ -693,6 +729,7 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   }
   __syncthreads();
   const int tot = sm.wcnt[0];
+  if (l == 0 && w == 0 && tid == 0 && a.route_out) a.route_out[0] = (uint8_t)(base0 | (lent != 0));
   if (l == 0) SATS_TRACE_POINT(4);
 
   // ---- rows: group gr takes list[b, e)
@@ -704,8 +741,8 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
   u32x4 au[RB][NCH], ad[RB][NCH], cu[RB][NCH], cd[RB][NCH];
   LoraPrepRegs<T> lp;
   if (lora) lora_prep_load<T>(a, l, sm, 0, tot, 0, lp);
-  if (nbt > 0) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b, e, d, au, ad);
-  if (nbt > 1) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + RB, e, d, cu, cd);
+  rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b, e, d, au, ad);
+  rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + RB, e, d, cu, cd);
 #pragma unroll
   for (int c = 0; c < NCH; ++c)
 #pragma unroll
@@ -720,16 +757,27 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
     __syncthreads();
   }
   int par = 0;  // LDS slot parity for the parts of u
-  for (int i = 0; i < nbt; i += 2) {
+  // batches issued on every pass and the last pass taken out, as the gate
+  // pieces (past the end they read zeros)
+  int i = 0;
+  for (; i + 2 < nbt; i += 2) {
     rows_consume<T, RB, NCH, HW>(sm, hreg, yacc, b + i * RB, e, par, au, ad, lora, lr, a.rank, zh);
     par ^= 1;
-    if (i + 2 < nbt) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
-    if (i + 1 < nbt) {
-      rows_consume<T, RB, NCH, HW>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
-      par ^= 1;
-      if (i + 3 < nbt) rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
-    }
+    // (a batch's loads are not moved above the last uses of the buffer they
+    // refill: they then take its registers, with no copy that would wait
+    // for them at the end of the pass)
+    __builtin_amdgcn_sched_barrier(0);
+    rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + (i + 2) * RB, e, d, au, ad);
+    rows_consume<T, RB, NCH, HW>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
+    par ^= 1;
+    __builtin_amdgcn_sched_barrier(0);
+    rows_issue<T, RB, NCH, HW>(Wu, Wd, sm, b + (i + 3) * RB, e, d, cu, cd);
   }
+  if (i < nbt) {
+    rows_consume<T, RB, NCH, HW>(sm, hreg, yacc, b + i * RB, e, par, au, ad, lora, lr, a.rank, zh);
+    par ^= 1;
+  }
+  if (i + 1 < nbt) rows_consume<T, RB, NCH, HW>(sm, hreg, yacc, b + (i + 1) * RB, e, par, cu, cd, lora, lr, a.rank, zh);
   __syncthreads();
   if (lora) {  // z = the groups' sums, added in group order
     if (hw == 0 && gr > 0 && lane < a.rank) sm.lv[1][gr][lane] = zh;
