@@ -336,7 +336,9 @@ bool make_decode_plan(int64_t d, int64_t d_ff, int esz, DecodePlan *dp, int lora
   q.G = (int)std::min<int64_t>(G, sats::kDecodeMaxG + 1);
   q.nvc = (int)((d + sats::kVRows - 1) / sats::kVRows);
   if (lora_rank > 0) {
-    const int64_t rw0 = (d + 63) / 64;
+    // second stage with adapters: slices of 32 columns (128 workgroups at
+    // d = 4096; 64-column slices measured 0.6 us slower, 16-column ones 0.2)
+    const int64_t rw0 = (d + 31) / 32;
     const int64_t cpw = (((d + rw0 - 1) / rw0 + sats::kRedCols - 1) / sats::kRedCols) * sats::kRedCols;
     q.RW = (int)((d + cpw - 1) / cpw);
   } else {
