@@ -1,4 +1,4 @@
-"""Seeded random parity cases of the single-token path (decode batch 1).
+"""Seeded random parity cases of the single-token path (decode batch 1) and of the batch paths.
 
 Each case draws a shape, a precision, a number of layers, a threshold level
 (CATS percentiles of Eq. 3, or t = 0), a route (with or without a routing
@@ -51,6 +51,42 @@ def test_single_token_random_case(i):
     print(f"case {i}: {p}", flush=True)
     with sats_options(**({"dec_block_cols": p["cols"]} if p["cols"] else {})):
         assert sats_query_path(1, d, dff, 2 if dtype == "bf16" else 4) == SATS_PATH_SINGLE_TOKEN
+        r1 = run_gpu(c, ts, lut, dtype)
+        r2 = run_gpu(c, ts, lut, dtype)
+    check_against_oracle(c, ts, lut, dtype, r1)
+    for key in ("out", "layer_in", "count", "idx", "route"):
+        np.testing.assert_array_equal(r1[key], r2[key])
+
+
+def draw_batch(i):
+    rng = np.random.default_rng(2000 + i)
+    dtype = "bf16" if rng.random() < 0.75 else "f32"
+    dff = int(rng.choice([64, 128, 192, 448, 512, 1024, 1536, 3072, 4096]))
+    return dict(dtype=dtype, d=int(rng.choice([128, 256, 384, 512, 1024, 2048, 4096])),
+                dff=dff - dff % 4 if dtype == "f32" else dff,
+                n=int(rng.choice([2, 3, 5, 8, 15, 16, 17, 31, 33, 48, 63, 64, 65, 100])),
+                L=int(rng.integers(1, 4)), k=float(rng.choice([0.0, 0.3, 0.5, 0.7, 0.9])),
+                seed=int(rng.integers(0, 10000)), n_dense_ids=int(rng.integers(0, 40)),
+                path=str(rng.choice(["auto", "split", "compact"])), lut=bool(rng.random() < 0.7))
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_batch_random_case(i):
+    """Seeded random batches of 2-100 tokens on the batch paths (the matrix-core kernels where the
+    shape is on their tiles, the base-group-only split and the compacted kernels), against the
+    oracle and repeated bit for bit."""
+    from paper_2607_08991_amd import SATS_BATCH_COMPACT, SATS_BATCH_SPLIT
+    p = draw_batch(i)
+    dtype, d, dff, n = p["dtype"], p["d"], p["dff"], p["n"]
+    c = synth.small_case(p["seed"], p["L"], d, dff, dtype, n, vocab=40, n_dense_ids=p["n_dense_ids"],
+                         w_std=1.0 / np.sqrt(d))
+    ts = case_thresholds(c, dtype, k=p["k"] if p["k"] > 0 else 0.5, seed=p["seed"])
+    if p["k"] == 0.0:
+        ts = np.zeros_like(ts)
+    lut = c["route_lut"] if p["lut"] else None
+    print(f"case {i}: {p}", flush=True)
+    opt = {} if p["path"] == "auto" else {"batch_path": SATS_BATCH_SPLIT if p["path"] == "split" else SATS_BATCH_COMPACT}
+    with sats_options(**opt):
         r1 = run_gpu(c, ts, lut, dtype)
         r2 = run_gpu(c, ts, lut, dtype)
     check_against_oracle(c, ts, lut, dtype, r1)
