@@ -225,8 +225,10 @@ int sats_device_status(hipStream_t stream);
 /*
  * SATS calibration (Section 3.1, Eq. 6-10): the offline step that produces
  * the per-layer thresholds the forward calls take.  Unlike the forward
- * calls, these take and return their small arrays in HOST memory, allocate
- * device buffers of their own, and synchronise `stream` before returning.
+ * calls, these take and return their small arrays in HOST memory, use
+ * device buffers of their own (kept per device from call to call and grown
+ * when a call needs more; calls are serialised; sats_release frees them),
+ * and synchronise `stream` before returning, also when they fail.
  *
  * sats_calibration_curves -- one layer.  h [n][d] holds the layer's inputs
  * for n calibration rows (device, bf16; the base-path inputs in a stack),
@@ -346,8 +348,9 @@ enum { SATS_PATH_SINGLE_TOKEN = 1, SATS_PATH_BATCH_MFMA = 2, SATS_PATH_BATCH_SPL
 int sats_query_path(int64_t n_tokens, int64_t d, int64_t d_ff, int elem_bytes, int aligned16, int n_cus,
                     int *path);
 
-/* Free every workspace of the calling process, and the routing-table
- * construction's kept buffers (synchronises each device). */
+/* Free every workspace of the calling process, and the kept buffers of the
+ * routing-table construction and of the calibration (synchronises each
+ * device). */
 int sats_release(void);
 
 /* Thread-local text of the last error returned on this thread ("" if none). */

@@ -915,17 +915,50 @@ struct CalBuffers {
   unsigned long long *hist16 = nullptr;
   double *errsum = nullptr;
   int *ctl = nullptr;              // [passes][2] rows of each gate/up pass, MFMA on
-  ~CalBuffers() {
-    for (void *q : {(void *)G, (void *)ph, (void *)pl, (void *)cnt, (void *)WdT, (void *)part, (void *)hpart, (void *)hist,
-                    (void *)prefix, (void *)rank, (void *)tk, (void *)thr15, (void *)hist16,
-                    (void *)errsum, (void *)ctl})
-      if (q) (void)hipFree(q);
-  }
 };
 
-template <typename P> int cal_alloc(P **p, size_t count) {
+// The calibration buffers are kept per device from call to call (grown when
+// a call needs more, freed by sats_release): a call allocates nothing once
+// they are large enough, where allocating and freeing ~250 MB per call cost
+// more than a millisecond.  Calls hold g_cal_mu throughout and synchronise
+// their stream before they return, so two calls never share them at once.
+struct CalCache {
+  CalBuffers b;
+  size_t cap[15] = {};  // elements of each buffer, in the order of cal_buffers
+};
+std::mutex g_cal_mu;
+std::map<int, CalCache> g_cal;
+
+template <typename P> int cal_alloc(P **p, size_t *cap, size_t count) {
+  if (*p && *cap >= count) return SATS_OK;
+  if (*p) HIP_TRY(hipFree(*p));
+  *p = nullptr;
+  *cap = 0;
   if (hipMalloc((void **)p, std::max<size_t>(count, 1) * sizeof(P)) != hipSuccess)
     return fail(SATS_ERR_WORKSPACE, "calibration buffer of %zu bytes failed", count * sizeof(P));
+  *cap = count;
+  return SATS_OK;
+}
+
+// A call's own temporary buffer (freed by the call).
+template <typename P> int cal_tmp_alloc(P **p, size_t count) {
+  if (hipMalloc((void **)p, std::max<size_t>(count, 1) * sizeof(P)) != hipSuccess)
+    return fail(SATS_ERR_WORKSPACE, "calibration buffer of %zu bytes failed", count * sizeof(P));
+  return SATS_OK;
+}
+
+int cal_release_all() {
+  std::lock_guard<std::mutex> lk(g_cal_mu);
+  for (auto &kv : g_cal) {
+    HIP_TRY(hipSetDevice(kv.first));
+    HIP_TRY(hipDeviceSynchronize());
+    const CalBuffers &b = kv.second.b;
+    for (void *q : {(void *)b.G, (void *)b.ph, (void *)b.pl, (void *)b.cnt, (void *)b.WdT, (void *)b.part,
+                    (void *)b.hpart, (void *)b.hist, (void *)b.prefix, (void *)b.rank, (void *)b.tk, (void *)b.thr15,
+                    (void *)b.hist16, (void *)b.errsum, (void *)b.ctl})
+      if (q) HIP_TRY(hipFree(q));
+  }
+  g_cal.clear();
   return SATS_OK;
 }
 
@@ -1069,19 +1102,27 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
   return SATS_OK;
 }
 
+// The buffers of a call with n rows of d x d_ff into cb, from the current
+// device's cache (the caller holds g_cal_mu).
 int cal_buffers(CalBuffers &cb, int64_t n, int64_t d, int64_t d_ff) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  CalCache &c = g_cal[dev];
+  CalBuffers &b = c.b;
+  size_t *k = c.cap;
   const size_t N = (size_t)n * d_ff;
   int rc = 0;
-  if ((rc = cal_alloc(&cb.G, N)) || (rc = cal_alloc(&cb.ph, N)) || (rc = cal_alloc(&cb.pl, N)) ||
-      (rc = cal_alloc(&cb.cnt, N)) || (rc = cal_alloc(&cb.WdT, (size_t)d * d_ff)) ||
-      (rc = cal_alloc(&cb.part, (size_t)(d / sats::kDenseDownNT) * n * 16)) ||
-      (rc = cal_alloc(&cb.hpart, (size_t)kCalHistParts * sats::kCalHistLds)) ||
-      (rc = cal_alloc(&cb.hist, sats::kCalHistLds)) || (rc = cal_alloc(&cb.prefix, sats::kCalMaxLevels)) ||
-      (rc = cal_alloc(&cb.rank, sats::kCalMaxLevels)) || (rc = cal_alloc(&cb.tk, sats::kCalMaxLevels)) ||
-      (rc = cal_alloc(&cb.thr15, sats::kCalCand)) || (rc = cal_alloc(&cb.hist16, 16)) ||
-      (rc = cal_alloc(&cb.errsum, sats::kCalCand)) ||
-      (rc = cal_alloc(&cb.ctl, 2 * ((n + sats::kDenseMaxTokens - 1) / sats::kDenseMaxTokens))))
+  if ((rc = cal_alloc(&b.G, &k[0], N)) || (rc = cal_alloc(&b.ph, &k[1], N)) || (rc = cal_alloc(&b.pl, &k[2], N)) ||
+      (rc = cal_alloc(&b.cnt, &k[3], N)) || (rc = cal_alloc(&b.WdT, &k[4], (size_t)d * d_ff)) ||
+      (rc = cal_alloc(&b.part, &k[5], (size_t)(d / sats::kDenseDownNT) * n * 16)) ||
+      (rc = cal_alloc(&b.hpart, &k[6], (size_t)kCalHistParts * sats::kCalHistLds)) ||
+      (rc = cal_alloc(&b.hist, &k[7], sats::kCalHistLds)) || (rc = cal_alloc(&b.prefix, &k[8], sats::kCalMaxLevels)) ||
+      (rc = cal_alloc(&b.rank, &k[9], sats::kCalMaxLevels)) || (rc = cal_alloc(&b.tk, &k[10], sats::kCalMaxLevels)) ||
+      (rc = cal_alloc(&b.thr15, &k[11], sats::kCalCand)) || (rc = cal_alloc(&b.hist16, &k[12], 16)) ||
+      (rc = cal_alloc(&b.errsum, &k[13], sats::kCalCand)) ||
+      (rc = cal_alloc(&b.ctl, &k[14], 2 * ((n + sats::kDenseMaxTokens - 1) / sats::kDenseMaxTokens))))
     return rc;
+  cb = b;
   return SATS_OK;
 }
 
@@ -1163,12 +1204,15 @@ int cal_stack(const uint16_t *x, int64_t n, const uint16_t *Wg, const uint16_t *
               float *thresholds, double *budget, double *realized, hipStream_t s) {
   int rc = cal_check_shape(n, d, d_ff);
   if (rc) return rc;
+  // held until the temporaries below are freed (hipFree synchronises the
+  // device), so the kept buffers are idle when the next call takes them
+  std::lock_guard<std::mutex> lk(g_cal_mu);
   if (L < 1 || !(coarse_step > 0.0 && coarse_step < 1.0) || !(fine_step > 0.0) || !(s_tar >= 0.0 && s_tar <= 1.0))
     return fail(SATS_ERR_ARG, "calibration needs L >= 1, 0 < coarse_step < 1, fine_step > 0, 0 <= s_tar <= 1");
   const size_t wl = (size_t)d * d_ff;
   // every layer's input on the base path (the stack's own forward, inputs exported)
   uint16_t *hin = nullptr, *out = nullptr;
-  if ((rc = cal_alloc(&hin, (size_t)L * n * d)) || (rc = cal_alloc(&out, (size_t)n * d))) {
+  if ((rc = cal_tmp_alloc(&hin, (size_t)L * n * d)) || (rc = cal_tmp_alloc(&out, (size_t)n * d))) {
     if (hin) (void)hipFree(hin);
     return rc;
   }
@@ -1557,6 +1601,7 @@ int sats_release(void) {
   g_ws.clear();
   HIP_TRY(hipSetDevice(cur));
   int rc = route_release_all();
+  if (!rc) rc = cal_release_all();
   HIP_TRY(hipSetDevice(cur));
   return rc;
 }
@@ -1574,11 +1619,13 @@ int sats_calibration_curves(const sats_bf16 *h, const sats_bf16 *W_gate, const s
       return fail(SATS_ERR_ARG, "levels must be ascending in [0, 1]");
   int rc = cal_check_shape(n, d, d_ff);
   if (rc) return rc;
+  std::lock_guard<std::mutex> lk(g_cal_mu);
   CalBuffers cb;
   if ((rc = cal_buffers(cb, n, d, d_ff))) return rc;
   rc = cal_layer(cb, h, W_gate, W_up_T, W_down, n, d, d_ff, levels, (int)n_levels, t_out, err_out, sp_out, err_rows,
                  stream);
-  if (!rc) HIP_TRY(hipStreamSynchronize(stream));
+  const hipError_t se = hipStreamSynchronize(stream);  // also on an error: the next call reuses the buffers
+  if (!rc && se != hipSuccess) return fail(SATS_ERR_HIP, "%s", hipGetErrorString(se));
   return rc;
 }
 
