@@ -51,6 +51,7 @@ constexpr int kDecodeMaxCols = 64;    // gate columns of a workgroup (one wavefr
 constexpr int kDecodeMaxG = 4096;     // layer workgroups (partials of y)
 constexpr int kRedThreads = 256, kRedCols = 16;  // second reduction stage: threads and columns per workgroup
 constexpr int kGateQ = 4;             // 16-byte loads per lane in one gate piece
+constexpr int kWarmRows = 8;          // next-layer W_gate rows an early workgroup warms (stacks)
 constexpr int kVRows = 256;           // input rows per workgroup of the LoRA input launch
 
 struct DecodeArgs {
@@ -820,6 +821,27 @@ __global__ __launch_bounds__(kDecodeThreads) void dec_layer_kernel(DecodeArgs a,
           store_coherent4(yr, (uint32_t)((k + v) * sizeof(float)), y[v], y[v + 1], y[v + 2], y[v + 3]);
       }
     }
+  }
+  // a workgroup that kept fewer than half its columns is done early: in a
+  // stack it warms the first rows of its next-layer W_gate block in the MALL
+  // (loads that allocate) while the heavier workgroups finish, so the next
+  // layer's gate starts on cache hits.  Nothing waits on these loads but the
+  // workgroup's own end.
+  if (!LORA && !a.fused_reduce && l + 1 < a.L && 2 * tot < gp.nc) {
+    constexpr int PFN = kWarmRows * kDecodeMaxD * (int)sizeof(T) / (kDecodeThreads * 16);
+    const uint32_t rowb = (uint32_t)(d * sizeof(T));
+    const __amdgpu_buffer_rsrc_t wn = weight_rsrc(static_cast<const T *>(a.Wg) + (size_t)(l + 1) * wl, wbytes);
+    u32x4 pf[PFN];
+#pragma unroll
+    for (int i = 0; i < PFN; ++i) {
+      const uint32_t byte = (uint32_t)(i * kDecodeThreads + tid) * 16u;
+      const int r = (int)(byte / rowb);  // row of the block
+      const bool on = r < kWarmRows && r < gp.nc;
+      pf[i] = __builtin_amdgcn_raw_buffer_load_b128(wn, on ? (int)((uint32_t)(gp.c0 + r) * rowb + byte % rowb)
+                                                           : (int)kOffNone, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < PFN; ++i) asm volatile("" ::"v"(pf[i]));
   }
   if (!LORA && a.fused_reduce && arrive_last(a.done, (unsigned)a.G, &sm.flag)) dec_reduce_all<T>(a, l, sm);
 }
