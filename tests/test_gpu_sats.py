@@ -155,3 +155,22 @@ def test_calibrate_stack_matches_oracle():
         k = int(np.argmin(np.abs(tsl - ts[l])))
         assert errl[k] <= b + slack, (l, errl[k], b)
         assert not np.any(errl[k + 1:] <= b - slack), (l, errl[k + 1:], b)
+
+
+def test_kept_buffers_across_shapes_and_release():
+    """The calibration keeps its device buffers from call to call (grown when a
+    call needs more, freed by sats_release): calls of different shapes in a row,
+    a smaller call after a larger one, and a call after sats_release give the
+    bits of the first call of their shape."""
+    import paper_2607_08991_amd as sats
+    small = _layer(64, 256, 1024, 24)
+    big = _layer(65, 512, 2048, 96)
+    first = _gpu_curves(*small, LEVELS)
+    fb = _gpu_curves(*big, LEVELS)
+    again = _gpu_curves(*small, LEVELS)        # reuses the grown buffers
+    sats.sats_release()
+    fresh = _gpu_curves(*small, LEVELS)        # buffers allocated anew
+    bb = _gpu_curves(*big, LEVELS)
+    for a, b in ((first, again), (first, fresh), (fb, bb)):
+        for u, v in zip(a, b):
+            np.testing.assert_array_equal(np.asarray(u), np.asarray(v))
