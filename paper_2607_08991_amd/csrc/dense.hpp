@@ -129,6 +129,12 @@ struct DenseArgs {
   int hcap;               // rows of H allocated (the first stages read them all, before the group's size is known)
   float *cal_g;           // calibration (gate/up): g = SiLU(a) in float32, [rows][N] (P unused) ...
   uint16_t *cal_ph, *cal_pl;  // ... and p = g u as two bf16 terms, hi = rne(p), lo = rne(p - hi)
+  // calibration in one launch (the CAL instance): workgroup b takes column tile
+  // (b / 8 / cal_passes) * 8 + b % 8 and pass (b / 8) % cal_passes (rows
+  // 64 pass ..; ctl, H, hcap and the cal outputs above are those of pass 0):
+  // the passes of a tile run at once on one XCD (workgroup b on XCD b mod 8)
+  // and read its weights through that XCD's L2; tiles past cal_tiles return
+  int cal_passes, cal_tiles;
   // LoRA adapters of the sparse path (gate/up with LORA): lv [2][kDenseMaxTokens][rank]
   // = s (h A_gate), s (h A_up) per group row; B_gate [rank][N], B_up_T [N][rank] and
   // A_down [N][rank] of the layer; zpart [tiles][kDenseMaxTokens][rank]: per column
@@ -299,7 +305,7 @@ __device__ __forceinline__ f32x4v mfma16(const bf16x8 &a, const bf16x8 &b, const
 // shapes).  Wavefronts 0-3 accumulate h W_gate, 4-7 h W_up, 16 columns each.
 // Groups of one row tile use the eight-stage ring of 18 KB stages, larger ones
 // six stages of 24 KB.
-template <int MT, bool LORA = false>
+template <int MT, bool LORA = false, bool CAL = false>
 __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a) {
   constexpr int NB = MT == 1 ? 8 : 6, SB = MT == 1 ? 18 * 1024 : kDenseStageBytes;  // ring stages and their bytes
   __shared__ __attribute__((aligned(1024))) uint8_t ring[NB * SB];
@@ -308,6 +314,19 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   uint8_t *const rg6 = ring + (NB > 6 ? 6 : 0) * SB, *const rg7 = ring + (NB > 7 ? 7 : 0) * SB;
   (void)rg6;
   (void)rg7;
+  int tile = blockIdx.x;
+  if (CAL) {  // calibration passes in one launch (see DenseArgs)
+    const int j = blockIdx.x >> 3, pass = j % a.cal_passes;
+    tile = (j / a.cal_passes) * 8 + (blockIdx.x & 7);
+    if (tile >= a.cal_tiles) return;
+    const size_t rows = (size_t)pass * kDenseMaxTokens;
+    a.ctl += 2 * pass;
+    a.H += rows * a.K;
+    a.hcap -= (int)rows;
+    a.cal_g += rows * a.N;
+    a.cal_ph += rows * a.N;
+    a.cal_pl += rows * a.N;
+  }
   // the group's control words are read while the first two stages load
   // (every allocated row of H: rows past the group feed only results that
   // are not stored); a workgroup of an empty group then waits for its loads
@@ -316,7 +335,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
   int nd = 16 * MT;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int mat = w >> 2, g = lane >> 4, l16 = lane & 15, c = 16 * (w & 3) + l16;
-  const int n0 = blockIdx.x * a.nt;
+  const int n0 = tile * a.nt;
   const int K = a.K, N = a.N;
   const int ncol = min(a.nt, N - n0);  // this workgroup's columns (a multiple of 8)
   const int S = K / kDenseKC;
@@ -516,7 +535,7 @@ __global__ __launch_bounds__(kDenseThreads) void dense_gateup_kernel(DenseArgs a
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = 16 * mt + 4 * g + r;
-        if (m < nd && i < R) a.zpart[((size_t)blockIdx.x * kDenseMaxTokens + m) * R + i] = a.gbase[m] ? 0.0f : z[r];
+        if (m < nd && i < R) a.zpart[((size_t)tile * kDenseMaxTokens + m) * R + i] = a.gbase[m] ? 0.0f : z[r];
       }
     }
   }

@@ -994,25 +994,27 @@ int cal_gate_up(const uint16_t *h, const uint16_t *Wg, const uint16_t *Wu, int64
     ctl[2 * i + 1] = 1;
   }
   HIP_TRY(hipMemcpyAsync(cb.ctl, ctl.data(), ctl.size() * sizeof(int), hipMemcpyHostToDevice, s));
-  for (int64_t i = 0; i < passes; ++i) {
-    DenseArgs da{};
-    da.ctl = cb.ctl + 2 * i;
-    da.H = h + i * kDenseMaxTokens * d;
-    da.Wg = Wg;
-    da.Wt = Wu;
-    da.K = (int)d;
-    da.N = (int)d_ff;
-    da.nt = dense_tile_cols(d_ff);
-    da.hcap = (int)(n - i * kDenseMaxTokens);  // calibration rows from this pass's first on
-    const size_t o = (size_t)i * kDenseMaxTokens * d_ff;
-    da.cal_g = cb.G + o;
-    da.cal_ph = cb.ph + o;
-    da.cal_pl = cb.pl + o;
-    TimedLaunch tl(SATS_K_CAL_GATEUP, s);
-    hipExtLaunchKernelGGL(dense_gateup_kernel<4>, dim3((unsigned)((d_ff + da.nt - 1) / da.nt)), dim3(kDenseThreads),
-                          0, s, tl.start, tl.stop, 0, da);
-    HIP_TRY(hipGetLastError());
-  }
+  // every pass in one launch, the passes of a column tile side by side on
+  // one XCD so that its weights come from HBM about once (see DenseArgs)
+  DenseArgs da{};
+  da.ctl = cb.ctl;
+  da.H = h;
+  da.Wg = Wg;
+  da.Wt = Wu;
+  da.K = (int)d;
+  da.N = (int)d_ff;
+  da.nt = dense_tile_cols(d_ff);
+  da.hcap = (int)n;  // calibration rows from pass 0's first on
+  da.cal_g = cb.G;
+  da.cal_ph = cb.ph;
+  da.cal_pl = cb.pl;
+  da.cal_passes = (int)passes;
+  da.cal_tiles = (int)((d_ff + da.nt - 1) / da.nt);
+  const int64_t grid = (int64_t)((da.cal_tiles + 7) / 8) * 8 * passes;
+  TimedLaunch tl(SATS_K_CAL_GATEUP, s);
+  hipExtLaunchKernelGGL(dense_gateup_kernel<4, false, true>, dim3((unsigned)grid), dim3(kDenseThreads), 0, s, tl.start,
+                        tl.stop, 0, da);
+  HIP_TRY(hipGetLastError());
   return SATS_OK;
 }
 
