@@ -9,12 +9,12 @@
 //       8 + 4 bits in four counting passes; every level is resolved at once.
 //   cal_bucket_kernel
 //       c = #{r : t_r <= |g|} per calibration value (the removed test of the
-//       error product), and the histogram of c, which gives the sparsity
-//       sp(t_r) = #{|g| < t_r} / (n d_ff) = #{c <= r} / (n d_ff).
+//       error product), and ge_r = #{|g| >= t_r}, which gives the sparsity
+//       sp(t_r) = #{|g| < t_r} / (n d_ff) = 1 - ge_r / (n d_ff).
 //   cal_transpose_kernel
 //       W_down^T for the error product (its B operands are k-contiguous).
-//   cal_reduce_kernel
-//       finishes Eq. 6 from the column-tile sums of squares: per row
+//   cal_reduce_kernel / cal_reduce_sum_kernel
+//       finish Eq. 6 from the column-tile sums of squares: per row
 //       e_r = ||y - y_t_r|| / (||y|| + eps), and Err(t_r) = mean of e_r.
 //
 // Counting uses integer atomics (exact in any order); every float sum has a
@@ -35,48 +35,124 @@ __device__ __forceinline__ uint32_t abs_bits(float v) { return __float_as_uint(v
 // Radix pass of the select: for each level k of [0, K), the histogram of
 // the `bits` bits at `shift` of the values whose higher bits (from shift +
 // bits up) equal the level's prefix so far (pass 0: every value, one
-// histogram).  Levels ascend, so their prefixes do too: the levels a value
-// counts for are the run of equal prefixes found by binary search.  Counted
-// in LDS per workgroup (K x 2^bits counters, at most kCalHistLds) and
-// written whole to part[workgroup] (no global atomics); cal_hist_reduce_kernel
-// adds the workgroups' histograms in workgroup order.
+// histogram).  Levels ascend, so their prefixes do too, and the levels of
+// one prefix are a run.  A value finds its run in a hash table in LDS
+// (slot = low kCalTabBits bits of the prefix, entry = prefix << 16 | run
+// length << 8 | first level; 0 = empty): one read rejects a value that
+// matches no level.  A slot that two prefixes share holds kCalTabMixed, and
+// its values find their run by binary search over the prefixes.  Counted in
+// LDS per workgroup (K x 2^bits counters, at most kCalHistLds) and written
+// whole to part[workgroup] (no global atomics); cal_hist_reduce_kernel adds
+// the workgroups' histograms.  A thread reads four values per 16-byte load
+// and has kCalLoads loads in flight; workgroup 0 takes the N % 4 tail.
 constexpr int kCalHistLds = 16384;
 constexpr int kCalHistThreads = 1024;
+constexpr int kCalLoads = 4;
+constexpr int kCalTabBits = 12;
+constexpr unsigned long long kCalTabMixed = 0xff00ull;  // run length 255: more than kCalMaxLevels
+__device__ __forceinline__ void hist_add(uint32_t b, unsigned long long e, const uint32_t *pf, int K, int hs,
+                                         int shift, int bins, uint32_t *h) {
+  const uint32_t key = (b >> shift) & (uint32_t)(bins - 1);
+  if (hs >= 32) {  // pass 0: one histogram
+    atomicAdd(&h[key], 1u);
+    return;
+  }
+  const uint32_t hi = b >> hs;
+  int k = 0, k1 = 0;
+  if (e == kCalTabMixed) {
+    int up = K;  // first level whose prefix is >= hi
+    while (k < up) {
+      const int mid = (k + up) >> 1;
+      if (pf[mid] < hi) k = mid + 1;
+      else up = mid;
+    }
+    for (k1 = k; k1 < K && pf[k1] == hi; ++k1) {
+    }
+  } else if (e != 0ull && (uint32_t)(e >> 16) == hi) {
+    k = (int)(e & 0xffu);
+    k1 = k + (int)((e >> 8) & 0xffu);
+  }
+  for (; k < k1; ++k) atomicAdd(&h[k * bins + key], 1u);
+}
+
 __global__ __launch_bounds__(kCalHistThreads) void cal_hist_kernel(const float *G, size_t N, const uint32_t *prefix,
                                                                    int K, int shift, int bits, uint32_t *part) {
   __shared__ uint32_t pf[kCalMaxLevels];
+  __shared__ uint32_t nslot[1 << kCalTabBits];
+  __shared__ unsigned long long tab[1 << kCalTabBits];
   __shared__ uint32_t h[kCalHistLds];
+  constexpr uint32_t kMask = (1u << kCalTabBits) - 1;
   const int bins = 1 << bits, nh = K * bins;
   const int hs = shift + bits;  // 32 on pass 0: no prefix
   for (int k = threadIdx.x; k < K; k += kCalHistThreads) pf[k] = hs >= 32 ? 0u : prefix[k];
   for (int i = threadIdx.x; i < nh; i += kCalHistThreads) h[i] = 0u;
+  for (int i = threadIdx.x; i < (1 << kCalTabBits); i += kCalHistThreads) {
+    tab[i] = 0ull;
+    nslot[i] = 0u;
+  }
   __syncthreads();
-  for (size_t i = blockIdx.x * (size_t)kCalHistThreads + threadIdx.x; i < N;
-       i += (size_t)gridDim.x * kCalHistThreads) {
-    const uint32_t b = abs_bits(G[i]);
-    const uint32_t hi = hs >= 32 ? 0u : b >> hs, key = (b >> shift) & (uint32_t)(bins - 1);
-    int lo = 0, up = K;  // first level whose prefix is >= hi
-    while (lo < up) {
-      const int mid = (lo + up) >> 1;
-      if (pf[mid] < hi) lo = mid + 1;
-      else up = mid;
+  // the level that starts a run enters it (K <= kCalMaxLevels <= the threads)
+  const int k = threadIdx.x;
+  const bool start = hs < 32 && k < K && (k == 0 || pf[k - 1] != pf[k]);
+  if (start) {
+    int n = 1;
+    while (k + n < K && pf[k + n] == pf[k]) ++n;
+    atomicAdd(&nslot[pf[k] & kMask], 1u);
+    tab[pf[k] & kMask] = (unsigned long long)pf[k] << 16 | (unsigned long long)n << 8 | (unsigned long long)k;
+  }
+  __syncthreads();
+  if (start && nslot[pf[k] & kMask] > 1u) tab[pf[k] & kMask] = kCalTabMixed;
+  __syncthreads();
+  const size_t N4 = N / 4, stride = (size_t)gridDim.x * kCalHistThreads;
+  const float4 *G4 = reinterpret_cast<const float4 *>(G);
+  for (size_t i = blockIdx.x * (size_t)kCalHistThreads + threadIdx.x; i < N4; i += kCalLoads * stride) {
+    float4 v[kCalLoads];
+#pragma unroll
+    for (int j = 0; j < kCalLoads; ++j) v[j] = G4[min(i + j * stride, N4 - 1)];  // clamped: loads stay unconditional
+    uint32_t b[4 * kCalLoads];
+    unsigned long long e[4 * kCalLoads];
+#pragma unroll
+    for (int j = 0; j < kCalLoads; ++j) {
+      b[4 * j] = abs_bits(v[j].x);
+      b[4 * j + 1] = abs_bits(v[j].y);
+      b[4 * j + 2] = abs_bits(v[j].z);
+      b[4 * j + 3] = abs_bits(v[j].w);
     }
-    for (int k = lo; k < K && pf[k] == hi; ++k) atomicAdd(&h[k * bins + key], 1u);
+#pragma unroll
+    for (int q = 0; q < 4 * kCalLoads; ++q) e[q] = hs >= 32 ? 0ull : tab[(b[q] >> hs) & kMask];
+#pragma unroll
+    for (int q = 0; q < 4 * kCalLoads; ++q)
+      if (i + (q / 4) * stride < N4) hist_add(b[q], e[q], pf, K, hs, shift, bins, h);
+  }
+  if (blockIdx.x == 0 && threadIdx.x < N - 4 * N4) {
+    const uint32_t b = abs_bits(G[4 * N4 + threadIdx.x]);
+    hist_add(b, hs >= 32 ? 0ull : tab[(b >> hs) & kMask], pf, K, hs, shift, bins, h);
   }
   __syncthreads();
   uint32_t *o = part + (size_t)blockIdx.x * nh;
   for (int i = threadIdx.x; i < nh; i += kCalHistThreads) o[i] = h[i];
 }
 
-// hist[i] = sum over the `parts` workgroup histograms of entry i, in order.
-__global__ __launch_bounds__(kCalThreads) void cal_hist_reduce_kernel(const uint32_t *part, int parts, int nh,
-                                                                      uint32_t *hist) {
-  const int i = blockIdx.x * kCalThreads + threadIdx.x;
-  if (i >= nh) return;
+// hist[i] = sum over the `parts` workgroup histograms of entry i: a
+// workgroup takes 64 entries, its 16 wavefronts one sixteenth of the parts
+// each (integer sums: exact in any order).
+constexpr int kCalHRBins = 64, kCalHRChunks = kCalHistThreads / kCalHRBins;
+__global__ __launch_bounds__(kCalHistThreads) void cal_hist_reduce_kernel(const uint32_t *part, int parts, int nh,
+                                                                          uint32_t *hist) {
+  __shared__ uint32_t acc[kCalHRChunks][kCalHRBins];
+  const int b = threadIdx.x % kCalHRBins, c = threadIdx.x / kCalHRBins, i = blockIdx.x * kCalHRBins + b;
   uint32_t s = 0u;
+  if (i < nh)
 #pragma unroll 8
-  for (int q = 0; q < parts; ++q) s += part[(size_t)q * nh + i];
-  hist[i] = s;
+    for (int q = c; q < parts; q += kCalHRChunks) s += part[(size_t)q * nh + i];
+  acc[c][b] = s;
+  __syncthreads();
+  if (c == 0 && i < nh) {
+    uint32_t t = 0u;
+#pragma unroll
+    for (int j = 0; j < kCalHRChunks; ++j) t += acc[j][b];
+    hist[i] = t;
+  }
 }
 
 // Level k (workgroup k): the bin holding its remaining rank (1-based) in its
@@ -150,68 +226,115 @@ __global__ __launch_bounds__(kCalThreads) void cal_transpose_kernel(const uint16
   }
 }
 
-// c = #{r < 15 : t_r <= |g|} as a byte, and the histogram of c over the
-// launch (16 counters).
+// c = #{r < 15 : t_r <= |g|} per value, as a byte (the error product
+// removes a neuron at candidate r when c <= r), and ge[r] = #{|g| >= t_r},
+// the values kept at t_r, over the launch (integer counts: exact in any
+// order; ge must be zero on entry).  A thread reads four values per 16-byte
+// load and has kCalLoads loads in flight; workgroup 0 takes the N % 4 tail.
 __global__ __launch_bounds__(kCalThreads) void cal_bucket_kernel(const float *G, size_t N, const float *thr15,
-                                                                 uint8_t *cnt, unsigned long long *hist16) {
-  __shared__ float t[kCalCand];
-  __shared__ unsigned int h[16];
-  if (threadIdx.x < kCalCand) t[threadIdx.x] = thr15[threadIdx.x];
-  if (threadIdx.x < 16) h[threadIdx.x] = 0u;
-  __syncthreads();
-  for (size_t i = blockIdx.x * (size_t)kCalThreads + threadIdx.x; i < N; i += (size_t)gridDim.x * kCalThreads) {
-    const float v = fabsf(G[i]);
-    int c = 0;
+                                                                 uint8_t *cnt, unsigned long long *ge) {
+  __shared__ unsigned int h[kCalCand];
+  if (threadIdx.x < kCalCand) h[threadIdx.x] = 0u;
+  float t[kCalCand];
+  uint32_t n_ge[kCalCand];
 #pragma unroll
-    for (int r = 0; r < kCalCand; ++r) c += (t[r] <= v) ? 1 : 0;
-    cnt[i] = (uint8_t)c;
-    atomicAdd(&h[c], 1u);
+  for (int r = 0; r < kCalCand; ++r) {
+    t[r] = thr15[r];
+    n_ge[r] = 0u;
   }
-  __syncthreads();
-  if (threadIdx.x < 16 && h[threadIdx.x]) atomicAdd(&hist16[threadIdx.x], (unsigned long long)h[threadIdx.x]);
-}
-
-// Eq. 6 from part[tile][m][16] (sums of squares over column tile `tile`):
-// one workgroup; thread i takes rows i, i + 1024, ... in order, and the
-// per-thread sums of e_r are added over threads by a fixed tree.  Row 15 of
-// every calibration row holds ||y||^2.
-constexpr int kCalReduceThreads = 1024;
-__global__ __launch_bounds__(kCalReduceThreads) void cal_reduce_kernel(const float *part, int ntiles, int n, int K,
-                                                                        float *err_rows, int rows_ld,
-                                                                        double *err_sum) {
-  __shared__ double red[kCalReduceThreads];
-  double s[kCalCand];
-#pragma unroll
-  for (int r = 0; r < kCalCand; ++r) s[r] = 0.0;
-  for (int m = threadIdx.x; m < n; m += kCalReduceThreads) {
-    float e2[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) e2[r] = 0.0f;
-    for (int tl = 0; tl < ntiles; ++tl) {
-      const float *p = part + ((size_t)tl * n + m) * 16;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) e2[r] += p[r];
-    }
-    const float ny = sqrtf(e2[15]);
+  auto bucket = [&](float g) -> uint32_t {
+    const float v = fabsf(g);
+    uint32_t c = 0u;
 #pragma unroll
     for (int r = 0; r < kCalCand; ++r) {
-      const float e = sqrtf(e2[r]) / (ny + kCalEps);
-      if (r < K) {
-        s[r] += (double)e;
-        if (err_rows) err_rows[(size_t)m * rows_ld + r] = e;
+      const uint32_t f = t[r] <= v ? 1u : 0u;
+      c += f;
+      n_ge[r] += f;
+    }
+    return c;
+  };
+  const size_t N4 = N / 4, stride = (size_t)gridDim.x * kCalThreads;
+  const float4 *G4 = reinterpret_cast<const float4 *>(G);
+  uint32_t *C4 = reinterpret_cast<uint32_t *>(cnt);
+  for (size_t i = blockIdx.x * (size_t)kCalThreads + threadIdx.x; i < N4; i += kCalLoads * stride) {
+    float4 v[kCalLoads];
+#pragma unroll
+    for (int j = 0; j < kCalLoads; ++j) v[j] = G4[min(i + j * stride, N4 - 1)];  // clamped: loads stay unconditional
+#pragma unroll
+    for (int j = 0; j < kCalLoads; ++j)
+      if (i + j * stride < N4)
+        C4[i + j * stride] = bucket(v[j].x) | bucket(v[j].y) << 8 | bucket(v[j].z) << 16 | bucket(v[j].w) << 24;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < N - 4 * N4) cnt[4 * N4 + threadIdx.x] = (uint8_t)bucket(G[4 * N4 + threadIdx.x]);
+#pragma unroll
+  for (int r = 0; r < kCalCand; ++r)
+    for (int o = 32; o > 0; o >>= 1) n_ge[r] += __shfl_xor(n_ge[r], o);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int r = 0; r < kCalCand; ++r)
+      if (n_ge[r]) atomicAdd(&h[r], n_ge[r]);
+  __syncthreads();
+  if (threadIdx.x < kCalCand && h[threadIdx.x]) atomicAdd(&ge[threadIdx.x], (unsigned long long)h[threadIdx.x]);
+}
+
+// Eq. 6 from part[tile][m][16] (sums of squares over column tile `tile`;
+// entry 15 of every calibration row holds ||y||^2): workgroup b takes rows
+// 64 b .. 64 b + 63 (a lane per row), its wavefront w the tiles w, w + 8,
+// ...; wavefront 0 adds the eight sums in order and forms per row
+// e_r = ||y - y_t_r|| / (||y|| + eps), and the sums of e_r over the rows
+// (a fixed tree over the lanes) go to rsum[b][r], which
+// cal_reduce_sum_kernel adds over workgroups in order.
+constexpr int kCalRedWaves = 8;
+__global__ __launch_bounds__(64 * kCalRedWaves) void cal_reduce_kernel(const float *part, int ntiles, int n, int K,
+                                                                       float *err_rows, int rows_ld, double *rsum) {
+  __shared__ float acc[kCalRedWaves][16][65];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, m = blockIdx.x * 64 + lane;
+  float e2[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) e2[r] = 0.0f;
+  if (m < n) {
+#pragma unroll 4
+    for (int tl = w; tl < ntiles; tl += kCalRedWaves) {
+      const float4 *p = reinterpret_cast<const float4 *>(part + ((size_t)tl * n + m) * 16);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 v = p[q];
+        e2[4 * q] += v.x;
+        e2[4 * q + 1] += v.y;
+        e2[4 * q + 2] += v.z;
+        e2[4 * q + 3] += v.w;
       }
     }
   }
-  for (int r = 0; r < K; ++r) {
-    red[threadIdx.x] = s[r];
-    __syncthreads();
-    for (int o = kCalReduceThreads / 2; o > 0; o >>= 1) {
-      if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-      __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[w][r][lane] = e2[r];
+  __syncthreads();
+  if (w != 0) return;
+#pragma unroll
+  for (int r = 0; r < 16; ++r)
+    for (int j = 1; j < kCalRedWaves; ++j) e2[r] += acc[j][r][lane];
+  const float ny = sqrtf(e2[15]);
+#pragma unroll
+  for (int r = 0; r < kCalCand; ++r) {
+    double s = 0.0;
+    if (m < n && r < K) {
+      const float e = sqrtf(e2[r]) / (ny + kCalEps);
+      if (err_rows) err_rows[(size_t)m * rows_ld + r] = e;
+      s = (double)e;
     }
-    if (threadIdx.x == 0) err_sum[r] = red[0];
-    __syncthreads();
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) rsum[(size_t)blockIdx.x * 16 + r] = s;
   }
+}
+
+// err_sum[r] = sum over the `blocks` workgroup sums rsum[b][r], in order.
+__global__ __launch_bounds__(64) void cal_reduce_sum_kernel(const double *rsum, int blocks, int K, double *err_sum) {
+  const int r = threadIdx.x;
+  if (r >= K) return;
+  double s = 0.0;
+  for (int b = 0; b < blocks; ++b) s += rsum[(size_t)b * 16 + r];
+  err_sum[r] = s;
 }
 
 }  // namespace sats

@@ -912,8 +912,9 @@ struct CalBuffers {
   float *part = nullptr;           // [d / 128][n][16]
   uint32_t *hpart = nullptr, *hist = nullptr, *prefix = nullptr, *rank = nullptr;
   float *tk = nullptr, *thr15 = nullptr;
-  unsigned long long *hist16 = nullptr;
+  unsigned long long *ge15 = nullptr;  // #{|g| >= t_r} of a product's candidates
   double *errsum = nullptr;
+  double *rsum = nullptr;          // [ceil(n / 64)][16] workgroup sums of the Eq. 6 terms
   int *ctl = nullptr;              // [passes][2] rows of each gate/up pass, MFMA on
 };
 
@@ -924,7 +925,7 @@ struct CalBuffers {
 // their stream before they return, so two calls never share them at once.
 struct CalCache {
   CalBuffers b;
-  size_t cap[15] = {};  // elements of each buffer, in the order of cal_buffers
+  size_t cap[16] = {};  // elements of each buffer, in the order of cal_buffers
 };
 std::mutex g_cal_mu;
 std::map<int, CalCache> g_cal;
@@ -955,7 +956,7 @@ int cal_release_all() {
     const CalBuffers &b = kv.second.b;
     for (void *q : {(void *)b.G, (void *)b.ph, (void *)b.pl, (void *)b.cnt, (void *)b.WdT, (void *)b.part,
                     (void *)b.hpart, (void *)b.hist, (void *)b.prefix, (void *)b.rank, (void *)b.tk, (void *)b.thr15,
-                    (void *)b.hist16, (void *)b.errsum, (void *)b.ctl})
+                    (void *)b.ge15, (void *)b.errsum, (void *)b.ctl, (void *)b.rsum})
       if (q) HIP_TRY(hipFree(q));
   }
   g_cal.clear();
@@ -1031,7 +1032,7 @@ int cal_quantiles(CalBuffers &cb, uint64_t N, const double *levels, int K, float
     const int kh = pass == 0 ? 1 : K, nh = kh << kBits[pass];
     hipLaunchKernelGGL(cal_hist_kernel, dim3(kCalHistParts), dim3(kCalHistThreads), 0, s, cb.G, (size_t)N,
                        cb.prefix, kh, kShift[pass], kBits[pass], cb.hpart);
-    hipLaunchKernelGGL(cal_hist_reduce_kernel, dim3((nh + kCalThreads - 1) / kCalThreads), dim3(kCalThreads), 0, s,
+    hipLaunchKernelGGL(cal_hist_reduce_kernel, dim3((nh + kCalHRBins - 1) / kCalHRBins), dim3(kCalHistThreads), 0, s,
                        cb.hpart, kCalHistParts, nh, cb.hist);
     hipLaunchKernelGGL(cal_select_kernel, dim3(K), dim3(kCalSelThreads), 0, s, cb.hist,
                        pass == 0 ? (size_t)0 : ((size_t)1 << kBits[pass]), 1 << kBits[pass], kBits[pass], cb.prefix,
@@ -1050,7 +1051,7 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
                double *err, double *sp, float *err_rows, hipStream_t s) {
   using namespace sats;
   const uint64_t N = (uint64_t)n * d_ff;
-  const int grid = (int)std::min<uint64_t>(2048, (N + kCalThreads - 1) / kCalThreads);
+  const int grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(2048, (N / 4 + kCalThreads - 1) / kCalThreads));
   if (err) {
     hipLaunchKernelGGL(cal_transpose_kernel, dim3(d / 64, d_ff / 64), dim3(kCalThreads), 0, s, Wd, (int)d_ff,
                        (int)d, cb.WdT);
@@ -1061,9 +1062,9 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
     float thr[kCalCand];
     for (int r = 0; r < kCalCand; ++r) thr[r] = r < kc ? t[k0 + r] : INFINITY;
     HIP_TRY(hipMemcpyAsync(cb.thr15, thr, sizeof thr, hipMemcpyHostToDevice, s));
-    HIP_TRY(hipMemsetAsync(cb.hist16, 0, 16 * sizeof(unsigned long long), s));
+    HIP_TRY(hipMemsetAsync(cb.ge15, 0, kCalCand * sizeof(unsigned long long), s));
     hipLaunchKernelGGL(cal_bucket_kernel, dim3(grid), dim3(kCalThreads), 0, s, cb.G, (size_t)N, cb.thr15, cb.cnt,
-                       cb.hist16);
+                       cb.ge15);
     if (err) {
       CalErrArgs ce{};
       ce.ph = cb.ph;
@@ -1084,21 +1085,21 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
           hipExtLaunchKernelGGL(cal_err_kernel<1>, dim3(d / kDenseDownNT, (n + kCalRows - 1) / kCalRows),
                                 dim3(kDenseThreads), 0, s, tl.start, tl.stop, 0, ce);
       }
-      hipLaunchKernelGGL(cal_reduce_kernel, dim3(1), dim3(kCalReduceThreads), 0, s, cb.part,
+      const int rblocks = (int)((n + 63) / 64);
+      hipLaunchKernelGGL(cal_reduce_kernel, dim3(rblocks), dim3(64 * kCalRedWaves), 0, s, cb.part,
                          (int)(d / kDenseDownNT), (int)n, kc, err_rows ? err_rows + k0 : (float *)nullptr, K,
-                         cb.errsum);
+                         cb.rsum);
+      hipLaunchKernelGGL(cal_reduce_sum_kernel, dim3(1), dim3(64), 0, s, cb.rsum, rblocks, kc, cb.errsum);
     }
     HIP_TRY(hipGetLastError());
     double es[kCalCand];
-    unsigned long long h16[16];
+    unsigned long long ge[kCalCand];
     if (err) HIP_TRY(hipMemcpyAsync(es, cb.errsum, kc * sizeof(double), hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipMemcpyAsync(h16, cb.hist16, sizeof h16, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(ge, cb.ge15, kc * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
-    unsigned long long below = 0;
     for (int r = 0; r < kc; ++r) {
-      below += h16[r];  // #{c <= r} = #{|g| < t_r}
       if (err) err[k0 + r] = es[r] / (double)n;
-      sp[k0 + r] = (double)below / (double)N;
+      sp[k0 + r] = (double)(N - ge[r]) / (double)N;  // #{|g| < t_r} / N
     }
   }
   return SATS_OK;
@@ -1120,9 +1121,10 @@ int cal_buffers(CalBuffers &cb, int64_t n, int64_t d, int64_t d_ff) {
       (rc = cal_alloc(&b.hpart, &k[6], (size_t)kCalHistParts * sats::kCalHistLds)) ||
       (rc = cal_alloc(&b.hist, &k[7], sats::kCalHistLds)) || (rc = cal_alloc(&b.prefix, &k[8], sats::kCalMaxLevels)) ||
       (rc = cal_alloc(&b.rank, &k[9], sats::kCalMaxLevels)) || (rc = cal_alloc(&b.tk, &k[10], sats::kCalMaxLevels)) ||
-      (rc = cal_alloc(&b.thr15, &k[11], sats::kCalCand)) || (rc = cal_alloc(&b.hist16, &k[12], 16)) ||
+      (rc = cal_alloc(&b.thr15, &k[11], sats::kCalCand)) || (rc = cal_alloc(&b.ge15, &k[12], sats::kCalCand)) ||
       (rc = cal_alloc(&b.errsum, &k[13], sats::kCalCand)) ||
-      (rc = cal_alloc(&b.ctl, &k[14], 2 * ((n + sats::kDenseMaxTokens - 1) / sats::kDenseMaxTokens))))
+      (rc = cal_alloc(&b.ctl, &k[14], 2 * ((n + sats::kDenseMaxTokens - 1) / sats::kDenseMaxTokens))) ||
+      (rc = cal_alloc(&b.rsum, &k[15], (size_t)((n + 63) / 64) * 16)))
     return rc;
   cb = b;
   return SATS_OK;
