@@ -762,9 +762,11 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
   for (int t = 0; t < NA; ++t)
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) acc[t][ct] = f32x4v{0.f, 0.f, 0.f, 0.f};
-  bf16x8 ah[NA], al[NA], bq[CT];
+  // two operand sets: the products of one half of a stage run while the
+  // operands of the next half are read and masked (set 0: first halves)
+  bf16x8 ah0[NA], al0[NA], bq0[CT], ah1[NA], al1[NA], bq1[CT];
   // stage buffer BUF, half j: this lane's masked A operands and the B operands
-  auto load_ops = [&](const uint8_t *buf, int j) {
+  auto load_ops = [&](const uint8_t *buf, int j, bf16x8(&ah)[NA], bf16x8(&al)[NA], bf16x8(&bq)[CT]) {
     const int k = 32 * j + 8 * g;
 #pragma unroll
     for (int t = 0; t < NA; ++t) {
@@ -790,7 +792,7 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
       bq[ct] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(buf + r * 128 + ct_pos(r, 4 * j + g) * 16));
     }
   };
-  auto mma = [&]() {
+  auto mma = [&](const bf16x8(&ah)[NA], const bf16x8(&al)[NA], const bf16x8(&bq)[CT]) {
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
@@ -799,6 +801,17 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
       for (int t = 0; t < NA; ++t) acc[t][ct] = mfma16(al[t], bq[ct], acc[t][ct]);
+  };
+  // the schedule of one half: each product followed by a few of the other
+  // half's operand instructions (VALU masks, LDS reads), so that the matrix
+  // core and the vector unit work at once
+  auto interleave = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2 * NA * CT; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // an LDS read
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+    }
   };
 #define SATS_CE_ISSUE(BUF, SN)                                                               \
   {                                                                                          \
@@ -811,17 +824,21 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
   // step s: wait until stage s + 1 has landed (the loads of s + 2 .. s + 4,
   // nine, may be outstanding) and every wavefront is done with stage s - 1,
   // whose buffer takes stage s + 5; then stage s, whose first-half operands
-  // are already in registers, and the first-half operands of stage s + 1
+  // are already in registers, with its second-half operands built under the
+  // first half's products and the first-half operands of stage s + 1 under
+  // the second half's (read but not used after the last stage)
 #define SATS_CE_STEP(CUR, NXT, FREE, P)                                                      \
   {                                                                                          \
     const int s_ = s0_ + (P);                                                                \
     dense_stage_barrier<9>();                                                                \
     SATS_CE_ISSUE(FREE, s_ + 5);                                                             \
     if (s_ < S) {                                                                            \
-      mma();                                                                                 \
-      load_ops((CUR), 1);                                                                    \
-      mma();                                                                                 \
-      if (s_ + 1 < S) load_ops((NXT), 0);                                                    \
+      load_ops((CUR), 1, ah1, al1, bq1);                                                     \
+      mma(ah0, al0, bq0);                                                                    \
+      interleave();                                                                          \
+      load_ops((NXT), 0, ah0, al0, bq0);                                                     \
+      mma(ah1, al1, bq1);                                                                    \
+      interleave();                                                                          \
     }                                                                                        \
   }
   SATS_CE_ISSUE(rg0, 0);
@@ -830,7 +847,7 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
   SATS_CE_ISSUE(rg3, 3);
   SATS_CE_ISSUE(rg4, 4);
   dense_stage_barrier<12>();  // stage 0 has landed
-  load_ops(rg0, 0);
+  load_ops(rg0, 0, ah0, al0, bq0);
   for (int s0_ = 0; s0_ < S; s0_ += 6) {
     SATS_CE_STEP(rg0, rg1, rg5, 0)
     SATS_CE_STEP(rg1, rg2, rg0, 1)
