@@ -174,3 +174,38 @@ def test_kept_buffers_across_shapes_and_release():
     for a, b in ((first, again), (first, fresh), (fb, bb)):
         for u, v in zip(a, b):
             np.testing.assert_array_equal(np.asarray(u), np.asarray(v))
+
+
+def test_many_levels_select_against_its_own_counts():
+    """1024 levels (16 select calls of 64 levels): the Eq. 3 order statistics
+    against the oracle's, and against the library's own count of the values
+    below each (#{|g| < t_k} = rank - 1 but for ties at t_k, which float32
+    makes rare).  With this many levels, distinct prefixes of one call share
+    a slot of the select's prefix table in its 20- or 28-bit passes (checked
+    on the returned thresholds), so its fallback search is reached."""
+    import math
+    from fractions import Fraction
+    n, d, dff = 64, 256, 1024
+    x, wg, wu, wd = _layer(71, d, dff, n)
+    levels = [round(float(q), 6) for q in np.linspace(0.0005, 0.9995, 1024)]
+    t, err, sp, _ = _gpu_curves(x, wg, wu, wd, levels, rows=False)
+    H = numerics.decode(x, "bf16")
+    W = [numerics.decode(w, "bf16") for w in (wg, wu, wd)]
+    absg = np.abs(osats.layer_terms(H, *W)[0])
+    N = absg.size
+    ref = np.array([calibrate.percentile_threshold(absg, q) for q in levels])
+    np.testing.assert_allclose(t, ref, rtol=1e-4, atol=1e-30)
+    assert np.all(np.diff(t) >= 0)
+    rank = np.array([min(max(math.ceil(Fraction(repr(q)) * N), 1), N) for q in levels])
+    below = np.rint(sp * N).astype(np.int64)
+    gap = (rank - 1) - below
+    assert gap.min() >= 0 and gap.max() <= 3, (gap.min(), gap.max())
+    assert np.count_nonzero(gap) <= 8
+    # slot sharing of the 20- and 28-bit prefixes within a call of 64 levels
+    bits = t.astype(np.float32).view(np.uint32).astype(np.int64)
+    shared = 0
+    for c0 in range(0, len(levels), 64):
+        for hs in (12, 4):
+            pre = np.unique(bits[c0:c0 + 64] >> hs)
+            shared += len(pre) - len(np.unique(pre & 0xFFF))
+    assert shared > 0
