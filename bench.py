@@ -371,21 +371,29 @@ def bench_calib(args):
         t, err, sp = sats.sats_calibration_curves(X, *W, n, d, d_ff, levels)
     dt = (time.perf_counter() - t0) / steps
     kern = {}
-    products = (K + 14) // 15
     for k in kinds:
         tot, c = sats.sats_timing_end(k)
         kern[sats.sats_kernel_name(k)] = {"avg_us": round(tot / c * 1e3, 2), "launches_per_step": c // steps}
-    # algorithmic flops of the error products of one step: per product of kc
-    # candidates, kc masked products and y itself per calibration row, each
-    # over d_ff x d; executed: hi and lo terms, and 16 MFMA rows per
-    # calibration row (8 when at most 7 candidates share a tile)
-    kcs = [min(15, K - k0) for k0 in range(0, K, 15)]
-    alg_flops = sum(2.0 * n * (kc + 1) * d_ff * d for kc in kcs)
-    exe_flops = sum(2.0 * 2 * n * (8 if kc <= 7 else 16) * d_ff * d for kc in kcs)
+    # the library's products: candidates at or below 0 (no neuron removed)
+    # take none; from the first positive one, 15 per product, the first with
+    # y; a later one of at most 4 candidates packs 4 calibration rows per tile
+    z = int(np.count_nonzero(np.asarray(t) <= 0))
+    kcs, packs = [], []
+    for k0 in range(z, K, 15):
+        kc = min(15, K - k0)
+        packs.append(4 if kcs and kc <= 4 else (2 if kc <= 7 else 1))
+        kcs.append(kc)
+    # algorithmic flops of the error products of one step: per calibration
+    # row, a masked product for every positive candidate and y once, each
+    # over d_ff x d; executed: hi and lo terms, 16 / pack MFMA rows per
+    # calibration row and product
+    alg_flops = 2.0 * n * (K - z + 1) * d_ff * d
+    exe_flops = sum(2.0 * 2 * n * (16 // pk) * d_ff * d for pk in packs)
     e = kern["cal_err_kernel"]
     e_step_us = e["avg_us"] * e["launches_per_step"]
     achieved = alg_flops / (e_step_us * 1e-6) / 1e12
-    e.update(candidates_per_launch=kcs, algorithmic_flops_per_step=alg_flops, achieved_tflops=round(achieved, 1),
+    e.update(candidates_per_launch=kcs, calibration_rows_per_tile=packs, algorithmic_flops_per_step=alg_flops,
+             achieved_tflops=round(achieved, 1),
              executed_flops_per_step=exe_flops, executed_tflops=round(exe_flops / (e_step_us * 1e-6) / 1e12, 1))
     cpu = None
     if not args.no_cpu:
@@ -406,7 +414,7 @@ def bench_calib(args):
         "ms_per_step": round(dt * 1e3, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16 (fp32 accumulate, p as bf16 hi + lo)", "data": "synthetic",
         "config": {"workload": f"sats_calib_{cfg.name}", "d": d, "d_ff": d_ff, "calibration_rows": n,
-                   "candidates": K, "error_products": products},
+                   "candidates": K, "error_products": len(kcs)},
         "kernels": kern,
         "roofline": {"kernel": "cal_err_kernel", "bound": "mfma", "achieved": round(achieved, 1),
                      "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -284,10 +284,13 @@ __global__ __launch_bounds__(kCalThreads) void cal_bucket_kernel(const float *G,
 // ...; wavefront 0 adds the eight sums in order and forms per row
 // e_r = ||y - y_t_r|| / (||y|| + eps), and the sums of e_r over the rows
 // (a fixed tree over the lanes) go to rsum[b][r], which
-// cal_reduce_sum_kernel adds over workgroups in order.
+// cal_reduce_sum_kernel adds over workgroups in order.  ny2_out (or null)
+// keeps ||y||^2 of each row for later products; a product without a y row
+// takes it from ny2_in.
 constexpr int kCalRedWaves = 8;
 __global__ __launch_bounds__(64 * kCalRedWaves) void cal_reduce_kernel(const float *part, int ntiles, int n, int K,
-                                                                       float *err_rows, int rows_ld, double *rsum) {
+                                                                       float *err_rows, int rows_ld, double *rsum,
+                                                                       const float *ny2_in, float *ny2_out) {
   __shared__ float acc[kCalRedWaves][16][65];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, m = blockIdx.x * 64 + lane;
   float e2[16];
@@ -314,7 +317,8 @@ __global__ __launch_bounds__(64 * kCalRedWaves) void cal_reduce_kernel(const flo
 #pragma unroll
   for (int r = 0; r < 16; ++r)
     for (int j = 1; j < kCalRedWaves; ++j) e2[r] += acc[j][r][lane];
-  const float ny = sqrtf(e2[15]);
+  if (ny2_out && m < n) ny2_out[m] = e2[15];
+  const float ny = sqrtf((ny2_in && m < n) ? ny2_in[m] : e2[15]);
 #pragma unroll
   for (int r = 0; r < kCalCand; ++r) {
     double s = 0.0;
@@ -335,6 +339,14 @@ __global__ __launch_bounds__(64) void cal_reduce_sum_kernel(const double *rsum, 
   double s = 0.0;
   for (int b = 0; b < blocks; ++b) s += rsum[(size_t)b * 16 + r];
   err_sum[r] = s;
+}
+
+// err_rows[m][k] = 0 for k < ncols: candidates at or below 0 remove no
+// neuron (no |g| is below them), so their Eq. 6 terms are 0 exactly.
+__global__ __launch_bounds__(kCalThreads) void cal_zero_cols_kernel(float *rows, size_t n, int ld, int ncols) {
+  const size_t tot = n * (size_t)ncols;
+  for (size_t i = blockIdx.x * (size_t)kCalThreads + threadIdx.x; i < tot; i += (size_t)gridDim.x * kCalThreads)
+    rows[(i / ncols) * ld + i % ncols] = 0.0f;
 }
 
 }  // namespace sats

@@ -704,7 +704,7 @@ struct CalErrArgs {
   const uint16_t *ph, *pl;  // [n][d_ff] bf16 hi and lo terms of p
   const uint8_t *cnt;       // [n][d_ff] candidates at or below |g|
   const uint16_t *WdT;      // W_down^T of the layer, [d][d_ff]
-  float *part;              // [d / 128][n][16] column-tile sums of squares
+  float *part;              // [d / 128][n][16] column-tile sums of squares ([d / 64] with PACK 4)
   int n, d, d_ff;
 };
 
@@ -712,15 +712,22 @@ constexpr int kCalRows = 16;  // calibration rows per workgroup (2 per wavefront
 
 __device__ __forceinline__ int ct_pos(int r, int q) { return q ^ (r & 7); }
 
+// PACK = calibration rows per A tile: 1 (15 candidates and y), 2 (up to 7
+// candidates and y), or 4 (up to 4 candidates, no y row: ||y||^2 comes from
+// an earlier product).  With PACK 4 wavefront w takes calibration rows
+// 4 (w & 3) .. 4 (w & 3) + 3 over the 64 columns of half w >> 2 of the tile,
+// and its sums of squares go to part tile 2 blockIdx.x + (w >> 2).
 template <int PACK>
 __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
-  static_assert(PACK == 1 || PACK == 2, "one or two calibration rows per A tile");
+  static_assert(PACK == 1 || PACK == 2 || PACK == 4, "one, two or four calibration rows per A tile");
   __shared__ __attribute__((aligned(1024))) uint8_t rg0[kDenseStageBytes], rg1[kDenseStageBytes],
       rg2[kDenseStageBytes], rg3[kDenseStageBytes], rg4[kDenseStageBytes], rg5[kDenseStageBytes];
-  constexpr int CT = kDenseDownNT / 16;  // column tiles of 16
-  constexpr int NA = 2 / PACK;           // A tiles per wavefront
-  constexpr int RPT = 16 / PACK;         // A rows per calibration row
+  constexpr int CT = kDenseDownNT / 16 / (PACK == 4 ? 2 : 1);  // column tiles of 16 per wavefront
+  constexpr int NA = PACK == 4 ? 1 : 2 / PACK;                 // A tiles per wavefront
+  constexpr int RPT = 16 / PACK;                               // A rows per calibration row
+  constexpr bool Y = PACK != 4;                                // the last of them is y
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ch = PACK == 4 ? w >> 2 : 0;  // column half (PACK 4)
   const int g = lane >> 4, l16 = lane & 15;
   const int n0 = blockIdx.x * kDenseDownNT, m0 = blockIdx.y * kCalRows;
   const int K = a.d_ff;
@@ -753,10 +760,11 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
   const int d3 = w < 4 ? 16384 + w * 1024 : 20480 + (w - 4) * 1024;
   const bool v3 = w < 4 ? arv : (w == 4 && crv);
   const uint32_t o3 = w < 4 ? oa : oc, st3 = w < 4 ? sk : (uint32_t)kDenseKC;
-  // A row of this lane: calibration row 2 w + t (tile t), candidate lim; the
-  // last row of a calibration row is y (lim 15: every neuron)
+  // A row of this lane: calibration row 2 w + t (tile t; PACK 4: 4 (w & 3) +
+  // l16 / 4), candidate lim; with a y row the last row of a calibration row
+  // is y (lim 15: every neuron)
   const int rr = l16 % RPT;
-  const uint32_t lim = rr == RPT - 1 ? 15u : (uint32_t)rr;
+  const uint32_t lim = (Y && rr == RPT - 1) ? 15u : (uint32_t)rr;
   f32x4v acc[NA][CT];
 #pragma unroll
   for (int t = 0; t < NA; ++t)
@@ -770,7 +778,7 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
     const int k = 32 * j + 8 * g;
 #pragma unroll
     for (int t = 0; t < NA; ++t) {
-      const int row = 2 * w + (PACK == 1 ? t : l16 / RPT);
+      const int row = PACK == 4 ? 4 * (w & 3) + l16 / RPT : 2 * w + (PACK == 1 ? t : l16 / RPT);
       const u32x4 hv = *reinterpret_cast<const u32x4 *>(buf + 16384 + row * 128 + 2 * k);
       const u32x4 lv = *reinterpret_cast<const u32x4 *>(buf + 18432 + row * 128 + 2 * k);
       const uint2 cv = *reinterpret_cast<const uint2 *>(buf + 20480 + row * 64 + k);
@@ -788,7 +796,7 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
     }
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct) {
-      const int r = 16 * ct + l16;
+      const int r = 16 * (CT * ch + ct) + l16;
       bq[ct] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(buf + r * 128 + ct_pos(r, 4 * j + g) * 16));
     }
   };
@@ -859,9 +867,9 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
   __builtin_amdgcn_s_waitcnt(0);  // the zero-filling loads past the range land too
 #undef SATS_CE_STEP
 #undef SATS_CE_ISSUE
-  // sums of squares over the tile's 128 columns: the 8 column tiles in order
-  // within the lane, then the 16 columns of a tile by lane exchange.  Lane
-  // (g, l16) of tile t holds A rows 4 g .. 4 g + 3.
+  // sums of squares over the wavefront's columns (128; PACK 4: 64): its
+  // column tiles in order within the lane, then the 16 columns of a tile by
+  // lane exchange.  Lane (g, l16) of tile t holds A rows 4 g .. 4 g + 3.
 #pragma unroll
   for (int t = 0; t < NA; ++t)
 #pragma unroll
@@ -872,10 +880,11 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
 #pragma unroll
       for (int o = 8; o >= 1; o >>= 1) v += __shfl_xor(v, o, 16);
       const int arow = 4 * g + r;
-      const int m = m0 + 2 * w + (PACK == 1 ? t : arow / RPT);
+      const int m = m0 + (PACK == 4 ? 4 * (w & 3) + arow / RPT : 2 * w + (PACK == 1 ? t : arow / RPT));
       const int cand = arow % RPT;
-      const int slot = cand == RPT - 1 ? 15 : cand;
-      if (l16 == 0 && m < a.n) a.part[((size_t)blockIdx.x * a.n + m) * 16 + slot] = v;
+      const int slot = (Y && cand == RPT - 1) ? 15 : cand;
+      const int tile = PACK == 4 ? 2 * blockIdx.x + ch : blockIdx.x;
+      if (l16 == 0 && m < a.n) a.part[((size_t)tile * a.n + m) * 16 + slot] = v;
     }
 }
 

@@ -909,12 +909,13 @@ struct CalBuffers {
   uint16_t *ph = nullptr, *pl = nullptr;  // [n][d_ff] p as bf16 hi + lo
   uint8_t *cnt = nullptr;          // [n][d_ff] candidates at or below |g|
   uint16_t *WdT = nullptr;         // [d][d_ff] W_down^T of the layer
-  float *part = nullptr;           // [d / 128][n][16]
+  float *part = nullptr;           // [d / 64][n][16] (products with a y row use the first d / 128 tiles)
   uint32_t *hpart = nullptr, *hist = nullptr, *prefix = nullptr, *rank = nullptr;
   float *tk = nullptr, *thr15 = nullptr;
   unsigned long long *ge15 = nullptr;  // #{|g| >= t_r} of a product's candidates
   double *errsum = nullptr;
   double *rsum = nullptr;          // [ceil(n / 64)][16] workgroup sums of the Eq. 6 terms
+  float *ny2 = nullptr;            // [n] ||y||^2 of each row (from the first product)
   int *ctl = nullptr;              // [passes][2] rows of each gate/up pass, MFMA on
 };
 
@@ -925,7 +926,7 @@ struct CalBuffers {
 // their stream before they return, so two calls never share them at once.
 struct CalCache {
   CalBuffers b;
-  size_t cap[16] = {};  // elements of each buffer, in the order of cal_buffers
+  size_t cap[17] = {};  // elements of each buffer, in the order of cal_buffers
 };
 std::mutex g_cal_mu;
 std::map<int, CalCache> g_cal;
@@ -956,7 +957,7 @@ int cal_release_all() {
     const CalBuffers &b = kv.second.b;
     for (void *q : {(void *)b.G, (void *)b.ph, (void *)b.pl, (void *)b.cnt, (void *)b.WdT, (void *)b.part,
                     (void *)b.hpart, (void *)b.hist, (void *)b.prefix, (void *)b.rank, (void *)b.tk, (void *)b.thr15,
-                    (void *)b.ge15, (void *)b.errsum, (void *)b.ctl, (void *)b.rsum})
+                    (void *)b.ge15, (void *)b.errsum, (void *)b.ctl, (void *)b.rsum, (void *)b.ny2})
       if (q) HIP_TRY(hipFree(q));
   }
   g_cal.clear();
@@ -1046,7 +1047,11 @@ int cal_quantiles(CalBuffers &cb, uint64_t N, const double *levels, int K, float
 
 // Eq. 6 error and sparsity of ascending candidates t[0..K) (any K), 15 per
 // product.  err_rows (device, [n][K]) is optional; without err only the
-// sparsities are computed.
+// sparsities are computed.  Candidates at or below 0 remove no neuron (no
+// |g| is below them): their error and sparsity are 0 exactly, and the
+// products start at the first positive candidate.  The first product carries
+// y and keeps ||y||^2 per row; a later product of at most 4 candidates takes
+// it from there and packs four calibration rows per MFMA tile.
 int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t d_ff, const float *t, int K,
                double *err, double *sp, float *err_rows, hipStream_t s) {
   using namespace sats;
@@ -1057,8 +1062,21 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
                        (int)d, cb.WdT);
     HIP_TRY(hipGetLastError());
   }
-  for (int k0 = 0; k0 < K; k0 += kCalCand) {
+  int z = 0;
+  while (z < K && t[z] <= 0.0f) ++z;
+  for (int k = 0; k < z; ++k) {
+    if (err) err[k] = 0.0;
+    sp[k] = 0.0;
+  }
+  if (err && err_rows && z > 0) {
+    hipLaunchKernelGGL(cal_zero_cols_kernel, dim3((unsigned)std::min<int64_t>(1024, (n * z + kCalThreads - 1) / kCalThreads)),
+                       dim3(kCalThreads), 0, s, err_rows, (size_t)n, K, z);
+    HIP_TRY(hipGetLastError());
+  }
+  bool have_y = false;  // ||y||^2 of every row is in cb.ny2
+  for (int k0 = z; k0 < K; k0 += kCalCand) {
     const int kc = std::min(kCalCand, K - k0);
+    const bool pack4 = have_y && kc <= 4;
     float thr[kCalCand];
     for (int r = 0; r < kCalCand; ++r) thr[r] = r < kc ? t[k0 + r] : INFINITY;
     HIP_TRY(hipMemcpyAsync(cb.thr15, thr, sizeof thr, hipMemcpyHostToDevice, s));
@@ -1077,8 +1095,12 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
       ce.d_ff = (int)d_ff;
       {
         TimedLaunch tl(SATS_K_CAL_ERR, s);
-        // at most 7 candidates: two calibration rows per MFMA tile
-        if (kc <= 7)
+        // at most 4 candidates and ||y||^2 known: four calibration rows per
+        // MFMA tile, no y row; at most 7: two per tile
+        if (pack4)
+          hipExtLaunchKernelGGL(cal_err_kernel<4>, dim3(d / kDenseDownNT, (n + kCalRows - 1) / kCalRows),
+                                dim3(kDenseThreads), 0, s, tl.start, tl.stop, 0, ce);
+        else if (kc <= 7)
           hipExtLaunchKernelGGL(cal_err_kernel<2>, dim3(d / kDenseDownNT, (n + kCalRows - 1) / kCalRows),
                                 dim3(kDenseThreads), 0, s, tl.start, tl.stop, 0, ce);
         else
@@ -1087,8 +1109,10 @@ int cal_curves(CalBuffers &cb, const uint16_t *Wd, int64_t n, int64_t d, int64_t
       }
       const int rblocks = (int)((n + 63) / 64);
       hipLaunchKernelGGL(cal_reduce_kernel, dim3(rblocks), dim3(64 * kCalRedWaves), 0, s, cb.part,
-                         (int)(d / kDenseDownNT), (int)n, kc, err_rows ? err_rows + k0 : (float *)nullptr, K,
-                         cb.rsum);
+                         (int)(d / kDenseDownNT) * (pack4 ? 2 : 1), (int)n, kc,
+                         err_rows ? err_rows + k0 : (float *)nullptr, K, cb.rsum,
+                         pack4 ? (const float *)cb.ny2 : (const float *)nullptr, have_y ? (float *)nullptr : cb.ny2);
+      have_y = true;
       hipLaunchKernelGGL(cal_reduce_sum_kernel, dim3(1), dim3(64), 0, s, cb.rsum, rblocks, kc, cb.errsum);
     }
     HIP_TRY(hipGetLastError());
@@ -1117,14 +1141,14 @@ int cal_buffers(CalBuffers &cb, int64_t n, int64_t d, int64_t d_ff) {
   int rc = 0;
   if ((rc = cal_alloc(&b.G, &k[0], N)) || (rc = cal_alloc(&b.ph, &k[1], N)) || (rc = cal_alloc(&b.pl, &k[2], N)) ||
       (rc = cal_alloc(&b.cnt, &k[3], N)) || (rc = cal_alloc(&b.WdT, &k[4], (size_t)d * d_ff)) ||
-      (rc = cal_alloc(&b.part, &k[5], (size_t)(d / sats::kDenseDownNT) * n * 16)) ||
+      (rc = cal_alloc(&b.part, &k[5], (size_t)(d / sats::kDenseDownNT) * 2 * n * 16)) ||
       (rc = cal_alloc(&b.hpart, &k[6], (size_t)kCalHistParts * sats::kCalHistLds)) ||
       (rc = cal_alloc(&b.hist, &k[7], sats::kCalHistLds)) || (rc = cal_alloc(&b.prefix, &k[8], sats::kCalMaxLevels)) ||
       (rc = cal_alloc(&b.rank, &k[9], sats::kCalMaxLevels)) || (rc = cal_alloc(&b.tk, &k[10], sats::kCalMaxLevels)) ||
       (rc = cal_alloc(&b.thr15, &k[11], sats::kCalCand)) || (rc = cal_alloc(&b.ge15, &k[12], sats::kCalCand)) ||
       (rc = cal_alloc(&b.errsum, &k[13], sats::kCalCand)) ||
       (rc = cal_alloc(&b.ctl, &k[14], 2 * ((n + sats::kDenseMaxTokens - 1) / sats::kDenseMaxTokens))) ||
-      (rc = cal_alloc(&b.rsum, &k[15], (size_t)((n + 63) / 64) * 16)))
+      (rc = cal_alloc(&b.rsum, &k[15], (size_t)((n + 63) / 64) * 16)) || (rc = cal_alloc(&b.ny2, &k[16], (size_t)n)))
     return rc;
   cb = b;
   return SATS_OK;

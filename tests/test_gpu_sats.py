@@ -67,16 +67,23 @@ def _gpu_curves(x, wg, wu, wd, levels, rows=True):
     return t, err, sp, (er.cpu().numpy() if rows else None)
 
 
-@pytest.mark.parametrize("seed,d,dff,n", [(61, 256, 1024, 40), (62, 128, 512, 17), (63, 512, 1536, 64)])
-def test_curves_match_oracle(seed, d, dff, n):
+# the benchmark's grid: 0 and 19 percentiles, i.e. products of 15 candidates
+# (with y) and of 4 (four calibration rows per tile, y from the first)
+LEVELS20 = [0.0] + [round(0.05 * i, 4) for i in range(1, 20)]
+
+
+@pytest.mark.parametrize("seed,d,dff,n,levels", [(61, 256, 1024, 40, LEVELS), (62, 128, 512, 17, LEVELS),
+                                                 (63, 512, 1536, 64, LEVELS), (64, 256, 1024, 37, LEVELS20),
+                                                 (65, 384, 768, 16, LEVELS20)])
+def test_curves_match_oracle(seed, d, dff, n, levels):
     x, wg, wu, wd = _layer(seed, d, dff, n)
-    t, err, sp, er = _gpu_curves(x, wg, wu, wd, LEVELS)
+    t, err, sp, er = _gpu_curves(x, wg, wu, wd, levels)
     H = numerics.decode(x, "bf16")
     W = [numerics.decode(w, "bf16") for w in (wg, wu, wd)]
     g = osats.layer_terms(H, *W)[0]
     absg = np.abs(g)
     # candidates: Eq. 3 order statistics
-    for k, q in enumerate(LEVELS):
+    for k, q in enumerate(levels):
         ref = calibrate.percentile_threshold(absg, q)
         assert t[k] == pytest.approx(ref, rel=1e-4, abs=1e-30), (k, q)
     assert t[0] == 0.0 and np.all(np.diff(t) >= 0)
