@@ -689,13 +689,16 @@ __global__ __launch_bounds__(kDenseThreads) void dense_down_kernel(DenseArgs a) 
 // 8 column tiles of W_down^T, so that no two wavefronts build the same
 // operand.  With PACK = 1 an A tile holds the 16 rows (15 candidates and y)
 // of one calibration row; with PACK = 2 (at most 7 candidates) it holds two
-// calibration rows of 8 (7 candidates and y), halving the MFMA work.
+// calibration rows of 8 (7 candidates and y), halving the MFMA work; with
+// PACK = 4 (at most 4 candidates, ||y||^2 known) four calibration rows of 4
+// and no y row, each wavefront over half of the 128 columns.
 // W_down enters transposed (W_down^T, [d][d_ff], made by
 // cal_transpose_kernel) so that each MFMA B operand is one 16-byte LDS read;
 // chunk q of tile row r sits at q ^ (r & 7), so the eight rows read by eight
 // consecutive lanes fall in distinct banks.  The operands of the first half
 // of stage s + 1 are read and masked at the end of stage s (the stage
-// barrier waits for two stages), so every stage starts with MFMAs.
+// barrier waits for two stages), so every stage starts with MFMAs; the
+// second half's operands are masked while the first half's products run.
 // Per row (m, r) the kernel writes the sum of the squares of its 128
 // outputs, the partial of ||y - y_t||^2 (and ||y||^2, slot 15) for the
 // column tile; cal_reduce_kernel finishes the norms.
