@@ -821,7 +821,7 @@ __global__ __launch_bounds__(kDenseThreads) void cal_err_kernel(CalErrArgs a) {
     for (int i = 0; i < 2 * NA * CT; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // an LDS read
-      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, PACK == 4 ? 6 : 2, 0);  // VALU (PACK 4: 8 products a half)
     }
   };
 #define SATS_CE_ISSUE(BUF, SN)                                                               \
